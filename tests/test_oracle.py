@@ -1,0 +1,355 @@
+"""Pins of the CPU oracle against things other than itself: hand-worked
+examples of the paper's cost model, closed forms, brute-force enumeration of
+every split on tiny inputs, and invariants of the min-max split.
+CPU only."""
+import copy
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import brute
+from oracle import oracle as O
+from workloads.gen import Profile, pack_stage, random_instance
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden", "worked_examples.json")
+
+
+def profile_from_json(d, cap=None, node=None):
+    a = lambda k, dt: np.array(d[k], dtype=dt)
+    return Profile(
+        L=d["L"], tp_degrees=a("tp_degrees", np.int32), ep_degrees=a("ep_degrees", np.int32),
+        layer_ns=a("layer_ns", np.int64), profiled=a("profiled", np.uint8), is_moe=a("is_moe", np.uint8),
+        state_bytes=a("state_bytes", np.int64), xstate_bytes=a("xstate_bytes", np.int64),
+        act_bytes=a("act_bytes", np.int64), grad_bytes=a("grad_bytes", np.int64),
+        xgrad_bytes=a("xgrad_bytes", np.int64), boundary_bytes=d["boundary_bytes"], a2a_bytes=d["a2a_bytes"],
+        mem_cap_bytes=np.array(cap if cap else d["mem_cap_bytes"], dtype=np.int64),
+        node_size=np.array(node if node else d["node_size"], dtype=np.int32), n_gpus=a("n_gpus", np.int32),
+        intra_bw_MBps=a("intra_bw_MBps", np.int64), link_bw_MBps=a("link_bw_MBps", np.int64)).check()
+
+
+def one_template(stages, s_max=None):
+    s_max = s_max or len(stages)
+    rec = np.zeros((1, s_max), dtype=np.uint32)
+    for s, (g, tp, ep, dp) in enumerate(stages):
+        rec[0, s] = pack_stage(g, int(np.log2(tp)), int(np.log2(ep)), dp)
+    return np.array([len(stages)], dtype=np.uint8), rec
+
+
+def price1(prof, stages, m, flags=0, s_max=None):
+    ns, rec = one_template(stages, s_max)
+    r = O.price_plans(O.OracleProfile(prof), ns, rec, np.array([m], dtype=np.int32), flags)
+    return {k: v[0, 0] for k, v in r.items()}
+
+
+# ---------------------------------------------------------------- closed forms
+
+def test_transfer_closed_forms():
+    g = json.load(open(GOLD))
+    for c in g["transfer"]:
+        assert O.xfer_ns(c["bytes"], c["MBps"]) == c["ns"], c
+    for c in g["allreduce"]:
+        assert O.allreduce_ns(c["bytes"], c["n"], c["MBps"]) == c["ns"], c
+
+
+@pytest.mark.parametrize("kind", ["dense", "moe"])
+def test_worked_examples(kind):
+    g = json.load(open(GOLD))
+    for c in g[f"{kind}_cases"]:
+        prof = profile_from_json(g[f"profile_{kind}"], cap=c.get("cap_override"), node=c.get("node_override"))
+        r = price1(prof, c["stages"], c["m"], c["flags"])
+        got = dict(status=int(r["status"]), iter=int(r["iter"]), bottleneck=int(r["bottleneck"]),
+                   peak_mem=int(r["peak_mem"]), layers=[int(x) for x in r["layers"]])
+        want = {k: c[k] for k in ("status", "iter", "bottleneck", "peak_mem", "layers")}
+        assert got == want, (c["_what"], got, want)
+
+
+def test_single_stage_takes_all_layers():
+    """S = 1: n_0 = L and B* = T(0, 0, L); iter = M_p * T + g."""
+    w = random_instance(7, L=9, n_types=2, moe=False, cap_scale=1000.0)
+    p = w.profile
+    p.profiled[:] = 1
+    r = price1(p, [(1, 1, 1, 1)], 6)
+    assert list(r["layers"]) == [9]
+    T = int(p.layer_ns[1, 0].sum())
+    assert r["bottleneck"] == T and r["iter"] == 6 * T
+
+
+@pytest.mark.parametrize("L,S", [(10, 4), (7, 3), (12, 5), (5, 5), (9, 2), (13, 6)])
+def test_uniform_costs_closed_form(L, S):
+    """Identical stages, unit layer costs, no communication, unbounded
+    memory: B* = ceil(L / S), and the lexicographically smallest optimal
+    split puts max(1, rest - B*(stages left - 1)) layers on each stage."""
+    d = dict(L=L, tp_degrees=[1], ep_degrees=[1], layer_ns=[[[1] * L]], profiled=[[1]], is_moe=[0] * L,
+             state_bytes=[[0] * L], xstate_bytes=[[0] * L], act_bytes=[[0] * L], grad_bytes=[[0] * L],
+             xgrad_bytes=[[0] * L], boundary_bytes=0, a2a_bytes=0, mem_cap_bytes=[1], node_size=[8],
+             n_gpus=[1000], intra_bw_MBps=[1000], link_bw_MBps=[[1000]])
+    r = price1(profile_from_json(d), [(0, 1, 1, 1)] * S, 1)
+    B = -(-L // S)
+    want, rest = [], L
+    for s in range(S):
+        n_s = max(1, rest - B * (S - 1 - s))
+        want.append(n_s)
+        rest -= n_s
+    assert r["bottleneck"] == B and list(r["layers"]) == want
+    assert r["iter"] == L        # M_p = 1: sum of stage times, no sync
+
+
+def test_1f1b_special_cases():
+    """(M-1) max t + sum t + max g: M_p = 1 gives sum t + max g; D = 1 gives g = 0."""
+    w = random_instance(11, L=8, n_types=2, moe=False, cap_scale=1000.0)
+    p = w.profile
+    p.profiled[:] = 1
+    p.node_size[:] = 8
+    st = [(0, 1, 1, 1), (1, 1, 1, 1), (0, 1, 1, 1)]
+    r1 = price1(p, st, 1)
+    r9 = price1(p, st, 9)
+    assert list(r1["layers"]) == list(r9["layers"])       # compute-bound split does not depend on m here
+    assert r9["iter"] - r1["iter"] == 8 * r1["bottleneck"]
+    # D = 2: the all-reduce term appears
+    st2 = [(0, 1, 1, 2), (1, 1, 1, 2), (0, 1, 1, 2)]
+    r2 = price1(p, st2, 2)
+    assert r2["iter"] >= r1["iter"]
+
+
+# ------------------------------------------------------------ brute force pins
+
+@pytest.mark.parametrize("flags", [0, O.F_COMPUTE_ONLY])
+def test_oracle_matches_brute_force(flags):
+    n_checked = 0
+    for seed in range(60):
+        w = random_instance(seed)
+        r = O.price_plans(O.OracleProfile(w.profile), w.n_stages, w.stages, w.m, flags)
+        for t in range(w.n):
+            for k, m in enumerate(w.m):
+                b = brute.price(w.profile, int(w.n_stages[t]), w.s_max, w.stages[t], int(m),
+                                compute_only=bool(flags & O.F_COMPUTE_ONLY))
+                assert b["status"] == r["status"][t, k], (seed, t, k)
+                assert b["layers"] == list(r["layers"][t, k]), (seed, t, k)
+                if b["iter"] is None:
+                    assert r["iter"][t, k] == np.iinfo(np.int64).max
+                    continue
+                assert (b["iter"], b["bottleneck"], b["peak_mem"]) == \
+                    (r["iter"][t, k], r["bottleneck"][t, k], r["peak_mem"][t, k]), (seed, t, k)
+                n_checked += 1
+        best = O.best_plan(w.m, r["iter"], r["status"])
+        assert best == brute.best_plan(w.m, r["iter"], r["status"])
+    assert n_checked > 1000
+
+
+@pytest.mark.parametrize("flags", [O.F_FP32, O.F_FP32 | O.F_COMPUTE_ONLY])
+def test_oracle_fp32_matches_brute_force(flags):
+    for seed in range(40):
+        w = random_instance(seed)
+        rng = np.random.default_rng(seed)
+        # fp32 costs with fractional parts so that roundings actually occur
+        w.profile.layer_ns_f32 = (w.profile.layer_ns * 1000003 + rng.integers(0, 4, w.profile.layer_ns.shape) * 0.25
+                                  ).astype(np.float32)
+        r = O.price_plans(O.OracleProfile(w.profile), w.n_stages, w.stages, w.m, flags)
+        for t in range(w.n):
+            for k, m in enumerate(w.m):
+                b = brute.price(w.profile, int(w.n_stages[t]), w.s_max, w.stages[t], int(m),
+                                compute_only=bool(flags & O.F_COMPUTE_ONLY), fp32=True)
+                assert b["status"] == r["status"][t, k]
+                assert b["layers"] == list(r["layers"][t, k]), (seed, t, k)
+                if b["iter"] is not None:
+                    assert b["iter"] == r["iter"][t, k] and b["bottleneck"] == r["bottleneck"][t, k]
+                    assert b["peak_mem"] == r["peak_mem"][t, k]
+        assert O.best_plan(w.m, r["iter"], r["status"], flags) == brute.best_plan(w.m, r["iter"], r["status"])
+
+
+def test_round_sum_f32_is_correctly_rounded():
+    """A stage time is the exact sum rounded once: 2^24 + 1 + 1 is exact in
+    reals (2^24 + 2, representable) although sequential fp32 adds lose both 1s."""
+    assert O.round_sum_f32([2.0 ** 24, 1.0, 1.0]) == np.float32(2.0 ** 24 + 2)
+    assert O.round_sum_f32([2.0 ** 24, 1.0]) == np.float32(2.0 ** 24)        # tie -> even
+    assert O.round_sum_f32([2.0 ** 24 + 2, 1.0]) == np.float32(2.0 ** 24 + 4)  # tie -> even (up)
+    assert O.round_sum_f32([0.1, 0.2]) == np.float32(Fraction(float(np.float32(0.1))) +
+                                                     Fraction(float(np.float32(0.2))))
+
+
+# ---------------------------------------------------------------- status codes
+
+def test_each_status_code():
+    g = json.load(open(GOLD))
+    p = profile_from_json(g["profile_moe"])
+    p.profiled[0, 1] = 0                                  # TP 2 unprofiled
+    cases = [
+        ([], 1),                                          # S = 0
+        ([(0, 1, 1, 1)] * 3, 1),                          # S > L = 2
+        ([(3, 1, 1, 1)], 2),                              # type out of range
+        ([(0, 8, 1, 1)], 3),                              # TP not in the TP set
+        ([(0, 2, 1, 2)], 4),                              # no profile entry for TP 2
+        ([(0, 1, 1, 0)], 5),                              # DP < 1
+        ([(0, 1, 1, 2), (0, 1, 1, 4)], 5),                # stages disagree on DP
+        ([(0, 1, 4, 4)], 6),                              # EP 4 not in the EP set
+        ([(0, 1, 2, 3)], 6),                              # EP does not divide DP
+        ([(0, 1, 1, 17)], 7),                             # 17 GPUs of a 16-GPU type
+    ]
+    for stages, want in cases:
+        ns, rec = one_template(stages, s_max=3) if stages else (np.array([0], np.uint8), np.zeros((1, 3), np.uint32))
+        r = O.price_plans(O.OracleProfile(p), ns, rec, np.array([4], np.int32))
+        assert r["status"][0, 0] == want, (stages, r["status"][0, 0])
+    # TP larger than the node: TP 2 on 1-GPU nodes
+    p2 = profile_from_json(g["profile_moe"], node=[1])
+    r = price1(p2, [(0, 2, 1, 1)], 4)
+    assert r["status"] == 3
+    # OOM: a cap below one layer
+    p3 = profile_from_json(g["profile_moe"], cap=[50])
+    assert price1(p3, [(0, 1, 1, 1)], 4)["status"] == 8
+
+
+# ------------------------------------------------------------------- invariants
+
+def split_B(plan, comp, Mp, check_mem, p):
+    cuts = np.concatenate([[0], np.cumsum(comp)]).astype(int)
+    out = []
+    for s in range(len(comp)):
+        t, mem, _ = plan.stage(s, cuts[s], cuts[s + 1], Mp)
+        if check_mem and mem > int(p.mem_cap_bytes[plan.st[s]["g"]]):
+            return None
+        out.append(t)
+    return max(out)
+
+
+def valid_plans(w, flags=0):
+    r = O.price_plans(O.OracleProfile(w.profile), w.n_stages, w.stages, w.m, flags)
+    for t in range(w.n):
+        stt, st = brute.status_of(w.profile, int(w.n_stages[t]), w.s_max, w.stages[t])
+        if stt == 0:
+            yield t, st, r
+
+
+def test_bottleneck_not_above_even_or_proportional_split():
+    """B* <= B(even split) (Sailor-style) and <= B(split proportional to stage
+    speed) (Heddle's Distribute), whenever those splits fit."""
+    seen = 0
+    for seed in range(40):
+        w = random_instance(seed, L=int(np.random.default_rng(seed).integers(6, 15)))
+        for t, st, r in valid_plans(w):
+            S, L, p = len(st), w.profile.L, w.profile
+            plan = brute.Plan(p, st)
+            for k, m in enumerate(w.m):
+                if r["status"][t, k] != 0:
+                    continue
+                Mp = -(-int(m) // st[0]["dp"])
+                even = [L // S + (1 if s < L % S else 0) for s in range(S)]
+                speed = np.array([1.0 / sum(x["cost"]) for x in st])
+                prop = np.maximum(1, np.floor(speed / speed.sum() * L)).astype(int)
+                while prop.sum() > L:
+                    prop[np.argmax(prop)] -= 1
+                prop[np.argmin(prop)] += L - prop.sum()
+                for comp in (even, list(prop)):
+                    if min(comp) < 1:
+                        continue
+                    b = split_B(plan, comp, Mp, True, p)
+                    if b is not None:
+                        assert r["bottleneck"][t, k] <= b
+                        seen += 1
+    assert seen > 200
+
+
+def test_bottleneck_monotone_in_layer_time():
+    """Raising any per-layer time never lowers B*."""
+    rng = np.random.default_rng(5)
+    for seed in range(25):
+        w = random_instance(seed)
+        base = O.price_plans(O.OracleProfile(w.profile), w.n_stages, w.stages, w.m)
+        p2 = copy.deepcopy(w.profile)
+        p2.layer_ns = p2.layer_ns + rng.integers(0, 3, p2.layer_ns.shape)
+        up = O.price_plans(O.OracleProfile(p2), w.n_stages, w.stages, w.m)
+        ok = base["status"] == 0
+        assert np.all(up["status"][ok] == 0)
+        assert np.all(up["bottleneck"][ok] >= base["bottleneck"][ok])
+
+
+def test_bottleneck_scales_with_times():
+    """With communication zeroed, scaling every layer time by c scales B*
+    by c and keeps the split."""
+    for seed in range(25):
+        w = random_instance(seed)
+        p = w.profile
+        p.boundary_bytes, p.a2a_bytes = 0, 0
+        a = O.price_plans(O.OracleProfile(p), w.n_stages, w.stages, w.m)
+        p2 = copy.deepcopy(p)
+        p2.layer_ns = p2.layer_ns * 7
+        b = O.price_plans(O.OracleProfile(p2), w.n_stages, w.stages, w.m)
+        ok = a["status"] == 0
+        assert np.array_equal(a["status"], b["status"])
+        assert np.array_equal(a["bottleneck"][ok] * 7, b["bottleneck"][ok])
+        assert np.array_equal(a["layers"], b["layers"])
+
+
+def test_memory_aware_not_below_compute_only():
+    for seed in range(30):
+        w = random_instance(seed)
+        ma = O.price_plans(O.OracleProfile(w.profile), w.n_stages, w.stages, w.m, 0)
+        co = O.price_plans(O.OracleProfile(w.profile), w.n_stages, w.stages, w.m, O.F_COMPUTE_ONLY)
+        ok = ma["status"] == 0
+        assert np.all(ma["bottleneck"][ok] >= co["bottleneck"][ok])
+        # where the compute-only split fits, both modes agree exactly
+        fit = co["status"] == 0
+        assert np.array_equal(ma["bottleneck"][fit], co["bottleneck"][fit])
+        assert np.array_equal(ma["layers"][fit], co["layers"][fit])
+        # with unbounded caps the modes coincide
+        p2 = copy.deepcopy(w.profile)
+        p2.mem_cap_bytes[:] = 1 << 50
+        a = O.price_plans(O.OracleProfile(p2), w.n_stages, w.stages, w.m, 0)
+        b = O.price_plans(O.OracleProfile(p2), w.n_stages, w.stages, w.m, O.F_COMPUTE_ONLY)
+        assert np.array_equal(a["bottleneck"], b["bottleneck"]) and np.array_equal(a["status"], b["status"])
+
+
+def test_mirror_symmetry():
+    """Reversing the layer order and the stage order leaves B* unchanged
+    (compute-only, no p2p, which is charged to the sending stage)."""
+    for seed in range(30):
+        w = random_instance(seed, moe=False)
+        p = w.profile
+        p.boundary_bytes = 0
+        a = O.price_plans(O.OracleProfile(p), w.n_stages, w.stages, w.m, O.F_COMPUTE_ONLY)
+        p2 = copy.deepcopy(p)
+        p2.layer_ns = np.ascontiguousarray(p2.layer_ns[:, :, ::-1])
+        rev = w.stages.copy()
+        for t in range(w.n):
+            S = min(int(w.n_stages[t]), w.s_max)
+            rev[t, :S] = w.stages[t, :S][::-1]
+        b = O.price_plans(O.OracleProfile(p2), w.n_stages, rev, w.m, O.F_COMPUTE_ONLY)
+        # memory is not mirror-symmetric (in-flight activations depend on the
+        # stage position), so compare every plan that has a split
+        split = (a["status"] == 0) | (a["status"] == 8)
+        assert np.array_equal(split, (b["status"] == 0) | (b["status"] == 8))
+        assert np.array_equal(a["bottleneck"][split], b["bottleneck"][split])
+
+
+def test_argmin_ties_and_ratio():
+    """Key iter/m compared exactly; ties go to the lowest template, then m index."""
+    m = np.array([2, 4], dtype=np.int32)
+    it = np.array([[10, 20], [5, 10], [10, 20]], dtype=np.int64)
+    st = np.zeros((3, 2), dtype=np.uint8)
+    assert O.best_plan(m, it, st) == (1, 0)            # 5/2 = 10/4: lower m index wins
+    st[1, :] = 8
+    assert O.best_plan(m, it, st) == (0, 0)            # 10/2 = 20/4 = 10/2 (t2): lowest t, lowest k
+    st[:] = 8
+    assert O.best_plan(m, it, st) is None
+    big = np.array([[2 ** 62, 2 ** 62 - 1]], dtype=np.int64)
+    m2 = np.array([2 ** 30, 2 ** 30 - 1], dtype=np.int32)
+    # (2^62)/(2^30) = 2^32 vs (2^62-1)/(2^30-1) > 2^32: products overflow int64, exact compare needed
+    assert O.best_plan(m2, big, np.zeros((1, 2), np.uint8)) == (0, 0)
+
+
+def test_count_relaxations_full_triangle():
+    """Compute-only work of one DP: stage 0 from row 0 only, the last stage
+    towards column L only, every other stage the full triangle."""
+    d = dict(L=10, tp_degrees=[1], ep_degrees=[1], layer_ns=[[[1] * 10]], profiled=[[1]], is_moe=[0] * 10,
+             state_bytes=[[0] * 10], xstate_bytes=[[0] * 10], act_bytes=[[0] * 10], grad_bytes=[[0] * 10],
+             xgrad_bytes=[[0] * 10], boundary_bytes=0, a2a_bytes=0, mem_cap_bytes=[1], node_size=[8],
+             n_gpus=[1000], intra_bw_MBps=[1000], link_bw_MBps=[[1000]])
+    op = O.OracleProfile(profile_from_json(d))
+    L = 10
+    for S in range(1, 8):
+        _, rec = one_template([(0, 1, 1, 1)] * S)
+        n = L - S + 1
+        want = 1 if S == 1 else n + (S - 2) * n * (n + 1) // 2 + n
+        assert O.count_relaxations(op, S, rec[0], S, 1) == want

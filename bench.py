@@ -1,0 +1,175 @@
+#!/usr/bin/env python3
+"""Benchmark of batched plan pricing on one MI355X.
+
+A step is one pass of the whole hot path over the batch: template decode and
+validation, PartitionLayers (min-max layer split), Evaluate (1F1B iteration
+time, peak memory) for every (template, m) plan -- one launch of the pricing
+kernel -- followed by the argmin over all plans. Inputs are resident in HBM
+before the timed region. Prints one JSON line.
+
+Default workload: the 70B-like dense config (L = 80 layers, 6 GPU types,
+1,000,000 templates of up to 16 stages, m = 64 micro-batches, int64 costs).
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9       # CUs x SIMDs x lanes x clock: 32-bit VALU lane-ops/s
+K_MIN = 3                                   # sub, max, min per relaxation (32-bit DP)
+WORKLOAD_TEXT = {
+    "c1_tiny_dense": "tiny dense: L=24, 2 GPU types, 1k templates S<=4, m=16",
+    "c2_7b_dense": "7B-like dense: L=32, 4 GPU types, 100k templates S<=8, m in {8,32}",
+    "c3_70b_dense": "70B-like dense: L=80, 6 GPU types, 1M templates S<=16, m=64",
+    "c4_moe": "MoE: L=48 alternating dense/MoE, 5 GPU types, 500k templates S<=12, EP<=8, m=32",
+    "c5_stress": "stress: L=128 MoE pattern, 8 GPU types, 4M templates S<=32, m in {8..256}",
+}
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def source_hash():
+    h = hashlib.sha256()
+    for f in ("price.hip", "heddle_internal.h"):
+        with open(os.path.join(ROOT, "paper_2609_34244_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(config, flags, n_plans):
+    """HBM bytes per launch from the committed rocprofv3 counter summary,
+    valid only for the kernel source it was measured on."""
+    path = os.path.join(ROOT, "profiles", f"price_kernel_{config}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_sha") != source_hash() or t.get("flags") != flags or t.get("plans") != n_plans:
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(w, flags, budget_s):
+    from oracle import oracle as O
+    op = O.OracleProfile(w.profile)
+    t0 = time.perf_counter()
+    probe = min(20, w.n)
+    O.price_plans(op, w.n_stages, w.stages, w.m, flags, 0, probe)
+    per = (time.perf_counter() - t0) / probe
+    n = int(max(probe, min(w.n, budget_s / max(per, 1e-9))))
+    t0 = time.perf_counter()
+    O.price_plans(op, w.n_stages, w.stages, w.m, flags, 0, n)
+    dt = time.perf_counter() - t0
+    return {"value": n * len(w.m) / dt, "unit": "plans/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n} of {w.n} templates x {len(w.m)} m, single-threaded plain C oracle, {dt:.1f} s",
+            "host_cores_available": len(os.sched_getaffinity(0))}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c3_70b_dense", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--fp32", action="store_true", help="fp32 cost variant")
+    ap.add_argument("--compute-only", action="store_true", help="split ignores memory; fit checked after")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py prices on one GPU; multi-GPU runs are not part of this build "
+              "(DESIGN.md describes how the batch would shard). Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_34244_amd import heddle as H
+    from workloads.gen import make_workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    flags = (H.HEDDLE_F_FP32 if args.fp32 else 0) | (H.HEDDLE_F_COMPUTE_ONLY if args.compute_only else 0)
+    t0 = time.perf_counter()
+    w = make_workload(args.config)
+    log(f"workload {args.config}: {w.n} templates x {len(w.m)} m generated in {time.perf_counter() - t0:.1f}s")
+
+    t0 = time.perf_counter()
+    prof = H.heddle_load_profile(w.profile)
+    load_ms = (time.perf_counter() - t0) * 1e3
+    info = H.heddle_profile_info_get(prof)
+    ns, st = H.to_device(w.n_stages, w.stages)
+    m = [int(x) for x in w.m]
+    out = H.alloc_outputs(w.n, len(m), w.s_max, flags)
+    torch.cuda.synchronize()
+    relax = H.heddle_count_work(prof, ns, st, m, flags)
+    n_plans = w.n * len(m)
+    log(f"profile loaded in {load_ms:.1f} ms; relaxations per step {relax:,} ({relax / w.n:.0f} per template); "
+        f"32-bit DP: {info['narrow_f32' if args.fp32 else 'narrow_i64']}")
+
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev:
+            ev[0].record(stream)
+        H.heddle_price_plans(prof, ns, st, m, flags, out)
+        if ev:
+            ev[1].record(stream)
+        return H.heddle_argmin_plans(m, flags, out["iter"], out["status"])
+
+    for i in range(args.warmup):
+        step()
+        log(f"warmup {i + 1}/{args.warmup} done")
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    best = None
+    for i in range(args.steps):
+        best = step(evs[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kern_ms = [a.elapsed_time(b) for a, b in evs]
+    log(f"timed {args.steps} steps in {elapsed:.3f}s; price kernel {np.mean(kern_ms):.3f} ms avg "
+        f"(min {np.min(kern_ms):.3f}); best plan {best}")
+    statuses = np.bincount(out["status"].cpu().numpy().ravel(), minlength=9).tolist()
+
+    kern_s = float(np.mean(kern_ms)) / 1e3
+    achieved = relax * K_MIN / kern_s
+    traffic = measured_traffic(args.config, flags, n_plans)
+    result = {
+        "metric": "candidate plans priced/sec (partition+evaluate) on 1 MI355X; % VALU roofline",
+        "value": n_plans * args.steps / elapsed,
+        "unit": "plans/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": ("fp32" if args.fp32 else "int64") + (" (exact 32-bit DP)" if info["narrow_f32" if args.fp32 else "narrow_i64"] else ""),
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[args.config], "name": args.config, "templates": w.n, "m": m,
+                   "plans": n_plans, "memory_aware": not args.compute_only, "seed": w.meta["seed"]},
+        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
+                     "unit": "Tlane-op/s", "frac": achieved / PEAK_LANE_OPS, "traffic": traffic,
+                     "kernel": "price_kernel", "kernel_ms": float(np.mean(kern_ms)),
+                     "relaxations_per_launch": relax, "ops_per_relaxation": K_MIN},
+        "statuses": statuses,
+        "best_plan": {"template": best[0], "m_index": best[1], "iter": best[2]} if best else None,
+        "profile_load_ms": load_ms,
+    }
+    if not args.no_cpu_baseline:
+        log(f"oracle baseline, about {args.cpu_seconds:.0f} s on one host core")
+        result["cpu_baseline"] = cpu_baseline(w, flags, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

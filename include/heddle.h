@@ -1,0 +1,241 @@
+/*
+ * heddle.h -- C ABI of the MI355X (gfx950) batched plan-pricing library.
+ *
+ * The library prices a batch of candidate parallelism plans of one model on
+ * one heterogeneous GPU cluster, following the profile-based cost model of
+ * Heddle (arXiv 2609.34244):
+ *
+ *   - a plan is a structural template (section 5.1: pipeline depth, and per
+ *     stage a GPU type and a TP degree; here also the DP degree and the EP
+ *     degree of each stage) together with a global micro-batch count m;
+ *   - PartitionLayers (the layer-split step of the nested-loop backbone in
+ *     section 3.1) splits the model's L layers over the S stages so that the
+ *     slowest stage is as fast as possible, every stage holding at least one
+ *     layer and fitting its GPUs' memory (memory validation, section 5.2);
+ *   - Evaluate (section 3.1 backbone; section 5.2 cost model) returns the
+ *     1F1B iteration time (M-1) max_s t_s + sum_s t_s + max_s g_s (section
+ *     5.3, expert tiling paragraph) and the per-GPU peak memory;
+ *   - the best plan is the one of highest throughput m / iter among the
+ *     feasible ones ("ranks the resulting plans by predicted throughput",
+ *     section 5 overview).
+ *
+ * All time quantities are int64 nanoseconds and all sizes int64 bytes; with
+ * HEDDLE_F_FP32 the time quantities are fp32 (see heddle_price_plans).
+ *
+ * Threading: every entry point may be called from any host thread. A loaded
+ * profile is immutable, so concurrent pricing calls on different streams
+ * may share it. heddle_last_error() is per host thread.
+ */
+#ifndef HEDDLE_H
+#define HEDDLE_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- return codes of the entry points (call-level errors are negative) ---- */
+#define HEDDLE_OK            0
+#define HEDDLE_E_INVAL      -1  /* bad argument: null pointer, size or flag out of range    */
+#define HEDDLE_E_NOMEM      -2  /* host or device allocation failed                         */
+#define HEDDLE_E_DEVICE     -3  /* a HIP call failed (message from hipGetErrorString)       */
+#define HEDDLE_E_RANGE      -4  /* table values could overflow the exact integer arithmetic */
+#define HEDDLE_E_NOFEASIBLE -5  /* best-plan queries only: no plan has status OK            */
+
+/* ---- flags ---- */
+#define HEDDLE_F_FP32         1u  /* fp32 time quantities (iter, bottleneck outputs are float) */
+#define HEDDLE_F_COMPUTE_ONLY 2u  /* split ignores memory; the fit is checked afterwards       */
+
+/* ---- per-plan status codes (data, not errors); the first failing check wins ---- */
+#define HEDDLE_S_OK             0  /* priced and fits                                         */
+#define HEDDLE_S_BAD_SHAPE      1  /* S < 1, S > s_max or S > L                               */
+#define HEDDLE_S_BAD_TYPE       2  /* a stage's GPU type >= n_types                           */
+#define HEDDLE_S_BAD_TP         3  /* TP not a profiled degree, or TP > node size (5.1 mask)  */
+#define HEDDLE_S_UNPROFILED     4  /* no profile entry for (type, TP): exact match only (5.2) */
+#define HEDDLE_S_BAD_DP         5  /* DP < 1, or stages disagree on DP                        */
+#define HEDDLE_S_BAD_EP         6  /* EP not an allowed degree, or EP does not divide DP      */
+#define HEDDLE_S_OVERSUBSCRIBED 7  /* sum over a type's stages of TP * DP > its GPU count     */
+#define HEDDLE_S_OOM            8  /* no split fits memory (or, compute-only, the split OOMs) */
+
+/* ---- limits ---- */
+#define HEDDLE_MAX_LAYERS  255     /* L (layer counts are returned as uint8)   */
+#define HEDDLE_MAX_STAGES  64      /* s_max                                     */
+#define HEDDLE_MAX_TYPES   255     /* n_types                                   */
+#define HEDDLE_MAX_MLIST   64      /* n_m                                       */
+#define HEDDLE_MAX_M       (1 << 24) /* each m                                  */
+
+/*
+ * Stage record of a template: one uint32 per stage,
+ *   bits  0..7   GPU type index g          (0 .. n_types-1)
+ *   bits  8..11  log2 of the TP degree
+ *   bits 12..15  log2 of the EP degree     (0 for a dense model)
+ *   bits 16..31  DP degree D (pipeline replica count; equal on all stages)
+ * The expert layout of a stage is EP = e, ETP = TP, EDP = D / e, so that
+ * EP * ETP * EDP equals the stage's TP * D GPUs (section 3.2).
+ */
+#define HEDDLE_STAGE(g, log2_tp, log2_ep, dp) \
+    ((uint32_t)(g) | ((uint32_t)(log2_tp) << 8) | ((uint32_t)(log2_ep) << 12) | ((uint32_t)(dp) << 16))
+
+/*
+ * Profile of one model on one cluster (the offline profiles of section 5.2,
+ * keyed by GPU type and TP degree at one fixed micro-batch size).
+ * All pointers are HOST memory and are only read during heddle_load_profile.
+ * Index k runs over tp_degrees, e over ep_degrees, l over layers.
+ */
+typedef struct heddle_profile_desc {
+    int32_t L;                    /* layers, 1..255                                        */
+    int32_t n_types;              /* GPU types, 1..255                                     */
+    int32_t n_tp, n_ep;           /* entries of tp_degrees / ep_degrees (each 1..16)       */
+    const int32_t *tp_degrees;    /* [n_tp] distinct powers of two, 1..32768               */
+    const int32_t *ep_degrees;    /* [n_ep] distinct powers of two; {1} for a dense model  */
+    const int64_t *layer_ns;      /* [n_types][n_tp][L] fwd+bwd ns per micro-batch
+                                     (computation + TP communication), each >= 1          */
+    const uint8_t *profiled;      /* [n_types][n_tp] 0: no profile entry                   */
+    const float   *layer_ns_f32;  /* [n_types][n_tp][L] fp32 costs for HEDDLE_F_FP32, each
+                                     finite and > 0; NULL: the int64 table rounded to fp32 */
+    const uint8_t *is_moe;        /* [L] 1 for a mixture-of-experts layer                  */
+    const int64_t *state_bytes;   /* [n_tp][L] per-GPU params+grads+optimizer, dense part  */
+    const int64_t *xstate_bytes;  /* [n_tp][L] the same for the experts at EP = 1          */
+    const int64_t *act_bytes;     /* [n_tp][L] per-GPU activations of one micro-batch      */
+    const int64_t *grad_bytes;    /* [n_tp][L] per-GPU gradient bytes, dense part          */
+    const int64_t *xgrad_bytes;   /* [n_tp][L] per-GPU gradient bytes of experts at EP = 1 */
+    int64_t boundary_bytes;       /* activation tensor crossing a stage boundary, one way  */
+    int64_t a2a_bytes;            /* all-to-all bytes of one MoE layer per micro-batch     */
+    const int64_t *mem_cap_bytes; /* [n_types] physical memory per GPU                     */
+    const int32_t *node_size;     /* [n_types] GPUs in the largest node of the type        */
+    const int32_t *n_gpus;        /* [n_types] GPUs of the type in the cluster             */
+    const int64_t *intra_bw_MBps; /* [n_types] intra-node bandwidth, MB/s, >= 1            */
+    const int64_t *link_bw_MBps;  /* [n_types][n_types] inter-node bandwidth, MB/s, >= 1   */
+} heddle_profile_desc;
+
+typedef struct heddle_profile heddle_profile;   /* opaque, device-resident tables */
+
+/*
+ * heddle_load_profile -- validate a profile, build its derived tables
+ * (exclusive prefix sums of per-layer time, memory and gradient bytes; the
+ * transfer-time terms of every type and type pair) and upload them to the
+ * current HIP device.
+ *   d    host descriptor; only read during the call.
+ *   out  receives a handle owned by the caller, released with
+ *        heddle_free_profile. The handle may be used on the device that was
+ *        current at load time only.
+ * Returns HEDDLE_OK, HEDDLE_E_INVAL (null pointer, size out of range, a
+ * non-power-of-two degree, a cost < 1, a negative byte count, a bandwidth
+ * < 1), HEDDLE_E_RANGE (prefix totals or transfer times would exceed 2^62),
+ * HEDDLE_E_NOMEM or HEDDLE_E_DEVICE. On error *out is set to NULL.
+ * Cost: O(n_types * n_tp * L) host work and one host-to-device copy.
+ */
+int heddle_load_profile(const heddle_profile_desc *d, heddle_profile **out);
+
+/* Release a profile. NULL is ignored. No call using it may be in flight. */
+void heddle_free_profile(heddle_profile *p);
+
+/*
+ * heddle_price_plans -- price n templates at each of n_m micro-batch counts
+ * (the "plans" are the n * n_m pairs). Asynchronous: enqueued on `stream`;
+ * outputs are valid once the stream has completed the work.
+ *   p            profile from heddle_load_profile.
+ *   n            templates (>= 0; n = 0 enqueues nothing).
+ *   s_max        stage slots per template record, 1..64.
+ *   d_n_stages   DEVICE [n] uint8, stage count S of each template.
+ *   d_stages     DEVICE [n][s_max] uint32 stage records (HEDDLE_STAGE);
+ *                slots s >= S are ignored.
+ *   h_m          HOST [n_m] micro-batch counts, each 1..HEDDLE_MAX_M; read
+ *                during the call. Micro-batches per replica: M_p = ceil(m/D).
+ *   n_m          1..HEDDLE_MAX_MLIST.
+ *   flags        HEDDLE_F_FP32 | HEDDLE_F_COMPUTE_ONLY, or 0.
+ * Outputs (DEVICE, caller-allocated, index o = t * n_m + k):
+ *   d_iter        [n][n_m] iteration time: int64 ns, or float with FP32.
+ *   d_bottleneck  [n][n_m] slowest stage time B* (same type as d_iter).
+ *   d_peak_mem    [n][n_m] int64 max over stages of per-GPU peak bytes.
+ *   d_layers      [n][n_m][s_max] uint8 layers of each stage (0 beyond S).
+ *   d_status      [n][n_m] uint8 HEDDLE_S_*.
+ * Split: lexicographically smallest (n_0..n_{S-1}) among the splits of
+ * minimum bottleneck, where a stage's time is its layers' profiled cost
+ * plus, for MoE layers with EP > 1, one all-to-all, plus its outbound p2p of
+ * 2 * boundary_bytes; a stage holds min(S - s, M_p) micro-batches of
+ * activations (1F1B). Without COMPUTE_ONLY only splits that fit memory
+ * qualify. Plans with status 1..7, and OOM plans without COMPUTE_ONLY, get
+ * iter = bottleneck = peak_mem = INT64_MAX (float: +inf) and zero layers;
+ * COMPUTE_ONLY OOM plans carry their computed values.
+ * FP32: every time quantity is the fp32 nearest (ties to even) to its exact
+ * value computed from fp32 per-layer costs and fp32-rounded transfer terms
+ * (one rounding per stage time and one for the iteration time).
+ * Returns HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_RANGE (the iteration time could
+ * exceed 2^62 for these m, or the fp32 costs span too wide a range to sum
+ * exactly) or HEDDLE_E_DEVICE. On error nothing is enqueued.
+ */
+int heddle_price_plans(const heddle_profile *p, int64_t n, int32_t s_max,
+                       const uint8_t *d_n_stages, const uint32_t *d_stages,
+                       const int32_t *h_m, int32_t n_m, uint32_t flags,
+                       void *d_iter, void *d_bottleneck, int64_t *d_peak_mem,
+                       uint8_t *d_layers, uint8_t *d_status, hipStream_t stream);
+
+/*
+ * heddle_argmin_plans -- best plan among priced outputs: the plan of status
+ * OK with the smallest iter / m (highest throughput m / iter), compared
+ * exactly as iter_a * m_b < iter_b * m_a; ties go to the lowest template
+ * index, then the lowest m index (section 5.3: "keeps the fastest").
+ * Synchronous: waits for `stream`.
+ *   d_iter, d_status  DEVICE outputs of heddle_price_plans with the same
+ *                     n, n_m, h_m and the same FP32 flag.
+ *   h_best_template, h_best_m_index  HOST results.
+ *   h_best_iter       HOST int64 (or float with FP32) iteration time; may be NULL.
+ * Returns HEDDLE_OK, HEDDLE_E_NOFEASIBLE (nothing written), HEDDLE_E_INVAL,
+ * HEDDLE_E_NOMEM or HEDDLE_E_DEVICE.
+ */
+int heddle_argmin_plans(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t flags,
+                        const void *d_iter, const uint8_t *d_status,
+                        int64_t *h_best_template, int32_t *h_best_m_index, void *h_best_iter,
+                        hipStream_t stream);
+
+/*
+ * heddle_best_plan -- heddle_price_plans into library-allocated device
+ * buffers followed by heddle_argmin_plans. Synchronous. Arguments as in
+ * those two calls. The library allocates and frees its own buffers with
+ * stream-ordered allocation on `stream`.
+ */
+int heddle_best_plan(const heddle_profile *p, int64_t n, int32_t s_max,
+                     const uint8_t *d_n_stages, const uint32_t *d_stages,
+                     const int32_t *h_m, int32_t n_m, uint32_t flags,
+                     int64_t *h_best_template, int32_t *h_best_m_index, void *h_best_iter,
+                     hipStream_t stream);
+
+/*
+ * heddle_count_work -- algorithmic work of pricing this batch: the number of
+ * (row i, end j) pairs the min-max recurrence relaxes, summed over the
+ * distinct splits the batch needs (a template's m values that imply the
+ * same in-flight activation counts share one split). Stage 0 starts at row
+ * 0 only, the last stage ends at L only, and pairs whose stage does not fit
+ * memory are excluded (none with COMPUTE_ONLY). Synchronous.
+ *   h_relaxations  HOST result.
+ * Returns HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_NOMEM or HEDDLE_E_DEVICE.
+ */
+int heddle_count_work(const heddle_profile *p, int64_t n, int32_t s_max,
+                      const uint8_t *d_n_stages, const uint32_t *d_stages,
+                      const int32_t *h_m, int32_t n_m, uint32_t flags,
+                      int64_t *h_relaxations, hipStream_t stream);
+
+/*
+ * heddle_profile_info -- facts about a loaded profile for tests and reports.
+ *   narrow[0]  1 if the int64 split runs in exact 32-bit arithmetic
+ *   narrow[1]  1 if the fp32 split does
+ *   fx_exp     exponent of the fixed-point unit of the fp32 variant (<= 0)
+ */
+typedef struct heddle_profile_info {
+    int32_t narrow[2];
+    int32_t fx_exp;
+    int32_t L, n_types, n_tp, n_ep;
+    int64_t max_stage_ns;        /* bound on any stage time, ns            */
+} heddle_profile_info;
+int heddle_profile_info_get(const heddle_profile *p, heddle_profile_info *info);
+
+/* Message of the last negative return on this host thread ("" if none). */
+const char *heddle_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HEDDLE_H */

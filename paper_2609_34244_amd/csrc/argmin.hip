@@ -1,0 +1,220 @@
+// Argmin over priced plans: the feasible plan of highest throughput m / iter
+// (Heddle, arXiv 2609.34244: the cost model "ranks the resulting plans by
+// predicted throughput" and the fill "keeps the fastest", section 5).
+//
+// Key: iter / m, compared exactly by cross-multiplication (128-bit for int64
+// iteration times; fp32 times scaled by m <= 2^24 are exact in fp64). Ties
+// go to the lowest flat index t * n_m + k, i.e. the lowest template, then
+// the lowest m index. The comparison is a total order, so the two-pass
+// reduction (wave shuffles -> LDS -> one block over the partials) returns
+// the same answer for any grid shape; no atomics are involved.
+#include <cstring>
+
+#include "heddle_internal.h"
+
+namespace heddle {
+
+constexpr int kArgBlock = 256;
+constexpr int kArgMaxBlocks = 2048;
+
+struct Cand {
+    uint64_t iter;   // int64 value, or the bit pattern of a non-negative float
+    int64_t idx;     // flat index; -1 = none
+    int32_t m;
+};
+
+__device__ __forceinline__ bool better(const Cand &a, const Cand &b, bool f32)
+{
+    if (a.idx < 0) return false;
+    if (b.idx < 0) return true;
+    bool lt, eq;
+    if (f32) {
+        const double x = (double)__uint_as_float((uint32_t)a.iter) * (double)b.m;
+        const double y = (double)__uint_as_float((uint32_t)b.iter) * (double)a.m;
+        lt = x < y;
+        eq = x == y;
+    } else {
+        const unsigned __int128 x = (unsigned __int128)a.iter * (uint32_t)b.m;
+        const unsigned __int128 y = (unsigned __int128)b.iter * (uint32_t)a.m;
+        lt = x < y;
+        eq = x == y;
+    }
+    return lt || (eq && a.idx < b.idx);
+}
+
+__device__ __forceinline__ Cand shfl_xor_cand(const Cand &c, int o)
+{
+    Cand r;
+    r.iter = __shfl_xor((unsigned long long)c.iter, o);
+    r.idx = __shfl_xor((long long)c.idx, o);
+    r.m = __shfl_xor(c.m, o);
+    return r;
+}
+
+__device__ Cand block_best(Cand c, bool f32)
+{
+    __shared__ Cand part[kArgBlock / 64];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        Cand u = shfl_xor_cand(c, o);
+        if (better(u, c, f32)) c = u;
+    }
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    if (lane == 0) part[w] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int i = 1; i < (int)(blockDim.x >> 6); i++)
+            if (better(part[i], c, f32)) c = part[i];
+    }
+    return c;
+}
+
+struct ArgArgs {
+    int64_t total;          // n * n_m
+    int32_t n_m, f32;
+    int32_t m[kMaxMList];
+    const void *iter;
+    const uint8_t *status;
+    Cand *partial;
+};
+
+__global__ void __launch_bounds__(kArgBlock) argmin_pass1(ArgArgs A)
+{
+    __shared__ int32_t sm[kMaxMList];
+    for (int k = 0; k < A.n_m; k++)
+        if ((int)threadIdx.x == k) sm[k] = A.m[k];
+    __syncthreads();
+    Cand best;
+    best.idx = -1;
+    best.iter = 0;
+    best.m = 1;
+    const bool f32 = A.f32 != 0;
+    for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < A.total; o += (int64_t)gridDim.x * blockDim.x) {
+        if (A.status[o] != HEDDLE_S_OK) continue;
+        Cand c;
+        c.idx = o;
+        c.m = sm[o % A.n_m];
+        c.iter = f32 ? (uint64_t)__float_as_uint(((const float *)A.iter)[o]) : (uint64_t)((const int64_t *)A.iter)[o];
+        if (better(c, best, f32)) best = c;
+    }
+    best = block_best(best, f32);
+    if (threadIdx.x == 0) A.partial[blockIdx.x] = best;
+}
+
+__global__ void __launch_bounds__(kArgBlock) argmin_pass2(const Cand *partial, int n_part, int f32, Cand *out)
+{
+    Cand best;
+    best.idx = -1;
+    best.iter = 0;
+    best.m = 1;
+    for (int i = threadIdx.x; i < n_part; i += blockDim.x)
+        if (better(partial[i], best, f32 != 0)) best = partial[i];
+    best = block_best(best, f32 != 0);
+    if (threadIdx.x == 0) *out = best;
+}
+
+int launch_argmin(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t flags, const void *d_iter,
+                  const uint8_t *d_status, int64_t *h_best_template, int32_t *h_best_m_index,
+                  void *h_best_iter, hipStream_t stream)
+{
+    const int64_t total = n * n_m;
+    if (total == 0) return fail(HEDDLE_E_NOFEASIBLE, "no plans");
+    ArgArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.total = total;
+    a.n_m = n_m;
+    a.f32 = (flags & HEDDLE_F_FP32) ? 1 : 0;
+    for (int k = 0; k < n_m; k++) a.m[k] = h_m[k];
+    a.iter = d_iter;
+    a.status = d_status;
+    const int64_t want = (total + kArgBlock * 8 - 1) / (kArgBlock * 8);
+    const int blocks = (int)(want < kArgMaxBlocks ? (want > 0 ? want : 1) : kArgMaxBlocks);
+    Cand *scratch = nullptr;
+    hipError_t e = hipMallocAsync((void **)&scratch, sizeof(Cand) * (blocks + 1), stream);
+    if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "hipMallocAsync of argmin partials failed");
+    a.partial = scratch;
+    hipLaunchKernelGGL(argmin_pass1, dim3(blocks), dim3(kArgBlock), 0, stream, a);
+    hipLaunchKernelGGL(argmin_pass2, dim3(1), dim3(kArgBlock), 0, stream, (const Cand *)scratch, blocks, a.f32,
+                       scratch + blocks);
+    Cand h;
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipMemcpyAsync(&h, scratch + blocks, sizeof(h), hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    (void)hipFreeAsync(scratch, stream);
+    if (e != hipSuccess) return hip_fail(e, "argmin");
+    if (h.idx < 0) return fail(HEDDLE_E_NOFEASIBLE, "no plan has status OK");
+    *h_best_template = h.idx / n_m;
+    *h_best_m_index = (int32_t)(h.idx % n_m);
+    if (h_best_iter) {
+        if (a.f32) {
+            const uint32_t bits = (uint32_t)h.iter;
+            std::memcpy(h_best_iter, &bits, 4);
+        } else {
+            const int64_t v = (int64_t)h.iter;
+            std::memcpy(h_best_iter, &v, 8);
+        }
+    }
+    return HEDDLE_OK;
+}
+
+}  // namespace heddle
+
+using namespace heddle;
+
+extern "C" int heddle_argmin_plans(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t flags,
+                                   const void *d_iter, const uint8_t *d_status,
+                                   int64_t *h_best_template, int32_t *h_best_m_index, void *h_best_iter,
+                                   hipStream_t stream)
+{
+    if (n < 0 || n_m < 1 || n_m > HEDDLE_MAX_MLIST || !h_m) return fail(HEDDLE_E_INVAL, "bad n / n_m / h_m");
+    if (flags & ~(HEDDLE_F_FP32 | HEDDLE_F_COMPUTE_ONLY)) return fail(HEDDLE_E_INVAL, "unknown flag bits");
+    for (int k = 0; k < n_m; k++)
+        if (h_m[k] < 1 || h_m[k] > HEDDLE_MAX_M) return fail(HEDDLE_E_INVAL, "m out of range 1..2^24");
+    if (!h_best_template || !h_best_m_index) return fail(HEDDLE_E_INVAL, "result pointer is NULL");
+    if (n > 0 && (!d_iter || !d_status)) return fail(HEDDLE_E_INVAL, "device pointer is NULL");
+    return launch_argmin(n, h_m, n_m, flags, d_iter, d_status, h_best_template, h_best_m_index, h_best_iter,
+                         stream);
+}
+
+extern "C" int heddle_best_plan(const heddle_profile *p, int64_t n, int32_t s_max,
+                                const uint8_t *d_n_stages, const uint32_t *d_stages,
+                                const int32_t *h_m, int32_t n_m, uint32_t flags,
+                                int64_t *h_best_template, int32_t *h_best_m_index, void *h_best_iter,
+                                hipStream_t stream)
+{
+    int rc = validate_price_args(p, n, s_max, d_n_stages, d_stages, h_m, n_m, flags);
+    if (rc) return rc;
+    if (!h_best_template || !h_best_m_index) return fail(HEDDLE_E_INVAL, "result pointer is NULL");
+    if (n == 0) return fail(HEDDLE_E_NOFEASIBLE, "no plans");
+    const size_t total = (size_t)n * n_m;
+    // iter | bottleneck | peak_mem | status | layers, one stream-ordered allocation
+    const size_t o_iter = 0, o_bn = o_iter + total * 8, o_pk = o_bn + total * 8, o_st = o_pk + total * 8,
+                 o_ly = (o_st + total + 255) & ~size_t(255), bytes = o_ly + total * (size_t)s_max;
+    unsigned char *buf = nullptr;
+    hipError_t e = hipMallocAsync((void **)&buf, bytes, stream);
+    if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "hipMallocAsync of pricing outputs failed");
+    PriceArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.n = n;
+    a.s_max = s_max;
+    a.n_m = n_m;
+    a.flags = (int32_t)flags;
+    for (int k = 0; k < n_m; k++) a.m[k] = h_m[k];
+    a.n_stages = d_n_stages;
+    a.stages = d_stages;
+    a.iter = buf + o_iter;
+    a.bottleneck = buf + o_bn;
+    a.peak_mem = (int64_t *)(buf + o_pk);
+    a.status = buf + o_st;
+    a.layers = buf + o_ly;
+    rc = launch_price(p, a, stream, false);
+    if (rc == HEDDLE_OK)
+        rc = launch_argmin(n, h_m, n_m, flags, a.iter, a.status, h_best_template, h_best_m_index, h_best_iter,
+                           stream);
+    (void)hipFreeAsync(buf, stream);
+    if (rc == HEDDLE_OK) {
+        e = hipStreamSynchronize(stream);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    }
+    return rc;
+}

@@ -1,0 +1,97 @@
+// Internal declarations of the gfx950 plan-pricing library (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string>
+
+#include "../../include/heddle.h"
+
+namespace heddle {
+
+constexpr int kWave = 64;
+constexpr int kMaxStages = HEDDLE_MAX_STAGES;
+constexpr int kMaxMList = HEDDLE_MAX_MLIST;
+constexpr int64_t kLimit62 = int64_t(1) << 62;
+constexpr uint32_t kNarrowLimit = 0x7FFFFFFFu;   // exact 32-bit DP when every stage time is below this
+
+// a2a variant of a stage: no all-to-all (EP = 1), EP x TP group inside one
+// node (intra-node bandwidth), or spanning nodes (same-type inter-node link)
+enum A2AVariant { kA2ANone = 0, kA2AIntra = 1, kA2AInter = 2 };
+
+// Device-resident derived tables of one profile. Passed by value to kernels.
+// Prefix rows have L + 1 entries: row[j] = sum over layers l < j.
+struct DevProfile {
+    int32_t L, n_types, n_tp, n_ep;
+    int32_t fx_exp;                  // fixed-point unit of the fp32 variant is 2^fx_exp
+    uint32_t tp_present, ep_present; // bit l set: 2^l is a profiled TP / an allowed EP degree
+    uint64_t tp_index, ep_index;     // nibble l: index of 2^l in tp_degrees / ep_degrees
+    const int64_t *pre_time;         // [n_types][n_tp][L+1] prefix of layer_ns
+    const int64_t *pre_time_fx;      // [n_types][n_tp][L+1] prefix of fp32 costs in 2^fx_exp units
+    const int32_t *pre_moe;          // [L+1] prefix count of MoE layers
+    const int64_t *pre_state;        // [n_tp][n_ep][L+1] prefix of state + ceil(xstate / e)
+    const int64_t *pre_act;          // [n_tp][L+1] prefix of act
+    const int64_t *pre_grad;         // [n_tp][L+1] prefix of grad
+    const int64_t *pre_xgrad;        // [n_tp][n_ep][L+1] prefix of ceil(xgrad / e)
+    const uint8_t *profiled;         // [n_types][n_tp]
+    const int64_t *a2a_ns;           // [n_types][3] all-to-all time per MoE layer by variant
+    const int64_t *a2a_fx;           // [n_types][3] fp32-rounded, in fixed-point units
+    const int64_t *p2p_ns;           // [n_types][n_types] p2p time, sender type x receiver type
+    const int64_t *p2p_fx;           // [n_types][n_types] fp32-rounded, fixed-point units
+    const int64_t *mem_cap;          // [n_types]
+    const int32_t *node_size;        // [n_types]
+    const int32_t *n_gpus;           // [n_types]
+    const int64_t *intra_bw;         // [n_types] MB/s
+    const int64_t *link_bw;          // [n_types][n_types] MB/s
+    const int32_t *ep_degrees;       // [n_ep]
+};
+
+}  // namespace heddle
+
+struct heddle_profile {
+    heddle::DevProfile dev;
+    void *dev_block;                 // one device allocation holding every table
+    int device;
+    int narrow_i64, narrow_f32;      // 32-bit DP proven exact
+    int64_t max_stage_ns;            // bound on any int64 stage time
+    int64_t max_stage_fx;            // bound on any fp32 stage time, fixed-point units
+    int64_t max_ar_ns;               // bound on any stage's gradient synchronisation time
+    int64_t max_ar_fx;               // the same, fp32-rounded, fixed-point units
+};
+
+namespace heddle {
+
+// thread-local last error
+void set_error(const std::string &msg);
+int fail(int code, const std::string &msg);
+int hip_fail(hipError_t e, const char *what);
+
+#define HEDDLE_HIP(call)                                         \
+    do {                                                         \
+        hipError_t _e = (call);                                  \
+        if (_e != hipSuccess) return ::heddle::hip_fail(_e, #call); \
+    } while (0)
+
+// Arguments of one pricing launch (host-validated).
+struct PriceArgs {
+    int64_t n;
+    int32_t s_max, n_m, flags;
+    int32_t m[kMaxMList];
+    const uint8_t *n_stages;
+    const uint32_t *stages;
+    void *iter, *bottleneck;
+    int64_t *peak_mem;
+    uint8_t *layers, *status;
+    unsigned long long *work;        // count-only launches: accumulated relaxations
+    int32_t g_stride;                // LDS entries per DP table row (L + 1)
+    int32_t lds_per_wave;            // bytes
+};
+
+int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,
+                        const uint32_t *d_stages, const int32_t *h_m, int32_t n_m, uint32_t flags);
+int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool count_only);
+int launch_argmin(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t flags, const void *d_iter,
+                  const uint8_t *d_status, int64_t *h_best_template, int32_t *h_best_m_index,
+                  void *h_best_iter, hipStream_t stream);
+
+}  // namespace heddle

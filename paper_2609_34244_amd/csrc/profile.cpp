@@ -1,0 +1,315 @@
+// Profile loading: validation of the descriptor, derived prefix tables and
+// transfer-time terms, range proofs, and upload to the device.
+//
+// Derived tables follow the profile-based cost model (Heddle, section 5.2):
+// per-(type, TP) layer costs are summed into prefix rows so that a stage's
+// time over layers [i, j) is one subtraction; memory and gradient bytes per
+// TP degree likewise. Transfer times of the MoE all-to-all (section 5.3,
+// expert tiling) and the inter-stage p2p are precomputed per type and per
+// type pair.
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "heddle_internal.h"
+
+namespace heddle {
+
+static thread_local std::string g_last_error;
+
+void set_error(const std::string &msg) { g_last_error = msg; }
+
+int fail(int code, const std::string &msg)
+{
+    g_last_error = msg;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char *what)
+{
+    g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+    return HEDDLE_E_DEVICE;
+}
+
+typedef __int128 i128;
+
+// ceil(b * 1000 / MBps) ns: b bytes at MBps megabytes per second
+static i128 transfer_ns(int64_t bytes, int64_t MBps) { return ((i128)bytes * 1000 + MBps - 1) / MBps; }
+
+static int log2_exact(int32_t v)
+{
+    if (v < 1 || (v & (v - 1))) return -1;
+    int l = 0;
+    while ((1 << l) < v) l++;
+    return l;
+}
+
+// exponent of the lowest set bit of a positive finite float (v = odd * 2^e)
+static int low_bit_exp(float v)
+{
+    int e;
+    double fr = std::frexp((double)v, &e);
+    int64_t mant = (int64_t)std::ldexp(fr, 24);   // exact 24-bit integer
+    int tz = 0;
+    while (!(mant & 1)) { mant >>= 1; tz++; }
+    return e - 24 + tz;
+}
+
+struct Builder {
+    std::vector<unsigned char> bytes;
+    size_t add(const void *src, size_t n)
+    {
+        size_t off = (bytes.size() + 255) & ~size_t(255);
+        bytes.resize(off + n);
+        std::memcpy(bytes.data() + off, src, n);
+        return off;
+    }
+    template <class T> size_t add(const std::vector<T> &v) { return add(v.data(), v.size() * sizeof(T)); }
+};
+
+}  // namespace heddle
+
+using namespace heddle;
+
+extern "C" const char *heddle_last_error(void) { return g_last_error.c_str(); }
+
+extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile **out)
+{
+    if (!out) return fail(HEDDLE_E_INVAL, "out is NULL");
+    *out = nullptr;
+    if (!d) return fail(HEDDLE_E_INVAL, "descriptor is NULL");
+    const int L = d->L, N = d->n_types, K = d->n_tp, E = d->n_ep;
+    if (L < 1 || L > HEDDLE_MAX_LAYERS) return fail(HEDDLE_E_INVAL, "L out of range 1..255");
+    if (N < 1 || N > HEDDLE_MAX_TYPES) return fail(HEDDLE_E_INVAL, "n_types out of range 1..255");
+    if (K < 1 || K > 16 || E < 1 || E > 16) return fail(HEDDLE_E_INVAL, "n_tp / n_ep out of range 1..16");
+    if (!d->tp_degrees || !d->ep_degrees || !d->layer_ns || !d->profiled || !d->is_moe || !d->state_bytes ||
+        !d->xstate_bytes || !d->act_bytes || !d->grad_bytes || !d->xgrad_bytes || !d->mem_cap_bytes ||
+        !d->node_size || !d->n_gpus || !d->intra_bw_MBps || !d->link_bw_MBps)
+        return fail(HEDDLE_E_INVAL, "a required table pointer is NULL");
+
+    DevProfile dp;
+    std::memset(&dp, 0, sizeof(dp));
+    dp.L = L; dp.n_types = N; dp.n_tp = K; dp.n_ep = E;
+    for (int k = 0; k < K; k++) {
+        int l = log2_exact(d->tp_degrees[k]);
+        if (l < 0 || l > 15 || ((dp.tp_present >> l) & 1)) return fail(HEDDLE_E_INVAL, "tp_degrees must be distinct powers of two <= 32768");
+        dp.tp_present |= 1u << l;
+        dp.tp_index |= (uint64_t)k << (4 * l);
+    }
+    for (int e = 0; e < E; e++) {
+        int l = log2_exact(d->ep_degrees[e]);
+        if (l < 0 || l > 15 || ((dp.ep_present >> l) & 1)) return fail(HEDDLE_E_INVAL, "ep_degrees must be distinct powers of two <= 32768");
+        dp.ep_present |= 1u << l;
+        dp.ep_index |= (uint64_t)e << (4 * l);
+    }
+    for (int g = 0; g < N; g++) {
+        if (d->node_size[g] < 1) return fail(HEDDLE_E_INVAL, "node_size must be >= 1");
+        if (d->n_gpus[g] < 0 || d->mem_cap_bytes[g] < 0) return fail(HEDDLE_E_INVAL, "negative GPU count or memory");
+        if (d->intra_bw_MBps[g] < 1) return fail(HEDDLE_E_INVAL, "bandwidths must be >= 1 MB/s");
+        for (int h = 0; h < N; h++)
+            if (d->link_bw_MBps[g * N + h] < 1) return fail(HEDDLE_E_INVAL, "bandwidths must be >= 1 MB/s");
+    }
+    if (d->boundary_bytes < 0 || d->a2a_bytes < 0 || d->boundary_bytes > kLimit62 / 2000 ||
+        d->a2a_bytes > kLimit62 / 1000)
+        return fail(HEDDLE_E_RANGE, "boundary_bytes / a2a_bytes out of range");
+
+    const size_t R = (size_t)L + 1;
+    int n_moe = 0;
+    std::vector<int32_t> pre_moe(R, 0);
+    for (int l = 0; l < L; l++) {
+        n_moe += d->is_moe[l] ? 1 : 0;
+        pre_moe[l + 1] = n_moe;
+    }
+
+    // ---- int64 time prefix rows and transfer terms
+    std::vector<int64_t> pre_time((size_t)N * K * R);
+    for (int g = 0; g < N; g++)
+        for (int k = 0; k < K; k++) {
+            i128 acc = 0;
+            int64_t *row = &pre_time[((size_t)g * K + k) * R];
+            row[0] = 0;
+            for (int l = 0; l < L; l++) {
+                int64_t c = d->layer_ns[((size_t)g * K + k) * L + l];
+                if (c < 1) return fail(HEDDLE_E_INVAL, "layer_ns entries must be >= 1 ns");
+                acc += c;
+                if (acc >= kLimit62) return fail(HEDDLE_E_RANGE, "layer_ns row total exceeds 2^62");
+                row[l + 1] = (int64_t)acc;
+            }
+        }
+    std::vector<int64_t> a2a_ns((size_t)N * 3), p2p_ns((size_t)N * N);
+    for (int g = 0; g < N; g++) {
+        a2a_ns[g * 3 + kA2ANone] = 0;
+        a2a_ns[g * 3 + kA2AIntra] = (int64_t)transfer_ns(d->a2a_bytes, d->intra_bw_MBps[g]);
+        a2a_ns[g * 3 + kA2AInter] = (int64_t)transfer_ns(d->a2a_bytes, d->link_bw_MBps[g * N + g]);
+        for (int h = 0; h < N; h++) p2p_ns[g * N + h] = (int64_t)transfer_ns(2 * d->boundary_bytes, d->link_bw_MBps[g * N + h]);
+    }
+    // bound on any stage time: full row + all-to-all on every MoE layer + the largest p2p
+    i128 max_stage = 0;
+    for (int g = 0; g < N; g++)
+        for (int k = 0; k < K; k++) {
+            int64_t a2a_max = a2a_ns[g * 3 + 1] > a2a_ns[g * 3 + 2] ? a2a_ns[g * 3 + 1] : a2a_ns[g * 3 + 2];
+            int64_t p2p_max = 0;
+            for (int h = 0; h < N; h++) p2p_max = p2p_ns[g * N + h] > p2p_max ? p2p_ns[g * N + h] : p2p_max;
+            i128 b = (i128)pre_time[((size_t)g * K + k) * R + L] + (i128)n_moe * a2a_max + p2p_max;
+            if (b > max_stage) max_stage = b;
+        }
+    if (max_stage >= kLimit62) return fail(HEDDLE_E_RANGE, "stage times could exceed 2^62 ns");
+
+    // ---- memory and gradient prefix rows
+    std::vector<int64_t> pre_state((size_t)K * E * R), pre_act((size_t)K * R), pre_grad((size_t)K * R),
+        pre_xgrad((size_t)K * E * R);
+    i128 max_grad = 0;
+    for (int k = 0; k < K; k++) {
+        i128 a = 0, gsum = 0;
+        pre_act[k * R] = pre_grad[k * R] = 0;
+        for (int l = 0; l < L; l++) {
+            int64_t av = d->act_bytes[(size_t)k * L + l], gv = d->grad_bytes[(size_t)k * L + l];
+            if (av < 0 || gv < 0) return fail(HEDDLE_E_INVAL, "byte counts must be >= 0");
+            a += av;
+            gsum += gv;
+            if (a >= kLimit62 / 64 || gsum >= kLimit62 / 4096) return fail(HEDDLE_E_RANGE, "byte totals too large");
+            pre_act[k * R + l + 1] = (int64_t)a;
+            pre_grad[k * R + l + 1] = (int64_t)gsum;
+        }
+        for (int e = 0; e < E; e++) {
+            const int64_t ep = d->ep_degrees[e];
+            i128 w = 0, xg = 0;
+            pre_state[(k * E + e) * R] = pre_xgrad[(k * E + e) * R] = 0;
+            for (int l = 0; l < L; l++) {
+                int64_t sv = d->state_bytes[(size_t)k * L + l], xv = d->xstate_bytes[(size_t)k * L + l];
+                int64_t xgv = d->xgrad_bytes[(size_t)k * L + l];
+                if (sv < 0 || xv < 0 || xgv < 0) return fail(HEDDLE_E_INVAL, "byte counts must be >= 0");
+                w += (i128)sv + (xv + ep - 1) / ep;
+                xg += (xgv + ep - 1) / ep;
+                if (w >= kLimit62 / 2 || xg >= kLimit62 / 4096) return fail(HEDDLE_E_RANGE, "byte totals too large");
+                pre_state[(k * E + e) * R + l + 1] = (int64_t)w;
+                pre_xgrad[(k * E + e) * R + l + 1] = (int64_t)xg;
+            }
+            if (gsum + xg > max_grad) max_grad = gsum + xg;
+        }
+    }
+    // gradient synchronisation is below 2 * bytes * 1000 / min bandwidth (+1 per ceiling)
+    int64_t min_bw = INT64_MAX;
+    for (int g = 0; g < N; g++) {
+        min_bw = d->intra_bw_MBps[g] < min_bw ? d->intra_bw_MBps[g] : min_bw;
+        for (int h = 0; h < N; h++) min_bw = d->link_bw_MBps[g * N + h] < min_bw ? d->link_bw_MBps[g * N + h] : min_bw;
+    }
+    i128 max_ar = (2 * max_grad * 1000) / min_bw + 2;
+    if (max_ar >= kLimit62) return fail(HEDDLE_E_RANGE, "gradient synchronisation time could exceed 2^62 ns");
+
+    // ---- fp32 variant: exact fixed-point image of the fp32 costs
+    std::vector<float> cost32((size_t)N * K * L);
+    for (size_t i = 0; i < cost32.size(); i++) {
+        float v = d->layer_ns_f32 ? d->layer_ns_f32[i] : (float)d->layer_ns[i];
+        if (!(v > 0.0f) || !std::isfinite(v)) return fail(HEDDLE_E_INVAL, "layer_ns_f32 entries must be finite and > 0");
+        cost32[i] = v;
+    }
+    std::vector<float> a2a32((size_t)N * 3), p2p32((size_t)N * N);
+    for (size_t i = 0; i < a2a32.size(); i++) a2a32[i] = (float)a2a_ns[i];
+    for (size_t i = 0; i < p2p32.size(); i++) p2p32[i] = (float)p2p_ns[i];
+    int e0 = 0;
+    for (float v : cost32) e0 = std::min(e0, low_bit_exp(v));
+    for (float v : a2a32) if (v > 0) e0 = std::min(e0, low_bit_exp(v));
+    for (float v : p2p32) if (v > 0) e0 = std::min(e0, low_bit_exp(v));
+    bool fx_ok = e0 > -80;
+    auto to_fx = [&](float v, bool &ok) -> int64_t {
+        if (v == 0.0f) return 0;
+        long double x = std::ldexp((long double)v, -e0);      // exact: v is a multiple of 2^e0
+        if (x >= (long double)kLimit62) { ok = false; return 0; }
+        return (int64_t)x;
+    };
+    std::vector<int64_t> pre_time_fx((size_t)N * K * R, 0), a2a_fx((size_t)N * 3, 0), p2p_fx((size_t)N * N, 0);
+    i128 max_stage_fx = 0;
+    if (fx_ok) {
+        for (size_t i = 0; i < a2a32.size() && fx_ok; i++) a2a_fx[i] = to_fx(a2a32[i], fx_ok);
+        for (size_t i = 0; i < p2p32.size() && fx_ok; i++) p2p_fx[i] = to_fx(p2p32[i], fx_ok);
+        for (int g = 0; g < N && fx_ok; g++)
+            for (int k = 0; k < K && fx_ok; k++) {
+                i128 acc = 0;
+                int64_t *row = &pre_time_fx[((size_t)g * K + k) * R];
+                for (int l = 0; l < L && fx_ok; l++) {
+                    acc += to_fx(cost32[((size_t)g * K + k) * L + l], fx_ok);
+                    if (acc >= kLimit62) fx_ok = false;
+                    row[l + 1] = (int64_t)acc;
+                }
+                int64_t a2a_max = std::max(a2a_fx[g * 3 + 1], a2a_fx[g * 3 + 2]), p2p_max = 0;
+                for (int h = 0; h < N; h++) p2p_max = std::max(p2p_max, p2p_fx[g * N + h]);
+                i128 b = (i128)row[L] + (i128)n_moe * a2a_max + p2p_max;
+                if (b >= kLimit62) fx_ok = false;
+                if (b > max_stage_fx) max_stage_fx = b;
+            }
+    }
+
+    // ---- upload
+    Builder B;
+    size_t o_time = B.add(pre_time), o_time_fx = B.add(pre_time_fx), o_moe = B.add(pre_moe),
+           o_state = B.add(pre_state), o_act = B.add(pre_act), o_grad = B.add(pre_grad),
+           o_xgrad = B.add(pre_xgrad), o_prof = B.add(d->profiled, (size_t)N * K),
+           o_a2a = B.add(a2a_ns), o_a2a_fx = B.add(a2a_fx), o_p2p = B.add(p2p_ns), o_p2p_fx = B.add(p2p_fx),
+           o_cap = B.add(d->mem_cap_bytes, (size_t)N * 8), o_node = B.add(d->node_size, (size_t)N * 4),
+           o_ngpu = B.add(d->n_gpus, (size_t)N * 4), o_intra = B.add(d->intra_bw_MBps, (size_t)N * 8),
+           o_link = B.add(d->link_bw_MBps, (size_t)N * N * 8), o_epd = B.add(d->ep_degrees, (size_t)E * 4);
+
+    heddle_profile *p = new (std::nothrow) heddle_profile;
+    if (!p) return fail(HEDDLE_E_NOMEM, "host allocation failed");
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) { delete p; return hip_fail(e, "hipGetDevice"); }
+    e = hipMalloc(&p->dev_block, B.bytes.size());
+    if (e != hipSuccess) { delete p; return e == hipErrorOutOfMemory ? fail(HEDDLE_E_NOMEM, "hipMalloc of profile tables failed") : hip_fail(e, "hipMalloc"); }
+    e = hipMemcpy(p->dev_block, B.bytes.data(), B.bytes.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) { (void)hipFree(p->dev_block); delete p; return hip_fail(e, "hipMemcpy"); }
+    unsigned char *base = (unsigned char *)p->dev_block;
+    dp.fx_exp = e0;
+    dp.pre_time = (const int64_t *)(base + o_time);
+    dp.pre_time_fx = (const int64_t *)(base + o_time_fx);
+    dp.pre_moe = (const int32_t *)(base + o_moe);
+    dp.pre_state = (const int64_t *)(base + o_state);
+    dp.pre_act = (const int64_t *)(base + o_act);
+    dp.pre_grad = (const int64_t *)(base + o_grad);
+    dp.pre_xgrad = (const int64_t *)(base + o_xgrad);
+    dp.profiled = (const uint8_t *)(base + o_prof);
+    dp.a2a_ns = (const int64_t *)(base + o_a2a);
+    dp.a2a_fx = (const int64_t *)(base + o_a2a_fx);
+    dp.p2p_ns = (const int64_t *)(base + o_p2p);
+    dp.p2p_fx = (const int64_t *)(base + o_p2p_fx);
+    dp.mem_cap = (const int64_t *)(base + o_cap);
+    dp.node_size = (const int32_t *)(base + o_node);
+    dp.n_gpus = (const int32_t *)(base + o_ngpu);
+    dp.intra_bw = (const int64_t *)(base + o_intra);
+    dp.link_bw = (const int64_t *)(base + o_link);
+    dp.ep_degrees = (const int32_t *)(base + o_epd);
+    p->dev = dp;
+    p->max_stage_ns = (int64_t)max_stage;
+    p->max_ar_ns = (int64_t)max_ar;
+    p->narrow_i64 = max_stage < (i128)kNarrowLimit;
+    p->max_stage_fx = fx_ok ? (int64_t)max_stage_fx : -1;
+    // fp32-rounded all-reduce terms are within a factor (1 + 2^-24) of the int64 ones
+    {
+        long double b = std::ldexp((long double)max_ar * (1.0L + std::ldexp(1.0L, -20)) + 1.0L, -e0);
+        p->max_ar_fx = !fx_ok ? -1 : (b >= (long double)kLimit62 ? kLimit62 : (int64_t)b);
+    }
+    p->narrow_f32 = fx_ok && max_stage_fx < (i128)kNarrowLimit;
+    *out = p;
+    return HEDDLE_OK;
+}
+
+extern "C" void heddle_free_profile(heddle_profile *p)
+{
+    if (!p) return;
+    (void)hipFree(p->dev_block);
+    delete p;
+}
+
+extern "C" int heddle_profile_info_get(const heddle_profile *p, heddle_profile_info *info)
+{
+    if (!p || !info) return fail(HEDDLE_E_INVAL, "NULL argument");
+    info->narrow[0] = p->narrow_i64;
+    info->narrow[1] = p->narrow_f32;
+    info->fx_exp = p->dev.fx_exp;
+    info->L = p->dev.L;
+    info->n_types = p->dev.n_types;
+    info->n_tp = p->dev.n_tp;
+    info->n_ep = p->dev.n_ep;
+    info->max_stage_ns = p->max_stage_ns;
+    return HEDDLE_OK;
+}

@@ -1,0 +1,396 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle on
+the same seeded inputs, bit for bit. Needs an MI355X."""
+import os
+import sys
+import time
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from gpu_common import CO, F32, POISON, assert_same, gpu_price, key_lt, oracle_price, sub_workload
+from oracle import oracle as O
+from workloads.gen import Profile, make_workload, pack_stage, random_instance
+
+pytestmark = pytest.mark.gpu
+
+FLAG_SETS = [0, CO, F32, F32 | CO]
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="session")
+def H():
+    import torch
+    assert torch.cuda.is_available(), "no GPU"
+    from paper_2609_34244_amd import heddle
+    heddle.lib()
+    return heddle
+
+
+_wl_cache = {}
+
+
+def workload(name, n=None):
+    key = (name, n)
+    if key not in _wl_cache:
+        _wl_cache.clear() if len(_wl_cache) > 3 else None
+        _wl_cache[key] = make_workload(name, n=n)
+    return _wl_cache[key]
+
+
+def with_f32_table(w, seed):
+    """give the profile fractional fp32 costs so that fp32 roundings occur"""
+    rng = np.random.default_rng(seed)
+    w.profile.layer_ns_f32 = (w.profile.layer_ns * 1.0 + rng.integers(0, 8, w.profile.layer_ns.shape) * 0.125
+                              ).astype(np.float32)
+    return w
+
+
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("flags", FLAG_SETS)
+def test_random_instances(H, flags):
+    """tiny instances with ties, every status code, memory that binds and not"""
+    n_plans = 0
+    for seed in range(120):
+        w = random_instance(seed)
+        if flags & F32 and seed % 2:
+            with_f32_table(w, seed)
+        prof = H.heddle_load_profile(w.profile)
+        g = gpu_price(H, prof, w, flags)
+        o = oracle_price(w, flags)
+        assert_same(g, o, flags, f"random seed {seed} flags {flags}")
+        n_plans += g["status"].size
+    say("random plans checked", n_plans)
+
+
+SUBSETS = {"c1_tiny_dense": 1000, "c2_7b_dense": 3000, "c3_70b_dense": 400, "c4_moe": 1500, "c5_stress": 40}
+
+
+@pytest.mark.parametrize("name", list(SUBSETS))
+@pytest.mark.parametrize("flags", [0, CO])
+def test_config_subsets(H, name, flags):
+    """the first templates of every config (several waves' worth and a ragged tail)"""
+    w = sub_workload(workload(name), np.arange(SUBSETS[name]))
+    prof = H.heddle_load_profile(w.profile)
+    t0 = time.time()
+    g = gpu_price(H, prof, w, flags)
+    o = oracle_price(w, flags)
+    assert_same(g, o, flags, f"{name} flags {flags}")
+    say(name, flags, "statuses", np.bincount(g["status"].ravel(), minlength=9).tolist(), f"{time.time() - t0:.1f}s")
+
+
+@pytest.mark.parametrize("name", ["c3_70b_dense", "c5_stress"])
+def test_config_subsets_fp32(H, name):
+    w = sub_workload(workload(name), np.arange(SUBSETS[name]))
+    prof = H.heddle_load_profile(w.profile)
+    g = gpu_price(H, prof, w, F32)
+    o = oracle_price(w, F32)
+    assert_same(g, o, F32, f"{name} fp32")
+
+
+def check_argmin_full(H, g, m, flags):
+    """the GPU argmin is a minimiser of iter/m over OK plans, lowest index among ties"""
+    import torch
+    st = g["status"]
+    ok = st == 0
+    if not ok.any():
+        return None
+    it = torch.from_numpy(g["iter"]).cuda()
+    s = torch.from_numpy(st).cuda()
+    best = H.heddle_argmin_plans([int(x) for x in m], flags, it, s)
+    t, k, v = best
+    assert st[t, k] == 0
+    key = np.where(ok, g["iter"].astype(np.float64) / m[None, :].astype(np.float64), np.inf)
+    kmin = key.min()
+    near = np.argwhere(key <= kmin * (1 + 1e-9))
+    exact_min = None
+    for (a, b) in near:
+        if exact_min is None or key_lt(g["iter"][a, b], m[b], g["iter"][exact_min], m[exact_min[1]]):
+            exact_min = (a, b)
+    ties = [(a, b) for (a, b) in near if not key_lt(g["iter"][exact_min], m[exact_min[1]], g["iter"][a, b], m[b])]
+    assert (t, k) == min(ties), ((t, k), min(ties))
+    return t, k
+
+
+@pytest.mark.parametrize("name,n_sample", [("c2_7b_dense", 1500), ("c3_70b_dense", 300), ("c4_moe", 800),
+                                           ("c5_stress", 30)])
+def test_full_size_sampled(H, name, n_sample):
+    """full config on the GPU in the benchmark's launch configuration; a seeded
+    sample of templates recomputed by the oracle; the full-batch argmin
+    checked as a minimiser and its plan recomputed"""
+    w = workload(name)
+    prof = H.heddle_load_profile(w.profile)
+    t0 = time.time()
+    g = gpu_price(H, prof, w, 0)
+    say(name, "full", w.n, "templates priced", f"{time.time() - t0:.1f}s",
+        np.bincount(g["status"].ravel(), minlength=9).tolist())
+    assert not np.any(g["status"] == POISON)
+    idx = np.sort(np.random.default_rng(123).choice(w.n, size=n_sample, replace=False))
+    o = oracle_price(sub_workload(w, idx), 0)
+    gs = {k: v[idx] for k, v in g.items()}
+    assert_same(gs, o, 0, f"{name} sampled")
+    best = check_argmin_full(H, g, w.m, 0)
+    if best is not None:
+        o1 = oracle_price(sub_workload(w, [best[0]]), 0)
+        assert o1["iter"][0, best[1]] == g["iter"][best] and o1["status"][0, best[1]] == 0
+
+
+def test_full_size_c5_fp32_sampled(H):
+    w = workload("c5_stress")
+    prof = H.heddle_load_profile(w.profile)
+    g = gpu_price(H, prof, w, F32)
+    idx = np.sort(np.random.default_rng(7).choice(w.n, size=20, replace=False))
+    o = oracle_price(sub_workload(w, idx), F32)
+    assert_same({k: v[idx] for k, v in g.items()}, o, F32, "c5 fp32 sampled")
+    check_argmin_full(H, g, w.m, F32)
+
+
+# ------------------------------------------------------------------ fp32 vs int64
+@pytest.mark.parametrize("name", ["c3_70b_dense", "c5_stress", "c4_moe"])
+def test_fp32_within_1e5_of_int64(H, name):
+    """fp32 results agree with int64 within 1e-5 relative wherever the two
+    variants chose the same split (each fp32 time is one rounding of a sum of
+    fp32 terms, each term within 2^-24 of its int64 value)"""
+    w = sub_workload(workload(name), np.arange(2000 if name != "c5_stress" else 300))
+    prof = H.heddle_load_profile(w.profile)
+    a = gpu_price(H, prof, w, 0)
+    b = gpu_price(H, prof, w, F32)
+    same = (a["status"] == 0) & (b["status"] == 0) & np.all(a["layers"] == b["layers"], axis=2)
+    assert same.sum() > 0.9 * (a["status"] == 0).sum()
+    for k in ("iter", "bottleneck"):
+        x, y = a[k][same].astype(np.float64), b[k][same].astype(np.float64)
+        rel = np.abs(y - x) / x
+        assert rel.max() <= 1e-5, (k, rel.max())
+    say(name, "fp32 vs int64 max rel", float(np.abs(b["iter"][same] / a["iter"][same] - 1).max()))
+
+
+# ------------------------------------------------------------------ edge cases
+def synthetic_profile(L, n_types=2, cost=(1000, 5000), seed=0, caps=1 << 40, moe=False):
+    rng = np.random.default_rng(seed)
+    K = 2
+    return Profile(
+        L=L, tp_degrees=np.array([1, 2], np.int32), ep_degrees=np.array([1, 2], np.int32),
+        layer_ns=rng.integers(cost[0], cost[1], size=(n_types, K, L)).astype(np.int64),
+        profiled=np.ones((n_types, K), np.uint8),
+        is_moe=(np.arange(L) % 2).astype(np.uint8) if moe else np.zeros(L, np.uint8),
+        state_bytes=rng.integers(1, 100, size=(K, L)).astype(np.int64),
+        xstate_bytes=rng.integers(0, 100, size=(K, L)).astype(np.int64) * (np.arange(L) % 2 if moe else 0),
+        act_bytes=rng.integers(1, 50, size=(K, L)).astype(np.int64),
+        grad_bytes=rng.integers(1, 100, size=(K, L)).astype(np.int64),
+        xgrad_bytes=rng.integers(0, 100, size=(K, L)).astype(np.int64) * (np.arange(L) % 2 if moe else 0),
+        boundary_bytes=1000, a2a_bytes=2000 if moe else 0,
+        mem_cap_bytes=np.full(n_types, caps, np.int64), node_size=np.full(n_types, 8, np.int32),
+        n_gpus=np.full(n_types, 1 << 20, np.int32), intra_bw_MBps=np.full(n_types, 3000, np.int64),
+        link_bw_MBps=rng.integers(200, 900, size=(n_types, n_types)).astype(np.int64)).check()
+
+
+def templates(S_list, s_max, n_types=2, seed=0, dp=1, ep=False):
+    rng = np.random.default_rng(seed)
+    n = len(S_list)
+    rec = np.zeros((n, s_max), np.uint32)
+    for t, S in enumerate(S_list):
+        k = min(S, s_max)                  # S > s_max is a BAD_SHAPE template
+        g = rng.integers(0, n_types, size=k)
+        tp = rng.integers(0, 2, size=k)
+        e = rng.integers(0, 2, size=k) if ep else np.zeros(k, int)
+        rec[t, :k] = pack_stage(g, tp, e, dp)
+    return np.array(S_list, np.uint8), rec
+
+
+def run_pair(H, prof_np, ns, st, m, flags, s_max):
+    from workloads.gen import Workload
+    w = Workload(name="edge", profile=prof_np, n_stages=ns, stages=st, m=np.array(m, np.int32), s_max=s_max)
+    prof = H.heddle_load_profile(prof_np)
+    g = gpu_price(H, prof, w, flags)
+    o = oracle_price(w, flags)
+    assert_same(g, o, flags, "edge")
+    return g, prof
+
+
+def test_max_sizes(H):
+    """L = 255 layers and s_max = 64 stage slots: the largest shapes the ABI takes"""
+    p = synthetic_profile(255, caps=1 << 40)
+    ns, st = templates([1, 2, 3, 17, 63, 64, 64, 40], 64)
+    for flags in (0, CO):
+        g, prof = run_pair(H, p, ns, st, [1, 4, 200], flags, 64)
+    assert H.heddle_profile_info_get(prof)["narrow_i64"]
+
+
+def test_memory_binding_max_sizes(H):
+    p = synthetic_profile(200, caps=2500, moe=True)
+    ns, st = templates([1, 5, 20, 64, 50, 33], 64, dp=2, ep=True)
+    for flags in (0, F32):
+        run_pair(H, p, ns, st, [1, 3, 64], flags, 64)
+
+
+def test_wide_values_use_64bit_dp(H):
+    """stage times beyond 2^31 ns take the 64-bit DP instantiation"""
+    p = synthetic_profile(40, cost=(10 ** 8, 3 * 10 ** 8))
+    ns, st = templates([1, 2, 5, 9, 16, 40, 33], 40)
+    prof = H.heddle_load_profile(p)
+    info = H.heddle_profile_info_get(prof)
+    assert not info["narrow_i64"] and not info["narrow_f32"]
+    for flags in FLAG_SETS:
+        run_pair(H, p, ns, st, [1, 7], flags, 40)
+
+
+def test_every_stage_one_layer_and_m_extremes(H):
+    p = synthetic_profile(12)
+    ns, st = templates([12, 12, 11, 1], 12, dp=3)
+    for flags in (0, F32):
+        run_pair(H, p, ns, st, [1, 2, 3, 1 << 24], flags, 12)
+
+
+def test_max_m_list(H):
+    """64 micro-batch counts per template, many sharing one split"""
+    p = synthetic_profile(30, caps=900)
+    ns, st = templates([1, 3, 8, 15, 30, 4], 16, dp=2)
+    m = list(range(1, 129, 2))
+    assert len(m) == 64
+    for flags in (0, CO):
+        run_pair(H, p, ns, st, m, flags, 16)
+
+
+def test_empty_batch(H):
+    import torch
+    w = make_workload("c1_tiny_dense", n=8)
+    prof = H.heddle_load_profile(w.profile)
+    ns = torch.empty(0, dtype=torch.uint8, device="cuda")
+    st = torch.empty((0, 4), dtype=torch.int32, device="cuda")
+    out = H.alloc_outputs(0, 1, 4)
+    H.heddle_price_plans(prof, ns, st, [16], 0, out)
+    assert H.heddle_count_work(prof, ns, st, [16], 0) == 0
+    assert H.heddle_best_plan(prof, ns, st, [16], 0) is None
+
+
+def test_argument_errors(H):
+    import torch
+    w = make_workload("c1_tiny_dense", n=8)
+    prof = H.heddle_load_profile(w.profile)
+    ns, st = H.to_device(w.n_stages, w.stages)
+    out = H.alloc_outputs(8, 1, 4)
+    lib = H.lib()
+    import ctypes as C
+    m1 = (C.c_int32 * 1)(16)
+    s = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    p = lambda t: C.c_void_p(t.data_ptr())
+    args = lambda **kw: dict(dict(n=8, s_max=4, m=m1, n_m=1, flags=0, it=p(out["iter"])), **kw)
+
+    def call(a):
+        return lib.heddle_price_plans(prof.handle, a["n"], a["s_max"], p(ns), p(st), a["m"], a["n_m"], a["flags"],
+                                      a["it"], p(out["bottleneck"]), p(out["peak_mem"]), p(out["layers"]),
+                                      p(out["status"]), s)
+    assert call(args()) == H.HEDDLE_OK
+    assert call(args(s_max=0)) == H.HEDDLE_E_INVAL
+    assert call(args(s_max=65)) == H.HEDDLE_E_INVAL
+    assert call(args(n=-1)) == H.HEDDLE_E_INVAL
+    assert call(args(n_m=0)) == H.HEDDLE_E_INVAL
+    assert call(args(n_m=65)) == H.HEDDLE_E_INVAL
+    assert call(args(flags=4)) == H.HEDDLE_E_INVAL
+    assert call(args(m=(C.c_int32 * 1)(0))) == H.HEDDLE_E_INVAL
+    assert call(args(m=(C.c_int32 * 1)((1 << 24) + 1))) == H.HEDDLE_E_INVAL
+    assert call(args(it=None)) == H.HEDDLE_E_INVAL
+    assert "NULL" in H.heddle_last_error()
+    # iteration times that could overflow: huge costs with the largest m
+    pbig = synthetic_profile(8, cost=(1 << 40, (1 << 40) + 5))
+    big = H.heddle_load_profile(pbig)
+    assert lib.heddle_price_plans(big.handle, 8, 4, p(ns), p(st), (C.c_int32 * 1)(1 << 24), 1, 0, p(out["iter"]),
+                                  p(out["bottleneck"]), p(out["peak_mem"]), p(out["layers"]), p(out["status"]),
+                                  s) == H.HEDDLE_E_RANGE
+    torch.cuda.synchronize()
+
+
+# ------------------------------------------------------------------ determinism
+def test_determinism_streams_chunks_permutation(H):
+    import torch
+    w = sub_workload(workload("c4_moe"), np.arange(3000))
+    prof = H.heddle_load_profile(w.profile)
+    a = gpu_price(H, prof, w, 0)
+    b = gpu_price(H, prof, w, 0)
+    for k in a:
+        assert np.array_equal(a[k], b[k])
+    s2 = torch.cuda.Stream()
+    with torch.cuda.stream(s2):
+        c = gpu_price(H, prof, w, 0)
+    for k in a:
+        assert np.array_equal(a[k], c[k])
+    perm = np.random.default_rng(1).permutation(w.n)
+    d = gpu_price(H, prof, sub_workload(w, perm), 0)
+    inv = np.argsort(perm)
+    for k in a:
+        assert np.array_equal(a[k], d[k][inv])
+    parts = [gpu_price(H, prof, sub_workload(w, np.arange(lo, hi)), 0) for lo, hi in ((0, 1), (1, 1234), (1234, 3000))]
+    for k in a:
+        assert np.array_equal(a[k], np.concatenate([q[k] for q in parts]))
+
+
+# ------------------------------------------------------------------ argmin
+@pytest.mark.parametrize("flags", [0, F32, CO])
+def test_argmin_matches_oracle(H, flags):
+    import torch
+    for seed in list(range(40)) + ["c1_tiny_dense", "c2_7b_dense"]:
+        w = random_instance(seed) if isinstance(seed, int) else sub_workload(workload(seed), np.arange(2000 if seed != "c1_tiny_dense" else 1000))
+        prof = H.heddle_load_profile(w.profile)
+        g = gpu_price(H, prof, w, flags)
+        want = O.best_plan(w.m, g["iter"], g["status"], flags)
+        got = H.heddle_argmin_plans([int(x) for x in w.m], flags, torch.from_numpy(g["iter"]).cuda(),
+                                    torch.from_numpy(g["status"]).cuda())
+        assert (None if got is None else got[:2]) == want, seed
+        ns, st = H.to_device(w.n_stages, w.stages)
+        bp = H.heddle_best_plan(prof, ns, st, [int(x) for x in w.m], flags)
+        assert (None if bp is None else bp[:2]) == want, seed
+        if want is not None:
+            v = g["iter"][want]
+            assert bp[2] == (float(v) if flags & F32 else int(v))
+
+
+def test_argmin_ties_and_large_products(H):
+    import torch
+    m = [2, 4]
+    it = torch.tensor([[10, 20], [5, 10], [10, 20]], dtype=torch.int64, device="cuda")
+    st = torch.zeros((3, 2), dtype=torch.uint8, device="cuda")
+    assert H.heddle_argmin_plans(m, 0, it, st)[:2] == (1, 0)
+    st[1] = 8
+    assert H.heddle_argmin_plans(m, 0, it, st)[:2] == (0, 0)
+    st[:] = 8
+    assert H.heddle_argmin_plans(m, 0, it, st) is None
+    big = torch.tensor([[2 ** 62, 2 ** 62 - 1]], dtype=torch.int64, device="cuda")
+    assert H.heddle_argmin_plans([2 ** 24, 2 ** 24 - 1], 0, big, torch.zeros((1, 2), dtype=torch.uint8, device="cuda"))[:2] == (0, 0)
+    # many blocks: the best plan far from the start of the array
+    n = 3_000_000
+    it = torch.full((n, 1), 1000, dtype=torch.int64, device="cuda")
+    it[2_345_678, 0] = 999
+    it[2_999_999, 0] = 999
+    st = torch.zeros((n, 1), dtype=torch.uint8, device="cuda")
+    assert H.heddle_argmin_plans([1], 0, it, st)[:2] == (2_345_678, 0)
+
+
+# ------------------------------------------------------------------ work count
+def oracle_work(w, flags):
+    """sum over templates of the relaxations of each distinct split the m values need"""
+    op = O.OracleProfile(w.profile)
+    total = 0
+    for t in range(w.n):
+        S = int(w.n_stages[t])
+        seen = set()
+        D = int(w.stages[t, 0] >> 16) if S >= 1 else 1
+        for m in w.m:
+            key = 0 if flags & CO else min(-(-int(m) // max(D, 1)), S)
+            if key in seen:
+                continue
+            seen.add(key)
+            total += O.count_relaxations(op, S, w.stages[t], w.s_max, int(m), flags)
+    return total
+
+
+@pytest.mark.parametrize("flags", [0, CO])
+def test_count_work(H, flags):
+    for w in [random_instance(s) for s in range(30)] + [sub_workload(workload("c3_70b_dense"), np.arange(200)),
+                                                       sub_workload(workload("c5_stress"), np.arange(20))]:
+        prof = H.heddle_load_profile(w.profile)
+        ns, st = H.to_device(w.n_stages, w.stages)
+        assert H.heddle_count_work(prof, ns, st, [int(x) for x in w.m], flags) == oracle_work(w, flags), w.name

@@ -182,24 +182,43 @@ def make_profile(cfg, rng):
 
 
 def _draw_templates(rng, n, s_max, N, tp_sets, dp_choices, ep_degrees):
-    S = rng.integers(1, s_max + 1, size=n)
-    g = rng.integers(0, N, size=(n, s_max))
-    tu = rng.random((n, s_max))
-    D = np.asarray(dp_choices, dtype=np.int64)[rng.integers(0, len(dp_choices), size=n)]
-    eu = rng.random((n, s_max))
-    ntp = np.array([len(t) for t in tp_sets])
-    tp_tab = np.zeros((N, max(ntp)), dtype=np.int64)
+    """One batch of draws, in this order: S, per-stage type, per-stage TP
+    uniform, DP choice, per-stage EP uniform."""
+    S = rng.integers(1, s_max + 1, size=n, dtype=np.int64)
+    g = rng.integers(0, N, size=(n, s_max), dtype=np.uint8)
+    tu = rng.random((n, s_max), dtype=np.float32)
+    dsel = rng.integers(0, len(dp_choices), size=n, dtype=np.int64)
+    eu = rng.random((n, s_max), dtype=np.float32)
+    ntp = np.array([len(t) for t in tp_sets], dtype=np.int64)
+    tp_tab = np.zeros((N, int(ntp.max())), dtype=np.int32)
     for i, t in enumerate(tp_sets):
         tp_tab[i, :len(t)] = t
-    tidx = np.minimum((tu * ntp[g]).astype(np.int64), ntp[g] - 1)
+    nt = ntp[g]
+    tidx = np.minimum((tu * nt).astype(np.int64), nt - 1)
     tp = tp_tab[g, tidx]
-    ep_all = np.asarray(ep_degrees, dtype=np.int64)
-    ok = (D[:, None] % ep_all[None, :]) == 0                       # [n, n_ep] allowed EP
-    nok = ok.sum(axis=1)
-    pick = np.minimum((eu * nok[:, None]).astype(np.int64), nok[:, None] - 1)
-    order = np.argsort(~ok, axis=1, kind="stable")                 # allowed EPs first, ascending
-    ep = ep_all[np.take_along_axis(order, pick, axis=1)]
-    return S, g, tp, D, ep
+    dps = np.asarray(dp_choices, dtype=np.int64)
+    eps = np.asarray(ep_degrees, dtype=np.int64)
+    # EP degrees allowed for each DP choice (those dividing it), ascending
+    allowed = [eps[(d % eps) == 0] for d in dps]
+    nok = np.array([len(a) for a in allowed], dtype=np.int64)
+    ep_tab = np.zeros((len(dps), int(nok.max())), dtype=np.int32)
+    for i, a in enumerate(allowed):
+        ep_tab[i, :len(a)] = a
+    nk = nok[dsel][:, None]
+    pick = np.minimum((eu * nk).astype(np.int64), nk - 1)
+    ep = ep_tab[dsel[:, None], pick]
+    return S, g, tp, dps[dsel], ep
+
+
+def _gpus_per_type(S, g, tp, D, N):
+    n, s_max = g.shape
+    used = np.arange(s_max)[None, :] < S[:, None]
+    idx = (np.arange(n, dtype=np.int64)[:, None] * N + g.astype(np.int64))[used]
+    w = (tp.astype(np.int64) * D[:, None])[used]
+    return np.bincount(idx, weights=w, minlength=n * N).reshape(n, N)
+
+
+TEMPLATE_CHUNK = 1 << 16
 
 
 def make_templates(cfg, profile, rng, n=None):
@@ -207,28 +226,32 @@ def make_templates(cfg, profile, rng, n=None):
     TP degree from that type's TP set (powers of two up to its node size);
     one DP degree per template copied into every stage; per stage a uniform EP
     degree among those dividing DP. Templates that use more GPUs of a type than
-    the cluster holds are redrawn (the device mask of the planner)."""
+    the cluster holds are redrawn (the device mask of the planner).
+    Drawn in chunks of TEMPLATE_CHUNK templates, each chunk's redraws right
+    after its own draws."""
     n = cfg["n_templates"] if n is None else n
     s_max, N = cfg["s_max"], profile.n_types
     tp_sets = [[int(k) for k in profile.tp_degrees if k <= profile.node_size[g]] for g in range(N)]
-    S, g, tp, D, ep = _draw_templates(rng, n, s_max, N, tp_sets, cfg["dp_choices"], cfg["ep_degrees"])
-    for _ in range(1000):
+    n_st = np.empty(n, dtype=np.uint8)
+    out = np.empty((n, s_max), dtype=np.uint32)
+    log2 = lambda a: np.log2(a).round().astype(np.uint32)
+    for c0 in range(0, n, TEMPLATE_CHUNK):
+        cn = min(TEMPLATE_CHUNK, n - c0)
+        S, g, tp, D, ep = _draw_templates(rng, cn, s_max, N, tp_sets, cfg["dp_choices"], cfg["ep_degrees"])
+        for _ in range(1000):
+            bad = np.nonzero((_gpus_per_type(S, g, tp, D, N) > profile.n_gpus[None, :]).any(axis=1))[0]
+            if bad.size == 0:
+                break
+            S2, g2, tp2, D2, ep2 = _draw_templates(rng, bad.size, s_max, N, tp_sets, cfg["dp_choices"],
+                                                   cfg["ep_degrees"])
+            S[bad], g[bad], tp[bad], D[bad], ep[bad] = S2, g2, tp2, D2, ep2
+        else:
+            raise RuntimeError("template rejection did not converge")
         used = np.arange(s_max)[None, :] < S[:, None]
-        gpus = np.zeros((n, N), dtype=np.int64)
-        for t in range(N):
-            gpus[:, t] = ((g == t) & used).astype(np.int64).__mul__(tp).sum(axis=1) * D
-        bad = np.nonzero((gpus > profile.n_gpus[None, :].astype(np.int64)).any(axis=1))[0]
-        if bad.size == 0:
-            break
-        S2, g2, tp2, D2, ep2 = _draw_templates(rng, bad.size, s_max, N, tp_sets, cfg["dp_choices"], cfg["ep_degrees"])
-        S[bad], g[bad], tp[bad], D[bad], ep[bad] = S2, g2, tp2, D2, ep2
-    else:
-        raise RuntimeError("template rejection did not converge")
-    used = np.arange(s_max)[None, :] < S[:, None]
-    log2 = lambda a: np.round(np.log2(a)).astype(np.uint32)
-    rec = pack_stage(g, log2(tp), log2(ep), np.broadcast_to(D[:, None], g.shape))
-    rec = np.where(used, rec, np.uint32(0)).astype(np.uint32)
-    return S.astype(np.uint8), np.ascontiguousarray(rec)
+        rec = pack_stage(g, log2(tp), log2(ep), D[:, None])
+        out[c0:c0 + cn] = np.where(used, rec, np.uint32(0))
+        n_st[c0:c0 + cn] = S
+    return n_st, out
 
 
 def make_workload(name, n=None):

@@ -82,6 +82,8 @@ def main():
     ap.add_argument("--compute-only", action="store_true", help="split ignores memory; fit checked after")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device-to-device copy of BYTES (reference for HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py prices on one GPU; multi-GPU runs are not part of this build "
@@ -95,6 +97,14 @@ def main():
     from workloads.gen import make_workload
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_calibration:
+        src = torch.ones(args.copy_calibration, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": args.copy_calibration}))
+        return
     flags = (H.HEDDLE_F_FP32 if args.fp32 else 0) | (H.HEDDLE_F_COMPUTE_ONLY if args.compute_only else 0)
     t0 = time.perf_counter()
     w = make_workload(args.config)

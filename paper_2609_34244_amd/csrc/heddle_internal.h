@@ -13,6 +13,8 @@ constexpr int kWave = 64;
 constexpr int kMaxStages = HEDDLE_MAX_STAGES;
 constexpr int kMaxMList = HEDDLE_MAX_MLIST;
 constexpr int64_t kLimit62 = int64_t(1) << 62;
+constexpr size_t kMaxLimitTable = size_t(256) << 20;       // bytes of the memory-limit table
+constexpr int64_t kMaxBandwidth = (int64_t(1) << 34) - 1;   // MB/s; keeps n * bw below 2^50
 constexpr uint32_t kNarrowLimit = 0x7FFFFFFFu;   // exact 32-bit DP when every stage time is below this
 
 // a2a variant of a stage: no all-to-all (EP = 1), EP x TP group inside one
@@ -44,6 +46,8 @@ struct DevProfile {
     const int64_t *intra_bw;         // [n_types] MB/s
     const int64_t *link_bw;          // [n_types][n_types] MB/s
     const int32_t *ep_degrees;       // [n_ep]
+    const uint8_t *mem_lim;          // [n_types][n_tp][n_ep][n_f][L+1] largest end that fits from row i
+    int32_t n_f;                     // in-flight counts covered by mem_lim: 1 .. min(L, 64)
 };
 
 }  // namespace heddle
@@ -84,7 +88,9 @@ struct PriceArgs {
     uint8_t *layers, *status;
     unsigned long long *work;        // count-only launches: accumulated relaxations
     int32_t g_stride;                // LDS entries per DP table row (L + 1)
-    int32_t lds_per_wave;            // bytes
+    int32_t s_cap;                   // DP table rows: min(s_max, L)
+    int32_t lds_per_wave;            // bytes of one wavefront's LDS region
+    int32_t off_j;                   // byte offset of the end-limit table
 };
 
 int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,

@@ -3,28 +3,33 @@
 // Evaluate (1F1B iteration time and per-GPU peak memory).
 //
 // Method: Heddle (arXiv 2609.34244). The layer split is the PartitionLayers
-// step of the planners' nested-loop backbone (section 3.1), made aware of
-// per-stage GPU speed (the straggler criticism of speed-blind splits in the
-// same section) and of memory (section 5.2, memory validation). Evaluate is
-// the profile-based cost model of section 5.2 and the 1F1B formula
+// step of the planners' nested-loop backbone (section 3.1), aware of per-stage
+// GPU speed (the straggler criticism of speed-blind splits in the same
+// section) and of memory (section 5.2, memory validation). Evaluate is the
+// profile-based cost model of section 5.2 with the 1F1B iteration time
 // (M-1) max_s t_s + sum_s t_s + max_s g_s of section 5.3.
-//
-// Mapping: one wavefront prices one template at a time (grid-stride over
-// templates). Lanes are pipeline stages during decode, validation and
-// Evaluate, and split rows during the DP. The DP table of the template
-// (stage rows of L+1 entries) and the time-prefix row of the stage being
-// relaxed live in LDS; profile tables are read from global memory, where
-// they stay cache resident (a few KB to a few hundred KB per profile).
 //
 // Recurrence (suffix form): G[s][i] is the smallest achievable bottleneck
 // when stages s..S-1 hold layers [i, L):
-//   G[S-1][i] = T(S-1, i, L)                        if it fits, else inf
-//   G[s][i]   = min over i < j <= L-(S-1-s), Fits(s,i,j) of max(T(s,i,j), G[s+1][j])
-// and B* = G[0][0]. Memory use of a stage grows with j for fixed i, so the
-// feasible ends of row i form a prefix (i, jlim(i)] found by binary search;
-// the relaxation loop then carries no memory test.
+//   G[S-1][i] = T(S-1, i, L)                                    if it fits
+//   G[s][i]   = min over i < j <= jlim_s(i) of max(T(s,i,j), G[s+1][j])
+// with jlim_s(i) the largest end that fits memory (and leaves one layer per
+// later stage); B* = G[0][0]. Memory grows with j for fixed i, so the
+// feasible ends of a row form the prefix (i, jlim_s(i)].
+//
+// Mapping. One wavefront prices one template at a time (grid-stride over
+// templates). Lanes are pipeline stages for decode, validation and Evaluate,
+// and split rows i of one stage during the DP, each lane walking its own ends
+// j. Per wavefront LDS holds, for every stage s, the pairs
+//   X[s][j] = { P_s[j], G[s+1][j] }
+// where P_s is the stage's time prefix (layer costs + MoE all-to-all), so one
+// 64-bit LDS read feeds one relaxation (sub, max, min); the stage's memory
+// prefix U; and the memory limits jlim_s(i) as bytes, which the
+// reconstruction reuses. The profile rows of the next stage are fetched from
+// global memory into registers while the current stage relaxes.
 #include <cstring>
 
+#include "exact_math.h"
 #include "heddle_internal.h"
 
 namespace heddle {
@@ -75,7 +80,7 @@ template <class T> __device__ __forceinline__ T wave_sum(T v)
 }
 
 // Nearest value with at most 24 significant bits (ties to even) of a
-// non-negative integer: the fp32 rounding of x, kept as an exact integer.
+// non-negative integer below 2^63: its fp32 rounding, kept as an exact integer.
 __device__ __forceinline__ uint64_t rne24(uint64_t x)
 {
     if (x < (1ull << 24)) return x;
@@ -93,110 +98,123 @@ __device__ __forceinline__ float exact_float(uint64_t x, int e)
     return ldexpf((float)(uint32_t)(x >> sh), sh + e);
 }
 
-// ceil(2 (n-1) b * 1000 / (n bw)): ring all-reduce of b bytes over n ranks
-__device__ __forceinline__ int64_t allreduce_ns(int64_t b, int64_t n, int64_t bw)
-{
-    if (n <= 1 || b == 0) return 0;
-    const unsigned __int128 num = (unsigned __int128)(uint64_t)(2 * (n - 1)) * (uint64_t)b * 1000u;
-    const unsigned __int128 den = (unsigned __int128)(uint64_t)n * (uint64_t)bw;
-    return (int64_t)((num + den - 1) / den);
-}
-
 __device__ __forceinline__ int nibble(uint64_t w, int l) { return (int)((w >> (4 * l)) & 15); }
+
+template <class V> struct Vec2;
+template <> struct Vec2<uint32_t> { typedef uint32_t type __attribute__((ext_vector_type(2))); };
+template <> struct Vec2<uint64_t> { typedef uint64_t type __attribute__((ext_vector_type(2))); };
+template <class V> struct DPInf { static constexpr V value = ~V(0); };
 
 // Per-lane (lane = stage s) decoded record and stage constants.
 struct StageInfo {
-    int status;          // uniform: HEDDLE_S_* of the template (0 if valid)
-    int S, D;            // uniform
-    int g, tp, ep, ki, ei;
-    int64_t a2a, p2p;    // all-to-all per MoE layer, outbound p2p (ns, or fixed-point for fp32)
-    int64_t a2a_ns, p2p_ns;
+    int status;              // uniform: HEDDLE_S_* of the template (0 if valid)
+    int S, D;                // uniform
+    int tp, ep;
+    int64_t a2a, p2p;        // all-to-all per MoE layer, outbound p2p (ns, or fixed point for fp32)
     int64_t cap, bw_dp;
-    int trow, srow, arow; // offsets of the stage's rows in the prefix tables
+    int trow, srow, arow;    // offsets of the stage's rows in the prefix tables
+    int lrow;                // offset of the stage's memory-limit rows (in-flight count 1)
 };
 
-// Template decode and validation (feasibility masks of section 5.1; exact
-// profile match of section 5.2). Checks run in status order over all stages.
+// Template decode and validation (feasibility masks of section 5.1, exact
+// profile match of section 5.2). All per-lane table reads are issued at once
+// on clamped indices; the checks then run in status order over all stages.
 template <bool F32>
 __device__ StageInfo decode(const DevProfile &P, const PriceArgs &A, int64_t t, int lane)
 {
     StageInfo x;
-    const int L = P.L, R = L + 1;
+    const int L = P.L, R = L + 1, N = P.n_types;
     x.S = A.n_stages[t];
     x.status = 0;
     x.D = 1;
     const bool act = lane < x.S && lane < A.s_max;
     const uint32_t rec = act ? A.stages[t * A.s_max + lane] : 0u;
-    x.g = rec & 0xFF;
+    const int g = rec & 0xFF;
     const int l2tp = (rec >> 8) & 15, l2ep = (rec >> 12) & 15;
     const int dpv = (int)(rec >> 16);
     x.tp = 1 << l2tp;
     x.ep = 1 << l2ep;
-    x.ki = nibble(P.tp_index, l2tp);
-    x.ei = nibble(P.ep_index, l2ep);
-    x.a2a = x.p2p = x.a2a_ns = x.p2p_ns = x.cap = x.bw_dp = 0;
-    x.trow = x.srow = x.arow = 0;
+    const int ki = nibble(P.tp_index, l2tp), ei = nibble(P.ep_index, l2ep);
+    const int gc = g < N ? g : N - 1;                          // clamped for speculative reads
+    const int gn = __shfl(gc, lane + 1 < 64 ? lane + 1 : 63);
+    const int node = P.node_size[gc];
+    const int prof = P.profiled[gc * P.n_tp + ki];
+    const int ngpu = P.n_gpus[gc];
+    const int var = x.ep == 1 ? kA2ANone : (x.ep * x.tp <= node ? kA2AIntra : kA2AInter);
+    const int64_t a2a = F32 ? P.a2a_fx[gc * 3 + var] : P.a2a_ns[gc * 3 + var];
+    const int64_t p2p = F32 ? P.p2p_fx[gc * N + gn] : P.p2p_ns[gc * N + gn];
+    const int64_t cap = P.mem_cap[gc], intra = P.intra_bw[gc], self = P.link_bw[gc * N + gc];
+
+    x.a2a = x.p2p = x.cap = x.bw_dp = 0;
+    x.trow = x.srow = x.arow = x.lrow = 0;
     if (x.S < 1 || x.S > A.s_max || x.S > L) { x.status = HEDDLE_S_BAD_SHAPE; return x; }
-    if (__ballot(act && x.g >= P.n_types)) { x.status = HEDDLE_S_BAD_TYPE; return x; }
-    const int node = act ? P.node_size[x.g] : 0;
+    if (__ballot(act && g >= N)) { x.status = HEDDLE_S_BAD_TYPE; return x; }
     if (__ballot(act && (!((P.tp_present >> l2tp) & 1) || x.tp > node))) { x.status = HEDDLE_S_BAD_TP; return x; }
-    if (__ballot(act && !P.profiled[x.g * P.n_tp + x.ki])) { x.status = HEDDLE_S_UNPROFILED; return x; }
+    if (__ballot(act && !prof)) { x.status = HEDDLE_S_UNPROFILED; return x; }
     x.D = rl32(dpv, 0);
     if (__ballot(act && (dpv < 1 || dpv != x.D))) { x.status = HEDDLE_S_BAD_DP; return x; }
-    if (__ballot(act && (!((P.ep_present >> l2ep) & 1) || (x.D % x.ep) != 0))) { x.status = HEDDLE_S_BAD_EP; return x; }
-    int64_t used = 0;
+    if (__ballot(act && (!((P.ep_present >> l2ep) & 1) || ((uint32_t)x.D % (uint32_t)x.ep) != 0))) {
+        x.status = HEDDLE_S_BAD_EP;
+        return x;
+    }
+    int used = 0;                                              // this lane's type: sum of TP over its stages
     for (int s2 = 0; s2 < x.S; s2++)
-        if (rl32(x.g, s2) == x.g) used += rl32(x.tp, s2);
-    if (__ballot(act && used * x.D > P.n_gpus[x.g])) { x.status = HEDDLE_S_OVERSUBSCRIBED; return x; }
+        if (rl32(g, s2) == g) used += rl32(x.tp, s2);
+    if (__ballot(act && (int64_t)used * x.D > ngpu)) { x.status = HEDDLE_S_OVERSUBSCRIBED; return x; }
 
-    // stage constants
-    const int N = P.n_types;
-    const int gn = __shfl(x.g, lane + 1 < 64 ? lane + 1 : 63);
     if (act) {
-        const int var = x.ep == 1 ? 0 : (x.ep * x.tp <= node ? 1 : 2);
-        x.a2a_ns = P.a2a_ns[x.g * 3 + var];
-        x.p2p_ns = lane < x.S - 1 ? P.p2p_ns[x.g * N + gn] : 0;
-        x.a2a = F32 ? P.a2a_fx[x.g * 3 + var] : x.a2a_ns;
-        x.p2p = lane < x.S - 1 ? (F32 ? P.p2p_fx[x.g * N + gn] : x.p2p_ns) : 0;
-        x.cap = P.mem_cap[x.g];
-        x.bw_dp = (int64_t)x.tp * x.D <= node ? P.intra_bw[x.g] : P.link_bw[x.g * N + x.g];
-        x.trow = (x.g * P.n_tp + x.ki) * R;
-        x.srow = (x.ki * P.n_ep + x.ei) * R;
-        x.arow = x.ki * R;
+        x.a2a = a2a;
+        x.p2p = lane < x.S - 1 ? p2p : 0;
+        x.cap = cap;
+        x.bw_dp = (int64_t)x.tp * x.D <= node ? intra : self;
+        x.trow = (g * P.n_tp + ki) * R;
+        x.srow = (ki * P.n_ep + ei) * R;
+        x.arow = ki * R;
+        x.lrow = ((g * P.n_tp + ki) * P.n_ep + ei) * P.n_f * R;
     }
     return x;
 }
 
-// Largest end j in [i, jhi] such that stage layers [i, j) fit the cap with
-// `f` micro-batches of activations in flight (j = i always "fits").
-__device__ __forceinline__ int mem_limit(const int64_t *w, const int64_t *a, int64_t f, int64_t cap, int i, int jhi)
-{
-    const int64_t wi = w[i], ai = a[i];
-    int lo = i, hi = jhi;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if ((w[mid] - wi) + f * (a[mid] - ai) <= cap) lo = mid;
-        else hi = mid - 1;
-    }
-    return lo;
-}
+// Profile rows of one stage, fetched into registers ahead of use: the time
+// prefix, the MoE prefix count and the memory limits of every row.
+constexpr int kRowSlots = 4;                       // (L + 1) <= 256 entries, 64 per slot
+struct RowRegs {
+    int64_t t[kRowSlots];
+    int32_t m[kRowSlots];
+    int32_t l[kRowSlots];
+};
 
-template <class V> struct DPInf { static constexpr V value = ~V(0); };
+__device__ __forceinline__ void fetch_rows(RowRegs &r, const int64_t *trow, const int32_t *moe,
+                                           const uint8_t *lrow, int L, int lane, bool need_mem)
+{
+#pragma unroll
+    for (int q = 0; q < kRowSlots; q++) {
+        const int j = lane + 64 * q;
+        if (j <= L) {
+            r.t[q] = trow[j];
+            r.m[q] = moe[j];
+            r.l[q] = need_mem ? lrow[j] : L;
+        }
+    }
+}
 
 // ------------------------------------------------------------ price kernel
 
 template <class V, bool F32, bool COUNT>
 __global__ void __launch_bounds__(256) price_kernel(DevProfile P, PriceArgs A)
 {
+    typedef typename Vec2<V>::type V2;
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63, wib = threadIdx.x >> 6, wpb = blockDim.x >> 6;
     const int L = P.L, gs = A.g_stride;
     const bool compute_only = (A.flags & HEDDLE_F_COMPUTE_ONLY) != 0;
     const V INF = DPInf<V>::value;
-    V *G = (V *)(smem + (size_t)wib * A.lds_per_wave);
+    unsigned char *wave_lds = smem + (size_t)wib * A.lds_per_wave;
+    V2 *X = (V2 *)wave_lds;                                   // [s_cap][gs] pairs {P_s, G_{s+1}}
+    uint8_t *J = wave_lds + A.off_j;                          // [s_cap][gs] memory limits
     const int64_t *time_tab = F32 ? P.pre_time_fx : P.pre_time;
 
-    int my_m = 1;                        // lane k holds the k-th micro-batch count
+    int my_m = 1;                                             // lane k: the k-th micro-batch count
     for (int k = 0; k < A.n_m; k++) my_m = lane == k ? A.m[k] : my_m;
     unsigned long long work = 0;
 
@@ -204,188 +222,209 @@ __global__ void __launch_bounds__(256) price_kernel(DevProfile P, PriceArgs A)
         const StageInfo x = decode<F32>(P, A, t, lane);
         const int S = x.S;
         const size_t obase = (size_t)t * A.n_m;
-        if (x.status != 0) {
-            if (!COUNT) {
-                for (int k = lane; k < A.n_m; k += 64) {
-                    A.status[obase + k] = (uint8_t)x.status;
-                    if (F32) {
-                        ((float *)A.iter)[obase + k] = __builtin_inff();
-                        ((float *)A.bottleneck)[obase + k] = __builtin_inff();
-                    } else {
-                        ((int64_t *)A.iter)[obase + k] = INT64_MAX;
-                        ((int64_t *)A.bottleneck)[obase + k] = INT64_MAX;
-                    }
-                    A.peak_mem[obase + k] = INT64_MAX;
-                }
-                for (int q = lane; q < A.n_m * A.s_max; q += 64) A.layers[obase * A.s_max + q] = 0;
-            }
-            continue;
-        }
-        const int D = x.D;
-        // in-flight key of each micro-batch count: min(M_p, S) decides the split
-        const int64_t Mp_k = ((int64_t)my_m + D - 1) / D;
-        const int key_k = compute_only ? 0 : (int)(Mp_k < S ? Mp_k : S);
-        uint64_t todo = __ballot(lane < A.n_m);
+        // results of m index k live in lane k until the end of the template
+        bool r_priced = false, r_oom = false;
+        int64_t r_iter = INT64_MAX, r_bn = INT64_MAX, r_peak = INT64_MAX;
+        float r_iter_f = __builtin_inff(), r_bn_f = __builtin_inff();
 
-        while (todo) {
-            const int key = wave_min(((todo >> lane) & 1) ? key_k : 0x7FFFFFFF);
-            const uint64_t cls = __ballot(lane < A.n_m && key_k == key) & todo;
-            todo &= ~cls;
+        if (x.status == 0) {
+            const int D = x.D;
+            // micro-batches per replica M_p = ceil(m / D); min(M_p, S) fixes the split
+            const int Mp_k = (int)(((uint32_t)my_m + (uint32_t)D - 1) / (uint32_t)D);
+            const int key_k = compute_only ? 0 : (Mp_k < S ? Mp_k : S);
+            uint64_t todo = __ballot(lane < A.n_m);
 
-            // ---------------- PartitionLayers: suffix min-max DP
-            for (int s = S - 1; s >= 0; s--) {
-                const int64_t *trow = time_tab + rl32(x.trow, s);
-                const int64_t a2a = rl64(x.a2a, s), cap = rl64(x.cap, s);
-                const V p2p = (V)rl64(x.p2p, s);
-                const int64_t *wrow = P.pre_state + rl32(x.srow, s);
-                const int64_t *arow = P.pre_act + rl32(x.arow, s);
-                const int64_t f = (S - s) < key ? (S - s) : key;
-                const int jhi = L - (S - 1 - s);
-                const int ihi = (s == 0) ? 0 : L - (S - s);
-                V *prow = G + (size_t)S * gs;           // time prefix of stage s
-                V *Gs = G + (size_t)s * gs, *Gn = G + (size_t)(s + 1) * gs;
-                for (int j = lane; j <= L; j += 64) prow[j] = (V)(trow[j] + a2a * P.pre_moe[j]);
-                wave_sync();
-                if (s == S - 1) {
-                    for (int i = s + lane; i <= ihi; i += 64) {
-                        const bool fit = compute_only || (wrow[L] - wrow[i]) + f * (arow[L] - arow[i]) <= cap;
-                        if (COUNT) work += fit ? 1 : 0;
-                        else Gs[i] = fit ? (V)(prow[L] - prow[i]) : INF;
-                    }
-                } else if (s > 0) {
-                    for (int i = s + lane; i <= ihi; i += 64) {
-                        const int jl = compute_only ? jhi : mem_limit(wrow, arow, f, cap, i, jhi);
-                        if (COUNT) { work += (unsigned long long)(jl - i); continue; }
-                        const V pi = prow[i];
-                        V acc = INF;
-                        for (int j = i + 1; j <= jl; j++) {
-                            const V tt = prow[j] - pi + p2p;
-                            const V gn = Gn[j];
-                            const V c = tt > gn ? tt : gn;
-                            acc = c < acc ? c : acc;
+            while (todo) {
+                const int key = wave_min(((todo >> lane) & 1) ? key_k : 0x7FFFFFFF);
+                const uint64_t cls = __ballot(lane < A.n_m && key_k == key) & todo;
+                todo &= ~cls;
+
+                // ---------------- PartitionLayers: suffix min-max DP, stages S-1 .. 0
+                const int R = L + 1;
+                auto lim_row = [&](int s) {                 // memory limits of stage s at this class
+                    const int f = (S - s) < key ? (S - s) : key;
+                    return P.mem_lim + rl32(x.lrow, s) + (size_t)(f - 1) * R;
+                };
+                RowRegs rr;
+                fetch_rows(rr, time_tab + rl32(x.trow, S - 1), P.pre_moe, lim_row(S - 1), L, lane, !compute_only);
+                V Bv = INF;
+                for (int s = S - 1; s >= 0; s--) {
+                    const int64_t a2a = rl64(x.a2a, s);
+                    const V p2p = (V)rl64(x.p2p, s);
+                    const int jhi = L - (S - 1 - s);
+                    const int ihi = (s == 0) ? 0 : L - (S - s);
+                    V2 *Xs = X + (size_t)s * gs;
+                    // commit the fetched rows of stage s to LDS: the time prefix, and
+                    // the last admissible end of every row (memory limit, and room
+                    // for one layer per later stage)
+                    uint8_t *Js = J + (size_t)s * gs;
+#pragma unroll
+                    for (int q = 0; q < kRowSlots; q++) {
+                        const int j = lane + 64 * q;
+                        if (j <= L) {
+                            ((V *)&Xs[j])[0] = (V)(rr.t[q] + a2a * rr.m[q]);
+                            Js[j] = (uint8_t)(rr.l[q] < jhi ? rr.l[q] : jhi);
                         }
-                        Gs[i] = acc;
                     }
-                } else {                                   // stage 0: row 0 only, lanes split the ends
-                    const int jl = compute_only ? jhi : mem_limit(wrow, arow, f, cap, 0, jhi);
-                    if (COUNT) {
-                        if (lane == 0) work += (unsigned long long)jl;
-                    } else {
-                        V acc = INF;
-                        for (int j = 1 + lane; j <= jl; j += 64) {
-                            const V tt = prow[j] - prow[0] + p2p;
-                            const V gn = Gn[j];
-                            const V c = tt > gn ? tt : gn;
-                            acc = c < acc ? c : acc;
+                    if (s > 0) fetch_rows(rr, time_tab + rl32(x.trow, s - 1), P.pre_moe, lim_row(s - 1), L, lane, !compute_only);
+                    wave_sync();
+                    if (s == S - 1) {
+                        // last stage: its rows must end at L
+                        for (int i = s + lane; i <= ihi; i += 64) {
+                            const bool fit = Js[i] == L;
+                            if (COUNT) {
+                                work += fit ? 1 : 0;
+                            } else {
+                                const V gv = fit ? (V)(((V *)&Xs[L])[0] - ((V *)&Xs[i])[0]) : INF;
+                                if (s > 0) ((V *)&X[(size_t)(s - 1) * gs + i])[1] = gv;
+                                else Bv = gv;                   // S = 1: row 0, lane 0
+                            }
                         }
-                        acc = wave_min(acc);
-                        if (lane == 0) Gs[0] = acc;
+                    } else if (s > 0) {
+                        // rows of a middle stage: lane = row i relaxes its admissible ends
+                        // (i, jl], four per step (X is padded by four entries)
+                        V2 *Xp = X + (size_t)(s - 1) * gs;
+                        for (int i = s + lane; i <= ihi; i += 64) {
+                            const int jl = Js[i];
+                            if (COUNT) {
+                                work += (unsigned long long)(jl - i);
+                                continue;
+                            }
+                            const V pi = ((V *)&Xs[i])[0] - p2p;        // T(s,i,j) = P_s[j] - pi
+                            V acc = INF;
+                            for (int j = i + 1; j <= jl; j += 4) {
+                                const int rem = jl - j;                  // ends beyond j still admissible
+                                const V2 a = Xs[j], b = Xs[j + 1], c = Xs[j + 2], d = Xs[j + 3];
+                                const V ta = a.x - pi, tb = b.x - pi, tc = c.x - pi, td = d.x - pi;
+                                const V ca = ta > a.y ? ta : a.y;
+                                const V cb = rem >= 1 ? (tb > b.y ? tb : b.y) : INF;
+                                const V cc = rem >= 2 ? (tc > c.y ? tc : c.y) : INF;
+                                const V cd = rem >= 3 ? (td > d.y ? td : d.y) : INF;
+                                const V m1 = ca < cb ? ca : cb, m2 = cc < cd ? cc : cd;
+                                const V m3 = m1 < m2 ? m1 : m2;
+                                acc = m3 < acc ? m3 : acc;
+                            }
+                            ((V *)&Xp[i])[1] = acc;
+                        }
+                    } else {
+                        // stage 0 (S > 1): row 0 only; the lanes split its ends
+                        const int jl = Js[0];
+                        if (COUNT) {
+                            if (lane == 0) work += (unsigned long long)jl;
+                        } else {
+                            const V pi = ((V *)&Xs[0])[0] - p2p;
+                            V acc = INF;
+                            for (int j = 1 + lane; j <= jl; j += 64) {
+                                const V2 a = Xs[j];
+                                const V ta = a.x - pi;
+                                const V ca = ta > a.y ? ta : a.y;
+                                acc = ca < acc ? ca : acc;
+                            }
+                            Bv = wave_min(acc);
+                        }
                     }
+                    wave_sync();
                 }
-                wave_sync();
-            }
-            if (COUNT) continue;
+                if (COUNT) continue;
+                if (S == 1) Bv = (V)rl64((int64_t)Bv, 0);      // computed by lane 0 only
+                if (Bv == INF) {                              // no split fits memory
+                    if ((cls >> lane) & 1) r_oom = true;
+                    continue;
+                }
+                const uint64_t B = (uint64_t)Bv;
+                const uint64_t B24 = F32 ? rne24(B) : B;      // fp32 bottleneck, as an exact integer
 
-            const V Bv = G[0];
-            if (Bv == INF) {                               // no split fits memory
+                // ---------------- canonical reconstruction: smallest admissible end per stage
+                int cs = 0, my_start = 0, my_end = 0;
+                for (int s = 0; s < S; s++) {
+                    const V2 *Xs = X + (size_t)s * gs;
+                    const V pc = ((const V *)&Xs[cs])[0] - (V)rl64(x.p2p, s);
+                    const int jl = J[(size_t)s * gs + cs];
+                    int found = -1;
+                    for (int base = cs + 1; base <= jl && found < 0; base += 64) {
+                        const int j = base + lane;
+                        bool ok = false;
+                        if (j <= jl) {
+                            const V2 a = Xs[j];
+                            const uint64_t T = (uint64_t)(V)(a.x - pc);
+                            bool rest_ok;                     // the later stages complete within B*
+                            if (s == S - 1) rest_ok = j == L;
+                            else rest_ok = a.y != INF && (F32 ? rne24((uint64_t)a.y) <= B24 : (uint64_t)a.y <= B);
+                            ok = rest_ok && (F32 ? rne24(T) <= B24 : T <= B);
+                        }
+                        const uint64_t bal = __ballot(ok);
+                        if (bal) found = base + __ffsll((unsigned long long)bal) - 1;
+                    }
+                    // an end always exists (G[s][cs] <= B* has a witness); the clamp
+                    // only keeps indexing in bounds should that ever fail
+                    if (found < 0) found = jl;
+                    if (lane == s) {
+                        my_start = cs;
+                        my_end = found;
+                    }
+                    cs = found;
+                }
+
+                // ---------------- Evaluate (lane = stage) for the m values of this class
+                const bool act = lane < S;
+                uint64_t Tst = 0;
+                int64_t gsync = 0, wdiff = 0, adiff = 0;
+                if (act) {
+                    const int i = my_start, j = my_end;
+                    const V2 *Xs = X + (size_t)lane * gs;
+                    Tst = (uint64_t)(V)(((const V *)&Xs[j])[0] - ((const V *)&Xs[i])[0] + (V)x.p2p);
+                    wdiff = P.pre_state[x.srow + j] - P.pre_state[x.srow + i];
+                    adiff = P.pre_act[x.arow + j] - P.pre_act[x.arow + i];
+                    const int64_t gd = P.pre_grad[x.arow + j] - P.pre_grad[x.arow + i];
+                    const int64_t gx = P.pre_xgrad[x.srow + j] - P.pre_xgrad[x.srow + i];
+                    gsync = allreduce_ns(gd, D, x.bw_dp) + allreduce_ns(gx, (int64_t)((uint32_t)D / (uint32_t)x.ep), x.bw_dp);
+                }
+                const int64_t sumT = wave_sum(act ? (int64_t)(F32 ? rne24(Tst) : Tst) : int64_t(0));
+                const int64_t maxg = wave_max(gsync);
+                const int64_t maxg_v = F32 ? (int64_t)(rne24((uint64_t)maxg) << (-P.fx_exp)) : maxg;
                 for (uint64_t c = cls; c; c &= c - 1) {
                     const int k = __ffsll((unsigned long long)c) - 1;
-                    if (lane == 0) {
-                        A.status[obase + k] = HEDDLE_S_OOM;
+                    const int64_t Mp = rl32(Mp_k, k);
+                    const int64_t fl = (int64_t)(S - lane) < Mp ? (int64_t)(S - lane) : Mp;
+                    const int64_t mem = act ? wdiff + fl * adiff : 0;
+                    const int64_t peak = wave_max(mem);
+                    const bool any_oom = __ballot(act && mem > x.cap) != 0;
+                    const int64_t iter = (Mp - 1) * (int64_t)B24 + sumT + maxg_v;
+                    if (lane == k) {
+                        r_priced = true;
+                        r_oom = any_oom;
+                        r_peak = peak;
                         if (F32) {
-                            ((float *)A.iter)[obase + k] = __builtin_inff();
-                            ((float *)A.bottleneck)[obase + k] = __builtin_inff();
+                            r_iter_f = exact_float(rne24((uint64_t)iter), P.fx_exp);
+                            r_bn_f = exact_float(B24, P.fx_exp);
                         } else {
-                            ((int64_t *)A.iter)[obase + k] = INT64_MAX;
-                            ((int64_t *)A.bottleneck)[obase + k] = INT64_MAX;
+                            r_iter = iter;
+                            r_bn = (int64_t)B;
                         }
-                        A.peak_mem[obase + k] = INT64_MAX;
                     }
-                    for (int q = lane; q < A.s_max; q += 64) A.layers[(obase + k) * A.s_max + q] = 0;
+                    for (int q = lane; q < A.s_max; q += 64)
+                        A.layers[(obase + k) * A.s_max + q] = q < S ? (uint8_t)(my_end - my_start) : 0;
                 }
-                continue;
-            }
-            const uint64_t B = (uint64_t)Bv;
-            const uint64_t B24 = F32 ? rne24(B) : B;      // fp32 bottleneck, as an exact integer
-
-            // ---------------- canonical reconstruction: smallest feasible end per stage
-            int cs = 0, my_start = 0, my_end = 0;
-            for (int s = 0; s < S; s++) {
-                const int64_t *trow = time_tab + rl32(x.trow, s);
-                const int64_t a2a = rl64(x.a2a, s), p2p = rl64(x.p2p, s), cap = rl64(x.cap, s);
-                const int64_t *wrow = P.pre_state + rl32(x.srow, s);
-                const int64_t *arow = P.pre_act + rl32(x.arow, s);
-                const int64_t f = (S - s) < key ? (S - s) : key;
-                const int jhi = L - (S - 1 - s);
-                const V *Gn = G + (size_t)(s + 1) * gs;
-                const int64_t wi = wrow[cs], ai = arow[cs], ti = trow[cs] + a2a * P.pre_moe[cs];
-                int found = -1;
-                for (int base = cs + 1; base <= jhi && found < 0; base += 64) {
-                    const int j = base + lane;
-                    bool ok = false;
-                    if (j <= jhi) {
-                        const uint64_t T = (uint64_t)(trow[j] + a2a * P.pre_moe[j] - ti + p2p);
-                        bool rest_ok;                      // the later stages complete within B*
-                        if (s == S - 1) {
-                            rest_ok = j == L;
-                        } else {
-                            const V gv = Gn[j];
-                            rest_ok = gv != INF && (F32 ? rne24((uint64_t)gv) <= B24 : (uint64_t)gv <= B);
-                        }
-                        const bool fit = compute_only || (wrow[j] - wi) + f * (arow[j] - ai) <= cap;
-                        ok = fit && rest_ok && (F32 ? rne24(T) <= B24 : T <= B);
-                    }
-                    const uint64_t bal = __ballot(ok);
-                    if (bal) found = base + __ffsll((unsigned long long)bal) - 1;
-                }
-                // an end always exists: the DP value G[s][cs] <= B* has a witness.
-                // The clamp only keeps indexing in bounds should that ever fail.
-                if (found < 0) found = jhi;
-                if (lane == s) { my_start = cs; my_end = found; }
-                cs = found;
-            }
-
-            // ---------------- Evaluate (lane = stage), once per micro-batch count of this class
-            const bool act = lane < S;
-            int64_t Tst = 0, gsync = 0, wdiff = 0, adiff = 0;
-            if (act) {
-                const int i = my_start, j = my_end;
-                const int64_t *trow = time_tab + x.trow;
-                Tst = trow[j] - trow[i] + x.a2a * (P.pre_moe[j] - P.pre_moe[i]) + x.p2p;
-                wdiff = P.pre_state[x.srow + j] - P.pre_state[x.srow + i];
-                adiff = P.pre_act[x.arow + j] - P.pre_act[x.arow + i];
-                const int64_t gd = P.pre_grad[x.arow + j] - P.pre_grad[x.arow + i];
-                const int64_t gx = P.pre_xgrad[x.srow + j] - P.pre_xgrad[x.srow + i];
-                gsync = allreduce_ns(gd, D, x.bw_dp) + allreduce_ns(gx, D / x.ep, x.bw_dp);
-            }
-            const int64_t sumT = wave_sum(act ? (int64_t)(F32 ? rne24((uint64_t)Tst) : (uint64_t)Tst) : int64_t(0));
-            const int64_t maxg = wave_max(gsync);
-            const int64_t maxg_v = F32 ? (int64_t)(rne24((uint64_t)maxg) << (-P.fx_exp)) : maxg;
-            for (uint64_t c = cls; c; c &= c - 1) {
-                const int k = __ffsll((unsigned long long)c) - 1;
-                const int64_t m = rl32(my_m, k);
-                const int64_t Mp = (m + D - 1) / D;
-                const int64_t fl = (int64_t)(S - lane) < Mp ? (int64_t)(S - lane) : Mp;
-                const int64_t mem = act ? wdiff + fl * adiff : 0;
-                const bool oom = act && mem > x.cap;
-                const int64_t peak = wave_max(mem);
-                const bool any_oom = __ballot(oom) != 0;
-                const int64_t iter = (Mp - 1) * (int64_t)B24 + sumT + maxg_v;
-                if (lane == 0) {
-                    A.status[obase + k] = any_oom ? HEDDLE_S_OOM : HEDDLE_S_OK;
-                    if (F32) {
-                        ((float *)A.iter)[obase + k] = exact_float(rne24((uint64_t)iter), P.fx_exp);
-                        ((float *)A.bottleneck)[obase + k] = exact_float(B24, P.fx_exp);
-                    } else {
-                        ((int64_t *)A.iter)[obase + k] = iter;
-                        ((int64_t *)A.bottleneck)[obase + k] = (int64_t)B;
-                    }
-                    A.peak_mem[obase + k] = peak;
-                }
-                for (int q = lane; q < A.s_max; q += 64)
-                    A.layers[(obase + k) * A.s_max + q] = q < S ? (uint8_t)(my_end - my_start) : 0;
             }
         }
+        if (COUNT) continue;
+        if (lane < A.n_m) {
+            const size_t o = obase + lane;
+            A.status[o] = (uint8_t)(x.status != 0 ? x.status : (r_oom ? HEDDLE_S_OOM : HEDDLE_S_OK));
+            if (F32) {
+                ((float *)A.iter)[o] = r_iter_f;
+                ((float *)A.bottleneck)[o] = r_bn_f;
+            } else {
+                ((int64_t *)A.iter)[o] = r_iter;
+                ((int64_t *)A.bottleneck)[o] = r_bn;
+            }
+            A.peak_mem[o] = r_peak;
+        }
+        // zero layer counts of the plans without a split (invalid template, or no split fits)
+        const uint64_t priced = __ballot(r_priced);
+        if (priced != __ballot(lane < A.n_m))
+            for (int q = lane; q < A.n_m * A.s_max; q += 64)
+                if (!((priced >> (q / A.s_max)) & 1)) A.layers[obase * A.s_max + q] = 0;
     }
     if (COUNT) {
         work = wave_sum(work);
@@ -427,10 +466,12 @@ template <class V, bool F32, bool COUNT>
 static int launch_t(const heddle_profile *p, PriceArgs &a, hipStream_t stream)
 {
     const int L = p->dev.L;
-    const int s_cap = a.s_max < L ? a.s_max : L;
-    a.g_stride = L + 1;
-    // DP rows for stages 0..S-1, row S holds the stage's time prefix
-    a.lds_per_wave = (int32_t)(((size_t)(s_cap + 1) * a.g_stride * sizeof(V) + 15) & ~size_t(15));
+    a.s_cap = a.s_max < L ? a.s_max : L;
+    a.g_stride = L + 5;                                       // L + 1 ends and 4 of padding
+    // per wavefront: pairs {P_s, G_{s+1}} and the end limits of every stage
+    const size_t j_off = (size_t)a.s_cap * a.g_stride * 2 * sizeof(V);
+    a.off_j = (int32_t)j_off;
+    a.lds_per_wave = (int32_t)((j_off + (size_t)a.s_cap * a.g_stride + 15) & ~size_t(15));
     int max_lds = 0;
     HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
     int wpb = max_lds / a.lds_per_wave;

@@ -105,9 +105,11 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
     for (int g = 0; g < N; g++) {
         if (d->node_size[g] < 1) return fail(HEDDLE_E_INVAL, "node_size must be >= 1");
         if (d->n_gpus[g] < 0 || d->mem_cap_bytes[g] < 0) return fail(HEDDLE_E_INVAL, "negative GPU count or memory");
-        if (d->intra_bw_MBps[g] < 1) return fail(HEDDLE_E_INVAL, "bandwidths must be >= 1 MB/s");
+        if (d->intra_bw_MBps[g] < 1 || d->intra_bw_MBps[g] > kMaxBandwidth)
+            return fail(HEDDLE_E_INVAL, "bandwidths must be in 1 .. 2^34-1 MB/s");
         for (int h = 0; h < N; h++)
-            if (d->link_bw_MBps[g * N + h] < 1) return fail(HEDDLE_E_INVAL, "bandwidths must be >= 1 MB/s");
+            if (d->link_bw_MBps[g * N + h] < 1 || d->link_bw_MBps[g * N + h] > kMaxBandwidth)
+                return fail(HEDDLE_E_INVAL, "bandwidths must be in 1 .. 2^34-1 MB/s");
     }
     if (d->boundary_bytes < 0 || d->a2a_bytes < 0 || d->boundary_bytes > kLimit62 / 2000 ||
         d->a2a_bytes > kLimit62 / 1000)
@@ -188,6 +190,28 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
             if (gsum + xg > max_grad) max_grad = gsum + xg;
         }
     }
+    // Memory limits of a stage (section 5.2 memory validation): for GPU type g,
+    // TP index k, EP index e and f micro-batches of activations in flight,
+    // lim[g][k][e][f-1][i] is the largest end j >= i such that layers [i, j)
+    // fit one GPU's memory. Ends that fit form a prefix because every term is
+    // non-negative, so one two-pointer sweep per (g, k, e, f) builds a row.
+    const int F = std::min(L, HEDDLE_MAX_STAGES);
+    const size_t lim_entries = (size_t)N * K * E * F * R;
+    if (lim_entries > kMaxLimitTable) return fail(HEDDLE_E_RANGE, "memory-limit table would exceed 256 MB");
+    std::vector<uint8_t> lim_tab(lim_entries);
+    for (int g = 0; g < N; g++)
+        for (int k = 0; k < K; k++)
+            for (int e = 0; e < E; e++)
+                for (int f = 1; f <= F; f++) {
+                    const int64_t *w = &pre_state[(k * E + e) * R], *a = &pre_act[k * R];
+                    uint8_t *row = &lim_tab[((((size_t)g * K + k) * E + e) * F + (f - 1)) * R];
+                    int j = 0;
+                    for (int i = 0; i <= L; i++) {
+                        if (j < i) j = i;
+                        while (j < L && (w[j + 1] - w[i]) + (i128)f * (a[j + 1] - a[i]) <= d->mem_cap_bytes[g]) j++;
+                        row[i] = (uint8_t)j;
+                    }
+                }
     // gradient synchronisation is below 2 * bytes * 1000 / min bandwidth (+1 per ceiling)
     int64_t min_bw = INT64_MAX;
     for (int g = 0; g < N; g++) {
@@ -248,7 +272,8 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
            o_a2a = B.add(a2a_ns), o_a2a_fx = B.add(a2a_fx), o_p2p = B.add(p2p_ns), o_p2p_fx = B.add(p2p_fx),
            o_cap = B.add(d->mem_cap_bytes, (size_t)N * 8), o_node = B.add(d->node_size, (size_t)N * 4),
            o_ngpu = B.add(d->n_gpus, (size_t)N * 4), o_intra = B.add(d->intra_bw_MBps, (size_t)N * 8),
-           o_link = B.add(d->link_bw_MBps, (size_t)N * N * 8), o_epd = B.add(d->ep_degrees, (size_t)E * 4);
+           o_link = B.add(d->link_bw_MBps, (size_t)N * N * 8), o_epd = B.add(d->ep_degrees, (size_t)E * 4),
+           o_lim = B.add(lim_tab);
 
     heddle_profile *p = new (std::nothrow) heddle_profile;
     if (!p) return fail(HEDDLE_E_NOMEM, "host allocation failed");
@@ -278,6 +303,8 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
     dp.intra_bw = (const int64_t *)(base + o_intra);
     dp.link_bw = (const int64_t *)(base + o_link);
     dp.ep_degrees = (const int32_t *)(base + o_epd);
+    dp.mem_lim = (const uint8_t *)(base + o_lim);
+    dp.n_f = F;
     p->dev = dp;
     p->max_stage_ns = (int64_t)max_stage;
     p->max_ar_ns = (int64_t)max_ar;

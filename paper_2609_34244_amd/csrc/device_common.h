@@ -1,0 +1,89 @@
+// Device helpers shared by the pricing kernels (gfx950, wave64).
+#pragma once
+
+#include "exact_math.h"
+#include "heddle_internal.h"
+
+namespace heddle {
+
+// LDS writes of a wavefront become visible to its other lanes
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ int rl32(int v, int lane) { return __builtin_amdgcn_readlane(v, lane); }
+
+__device__ __forceinline__ int64_t rl64(int64_t v, int lane)
+{
+    uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+    uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), lane);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+template <class T> __device__ __forceinline__ T wave_min(T v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        T u = __shfl_xor(v, o);
+        v = u < v ? u : v;
+    }
+    return v;
+}
+
+template <class T> __device__ __forceinline__ T wave_max(T v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        T u = __shfl_xor(v, o);
+        v = u > v ? u : v;
+    }
+    return v;
+}
+
+// Nearest value with at most 24 significant bits (ties to even) of a
+// non-negative integer below 2^63: its fp32 rounding, kept as an exact integer.
+__device__ __forceinline__ uint64_t rne24(uint64_t x)
+{
+    if (x < (1ull << 24)) return x;
+    const int sh = 40 - __clzll(x);            // bits dropped: top bit lands at position 23
+    const uint64_t q = x >> sh, r = x & ((1ull << sh) - 1), half = 1ull << (sh - 1);
+    const uint64_t qr = q + ((r > half || (r == half && (q & 1))) ? 1 : 0);
+    return qr << sh;
+}
+
+// float of an integer with at most 24 significant bits, times 2^e
+__device__ __forceinline__ float exact_float(uint64_t x, int e)
+{
+    if (x == 0) return 0.0f;
+    const int sh = x < (1ull << 24) ? 0 : 40 - __clzll(x);
+    return ldexpf((float)(uint32_t)(x >> sh), sh + e);
+}
+
+// the integer x with x * 2^e == v, for a float v that is such a multiple
+__device__ __forceinline__ uint64_t fixed_of_float(float v, int e)
+{
+    if (v == 0.0f) return 0;
+    int ex;
+    const float fr = frexpf(v, &ex);                         // v = fr * 2^ex, 0.5 <= fr < 1
+    const uint64_t mant = (uint64_t)ldexpf(fr, 24);          // exact 24-bit integer
+    const int sh = ex - 24 - e;
+    return sh >= 0 ? mant << sh : mant >> (-sh);
+}
+
+__device__ __forceinline__ int nibble(uint64_t w, int l) { return (int)((w >> (4 * l)) & 15); }
+
+template <class V> struct Vec2;
+template <> struct Vec2<uint32_t> { typedef uint32_t type __attribute__((ext_vector_type(2))); };
+template <> struct Vec2<uint64_t> { typedef uint64_t type __attribute__((ext_vector_type(2))); };
+template <class V> struct DPInf { static constexpr V value = ~V(0); };
+
+// all-to-all variant of a stage: none (EP = 1), inside one node, across nodes
+__device__ __forceinline__ int a2a_variant(int ep, int tp, int node)
+{
+    return ep == 1 ? kA2ANone : (ep * tp <= node ? kA2AIntra : kA2AInter);
+}
+
+}  // namespace heddle

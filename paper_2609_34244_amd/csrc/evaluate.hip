@@ -1,0 +1,94 @@
+// Evaluate on gfx950: iteration time and per-GPU peak memory of every plan
+// whose split the split kernel found (Heddle, arXiv 2609.34244: the
+// profile-based cost model of section 5.2 and the 1F1B iteration time
+// (M-1) max_s t_s + sum_s t_s + max_s g_s of section 5.3).
+//
+// One lane prices one (template, m) plan, walking its stages: t_s is the
+// stage's time over its layers plus its outbound p2p, g_s the ring
+// all-reduce of its dense gradients over the D replicas plus that of its
+// expert gradients over D / EP replicas, and the memory of stage s holds
+// min(S - s, M_p) micro-batches of activations. Plans without a split keep
+// their status and get INT64_MAX (fp32: +inf) values.
+#include <cstring>
+
+#include "device_common.h"
+
+namespace heddle {
+
+template <bool F32>
+__global__ void __launch_bounds__(256) evaluate_kernel(DevProfile P, PriceArgs A)
+{
+    const int64_t total = A.n * A.n_m;
+    const int L = P.L, R = L + 1, N = P.n_types;
+    for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < total; o += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t t = o / A.n_m;
+        const int k = (int)(o - t * A.n_m);
+        if (A.status[o] != HEDDLE_S_OK) {                     // no split: invalid template or nothing fits
+            if (F32) ((float *)A.iter)[o] = __builtin_inff();
+            else ((int64_t *)A.iter)[o] = INT64_MAX;
+            A.peak_mem[o] = INT64_MAX;
+            continue;
+        }
+        int32_t m = A.m[0];
+        for (int q = 1; q < A.n_m; q++) m = q == k ? A.m[q] : m;
+        const int S = A.n_stages[t];
+        const uint32_t *rec = A.stages + t * A.s_max;
+        const uint8_t *lay = A.layers + o * A.s_max;
+        const int D = (int)(rec[0] >> 16);
+        const int64_t Mp = (int64_t)(((uint32_t)m + (uint32_t)D - 1) / (uint32_t)D);
+        const uint64_t B = F32 ? fixed_of_float(((const float *)A.bottleneck)[o], P.fx_exp)
+                               : (uint64_t)((const int64_t *)A.bottleneck)[o];
+        const uint64_t *rows = P.rows64[F32 ? 1 : 0];
+        uint64_t sumT = 0;
+        int64_t maxg = 0, peak = 0;
+        bool oom = false;
+        int i = 0;
+        uint32_t r_next = rec[0];
+        for (int s = 0; s < S; s++) {
+            const uint32_t r = r_next;
+            if (s + 1 < S) r_next = rec[s + 1];
+            const int g = r & 0xFF, l2tp = (r >> 8) & 15, l2ep = (r >> 12) & 15;
+            const int tp = 1 << l2tp, ep = 1 << l2ep;
+            const int ki = nibble(P.tp_index, l2tp), ei = nibble(P.ep_index, l2ep);
+            const int j = i + lay[s];
+            const int node = P.node_size[g];
+            const uint64_t *prow = rows + ((size_t)(g * P.n_tp + ki) * 3 + a2a_variant(ep, tp, node)) * R;
+            int64_t p2p = 0;
+            if (s + 1 < S) p2p = F32 ? P.p2p_fx[g * N + (int)(r_next & 0xFF)] : P.p2p_ns[g * N + (int)(r_next & 0xFF)];
+            const uint64_t T = prow[j] - prow[i] + (uint64_t)p2p;
+            sumT += F32 ? rne24(T) : T;
+            const int srow = (ki * P.n_ep + ei) * R, arow = ki * R;
+            const int64_t f = (int64_t)(S - s) < Mp ? (int64_t)(S - s) : Mp;
+            const int64_t mem = (P.pre_state[srow + j] - P.pre_state[srow + i]) + f * (P.pre_act[arow + j] - P.pre_act[arow + i]);
+            peak = mem > peak ? mem : peak;
+            oom = oom || mem > P.mem_cap[g];
+            const int64_t bw = (int64_t)tp * D <= node ? P.intra_bw[g] : P.link_bw[g * N + g];
+            const int64_t gsync = allreduce_ns(P.pre_grad[arow + j] - P.pre_grad[arow + i], D, bw) +
+                                  allreduce_ns(P.pre_xgrad[srow + j] - P.pre_xgrad[srow + i], (int64_t)((uint32_t)D / (uint32_t)ep), bw);
+            maxg = gsync > maxg ? gsync : maxg;
+            i = j;
+        }
+        const uint64_t maxg_v = F32 ? rne24((uint64_t)maxg) << (-P.fx_exp) : (uint64_t)maxg;
+        const uint64_t iter = (uint64_t)(Mp - 1) * B + sumT + maxg_v;
+        if (F32) ((float *)A.iter)[o] = exact_float(rne24(iter), P.fx_exp);
+        else ((int64_t *)A.iter)[o] = (int64_t)iter;
+        A.peak_mem[o] = peak;
+        if (oom) A.status[o] = HEDDLE_S_OOM;                  // compute-only splits that do not fit
+    }
+}
+
+int launch_evaluate(const heddle_profile *p, const PriceArgs &a, hipStream_t stream)
+{
+    const int64_t total = a.n * a.n_m;
+    if (total == 0) return HEDDLE_OK;
+    const int64_t want = (total + 255) / 256;
+    const int blocks = (int)(want < 65536 ? want : 65536);
+    if (a.flags & HEDDLE_F_FP32)
+        hipLaunchKernelGGL(evaluate_kernel<true>, dim3(blocks), dim3(256), 0, stream, p->dev, a);
+    else
+        hipLaunchKernelGGL(evaluate_kernel<false>, dim3(blocks), dim3(256), 0, stream, p->dev, a);
+    HEDDLE_HIP(hipGetLastError());
+    return HEDDLE_OK;
+}
+
+}  // namespace heddle

@@ -48,6 +48,11 @@ struct DevProfile {
     const int32_t *ep_degrees;       // [n_ep]
     const uint8_t *mem_lim;          // [n_types][n_tp][n_ep][n_f][L+1] largest end that fits from row i
     int32_t n_f;                     // in-flight counts covered by mem_lim: 1 .. min(L, 64)
+    // [n_types][n_tp][3][L+1] stage time prefix (layer costs + all-to-all of the
+    // variant); index 0: int64 ns, 1: fp32 image in fixed point; the 32-bit
+    // copies exist only when the range proof allows narrowing
+    const uint64_t *rows64[2];
+    const uint32_t *rows32[2];
 };
 
 }  // namespace heddle
@@ -90,12 +95,13 @@ struct PriceArgs {
     int32_t g_stride;                // LDS entries per DP table row (L + 1)
     int32_t s_cap;                   // DP table rows: min(s_max, L)
     int32_t lds_per_wave;            // bytes of one wavefront's LDS region
-    int32_t off_j;                   // byte offset of the end-limit table
+    int32_t off_g, off_j;            // byte offsets of the DP rows and of the end-limit table
 };
 
 int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,
                         const uint32_t *d_stages, const int32_t *h_m, int32_t n_m, uint32_t flags);
 int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool count_only);
+int launch_evaluate(const heddle_profile *p, const PriceArgs &a, hipStream_t stream);
 int launch_argmin(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t flags, const void *d_iter,
                   const uint8_t *d_status, int64_t *h_best_template, int32_t *h_best_m_index,
                   void *h_best_iter, hipStream_t stream);

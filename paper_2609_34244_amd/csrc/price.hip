@@ -1,119 +1,45 @@
-// Batched plan pricing on gfx950: template decode and validation,
-// PartitionLayers (exact min-max layer split), canonical reconstruction and
-// Evaluate (1F1B iteration time and per-GPU peak memory).
+// Batched plan pricing on gfx950, split kernel: template decode and
+// validation, PartitionLayers (exact min-max layer split) and its canonical
+// reconstruction. Evaluate runs in evaluate.hip on the split found here.
 //
 // Method: Heddle (arXiv 2609.34244). The layer split is the PartitionLayers
 // step of the planners' nested-loop backbone (section 3.1), aware of per-stage
 // GPU speed (the straggler criticism of speed-blind splits in the same
-// section) and of memory (section 5.2, memory validation). Evaluate is the
-// profile-based cost model of section 5.2 with the 1F1B iteration time
-// (M-1) max_s t_s + sum_s t_s + max_s g_s of section 5.3.
+// section) and of memory (section 5.2, memory validation).
 //
 // Recurrence (suffix form): G[s][i] is the smallest achievable bottleneck
 // when stages s..S-1 hold layers [i, L):
 //   G[S-1][i] = T(S-1, i, L)                                    if it fits
-//   G[s][i]   = min over i < j <= jlim_s(i) of max(T(s,i,j), G[s+1][j])
-// with jlim_s(i) the largest end that fits memory (and leaves one layer per
-// later stage); B* = G[0][0]. Memory grows with j for fixed i, so the
-// feasible ends of a row form the prefix (i, jlim_s(i)].
+//   G[s][i]   = min over i < j <= jl_s(i) of max(T(s,i,j), G[s+1][j])
+// with jl_s(i) the last admissible end of row i: the memory limit (a profile
+// table indexed by GPU type, TP, EP and in-flight count) capped so that every
+// later stage keeps one layer. B* = G[0][0]. T(s,i,j) = P_s[j] - P_s[i] + p2p_s
+// with P_s the stage's time prefix (layer costs + MoE all-to-all), also a
+// profile table.
 //
-// Mapping. One wavefront prices one template at a time (grid-stride over
-// templates). Lanes are pipeline stages for decode, validation and Evaluate,
-// and split rows i of one stage during the DP, each lane walking its own ends
-// j. Per wavefront LDS holds, for every stage s, the pairs
-//   X[s][j] = { P_s[j], G[s+1][j] }
-// where P_s is the stage's time prefix (layer costs + MoE all-to-all), so one
-// 64-bit LDS read feeds one relaxation (sub, max, min); the stage's memory
-// prefix U; and the memory limits jlim_s(i) as bytes, which the
-// reconstruction reuses. The profile rows of the next stage are fetched from
-// global memory into registers while the current stage relaxes.
+// Mapping. One wavefront splits one template at a time (grid-stride over
+// templates). Lanes are stages for decode and validation, and split rows i
+// during the DP: a row takes one lane and walks its ends four at a time; the
+// rows of a stage's ragged last slot take several lanes each, which stride
+// over the ends and combine with cross-lane minima. Per wavefront, LDS holds
+// the pairs W[j] = {P_s[j], G[s+1][j]} of the stage being relaxed, so one
+// 64-bit LDS read feeds one relaxation (sub, max, min), and, for every stage,
+// the DP row G[s][.] and the end limits J[s][.] that the reconstruction
+// needs. The profile rows of stage s-1 are fetched into registers while
+// stage s relaxes.
 #include <cstring>
 
-#include "exact_math.h"
-#include "heddle_internal.h"
+#include "device_common.h"
 
 namespace heddle {
-
-// ----------------------------------------------------------------- helpers
-
-__device__ __forceinline__ void wave_sync()
-{
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-__device__ __forceinline__ int rl32(int v, int lane) { return __builtin_amdgcn_readlane(v, lane); }
-
-__device__ __forceinline__ int64_t rl64(int64_t v, int lane)
-{
-    uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
-    uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), lane);
-    return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
-template <class T> __device__ __forceinline__ T wave_min(T v)
-{
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        T u = __shfl_xor(v, o);
-        v = u < v ? u : v;
-    }
-    return v;
-}
-
-template <class T> __device__ __forceinline__ T wave_max(T v)
-{
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        T u = __shfl_xor(v, o);
-        v = u > v ? u : v;
-    }
-    return v;
-}
-
-template <class T> __device__ __forceinline__ T wave_sum(T v)
-{
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    return v;
-}
-
-// Nearest value with at most 24 significant bits (ties to even) of a
-// non-negative integer below 2^63: its fp32 rounding, kept as an exact integer.
-__device__ __forceinline__ uint64_t rne24(uint64_t x)
-{
-    if (x < (1ull << 24)) return x;
-    const int sh = 40 - __clzll(x);            // bits dropped: top bit lands at position 23
-    const uint64_t q = x >> sh, r = x & ((1ull << sh) - 1), half = 1ull << (sh - 1);
-    const uint64_t qr = q + ((r > half || (r == half && (q & 1))) ? 1 : 0);
-    return qr << sh;
-}
-
-// float of an integer with at most 24 significant bits, times 2^e
-__device__ __forceinline__ float exact_float(uint64_t x, int e)
-{
-    if (x == 0) return 0.0f;
-    const int sh = x < (1ull << 24) ? 0 : 40 - __clzll(x);
-    return ldexpf((float)(uint32_t)(x >> sh), sh + e);
-}
-
-__device__ __forceinline__ int nibble(uint64_t w, int l) { return (int)((w >> (4 * l)) & 15); }
-
-template <class V> struct Vec2;
-template <> struct Vec2<uint32_t> { typedef uint32_t type __attribute__((ext_vector_type(2))); };
-template <> struct Vec2<uint64_t> { typedef uint64_t type __attribute__((ext_vector_type(2))); };
-template <class V> struct DPInf { static constexpr V value = ~V(0); };
 
 // Per-lane (lane = stage s) decoded record and stage constants.
 struct StageInfo {
     int status;              // uniform: HEDDLE_S_* of the template (0 if valid)
     int S, D;                // uniform
-    int tp, ep;
-    int64_t a2a, p2p;        // all-to-all per MoE layer, outbound p2p (ns, or fixed point for fp32)
-    int64_t cap, bw_dp;
-    int trow, srow, arow;    // offsets of the stage's rows in the prefix tables
+    int prow;                // offset of the stage's time-prefix row
     int lrow;                // offset of the stage's memory-limit rows (in-flight count 1)
+    int64_t p2p;             // outbound p2p (ns, or fixed point for fp32)
 };
 
 // Template decode and validation (feasibility masks of section 5.1, exact
@@ -127,92 +53,99 @@ __device__ StageInfo decode(const DevProfile &P, const PriceArgs &A, int64_t t, 
     x.S = A.n_stages[t];
     x.status = 0;
     x.D = 1;
+    x.prow = x.lrow = 0;
+    x.p2p = 0;
     const bool act = lane < x.S && lane < A.s_max;
     const uint32_t rec = act ? A.stages[t * A.s_max + lane] : 0u;
     const int g = rec & 0xFF;
     const int l2tp = (rec >> 8) & 15, l2ep = (rec >> 12) & 15;
     const int dpv = (int)(rec >> 16);
-    x.tp = 1 << l2tp;
-    x.ep = 1 << l2ep;
+    const int tp = 1 << l2tp, ep = 1 << l2ep;
     const int ki = nibble(P.tp_index, l2tp), ei = nibble(P.ep_index, l2ep);
     const int gc = g < N ? g : N - 1;                          // clamped for speculative reads
     const int gn = __shfl(gc, lane + 1 < 64 ? lane + 1 : 63);
     const int node = P.node_size[gc];
     const int prof = P.profiled[gc * P.n_tp + ki];
     const int ngpu = P.n_gpus[gc];
-    const int var = x.ep == 1 ? kA2ANone : (x.ep * x.tp <= node ? kA2AIntra : kA2AInter);
-    const int64_t a2a = F32 ? P.a2a_fx[gc * 3 + var] : P.a2a_ns[gc * 3 + var];
     const int64_t p2p = F32 ? P.p2p_fx[gc * N + gn] : P.p2p_ns[gc * N + gn];
-    const int64_t cap = P.mem_cap[gc], intra = P.intra_bw[gc], self = P.link_bw[gc * N + gc];
 
-    x.a2a = x.p2p = x.cap = x.bw_dp = 0;
-    x.trow = x.srow = x.arow = x.lrow = 0;
     if (x.S < 1 || x.S > A.s_max || x.S > L) { x.status = HEDDLE_S_BAD_SHAPE; return x; }
     if (__ballot(act && g >= N)) { x.status = HEDDLE_S_BAD_TYPE; return x; }
-    if (__ballot(act && (!((P.tp_present >> l2tp) & 1) || x.tp > node))) { x.status = HEDDLE_S_BAD_TP; return x; }
+    if (__ballot(act && (!((P.tp_present >> l2tp) & 1) || tp > node))) { x.status = HEDDLE_S_BAD_TP; return x; }
     if (__ballot(act && !prof)) { x.status = HEDDLE_S_UNPROFILED; return x; }
     x.D = rl32(dpv, 0);
     if (__ballot(act && (dpv < 1 || dpv != x.D))) { x.status = HEDDLE_S_BAD_DP; return x; }
-    if (__ballot(act && (!((P.ep_present >> l2ep) & 1) || ((uint32_t)x.D % (uint32_t)x.ep) != 0))) {
+    if (__ballot(act && (!((P.ep_present >> l2ep) & 1) || ((uint32_t)x.D % (uint32_t)ep) != 0))) {
         x.status = HEDDLE_S_BAD_EP;
         return x;
     }
     int used = 0;                                              // this lane's type: sum of TP over its stages
     for (int s2 = 0; s2 < x.S; s2++)
-        if (rl32(g, s2) == g) used += rl32(x.tp, s2);
+        if (rl32(g, s2) == g) used += rl32(tp, s2);
     if (__ballot(act && (int64_t)used * x.D > ngpu)) { x.status = HEDDLE_S_OVERSUBSCRIBED; return x; }
 
     if (act) {
-        x.a2a = a2a;
-        x.p2p = lane < x.S - 1 ? p2p : 0;
-        x.cap = cap;
-        x.bw_dp = (int64_t)x.tp * x.D <= node ? intra : self;
-        x.trow = (g * P.n_tp + ki) * R;
-        x.srow = (ki * P.n_ep + ei) * R;
-        x.arow = ki * R;
+        x.prow = ((g * P.n_tp + ki) * 3 + a2a_variant(ep, tp, node)) * R;
         x.lrow = ((g * P.n_tp + ki) * P.n_ep + ei) * P.n_f * R;
+        x.p2p = lane < x.S - 1 ? p2p : 0;
     }
     return x;
 }
 
-// Profile rows of one stage, fetched into registers ahead of use: the time
-// prefix, the MoE prefix count and the memory limits of every row.
+// Profile rows of one stage, fetched into registers ahead of use.
 constexpr int kRowSlots = 4;                       // (L + 1) <= 256 entries, 64 per slot
-struct RowRegs {
-    int64_t t[kRowSlots];
-    int32_t m[kRowSlots];
-    int32_t l[kRowSlots];
+template <class V> struct RowRegs {
+    V p[kRowSlots];                                // time prefix
+    int32_t l[kRowSlots];                          // last end that fits memory, from each row
 };
 
-__device__ __forceinline__ void fetch_rows(RowRegs &r, const int64_t *trow, const int32_t *moe,
-                                           const uint8_t *lrow, int L, int lane, bool need_mem)
+template <class V>
+__device__ __forceinline__ void fetch_rows(RowRegs<V> &r, const V *prow, const uint8_t *lrow, int L, int lane,
+                                           bool need_mem)
 {
 #pragma unroll
     for (int q = 0; q < kRowSlots; q++) {
         const int j = lane + 64 * q;
         if (j <= L) {
-            r.t[q] = trow[j];
-            r.m[q] = moe[j];
+            r.p[q] = prow[j];
             r.l[q] = need_mem ? lrow[j] : L;
         }
     }
 }
 
-// ------------------------------------------------------------ price kernel
+template <class V> __device__ __forceinline__ const V *stage_rows(const DevProfile &P, bool f32);
+template <> __device__ __forceinline__ const uint32_t *stage_rows<uint32_t>(const DevProfile &P, bool f32)
+{
+    return P.rows32[f32 ? 1 : 0];
+}
+template <> __device__ __forceinline__ const uint64_t *stage_rows<uint64_t>(const DevProfile &P, bool f32)
+{
+    return P.rows64[f32 ? 1 : 0];
+}
+
+// relaxation of one end: max(T(s,i,j), G[s+1][j]) with T = P_s[j] - pi
+template <class V, class V2> __device__ __forceinline__ V relax(const V2 &a, V pi)
+{
+    const V t = a.x - pi;
+    return t > a.y ? t : a.y;
+}
+
+// ------------------------------------------------------------ split kernel
 
 template <class V, bool F32, bool COUNT>
-__global__ void __launch_bounds__(256) price_kernel(DevProfile P, PriceArgs A)
+__global__ void __launch_bounds__(256, sizeof(V) == 4 ? 5 : 4) split_kernel(DevProfile P, PriceArgs A)
 {
     typedef typename Vec2<V>::type V2;
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63, wib = threadIdx.x >> 6, wpb = blockDim.x >> 6;
-    const int L = P.L, gs = A.g_stride;
+    const int L = P.L, R = L + 1, gs = A.g_stride;
     const bool compute_only = (A.flags & HEDDLE_F_COMPUTE_ONLY) != 0;
     const V INF = DPInf<V>::value;
     unsigned char *wave_lds = smem + (size_t)wib * A.lds_per_wave;
-    V2 *X = (V2 *)wave_lds;                                   // [s_cap][gs] pairs {P_s, G_{s+1}}
-    uint8_t *J = wave_lds + A.off_j;                          // [s_cap][gs] memory limits
-    const int64_t *time_tab = F32 ? P.pre_time_fx : P.pre_time;
+    V2 *W = (V2 *)wave_lds;                                   // [gs] pairs {P_s, G_{s+1}} of the current stage
+    V *G = (V *)(wave_lds + A.off_g);                         // [s_cap][gs] DP rows
+    uint8_t *J = wave_lds + A.off_j;                          // [s_cap][gs] last admissible ends
+    const V *rows = stage_rows<V>(P, F32);
 
     int my_m = 1;                                             // lane k: the k-th micro-batch count
     for (int k = 0; k < A.n_m; k++) my_m = lane == k ? A.m[k] : my_m;
@@ -222,10 +155,8 @@ __global__ void __launch_bounds__(256) price_kernel(DevProfile P, PriceArgs A)
         const StageInfo x = decode<F32>(P, A, t, lane);
         const int S = x.S;
         const size_t obase = (size_t)t * A.n_m;
-        // results of m index k live in lane k until the end of the template
-        bool r_priced = false, r_oom = false;
-        int64_t r_iter = INT64_MAX, r_bn = INT64_MAX, r_peak = INT64_MAX;
-        float r_iter_f = __builtin_inff(), r_bn_f = __builtin_inff();
+        bool r_split = false;                                 // lane k: a split was found for m index k
+        V r_b = INF;
 
         if (x.status == 0) {
             const int D = x.D;
@@ -238,35 +169,36 @@ __global__ void __launch_bounds__(256) price_kernel(DevProfile P, PriceArgs A)
                 const int key = wave_min(((todo >> lane) & 1) ? key_k : 0x7FFFFFFF);
                 const uint64_t cls = __ballot(lane < A.n_m && key_k == key) & todo;
                 todo &= ~cls;
-
-                // ---------------- PartitionLayers: suffix min-max DP, stages S-1 .. 0
-                const int R = L + 1;
-                auto lim_row = [&](int s) {                 // memory limits of stage s at this class
-                    const int f = (S - s) < key ? (S - s) : key;
+                auto lim_row = [&](int s) {                   // memory limits of stage s in this class
+                    int f = (S - s) < key ? (S - s) : key;
+                    f = f < 1 ? 1 : f;                        // compute-only: not read
                     return P.mem_lim + rl32(x.lrow, s) + (size_t)(f - 1) * R;
                 };
-                RowRegs rr;
-                fetch_rows(rr, time_tab + rl32(x.trow, S - 1), P.pre_moe, lim_row(S - 1), L, lane, !compute_only);
+
+                // ---------------- PartitionLayers: suffix min-max DP, stages S-1 .. 0
+                RowRegs<V> rr;
+                fetch_rows<V>(rr, rows + rl32(x.prow, S - 1), lim_row(S - 1), L, lane, !compute_only);
                 V Bv = INF;
                 for (int s = S - 1; s >= 0; s--) {
-                    const int64_t a2a = rl64(x.a2a, s);
                     const V p2p = (V)rl64(x.p2p, s);
-                    const int jhi = L - (S - 1 - s);
+                    const int jhi = L - (S - 1 - s);              // leaves one layer per later stage
                     const int ihi = (s == 0) ? 0 : L - (S - s);
-                    V2 *Xs = X + (size_t)s * gs;
-                    // commit the fetched rows of stage s to LDS: the time prefix, and
-                    // the last admissible end of every row (memory limit, and room
-                    // for one layer per later stage)
+                    V2 *Xs = W;
+                    V *Gs = G + (size_t)s * gs;
+                    const V *Gn = G + (size_t)(s + 1) * gs;            // row s + 1 (not read for s = S-1)
                     uint8_t *Js = J + (size_t)s * gs;
 #pragma unroll
                     for (int q = 0; q < kRowSlots; q++) {
                         const int j = lane + 64 * q;
                         if (j <= L) {
-                            ((V *)&Xs[j])[0] = (V)(rr.t[q] + a2a * rr.m[q]);
+                            V2 w;
+                            w.x = rr.p[q];
+                            w.y = s < S - 1 ? Gn[j] : INF;
+                            Xs[j] = w;
                             Js[j] = (uint8_t)(rr.l[q] < jhi ? rr.l[q] : jhi);
                         }
                     }
-                    if (s > 0) fetch_rows(rr, time_tab + rl32(x.trow, s - 1), P.pre_moe, lim_row(s - 1), L, lane, !compute_only);
+                    if (s > 0) fetch_rows<V>(rr, rows + rl32(x.prow, s - 1), lim_row(s - 1), L, lane, !compute_only);
                     wave_sync();
                     if (s == S - 1) {
                         // last stage: its rows must end at L
@@ -275,159 +207,146 @@ __global__ void __launch_bounds__(256) price_kernel(DevProfile P, PriceArgs A)
                             if (COUNT) {
                                 work += fit ? 1 : 0;
                             } else {
-                                const V gv = fit ? (V)(((V *)&Xs[L])[0] - ((V *)&Xs[i])[0]) : INF;
-                                if (s > 0) ((V *)&X[(size_t)(s - 1) * gs + i])[1] = gv;
+                                const V gv = fit ? (V)(Xs[L].x - Xs[i].x) : INF;
+                                if (s > 0) Gs[i] = gv;
                                 else Bv = gv;                   // S = 1: row 0, lane 0
                             }
                         }
-                    } else if (s > 0) {
-                        // rows of a middle stage: lane = row i relaxes its admissible ends
-                        // (i, jl], four per step (X is padded by four entries)
-                        V2 *Xp = X + (size_t)(s - 1) * gs;
-                        for (int i = s + lane; i <= ihi; i += 64) {
+                        if (S == 1) Bv = (V)rl64((int64_t)Bv, 0);
+                    } else {
+                        // rows [s, ihi] (stage 0: row 0 only); whole slots of 64 rows
+                        // take one lane per row, the ragged last slot several
+                        int base = s;
+                        for (; base + 63 <= ihi; base += 64) {
+                            const int i = base + lane;
                             const int jl = Js[i];
                             if (COUNT) {
                                 work += (unsigned long long)(jl - i);
                                 continue;
                             }
-                            const V pi = ((V *)&Xs[i])[0] - p2p;        // T(s,i,j) = P_s[j] - pi
+                            const V pi = Xs[i].x - p2p;                 // T(s,i,j) = P_s[j] - pi
                             V acc = INF;
-                            for (int j = i + 1; j <= jl; j += 4) {
-                                const int rem = jl - j;                  // ends beyond j still admissible
+                            int j = i + 1;
+                            for (; j + 3 <= jl; j += 4) {
                                 const V2 a = Xs[j], b = Xs[j + 1], c = Xs[j + 2], d = Xs[j + 3];
-                                const V ta = a.x - pi, tb = b.x - pi, tc = c.x - pi, td = d.x - pi;
-                                const V ca = ta > a.y ? ta : a.y;
-                                const V cb = rem >= 1 ? (tb > b.y ? tb : b.y) : INF;
-                                const V cc = rem >= 2 ? (tc > c.y ? tc : c.y) : INF;
-                                const V cd = rem >= 3 ? (td > d.y ? td : d.y) : INF;
+                                const V ca = relax<V>(a, pi), cb = relax<V>(b, pi);
+                                const V cc = relax<V>(c, pi), cd = relax<V>(d, pi);
                                 const V m1 = ca < cb ? ca : cb, m2 = cc < cd ? cc : cd;
                                 const V m3 = m1 < m2 ? m1 : m2;
                                 acc = m3 < acc ? m3 : acc;
                             }
-                            ((V *)&Xp[i])[1] = acc;
-                        }
-                    } else {
-                        // stage 0 (S > 1): row 0 only; the lanes split its ends
-                        const int jl = Js[0];
-                        if (COUNT) {
-                            if (lane == 0) work += (unsigned long long)jl;
-                        } else {
-                            const V pi = ((V *)&Xs[0])[0] - p2p;
-                            V acc = INF;
-                            for (int j = 1 + lane; j <= jl; j += 64) {
-                                const V2 a = Xs[j];
-                                const V ta = a.x - pi;
-                                const V ca = ta > a.y ? ta : a.y;
-                                acc = ca < acc ? ca : acc;
+                            if (j <= jl) {                               // 1 to 3 ends left (X padded by 4)
+                                const int rem = jl - j;
+                                const V2 a = Xs[j], b = Xs[j + 1], c = Xs[j + 2];
+                                const V ca = relax<V>(a, pi);
+                                const V cb = rem >= 1 ? relax<V>(b, pi) : INF;
+                                const V cc = rem >= 2 ? relax<V>(c, pi) : INF;
+                                const V m1 = ca < cb ? ca : cb;
+                                const V m3 = m1 < cc ? m1 : cc;
+                                acc = m3 < acc ? m3 : acc;
                             }
-                            Bv = wave_min(acc);
+                            Gs[i] = acc;
+                        }
+                        if (base <= ihi) {
+                            // r < 64 rows left: k lanes per row (k the largest power of two
+                            // with k * r <= 64), each striding over the row's ends by k
+                            const int r = ihi - base + 1;
+                            const int k = 1 << (31 - __clz(64 / r));
+                            const int part = lane & (k - 1);
+                            const int i = base + lane / k;
+                            const bool row_ok = i <= ihi;
+                            const int jl = row_ok ? Js[i] : 0;
+                            if (COUNT) {
+                                if (row_ok && part == 0) work += (unsigned long long)(jl - i);
+                            } else {
+                                const V pi = row_ok ? Xs[i].x - p2p : V(0);
+                                V acc = INF;
+                                for (int j = i + 1 + part; j <= jl; j += k) {
+                                    const V c = relax<V>(Xs[j], pi);
+                                    acc = c < acc ? c : acc;
+                                }
+                                for (int o = 1; o < k; o <<= 1) {
+                                    const V u = __shfl_xor(acc, o);
+                                    acc = u < acc ? u : acc;
+                                }
+                                if (s == 0) Bv = acc;                    // one row, all lanes hold its minimum
+                                else if (row_ok && part == 0) Gs[i] = acc;
+                            }
                         }
                     }
                     wave_sync();
                 }
                 if (COUNT) continue;
-                if (S == 1) Bv = (V)rl64((int64_t)Bv, 0);      // computed by lane 0 only
-                if (Bv == INF) {                              // no split fits memory
-                    if ((cls >> lane) & 1) r_oom = true;
-                    continue;
-                }
+                if (Bv == INF) continue;                      // no split fits memory
                 const uint64_t B = (uint64_t)Bv;
                 const uint64_t B24 = F32 ? rne24(B) : B;      // fp32 bottleneck, as an exact integer
 
                 // ---------------- canonical reconstruction: smallest admissible end per stage
+                // (time prefixes from the profile's stage rows, DP rows and limits from LDS)
                 int cs = 0, my_start = 0, my_end = 0;
                 for (int s = 0; s < S; s++) {
-                    const V2 *Xs = X + (size_t)s * gs;
-                    const V pc = ((const V *)&Xs[cs])[0] - (V)rl64(x.p2p, s);
-                    const int jl = J[(size_t)s * gs + cs];
+                    const V *prow = rows + rl32(x.prow, s);
+                    const V *Gn = G + (size_t)(s + 1) * gs;
+                    const uint8_t *Js = J + (size_t)s * gs;
+                    const V p2p = (V)rl64(x.p2p, s);
                     int found = -1;
-                    for (int base = cs + 1; base <= jl && found < 0; base += 64) {
+                    for (int base = cs + 1; found < 0; base += 64) {
                         const int j = base + lane;
+                        const int jc = j <= L ? j : L;
+                        const V pj = prow[jc];                   // issued together with the reads below
+                        const V pc = prow[cs] - p2p;
+                        const int jl = Js[cs];
+                        const V gj = s < S - 1 ? Gn[jc] : INF;
                         bool ok = false;
                         if (j <= jl) {
-                            const V2 a = Xs[j];
-                            const uint64_t T = (uint64_t)(V)(a.x - pc);
+                            const uint64_t T = (uint64_t)(V)(pj - pc);
                             bool rest_ok;                     // the later stages complete within B*
                             if (s == S - 1) rest_ok = j == L;
-                            else rest_ok = a.y != INF && (F32 ? rne24((uint64_t)a.y) <= B24 : (uint64_t)a.y <= B);
+                            else rest_ok = gj != INF && (F32 ? rne24((uint64_t)gj) <= B24 : (uint64_t)gj <= B);
                             ok = rest_ok && (F32 ? rne24(T) <= B24 : T <= B);
                         }
                         const uint64_t bal = __ballot(ok);
                         if (bal) found = base + __ffsll((unsigned long long)bal) - 1;
+                        else if (base + 63 >= jl) found = jl;     // unreachable: G[s][cs] <= B* has a witness;
+                                                                  // the fallback only keeps indexing in bounds
                     }
-                    // an end always exists (G[s][cs] <= B* has a witness); the clamp
-                    // only keeps indexing in bounds should that ever fail
-                    if (found < 0) found = jl;
                     if (lane == s) {
                         my_start = cs;
                         my_end = found;
                     }
                     cs = found;
                 }
-
-                // ---------------- Evaluate (lane = stage) for the m values of this class
-                const bool act = lane < S;
-                uint64_t Tst = 0;
-                int64_t gsync = 0, wdiff = 0, adiff = 0;
-                if (act) {
-                    const int i = my_start, j = my_end;
-                    const V2 *Xs = X + (size_t)lane * gs;
-                    Tst = (uint64_t)(V)(((const V *)&Xs[j])[0] - ((const V *)&Xs[i])[0] + (V)x.p2p);
-                    wdiff = P.pre_state[x.srow + j] - P.pre_state[x.srow + i];
-                    adiff = P.pre_act[x.arow + j] - P.pre_act[x.arow + i];
-                    const int64_t gd = P.pre_grad[x.arow + j] - P.pre_grad[x.arow + i];
-                    const int64_t gx = P.pre_xgrad[x.srow + j] - P.pre_xgrad[x.srow + i];
-                    gsync = allreduce_ns(gd, D, x.bw_dp) + allreduce_ns(gx, (int64_t)((uint32_t)D / (uint32_t)x.ep), x.bw_dp);
-                }
-                const int64_t sumT = wave_sum(act ? (int64_t)(F32 ? rne24(Tst) : Tst) : int64_t(0));
-                const int64_t maxg = wave_max(gsync);
-                const int64_t maxg_v = F32 ? (int64_t)(rne24((uint64_t)maxg) << (-P.fx_exp)) : maxg;
                 for (uint64_t c = cls; c; c &= c - 1) {
                     const int k = __ffsll((unsigned long long)c) - 1;
-                    const int64_t Mp = rl32(Mp_k, k);
-                    const int64_t fl = (int64_t)(S - lane) < Mp ? (int64_t)(S - lane) : Mp;
-                    const int64_t mem = act ? wdiff + fl * adiff : 0;
-                    const int64_t peak = wave_max(mem);
-                    const bool any_oom = __ballot(act && mem > x.cap) != 0;
-                    const int64_t iter = (Mp - 1) * (int64_t)B24 + sumT + maxg_v;
-                    if (lane == k) {
-                        r_priced = true;
-                        r_oom = any_oom;
-                        r_peak = peak;
-                        if (F32) {
-                            r_iter_f = exact_float(rne24((uint64_t)iter), P.fx_exp);
-                            r_bn_f = exact_float(B24, P.fx_exp);
-                        } else {
-                            r_iter = iter;
-                            r_bn = (int64_t)B;
-                        }
-                    }
                     for (int q = lane; q < A.s_max; q += 64)
                         A.layers[(obase + k) * A.s_max + q] = q < S ? (uint8_t)(my_end - my_start) : 0;
+                }
+                if ((cls >> lane) & 1) {
+                    r_split = true;
+                    r_b = Bv;
                 }
             }
         }
         if (COUNT) continue;
         if (lane < A.n_m) {
             const size_t o = obase + lane;
-            A.status[o] = (uint8_t)(x.status != 0 ? x.status : (r_oom ? HEDDLE_S_OOM : HEDDLE_S_OK));
-            if (F32) {
-                ((float *)A.iter)[o] = r_iter_f;
-                ((float *)A.bottleneck)[o] = r_bn_f;
-            } else {
-                ((int64_t *)A.iter)[o] = r_iter;
-                ((int64_t *)A.bottleneck)[o] = r_bn;
-            }
-            A.peak_mem[o] = r_peak;
+            A.status[o] = (uint8_t)(x.status != 0 ? x.status : (r_split ? HEDDLE_S_OK : HEDDLE_S_OOM));
+            if (F32) ((float *)A.bottleneck)[o] = r_split ? exact_float(rne24((uint64_t)r_b), P.fx_exp) : __builtin_inff();
+            else ((int64_t *)A.bottleneck)[o] = r_split ? (int64_t)r_b : INT64_MAX;
         }
         // zero layer counts of the plans without a split (invalid template, or no split fits)
-        const uint64_t priced = __ballot(r_priced);
-        if (priced != __ballot(lane < A.n_m))
+        const uint64_t with_split = __ballot(r_split);
+        if (with_split != __ballot(lane < A.n_m))
             for (int q = lane; q < A.n_m * A.s_max; q += 64)
-                if (!((priced >> (q / A.s_max)) & 1)) A.layers[obase * A.s_max + q] = 0;
+                if (!((with_split >> (q / A.s_max)) & 1)) A.layers[obase * A.s_max + q] = 0;
     }
     if (COUNT) {
-        work = wave_sum(work);
+        work = __shfl_xor(work, 32) + work;
+        work = __shfl_xor(work, 16) + work;
+        work = __shfl_xor(work, 8) + work;
+        work = __shfl_xor(work, 4) + work;
+        work = __shfl_xor(work, 2) + work;
+        work = __shfl_xor(work, 1) + work;
         if (lane == 0 && work) atomicAdd(A.work, work);
     }
 }
@@ -463,13 +382,16 @@ int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const
 }
 
 template <class V, bool F32, bool COUNT>
-static int launch_t(const heddle_profile *p, PriceArgs &a, hipStream_t stream)
+static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t stream)
 {
     const int L = p->dev.L;
     a.s_cap = a.s_max < L ? a.s_max : L;
     a.g_stride = L + 5;                                       // L + 1 ends and 4 of padding
-    // per wavefront: pairs {P_s, G_{s+1}} and the end limits of every stage
-    const size_t j_off = (size_t)a.s_cap * a.g_stride * 2 * sizeof(V);
+    // per wavefront: the pairs {P_s, G_{s+1}} of the current stage, then the
+    // DP rows and the end limits of every stage
+    const size_t g_off = (size_t)a.g_stride * 2 * sizeof(V);
+    const size_t j_off = g_off + (size_t)a.s_cap * a.g_stride * sizeof(V);
+    a.off_g = (int32_t)g_off;
     a.off_j = (int32_t)j_off;
     a.lds_per_wave = (int32_t)((j_off + (size_t)a.s_cap * a.g_stride + 15) & ~size_t(15));
     int max_lds = 0;
@@ -479,11 +401,11 @@ static int launch_t(const heddle_profile *p, PriceArgs &a, hipStream_t stream)
     const size_t lds = (size_t)wpb * a.lds_per_wave;
     if (lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "DP table of this (L, s_max) does not fit in LDS");
     if (lds > 65536)
-        HEDDLE_HIP(hipFuncSetAttribute((const void *)price_kernel<V, F32, COUNT>,
+        HEDDLE_HIP(hipFuncSetAttribute((const void *)split_kernel<V, F32, COUNT>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
     const int64_t want = (a.n + wpb - 1) / wpb;
     const int blocks = (int)(want < 65536 ? want : 65536);
-    hipLaunchKernelGGL((price_kernel<V, F32, COUNT>), dim3(blocks), dim3(64 * wpb), lds, stream, p->dev, a);
+    hipLaunchKernelGGL((split_kernel<V, F32, COUNT>), dim3(blocks), dim3(64 * wpb), lds, stream, p->dev, a);
     HEDDLE_HIP(hipGetLastError());
     return HEDDLE_OK;
 }
@@ -493,9 +415,12 @@ int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool
     if (a.n == 0) return HEDDLE_OK;
     const bool f32 = a.flags & HEDDLE_F_FP32;
     const bool narrow = f32 ? p->narrow_f32 : p->narrow_i64;
-    if (count_only) return launch_t<uint64_t, false, true>(p, a, stream);
-    if (f32) return narrow ? launch_t<uint32_t, true, false>(p, a, stream) : launch_t<uint64_t, true, false>(p, a, stream);
-    return narrow ? launch_t<uint32_t, false, false>(p, a, stream) : launch_t<uint64_t, false, false>(p, a, stream);
+    int rc;
+    if (count_only) return launch_split<uint64_t, false, true>(p, a, stream);
+    if (f32) rc = narrow ? launch_split<uint32_t, true, false>(p, a, stream) : launch_split<uint64_t, true, false>(p, a, stream);
+    else rc = narrow ? launch_split<uint32_t, false, false>(p, a, stream) : launch_split<uint64_t, false, false>(p, a, stream);
+    if (rc != HEDDLE_OK) return rc;
+    return launch_evaluate(p, a, stream);
 }
 
 static PriceArgs make_args(int64_t n, int32_t s_max, const uint8_t *d_n_stages, const uint32_t *d_stages,

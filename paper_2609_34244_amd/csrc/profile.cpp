@@ -264,8 +264,36 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
             }
     }
 
+    // ---- stage rows: time prefix of a stage per (type, TP, all-to-all variant),
+    // P[j] = pre_time[j] + a2a * (MoE layers before j), exact in 64 bits and, when
+    // the range proof allows, narrowed to 32 bits; the same for the fp32 image
+    const bool narrow_i64 = max_stage < (i128)kNarrowLimit;
+    const bool narrow_f32 = fx_ok && max_stage_fx < (i128)kNarrowLimit;
+    std::vector<uint64_t> rows64[2];
+    std::vector<uint32_t> rows32[2];
+    for (int v = 0; v < 2; v++) {
+        const std::vector<int64_t> &pt = v ? pre_time_fx : pre_time;
+        const std::vector<int64_t> &aa = v ? a2a_fx : a2a_ns;
+        rows64[v].assign((size_t)N * K * 3 * R, 0);
+        if (v == 1 && !fx_ok) continue;
+        for (int g = 0; g < N; g++)
+            for (int k = 0; k < K; k++)
+                for (int var = 0; var < 3; var++)
+                    for (int j = 0; j <= L; j++)
+                        rows64[v][(((size_t)g * K + k) * 3 + var) * R + j] =
+                            (uint64_t)(pt[((size_t)g * K + k) * R + j] + aa[g * 3 + var] * pre_moe[j]);
+        if (v ? narrow_f32 : narrow_i64) {
+            rows32[v].resize(rows64[v].size());
+            for (size_t i = 0; i < rows64[v].size(); i++) rows32[v][i] = (uint32_t)rows64[v][i];
+        } else {
+            rows32[v].assign(1, 0);
+        }
+    }
+
     // ---- upload
     Builder B;
+    const size_t o_r64a = B.add(rows64[0]), o_r64b = B.add(rows64[1]), o_r32a = B.add(rows32[0]),
+                 o_r32b = B.add(rows32[1]);
     size_t o_time = B.add(pre_time), o_time_fx = B.add(pre_time_fx), o_moe = B.add(pre_moe),
            o_state = B.add(pre_state), o_act = B.add(pre_act), o_grad = B.add(pre_grad),
            o_xgrad = B.add(pre_xgrad), o_prof = B.add(d->profiled, (size_t)N * K),
@@ -304,18 +332,22 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
     dp.link_bw = (const int64_t *)(base + o_link);
     dp.ep_degrees = (const int32_t *)(base + o_epd);
     dp.mem_lim = (const uint8_t *)(base + o_lim);
+    dp.rows64[0] = (const uint64_t *)(base + o_r64a);
+    dp.rows64[1] = (const uint64_t *)(base + o_r64b);
+    dp.rows32[0] = (const uint32_t *)(base + o_r32a);
+    dp.rows32[1] = (const uint32_t *)(base + o_r32b);
     dp.n_f = F;
     p->dev = dp;
     p->max_stage_ns = (int64_t)max_stage;
     p->max_ar_ns = (int64_t)max_ar;
-    p->narrow_i64 = max_stage < (i128)kNarrowLimit;
+    p->narrow_i64 = narrow_i64;
     p->max_stage_fx = fx_ok ? (int64_t)max_stage_fx : -1;
     // fp32-rounded all-reduce terms are within a factor (1 + 2^-24) of the int64 ones
     {
         long double b = std::ldexp((long double)max_ar * (1.0L + std::ldexp(1.0L, -20)) + 1.0L, -e0);
         p->max_ar_fx = !fx_ok ? -1 : (b >= (long double)kLimit62 ? kLimit62 : (int64_t)b);
     }
-    p->narrow_f32 = fx_ok && max_stage_fx < (i128)kNarrowLimit;
+    p->narrow_f32 = narrow_f32;
     *out = p;
     return HEDDLE_OK;
 }

@@ -43,6 +43,51 @@ template <class T> __device__ __forceinline__ T wave_max(T v)
     return v;
 }
 
+// uniform value into a scalar register
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// DPP lane permutations within rows of 16 lanes (lanes whose source is not
+// valid keep their own value, which is harmless for min/max)
+template <int CTRL> __device__ __forceinline__ uint32_t dpp32(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL> __device__ __forceinline__ uint64_t dpp64(uint64_t v)
+{
+    return ((uint64_t)dpp32<CTRL>((uint32_t)(v >> 32)) << 32) | dpp32<CTRL>((uint32_t)v);
+}
+template <int CTRL> __device__ __forceinline__ uint32_t dpp(uint32_t v) { return dpp32<CTRL>(v); }
+template <int CTRL> __device__ __forceinline__ uint64_t dpp(uint64_t v) { return dpp64<CTRL>(v); }
+
+constexpr int kDppXor1 = 0xB1;          // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;          // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;   // lane i <-> 7 - i within 8
+constexpr int kDppMirror = 0x140;       // lane i <-> 15 - i within 16
+
+// minimum over aligned groups of k lanes (k a power of two, 1 .. 64, uniform);
+// every lane of a group receives the group's minimum
+template <class T> __device__ __forceinline__ T group_min(T v, int k)
+{
+    T u;
+    if (k >= 2) { u = dpp<kDppXor1>(v); v = u < v ? u : v; }
+    if (k >= 4) { u = dpp<kDppXor2>(v); v = u < v ? u : v; }
+    if (k >= 8) { u = dpp<kDppHalfMirror>(v); v = u < v ? u : v; }
+    if (k >= 16) { u = dpp<kDppMirror>(v); v = u < v ? u : v; }
+    if (k >= 32) {                                   // rows of 16 combined through scalar reads
+        const int lane = __lane_id();
+        T r0 = (T)rl64((int64_t)v, 0), r1 = (T)rl64((int64_t)v, 16), r2 = (T)rl64((int64_t)v, 32),
+          r3 = (T)rl64((int64_t)v, 48);
+        if (k == 32) {
+            const T lo = r0 < r1 ? r0 : r1, hi = r2 < r3 ? r2 : r3;
+            v = lane < 32 ? lo : hi;
+        } else {
+            const T a = r0 < r1 ? r0 : r1, b = r2 < r3 ? r2 : r3;
+            v = a < b ? a : b;
+        }
+    }
+    return v;
+}
+
 // Nearest value with at most 24 significant bits (ties to even) of a
 // non-negative integer below 2^63: its fp32 rounding, kept as an exact integer.
 __device__ __forceinline__ uint64_t rne24(uint64_t x)

@@ -92,23 +92,24 @@ __device__ StageInfo decode(const DevProfile &P, const PriceArgs &A, int64_t t, 
     return x;
 }
 
-// Profile rows of one stage, fetched into registers ahead of use.
-constexpr int kRowSlots = 4;                       // (L + 1) <= 256 entries, 64 per slot
+// Profile rows of one stage, fetched into registers ahead of use: the time
+// prefix and the memory limit of every row (slots of 64 entries).
+constexpr int kRowSlots = 4;                       // (L + 1) <= 256 entries
 template <class V> struct RowRegs {
-    V p[kRowSlots];                                // time prefix
-    int32_t l[kRowSlots];                          // last end that fits memory, from each row
+    V p[kRowSlots];
+    uint32_t l[kRowSlots];
 };
 
 template <class V>
-__device__ __forceinline__ void fetch_rows(RowRegs<V> &r, const V *prow, const uint8_t *lrow, int L, int lane,
-                                           bool need_mem)
+__device__ __forceinline__ void fetch_rows(RowRegs<V> &r, const V *prow, const uint8_t *lrow, int L, int nslots,
+                                           int lane, bool need_mem)
 {
 #pragma unroll
     for (int q = 0; q < kRowSlots; q++) {
-        const int j = lane + 64 * q;
-        if (j <= L) {
+        if (q < nslots) {                                          // uniform
+            const int j = min(lane + 64 * q, L);                   // clamped: no divergent loads
             r.p[q] = prow[j];
-            r.l[q] = need_mem ? lrow[j] : L;
+            r.l[q] = need_mem ? (uint32_t)lrow[j] : (uint32_t)L;
         }
     }
 }
@@ -130,6 +131,8 @@ template <class V, class V2> __device__ __forceinline__ V relax(const V2 &a, V p
     return t > a.y ? t : a.y;
 }
 
+template <class T> __device__ __forceinline__ T vmin(T a, T b) { return a < b ? a : b; }
+
 // ------------------------------------------------------------ split kernel
 
 template <class V, bool F32, bool COUNT>
@@ -139,23 +142,26 @@ __global__ void __launch_bounds__(256, sizeof(V) == 4 ? 5 : 4) split_kernel(DevP
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63, wib = threadIdx.x >> 6, wpb = blockDim.x >> 6;
     const int L = P.L, R = L + 1, gs = A.g_stride;
+    const int nslots = (L + 64) / 64;                          // 64-entry slots covering [0, L]
     const bool compute_only = (A.flags & HEDDLE_F_COMPUTE_ONLY) != 0;
     const V INF = DPInf<V>::value;
     unsigned char *wave_lds = smem + (size_t)wib * A.lds_per_wave;
-    V2 *W = (V2 *)wave_lds;                                   // [gs] pairs {P_s, G_{s+1}} of the current stage
-    V *G = (V *)(wave_lds + A.off_g);                         // [s_cap][gs] DP rows
-    uint8_t *J = wave_lds + A.off_j;                          // [s_cap][gs] last admissible ends
+    // two pair rows {P_s, G_{s+1}}: stage s reads one and writes G_s into the
+    // other, which the commit of stage s-1 completes with P_{s-1}
+    V2 *Wbuf = (V2 *)wave_lds;                                 // [2][gs]
+    V *G = (V *)(wave_lds + A.off_g);                          // [s_cap][gs] DP rows, for the reconstruction
+    uint8_t *J = wave_lds + A.off_j;                           // [s_cap][gs] last admissible ends
     const V *rows = stage_rows<V>(P, F32);
 
-    int my_m = 1;                                             // lane k: the k-th micro-batch count
+    int my_m = 1;                                              // lane k: the k-th micro-batch count
     for (int k = 0; k < A.n_m; k++) my_m = lane == k ? A.m[k] : my_m;
     unsigned long long work = 0;
 
     for (int64_t t = (int64_t)blockIdx.x * wpb + wib; t < A.n; t += (int64_t)gridDim.x * wpb) {
         const StageInfo x = decode<F32>(P, A, t, lane);
-        const int S = x.S;
+        const int S = uni(x.S);
         const size_t obase = (size_t)t * A.n_m;
-        bool r_split = false;                                 // lane k: a split was found for m index k
+        bool r_split = false;                                  // lane k: a split was found for m index k
         V r_b = INF;
 
         if (x.status == 0) {
@@ -166,39 +172,36 @@ __global__ void __launch_bounds__(256, sizeof(V) == 4 ? 5 : 4) split_kernel(DevP
             uint64_t todo = __ballot(lane < A.n_m);
 
             while (todo) {
-                const int key = wave_min(((todo >> lane) & 1) ? key_k : 0x7FFFFFFF);
+                const int key = uni((int)group_min<uint32_t>(((todo >> lane) & 1) ? (uint32_t)key_k : 0x7FFFFFFFu, 64));
                 const uint64_t cls = __ballot(lane < A.n_m && key_k == key) & todo;
                 todo &= ~cls;
-                auto lim_row = [&](int s) {                   // memory limits of stage s in this class
+                auto lim_row = [&](int s) {                    // memory limits of stage s in this class
                     int f = (S - s) < key ? (S - s) : key;
-                    f = f < 1 ? 1 : f;                        // compute-only: not read
-                    return P.mem_lim + rl32(x.lrow, s) + (size_t)(f - 1) * R;
+                    f = f < 1 ? 1 : f;                         // compute-only: not read
+                    return P.mem_lim + uni(rl32(x.lrow, s) + (f - 1) * R);
                 };
 
                 // ---------------- PartitionLayers: suffix min-max DP, stages S-1 .. 0
                 RowRegs<V> rr;
-                fetch_rows<V>(rr, rows + rl32(x.prow, S - 1), lim_row(S - 1), L, lane, !compute_only);
+                fetch_rows<V>(rr, rows + uni(rl32(x.prow, S - 1)), lim_row(S - 1), L, nslots, lane, !compute_only);
                 V Bv = INF;
                 for (int s = S - 1; s >= 0; s--) {
                     const V p2p = (V)rl64(x.p2p, s);
-                    const int jhi = L - (S - 1 - s);              // leaves one layer per later stage
+                    const int jhi = L - (S - 1 - s);               // leaves one layer per later stage
                     const int ihi = (s == 0) ? 0 : L - (S - s);
-                    V2 *Xs = W;
+                    V2 *Xs = Wbuf + (size_t)(s & 1) * gs;          // {P_s, G_{s+1}}
+                    V2 *Xo = Wbuf + (size_t)((s & 1) ^ 1) * gs;    // receives G_s
                     V *Gs = G + (size_t)s * gs;
-                    const V *Gn = G + (size_t)(s + 1) * gs;            // row s + 1 (not read for s = S-1)
                     uint8_t *Js = J + (size_t)s * gs;
 #pragma unroll
                     for (int q = 0; q < kRowSlots; q++) {
-                        const int j = lane + 64 * q;
-                        if (j <= L) {
-                            V2 w;
-                            w.x = rr.p[q];
-                            w.y = s < S - 1 ? Gn[j] : INF;
-                            Xs[j] = w;
-                            Js[j] = (uint8_t)(rr.l[q] < jhi ? rr.l[q] : jhi);
+                        if (q < nslots) {
+                            const int j = min(lane + 64 * q, gs - 1);   // clamped into the padding
+                            ((V *)&Xs[j])[0] = rr.p[q];
+                            Js[j] = (uint8_t)min(rr.l[q], (uint32_t)jhi);
                         }
                     }
-                    if (s > 0) fetch_rows<V>(rr, rows + rl32(x.prow, s - 1), lim_row(s - 1), L, lane, !compute_only);
+                    if (s > 0) fetch_rows<V>(rr, rows + uni(rl32(x.prow, s - 1)), lim_row(s - 1), L, nslots, lane, !compute_only);
                     wave_sync();
                     if (s == S - 1) {
                         // last stage: its rows must end at L
@@ -208,14 +211,18 @@ __global__ void __launch_bounds__(256, sizeof(V) == 4 ? 5 : 4) split_kernel(DevP
                                 work += fit ? 1 : 0;
                             } else {
                                 const V gv = fit ? (V)(Xs[L].x - Xs[i].x) : INF;
-                                if (s > 0) Gs[i] = gv;
-                                else Bv = gv;                   // S = 1: row 0, lane 0
+                                if (s > 0) {
+                                    ((V *)&Xo[i])[1] = gv;
+                                    Gs[i] = gv;
+                                } else {
+                                    Bv = gv;                    // S = 1: row 0, lane 0
+                                }
                             }
                         }
                         if (S == 1) Bv = (V)rl64((int64_t)Bv, 0);
                     } else {
-                        // rows [s, ihi] (stage 0: row 0 only); whole slots of 64 rows
-                        // take one lane per row, the ragged last slot several
+                        // rows [s, ihi] (stage 0: row 0 only): whole slots of 64 rows take
+                        // one lane per row, the ragged last slot several lanes per row
                         int base = s;
                         for (; base + 63 <= ihi; base += 64) {
                             const int i = base + lane;
@@ -224,68 +231,63 @@ __global__ void __launch_bounds__(256, sizeof(V) == 4 ? 5 : 4) split_kernel(DevP
                                 work += (unsigned long long)(jl - i);
                                 continue;
                             }
-                            const V pi = Xs[i].x - p2p;                 // T(s,i,j) = P_s[j] - pi
+                            const V pi = Xs[i].x - p2p;                  // T(s,i,j) = P_s[j] - pi
                             V acc = INF;
                             int j = i + 1;
                             for (; j + 3 <= jl; j += 4) {
                                 const V2 a = Xs[j], b = Xs[j + 1], c = Xs[j + 2], d = Xs[j + 3];
-                                const V ca = relax<V>(a, pi), cb = relax<V>(b, pi);
-                                const V cc = relax<V>(c, pi), cd = relax<V>(d, pi);
-                                const V m1 = ca < cb ? ca : cb, m2 = cc < cd ? cc : cd;
-                                const V m3 = m1 < m2 ? m1 : m2;
-                                acc = m3 < acc ? m3 : acc;
+                                acc = vmin(acc, vmin(vmin(relax<V>(a, pi), relax<V>(b, pi)),
+                                                     vmin(relax<V>(c, pi), relax<V>(d, pi))));
                             }
-                            if (j <= jl) {                               // 1 to 3 ends left (X padded by 4)
+                            if (j <= jl) {                               // 1 to 3 ends left (padded by 4)
                                 const int rem = jl - j;
                                 const V2 a = Xs[j], b = Xs[j + 1], c = Xs[j + 2];
-                                const V ca = relax<V>(a, pi);
                                 const V cb = rem >= 1 ? relax<V>(b, pi) : INF;
                                 const V cc = rem >= 2 ? relax<V>(c, pi) : INF;
-                                const V m1 = ca < cb ? ca : cb;
-                                const V m3 = m1 < cc ? m1 : cc;
-                                acc = m3 < acc ? m3 : acc;
+                                acc = vmin(acc, vmin(relax<V>(a, pi), vmin(cb, cc)));
                             }
+                            ((V *)&Xo[i])[1] = acc;
                             Gs[i] = acc;
                         }
                         if (base <= ihi) {
-                            // r < 64 rows left: k lanes per row (k the largest power of two
-                            // with k * r <= 64), each striding over the row's ends by k
+                            // r < 64 rows left: k lanes per row, k = 64 >> ceil(log2 r), each
+                            // lane striding over the row's ends by k
                             const int r = ihi - base + 1;
-                            const int k = 1 << (31 - __clz(64 / r));
+                            const int k = 64 >> (r > 1 ? 32 - __clz(r - 1) : 0);
+                            const int lk = 31 - __clz(k);
                             const int part = lane & (k - 1);
-                            const int i = base + lane / k;
+                            const int i = base + (lane >> lk);
                             const bool row_ok = i <= ihi;
-                            const int jl = row_ok ? Js[i] : 0;
+                            const int ic = row_ok ? i : ihi;
+                            const int jl = row_ok ? Js[ic] : 0;
                             if (COUNT) {
                                 if (row_ok && part == 0) work += (unsigned long long)(jl - i);
                             } else {
-                                const V pi = row_ok ? Xs[i].x - p2p : V(0);
+                                const V pi = Xs[ic].x - p2p;
                                 V acc = INF;
-                                for (int j = i + 1 + part; j <= jl; j += k) {
-                                    const V c = relax<V>(Xs[j], pi);
-                                    acc = c < acc ? c : acc;
+                                for (int j = i + 1 + part; j <= jl; j += k) acc = vmin(acc, relax<V>(Xs[j], pi));
+                                acc = group_min<V>(acc, k);
+                                if (s == 0) {
+                                    Bv = (V)rl64((int64_t)acc, 0);       // one row: the whole wave's minimum
+                                } else if (row_ok && part == 0) {
+                                    ((V *)&Xo[i])[1] = acc;
+                                    Gs[i] = acc;
                                 }
-                                for (int o = 1; o < k; o <<= 1) {
-                                    const V u = __shfl_xor(acc, o);
-                                    acc = u < acc ? u : acc;
-                                }
-                                if (s == 0) Bv = acc;                    // one row, all lanes hold its minimum
-                                else if (row_ok && part == 0) Gs[i] = acc;
                             }
                         }
                     }
                     wave_sync();
                 }
                 if (COUNT) continue;
-                if (Bv == INF) continue;                      // no split fits memory
+                if (Bv == INF) continue;                       // no split fits memory
                 const uint64_t B = (uint64_t)Bv;
-                const uint64_t B24 = F32 ? rne24(B) : B;      // fp32 bottleneck, as an exact integer
+                const uint64_t B24 = F32 ? rne24(B) : B;       // fp32 bottleneck, as an exact integer
 
                 // ---------------- canonical reconstruction: smallest admissible end per stage
                 // (time prefixes from the profile's stage rows, DP rows and limits from LDS)
                 int cs = 0, my_start = 0, my_end = 0;
                 for (int s = 0; s < S; s++) {
-                    const V *prow = rows + rl32(x.prow, s);
+                    const V *prow = rows + uni(rl32(x.prow, s));
                     const V *Gn = G + (size_t)(s + 1) * gs;
                     const uint8_t *Js = J + (size_t)s * gs;
                     const V p2p = (V)rl64(x.p2p, s);
@@ -300,15 +302,15 @@ __global__ void __launch_bounds__(256, sizeof(V) == 4 ? 5 : 4) split_kernel(DevP
                         bool ok = false;
                         if (j <= jl) {
                             const uint64_t T = (uint64_t)(V)(pj - pc);
-                            bool rest_ok;                     // the later stages complete within B*
+                            bool rest_ok;                      // the later stages complete within B*
                             if (s == S - 1) rest_ok = j == L;
                             else rest_ok = gj != INF && (F32 ? rne24((uint64_t)gj) <= B24 : (uint64_t)gj <= B);
                             ok = rest_ok && (F32 ? rne24(T) <= B24 : T <= B);
                         }
                         const uint64_t bal = __ballot(ok);
                         if (bal) found = base + __ffsll((unsigned long long)bal) - 1;
-                        else if (base + 63 >= jl) found = jl;     // unreachable: G[s][cs] <= B* has a witness;
-                                                                  // the fallback only keeps indexing in bounds
+                        else if (base + 63 >= jl) found = jl;      // unreachable: G[s][cs] <= B* has a witness;
+                                                                   // the fallback only keeps indexing in bounds
                     }
                     if (lane == s) {
                         my_start = cs;
@@ -341,12 +343,12 @@ __global__ void __launch_bounds__(256, sizeof(V) == 4 ? 5 : 4) split_kernel(DevP
                 if (!((with_split >> (q / A.s_max)) & 1)) A.layers[obase * A.s_max + q] = 0;
     }
     if (COUNT) {
-        work = __shfl_xor(work, 32) + work;
-        work = __shfl_xor(work, 16) + work;
-        work = __shfl_xor(work, 8) + work;
-        work = __shfl_xor(work, 4) + work;
-        work = __shfl_xor(work, 2) + work;
-        work = __shfl_xor(work, 1) + work;
+        work += __shfl_xor(work, 32);
+        work += __shfl_xor(work, 16);
+        work += __shfl_xor(work, 8);
+        work += __shfl_xor(work, 4);
+        work += __shfl_xor(work, 2);
+        work += __shfl_xor(work, 1);
         if (lane == 0 && work) atomicAdd(A.work, work);
     }
 }
@@ -387,9 +389,9 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     const int L = p->dev.L;
     a.s_cap = a.s_max < L ? a.s_max : L;
     a.g_stride = L + 5;                                       // L + 1 ends and 4 of padding
-    // per wavefront: the pairs {P_s, G_{s+1}} of the current stage, then the
-    // DP rows and the end limits of every stage
-    const size_t g_off = (size_t)a.g_stride * 2 * sizeof(V);
+    // per wavefront: two rows of pairs {P_s, G_{s+1}}, then the DP rows and the
+    // end limits of every stage
+    const size_t g_off = (size_t)2 * a.g_stride * 2 * sizeof(V);
     const size_t j_off = g_off + (size_t)a.s_cap * a.g_stride * sizeof(V);
     a.off_g = (int32_t)g_off;
     a.off_j = (int32_t)j_off;

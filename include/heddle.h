@@ -207,9 +207,15 @@ int heddle_best_plan(const heddle_profile *p, int64_t n, int32_t s_max,
  * heddle_count_work -- algorithmic work of pricing this batch: the number of
  * (row i, end j) pairs the min-max recurrence relaxes, summed over the
  * distinct splits the batch needs (a template's m values that imply the
- * same in-flight activation counts share one split). Stage 0 starts at row
- * 0 only, the last stage ends at L only, and pairs whose stage does not fit
- * memory are excluded (none with COMPUTE_ONLY). Synchronous.
+ * same in-flight activation counts share one split). Only rows that can lie
+ * on a complete split are relaxed: with lim(s, i) the last admissible end of
+ * row i at stage s (memory limit, capped so that each later stage keeps a
+ * layer), stage s takes the rows from Bk_s (the smallest start from which
+ * lim reaches Bk_{s+1}, Bk_S = L) to min(R_s, L - (S - s)) (R_0 = 0,
+ * R_{s+1} = lim(s, R_s): the furthest reachable start; stage 0: row 0), each
+ * against the ends max(i + 1, Bk_{s+1}) .. lim(s, i); a last-stage row
+ * counts one. A template with an empty range at some stage has no split
+ * that fits memory and counts zero. Synchronous.
  *   h_relaxations  HOST result.
  * Returns HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_NOMEM or HEDDLE_E_DEVICE.
  */

@@ -266,9 +266,24 @@ static int64_t partition(const oracle_profile *p, const ostage *st, int S, int64
     return B;
 }
 
-/* number of (row, column) pairs the suffix DP relaxes: stage 0 only from
- * row 0, the last stage only towards column L, memory-infeasible pairs
- * excluded. This is the algorithmic work unit of the GPU kernel. */
+/* Largest admissible end of row i at stage s: the largest j in
+ * (i, L-(S-1-s)] with Fits(s,i,j), or i itself when no such j fits. */
+static int last_end(const oracle_profile *p, const ostage *st, int s, int S, int i, int64_t Mp, int co)
+{
+    int best = i;
+    for (int j = i + 1; j <= p->L - (S - 1 - s); j++)
+        if (fits(p, st, s, S, i, j, Mp, co)) best = j;
+    return best;
+}
+
+/* Work of the suffix DP over the rows that can lie on a complete split.
+ * R_s is the furthest start stage s can be reached at from row 0:
+ * R_0 = 0, R_{s+1} = last_end(s, R_s). Bk_s is the smallest start i in
+ * [s, min(R_s, L-(S-s))] with last_end(s, i) >= Bk_{s+1}, where Bk_S = L; when
+ * some stage has no such start, no split fits and there is no work. Stage
+ * s < S-1 relaxes each row i in [Bk_s, min(R_s, L-(S-s))] against the ends
+ * max(i+1, Bk_{s+1}) .. last_end(s, i); each row of the last stage counts one.
+ * This is the algorithmic work unit of the GPU kernel. */
 int64_t oracle_count_relaxations(const oracle_profile *p, int S, const uint32_t *rec, int s_max,
                                  int64_t m, uint32_t flags)
 {
@@ -276,14 +291,25 @@ int64_t oracle_count_relaxations(const oracle_profile *p, int S, const uint32_t 
     if (validate(p, S, s_max, rec, st) != OR_OK) return 0;
     int64_t Mp = ceil_div64(m, st[0].dp), count = 0;
     int L = p->L, co = (flags & OR_F_COMPUTE_ONLY) != 0;
-    for (int s = 0; s < S; s++) {
-        int ilo = s, ihi = (s == 0) ? 0 : L - (S - s);
-        for (int i = ilo; i <= ihi; i++) {
-            int jlo = (s == S - 1) ? L : i + 1;
-            for (int j = jlo; j <= L - (S - 1 - s); j++)
-                if (fits(p, st, s, S, i, j, Mp, co)) count++;
-        }
+    int R[257], Bk[258], top[257];
+    R[0] = 0;
+    for (int s = 0; s + 1 < S; s++) R[s + 1] = last_end(p, st, s, S, R[s], Mp, co);
+    Bk[S] = L;
+    for (int s = S - 1; s >= 0; s--) {
+        int ihi = (s == 0) ? 0 : L - (S - s);
+        top[s] = R[s] < ihi ? R[s] : ihi;
+        Bk[s] = -1;
+        for (int i = s; i <= top[s]; i++)
+            if (last_end(p, st, s, S, i, Mp, co) >= Bk[s + 1]) { Bk[s] = i; break; }
+        if (Bk[s] < 0) return 0;
     }
+    for (int s = 0; s < S; s++)
+        for (int i = Bk[s]; i <= top[s]; i++) {
+            if (s == S - 1) { count++; continue; }
+            int lo = i + 1 > Bk[s + 1] ? i + 1 : Bk[s + 1];
+            int hi = last_end(p, st, s, S, i, Mp, co);
+            if (hi >= lo) count += hi - lo + 1;
+        }
     return count;
 }
 

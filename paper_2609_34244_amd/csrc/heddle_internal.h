@@ -46,8 +46,9 @@ struct DevProfile {
     const int64_t *intra_bw;         // [n_types] MB/s
     const int64_t *link_bw;          // [n_types][n_types] MB/s
     const int32_t *ep_degrees;       // [n_ep]
-    const uint8_t *mem_lim;          // [n_types][n_tp][n_ep][n_f][L+1] largest end that fits from row i
+    const uint8_t *mem_lim;          // [n_types][n_tp][n_ep][n_f][lim_stride] largest end that fits from row i
     int32_t n_f;                     // in-flight counts covered by mem_lim: 1 .. min(L, 64)
+    int32_t lim_stride;              // bytes per mem_lim row: L + 1 rounded up to a multiple of 16
     // [n_types][n_tp][3][L+1] stage time prefix (layer costs + all-to-all of the
     // variant); index 0: int64 ns, 1: fp32 image in fixed point; the 32-bit
     // copies exist only when the range proof allows narrowing

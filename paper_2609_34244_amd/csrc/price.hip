@@ -18,15 +18,15 @@
 // profile table.
 //
 // Mapping. One wavefront splits one template at a time (grid-stride over
-// templates). Lanes are stages for decode and validation, and split rows i
-// during the DP: a row takes one lane and walks its ends four at a time; the
-// rows of a stage's ragged last slot take several lanes each, which stride
-// over the ends and combine with cross-lane minima. Per wavefront, LDS holds
-// the pairs W[j] = {P_s[j], G[s+1][j]} of the stage being relaxed, so one
-// 64-bit LDS read feeds one relaxation (sub, max, min), and, for every stage,
-// the DP row G[s][.] and the end limits J[s][.] that the reconstruction
-// needs. The profile rows of stage s-1 are fetched into registers while
-// stage s relaxes.
+// templates). Lanes are stages for decode and validation. The memory-limit
+// rows of all stages are copied into LDS first; two short scalar passes over
+// them give each stage's window of rows that can lie on a complete split (see
+// the split kernel), and the DP relaxes only those. Lanes are split rows
+// during the DP: r rows of a window take 64 >> ceil(log2 r) lanes each, which
+// share the row's ends and combine with a cross-lane minimum. Per wavefront,
+// LDS holds pairs W_s[j] = {P_s[j], G[s+1][j]}, so one 64-bit read feeds one
+// relaxation (sub, max, min). The time prefix of stage s-1 is fetched into
+// registers while stage s relaxes.
 #include <cstring>
 
 #include "device_common.h"
@@ -46,17 +46,17 @@ struct StageInfo {
 // profile match of section 5.2). All per-lane table reads are issued at once
 // on clamped indices; the checks then run in status order over all stages.
 template <bool F32>
-__device__ StageInfo decode(const DevProfile &P, const PriceArgs &A, int64_t t, int lane)
+__device__ StageInfo decode(const DevProfile &P, const PriceArgs &A, int S, uint32_t rec_in, int lane)
 {
     StageInfo x;
     const int L = P.L, R = L + 1, N = P.n_types;
-    x.S = A.n_stages[t];
+    x.S = S;
     x.status = 0;
     x.D = 1;
     x.prow = x.lrow = 0;
     x.p2p = 0;
     const bool act = lane < x.S && lane < A.s_max;
-    const uint32_t rec = act ? A.stages[t * A.s_max + lane] : 0u;
+    const uint32_t rec = act ? rec_in : 0u;
     const int g = rec & 0xFF;
     const int l2tp = (rec >> 8) & 15, l2ep = (rec >> 12) & 15;
     const int dpv = (int)(rec >> 16);
@@ -86,32 +86,25 @@ __device__ StageInfo decode(const DevProfile &P, const PriceArgs &A, int64_t t, 
 
     if (act) {
         x.prow = ((g * P.n_tp + ki) * 3 + a2a_variant(ep, tp, node)) * R;
-        x.lrow = ((g * P.n_tp + ki) * P.n_ep + ei) * P.n_f * R;
+        x.lrow = ((g * P.n_tp + ki) * P.n_ep + ei) * P.n_f * P.lim_stride;
         x.p2p = lane < x.S - 1 ? p2p : 0;
     }
     return x;
 }
 
-// Profile rows of one stage, fetched into registers ahead of use: the time
-// prefix and the memory limit of every row (slots of 64 entries).
+// Time prefix of one stage over the entries [a, e], fetched into registers
+// ahead of use (slots of 64 entries; lanes past e repeat entry e).
 constexpr int kRowSlots = 4;                       // (L + 1) <= 256 entries
 template <class V> struct RowRegs {
     V p[kRowSlots];
-    uint32_t l[kRowSlots];
 };
 
 template <class V>
-__device__ __forceinline__ void fetch_rows(RowRegs<V> &r, const V *prow, const uint8_t *lrow, int L, int nslots,
-                                           int lane, bool need_mem)
+__device__ __forceinline__ void fetch_rows(RowRegs<V> &r, const V *prow, int a, int e, int lane)
 {
 #pragma unroll
-    for (int q = 0; q < kRowSlots; q++) {
-        if (q < nslots) {                                          // uniform
-            const int j = min(lane + 64 * q, L);                   // clamped: no divergent loads
-            r.p[q] = prow[j];
-            r.l[q] = need_mem ? (uint32_t)lrow[j] : (uint32_t)L;
-        }
-    }
+    for (int q = 0; q < kRowSlots; q++)
+        if (64 * q <= e - a) r.p[q] = prow[min(a + lane + 64 * q, e)];     // uniform condition
 }
 
 template <class V> __device__ __forceinline__ const V *stage_rows(const DevProfile &P, bool f32);
@@ -133,32 +126,81 @@ template <class V, class V2> __device__ __forceinline__ V relax(const V2 &a, V p
 
 template <class T> __device__ __forceinline__ T vmin(T a, T b) { return a < b ? a : b; }
 
+// min over the ends [j, je] of one row, four ends per step (entries up to
+// je + 2 must lie inside the pair row)
+template <class V, class V2> __device__ __forceinline__ V relax_range(const V2 *X, int j, int je, V pi, V acc)
+{
+    const V INF = DPInf<V>::value;
+    for (; j + 3 <= je; j += 4) {
+        const V2 a = X[j], b = X[j + 1], c = X[j + 2], d = X[j + 3];
+        acc = vmin(acc, vmin(vmin(relax<V>(a, pi), relax<V>(b, pi)), vmin(relax<V>(c, pi), relax<V>(d, pi))));
+    }
+    if (j <= je) {                                       // 1 to 3 ends left
+        const int rem = je - j;
+        const V2 a = X[j], b = X[j + 1], c = X[j + 2];
+        const V cb = rem >= 1 ? relax<V>(b, pi) : INF;
+        const V cc = rem >= 2 ? relax<V>(c, pi) : INF;
+        acc = vmin(acc, vmin(relax<V>(a, pi), vmin(cb, cc)));
+    }
+    return acc;
+}
+
 // ------------------------------------------------------------ split kernel
+//
+// Row windows. With lim(s, i) the largest admissible end of row i at stage s
+// (memory limit capped so that every later stage keeps a layer), lim is
+// non-decreasing in i. So the starts stage s can be reached at from row 0 lie
+// in [s, R_s] with R_0 = 0 and R_{s+1} = lim(s, R_s), and the rows from which
+// stages s..S-1 can still complete lie in [Bk_s, L - (S - s)] with Bk_S = L and
+// Bk_s the smallest i with lim(s, i) >= Bk_{s+1}. Rows outside the window
+// W_s = [max(s, Bk_s), min(R_s, L - (S - s))] are unreachable or have G = inf,
+// so the DP relaxes only rows of W_s and ends in W_{s+1}, which gives the same
+// G on every row of every complete split, hence the same B* and the same
+// canonical split. An empty window means no split fits memory.
 
 template <class V, bool F32, bool COUNT>
-__global__ void __launch_bounds__(256, sizeof(V) == 4 ? 5 : 4) split_kernel(DevProfile P, PriceArgs A)
+__global__ void __launch_bounds__(64, sizeof(V) == 4 ? 5 : 3) split_kernel(DevProfile P, PriceArgs A)
 {
     typedef typename Vec2<V>::type V2;
+    constexpr int kBatch = 4;                                  // stages whose limit rows are loaded together
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63, wib = threadIdx.x >> 6, wpb = blockDim.x >> 6;
-    const int L = P.L, R = L + 1, gs = A.g_stride;
-    const int nslots = (L + 64) / 64;                          // 64-entry slots covering [0, L]
-    const bool compute_only = (A.flags & HEDDLE_F_COMPUTE_ONLY) != 0;
+    const int L = P.L, gs = A.g_stride, ls = P.lim_stride;
+    const bool mem_aware = (A.flags & HEDDLE_F_COMPUTE_ONLY) == 0;
     const V INF = DPInf<V>::value;
     unsigned char *wave_lds = smem + (size_t)wib * A.lds_per_wave;
-    // two pair rows {P_s, G_{s+1}}: stage s reads one and writes G_s into the
-    // other, which the commit of stage s-1 completes with P_{s-1}
-    V2 *Wbuf = (V2 *)wave_lds;                                 // [2][gs]
+    V2 *W = (V2 *)wave_lds;                                    // two alternating pair rows: [2][gs]
     V *G = (V *)(wave_lds + A.off_g);                          // [s_cap][gs] DP rows, for the reconstruction
-    uint8_t *J = wave_lds + A.off_j;                           // [s_cap][gs] last admissible ends
+    uint8_t *J = wave_lds + A.off_j;                           // [s_cap][ls] memory limits per stage
     const V *rows = stage_rows<V>(P, F32);
+    const int ldw = ls >> 2;                                   // dwords per limit row (<= 64)
+    auto pair_row = [&](int s) -> V2 * { return W + (size_t)(s & 1) * gs; };
+    auto put_g = [&](int s, int i, V g) {                      // G_s[i], s >= 1
+        ((V *)&pair_row(s - 1)[i])[1] = g;
+        G[(size_t)s * gs + i] = g;
+    };
 
     int my_m = 1;                                              // lane k: the k-th micro-batch count
     for (int k = 0; k < A.n_m; k++) my_m = lane == k ? A.m[k] : my_m;
     unsigned long long work = 0;
 
-    for (int64_t t = (int64_t)blockIdx.x * wpb + wib; t < A.n; t += (int64_t)gridDim.x * wpb) {
-        const StageInfo x = decode<F32>(P, A, t, lane);
+    // the template records of the next iteration are loaded one iteration ahead
+    const int64_t stride = (int64_t)gridDim.x * wpb;
+    int64_t t = (int64_t)blockIdx.x * wpb + wib;
+    int S_next = 0;
+    uint32_t rec_next = 0;
+    if (t < A.n) {
+        S_next = A.n_stages[t];
+        rec_next = lane < A.s_max ? A.stages[t * A.s_max + lane] : 0u;
+    }
+    for (; t < A.n; t += stride) {
+        const int S_in = S_next;
+        const uint32_t rec_in = rec_next;
+        if (t + stride < A.n) {
+            S_next = A.n_stages[t + stride];
+            rec_next = lane < A.s_max ? A.stages[(t + stride) * A.s_max + lane] : 0u;
+        }
+        const StageInfo x = decode<F32>(P, A, S_in, rec_in, lane);
         const int S = uni(x.S);
         const size_t obase = (size_t)t * A.n_m;
         bool r_split = false;                                  // lane k: a split was found for m index k
@@ -168,112 +210,132 @@ __global__ void __launch_bounds__(256, sizeof(V) == 4 ? 5 : 4) split_kernel(DevP
             const int D = x.D;
             // micro-batches per replica M_p = ceil(m / D); min(M_p, S) fixes the split
             const int Mp_k = (int)(((uint32_t)my_m + (uint32_t)D - 1) / (uint32_t)D);
-            const int key_k = compute_only ? 0 : (Mp_k < S ? Mp_k : S);
+            const int key_k = mem_aware ? (Mp_k < S ? Mp_k : S) : 0;
             uint64_t todo = __ballot(lane < A.n_m);
 
             while (todo) {
                 const int key = uni((int)group_min<uint32_t>(((todo >> lane) & 1) ? (uint32_t)key_k : 0x7FFFFFFFu, 64));
                 const uint64_t cls = __ballot(lane < A.n_m && key_k == key) & todo;
                 todo &= ~cls;
-                auto lim_row = [&](int s) {                    // memory limits of stage s in this class
-                    int f = (S - s) < key ? (S - s) : key;
-                    f = f < 1 ? 1 : f;                         // compute-only: not read
-                    return P.mem_lim + uni(rl32(x.lrow, s) + (f - 1) * R);
+                auto jhi_of = [&](int s) { return L - (S - 1 - s); };   // last end leaving a layer per later stage
+                auto lim_of = [&](int s, int i) {                       // lim(s, i), i uniform
+                    return mem_aware ? min((int)J[s * ls + i], jhi_of(s)) : jhi_of(s);
                 };
 
-                // ---------------- PartitionLayers: suffix min-max DP, stages S-1 .. 0
+                // ---------------- memory-limit rows of every stage (this class) into LDS,
+                // kBatch stages per round trip
+                if (mem_aware) {
+                    wave_sync();                                        // earlier reads of J are done
+                    int f = min(S - lane, key);
+                    f = f < 1 ? 1 : f;
+                    const int my_row = x.lrow + (f - 1) * ls;          // lane s: stage s's limit row, this class
+                    for (int s0 = 0; s0 < S; s0 += kBatch) {
+                        uint32_t jv[kBatch];
+#pragma unroll
+                        for (int u = 0; u < kBatch; u++)
+                            if (s0 + u < S && lane < ldw)
+                                jv[u] = ((const uint32_t *)P.mem_lim)[(uni(rl32(my_row, s0 + u)) >> 2) + lane];
+#pragma unroll
+                        for (int u = 0; u < kBatch; u++)
+                            if (s0 + u < S && lane < ldw) ((uint32_t *)J)[(s0 + u) * ldw + lane] = jv[u];
+                    }
+                    wave_sync();
+                }
+
+                // ---------------- row windows: lane s holds [a_s, b_s]
+                int Rl = 0;                                             // lane s: R_s
+                {
+                    int c = 0;
+                    for (int s = 1; s < S; s++) {
+                        c = uni(lim_of(s - 1, c));
+                        Rl = lane == s ? c : Rl;
+                    }
+                }
+                int Al = 0, Bl = 0;
+                bool feasible = true;
+                {
+                    int nxt = L;                                       // Bk_{s+1}
+                    for (int s = S - 1; s >= 0; s--) {
+                        const int ihi = (s == 0) ? 0 : L - (S - s);
+                        const int R_s = rl32(Rl, s);
+                        const int b = R_s < ihi ? R_s : ihi;
+                        int a = -1;
+                        if (!mem_aware) {
+                            a = s <= b ? s : -1;
+                        } else {
+                            for (int base = s; base <= b; base += 64) {   // J is non-decreasing along a row
+                                const int i = base + lane;
+                                const uint64_t hit = __ballot(i <= b && (int)J[s * ls + min(i, b)] >= nxt);
+                                if (hit) {
+                                    a = base + __ffsll((unsigned long long)hit) - 1;
+                                    break;
+                                }
+                            }
+                        }
+                        if (a < 0) {
+                            feasible = false;
+                            break;
+                        }
+                        Al = lane == s ? a : Al;
+                        Bl = lane == s ? b : Bl;
+                        nxt = a;
+                    }
+                }
+                if (!feasible) continue;                               // no split fits memory
+
+                // ---------------- PartitionLayers: suffix min-max DP over the windows, stages S-1 .. 0
                 RowRegs<V> rr;
-                fetch_rows<V>(rr, rows + uni(rl32(x.prow, S - 1)), lim_row(S - 1), L, nslots, lane, !compute_only);
+                fetch_rows<V>(rr, rows + uni(rl32(x.prow, S - 1)), uni(rl32(Al, S - 1)), L, lane);
                 V Bv = INF;
                 for (int s = S - 1; s >= 0; s--) {
-                    const V p2p = (V)rl64(x.p2p, s);
-                    const int jhi = L - (S - 1 - s);               // leaves one layer per later stage
-                    const int ihi = (s == 0) ? 0 : L - (S - s);
-                    V2 *Xs = Wbuf + (size_t)(s & 1) * gs;          // {P_s, G_{s+1}}
-                    V2 *Xo = Wbuf + (size_t)((s & 1) ^ 1) * gs;    // receives G_s
-                    V *Gs = G + (size_t)s * gs;
-                    uint8_t *Js = J + (size_t)s * gs;
+                    const int a = uni(rl32(Al, s)), b = uni(rl32(Bl, s));
+                    const int e = s == S - 1 ? L : uni(rl32(Bl, s + 1));     // last end of any row
+                    V2 *Xs = pair_row(s);
 #pragma unroll
-                    for (int q = 0; q < kRowSlots; q++) {
-                        if (q < nslots) {
-                            const int j = min(lane + 64 * q, gs - 1);   // clamped into the padding
-                            ((V *)&Xs[j])[0] = rr.p[q];
-                            Js[j] = (uint8_t)min(rr.l[q], (uint32_t)jhi);
-                        }
-                    }
-                    if (s > 0) fetch_rows<V>(rr, rows + uni(rl32(x.prow, s - 1)), lim_row(s - 1), L, nslots, lane, !compute_only);
+                    for (int q = 0; q < kRowSlots; q++)
+                        if (64 * q <= e - a) ((V *)&Xs[min(a + lane + 64 * q, e)])[0] = rr.p[q];
+                    if (s > 0) fetch_rows<V>(rr, rows + uni(rl32(x.prow, s - 1)), uni(rl32(Al, s - 1)), b, lane);
                     wave_sync();
                     if (s == S - 1) {
-                        // last stage: its rows must end at L
-                        for (int i = s + lane; i <= ihi; i += 64) {
-                            const bool fit = Js[i] == L;
-                            if (COUNT) {
-                                work += fit ? 1 : 0;
-                            } else {
-                                const V gv = fit ? (V)(Xs[L].x - Xs[i].x) : INF;
-                                if (s > 0) {
-                                    ((V *)&Xo[i])[1] = gv;
-                                    Gs[i] = gv;
-                                } else {
-                                    Bv = gv;                    // S = 1: row 0, lane 0
-                                }
+                        // last stage: every window row ends at L
+                        if (COUNT) {
+                            if (lane == 0) work += (unsigned long long)(b - a + 1);
+                        } else {
+                            for (int i = a + lane; i <= b; i += 64) {
+                                const V gv = (V)(Xs[L].x - Xs[i].x);
+                                if (s > 0) put_g(s, i, gv);
+                                else Bv = gv;                          // S = 1: row 0, lane 0
                             }
+                            if (S == 1) Bv = (V)rl64((int64_t)Bv, 0);
                         }
-                        if (S == 1) Bv = (V)rl64((int64_t)Bv, 0);
                     } else {
-                        // rows [s, ihi] (stage 0: row 0 only): whole slots of 64 rows take
-                        // one lane per row, the ragged last slot several lanes per row
-                        int base = s;
-                        for (; base + 63 <= ihi; base += 64) {
-                            const int i = base + lane;
-                            const int jl = Js[i];
+                        // r rows, k = 64 >> ceil(log2 r) lanes per row (one when r >= 64); the
+                        // k lanes of a row take consecutive shares of its ends
+                        const V p2p = (V)rl64(x.p2p, s);
+                        const int a_next = uni(rl32(Al, s + 1)), jhi = jhi_of(s);
+                        const int r = b - a + 1;
+                        const int lk = r >= 64 ? 0 : 6 - (r > 1 ? 32 - __clz(r - 1) : 0);
+                        const int k = 1 << lk;
+                        const int part = lane & (k - 1);
+                        for (int base = a; base <= b; base += 64 >> lk) {
+                            const int i = base + (lane >> lk);
+                            const bool row_ok = i <= b;
+                            const int ic = row_ok ? i : b;
+                            const int lo = ic + 1 > a_next ? ic + 1 : a_next;
+                            const int hi = mem_aware ? min((int)J[s * ls + ic], jhi) : jhi;
+                            const int n = row_ok && hi >= lo ? hi - lo + 1 : 0;
                             if (COUNT) {
-                                work += (unsigned long long)(jl - i);
+                                if (part == 0) work += (unsigned long long)n;
                                 continue;
                             }
-                            const V pi = Xs[i].x - p2p;                  // T(s,i,j) = P_s[j] - pi
-                            V acc = INF;
-                            int j = i + 1;
-                            for (; j + 3 <= jl; j += 4) {
-                                const V2 a = Xs[j], b = Xs[j + 1], c = Xs[j + 2], d = Xs[j + 3];
-                                acc = vmin(acc, vmin(vmin(relax<V>(a, pi), relax<V>(b, pi)),
-                                                     vmin(relax<V>(c, pi), relax<V>(d, pi))));
-                            }
-                            if (j <= jl) {                               // 1 to 3 ends left (padded by 4)
-                                const int rem = jl - j;
-                                const V2 a = Xs[j], b = Xs[j + 1], c = Xs[j + 2];
-                                const V cb = rem >= 1 ? relax<V>(b, pi) : INF;
-                                const V cc = rem >= 2 ? relax<V>(c, pi) : INF;
-                                acc = vmin(acc, vmin(relax<V>(a, pi), vmin(cb, cc)));
-                            }
-                            ((V *)&Xo[i])[1] = acc;
-                            Gs[i] = acc;
-                        }
-                        if (base <= ihi) {
-                            // r < 64 rows left: k lanes per row, k = 64 >> ceil(log2 r), each
-                            // lane striding over the row's ends by k
-                            const int r = ihi - base + 1;
-                            const int k = 64 >> (r > 1 ? 32 - __clz(r - 1) : 0);
-                            const int lk = 31 - __clz(k);
-                            const int part = lane & (k - 1);
-                            const int i = base + (lane >> lk);
-                            const bool row_ok = i <= ihi;
-                            const int ic = row_ok ? i : ihi;
-                            const int jl = row_ok ? Js[ic] : 0;
-                            if (COUNT) {
-                                if (row_ok && part == 0) work += (unsigned long long)(jl - i);
-                            } else {
-                                const V pi = Xs[ic].x - p2p;
-                                V acc = INF;
-                                for (int j = i + 1 + part; j <= jl; j += k) acc = vmin(acc, relax<V>(Xs[j], pi));
-                                acc = group_min<V>(acc, k);
-                                if (s == 0) {
-                                    Bv = (V)rl64((int64_t)acc, 0);       // one row: the whole wave's minimum
-                                } else if (row_ok && part == 0) {
-                                    ((V *)&Xo[i])[1] = acc;
-                                    Gs[i] = acc;
-                                }
-                            }
+                            const int c = (n + k - 1) >> lk;             // ends per lane
+                            const int js = lo + part * c;
+                            const int je = min(js + c - 1, hi);
+                            const V pi = Xs[ic].x - p2p;                 // T(s,i,j) = P_s[j] - pi
+                            V acc = relax_range<V>(Xs, js, row_ok ? je : js - 1, pi, INF);
+                            acc = group_min<V>(acc, k);
+                            if (s == 0) Bv = (V)rl64((int64_t)acc, 0);   // row 0 only: the whole wave's minimum
+                            else if (row_ok && part == 0) put_g(s, i, acc);
                         }
                     }
                     wave_sync();
@@ -284,32 +346,27 @@ __global__ void __launch_bounds__(256, sizeof(V) == 4 ? 5 : 4) split_kernel(DevP
                 const uint64_t B24 = F32 ? rne24(B) : B;       // fp32 bottleneck, as an exact integer
 
                 // ---------------- canonical reconstruction: smallest admissible end per stage
-                // (time prefixes from the profile's stage rows, DP rows and limits from LDS)
-                int cs = 0, my_start = 0, my_end = 0;
-                for (int s = 0; s < S; s++) {
+                int cs = 0, my_start = 0, my_end = L;
+                for (int s = 0; s < S - 1; s++) {
                     const V *prow = rows + uni(rl32(x.prow, s));
                     const V *Gn = G + (size_t)(s + 1) * gs;
-                    const uint8_t *Js = J + (size_t)s * gs;
                     const V p2p = (V)rl64(x.p2p, s);
+                    const int a_next = uni(rl32(Al, s + 1));
+                    const int lo = cs + 1 > a_next ? cs + 1 : a_next;
+                    const int hi = lim_of(s, cs);
+                    const V pc = prow[cs] - p2p;
                     int found = -1;
-                    for (int base = cs + 1; found < 0; base += 64) {
+                    for (int base = lo; found < 0; base += 64) {
                         const int j = base + lane;
-                        const int jc = j <= L ? j : L;
-                        const V pj = prow[jc];                   // issued together with the reads below
-                        const V pc = prow[cs] - p2p;
-                        const int jl = Js[cs];
-                        const V gj = s < S - 1 ? Gn[jc] : INF;
-                        bool ok = false;
-                        if (j <= jl) {
-                            const uint64_t T = (uint64_t)(V)(pj - pc);
-                            bool rest_ok;                      // the later stages complete within B*
-                            if (s == S - 1) rest_ok = j == L;
-                            else rest_ok = gj != INF && (F32 ? rne24((uint64_t)gj) <= B24 : (uint64_t)gj <= B);
-                            ok = rest_ok && (F32 ? rne24(T) <= B24 : T <= B);
-                        }
+                        const int jc = j <= hi ? j : hi;
+                        const V pj = prow[jc];                   // issued together with the read below
+                        const V gj = Gn[jc];
+                        const uint64_t T = (uint64_t)(V)(pj - pc);
+                        const bool ok = j <= hi && gj != INF &&
+                                        (F32 ? rne24((uint64_t)gj) <= B24 && rne24(T) <= B24 : (uint64_t)gj <= B && T <= B);
                         const uint64_t bal = __ballot(ok);
                         if (bal) found = base + __ffsll((unsigned long long)bal) - 1;
-                        else if (base + 63 >= jl) found = jl;      // unreachable: G[s][cs] <= B* has a witness;
+                        else if (base + 63 >= hi) found = hi;      // unreachable: G[s][cs] <= B* has a witness;
                                                                    // the fallback only keeps indexing in bounds
                     }
                     if (lane == s) {
@@ -318,6 +375,7 @@ __global__ void __launch_bounds__(256, sizeof(V) == 4 ? 5 : 4) split_kernel(DevP
                     }
                     cs = found;
                 }
+                if (lane == S - 1) my_start = cs;              // the last stage ends at L
                 for (uint64_t c = cls; c; c &= c - 1) {
                     const int k = __ffsll((unsigned long long)c) - 1;
                     for (int q = lane; q < A.s_max; q += 64)
@@ -386,20 +444,21 @@ int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const
 template <class V, bool F32, bool COUNT>
 static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t stream)
 {
-    const int L = p->dev.L;
+    const int L = p->dev.L, ls = p->dev.lim_stride;
     a.s_cap = a.s_max < L ? a.s_max : L;
     a.g_stride = L + 5;                                       // L + 1 ends and 4 of padding
-    // per wavefront: two rows of pairs {P_s, G_{s+1}}, then the DP rows and the
-    // end limits of every stage
+    // per wavefront: two alternating pair rows {P_s, G_{s+1}}, the DP row of
+    // every stage, then the memory-limit row of every stage
     const size_t g_off = (size_t)2 * a.g_stride * 2 * sizeof(V);
-    const size_t j_off = g_off + (size_t)a.s_cap * a.g_stride * sizeof(V);
+    const size_t j_off = (g_off + (size_t)a.s_cap * a.g_stride * sizeof(V) + 15) & ~size_t(15);
     a.off_g = (int32_t)g_off;
     a.off_j = (int32_t)j_off;
-    a.lds_per_wave = (int32_t)((j_off + (size_t)a.s_cap * a.g_stride + 15) & ~size_t(15));
+    a.lds_per_wave = (int32_t)((j_off + (size_t)a.s_cap * ls + 15) & ~size_t(15));
     int max_lds = 0;
     HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
-    int wpb = max_lds / a.lds_per_wave;
-    wpb = wpb > 4 ? 4 : (wpb < 1 ? 1 : wpb);
+    // one wavefront per workgroup: a wavefront's LDS is released as soon as it
+    // is done, whatever the other wavefronts on the CU are doing
+    const int wpb = 1;
     const size_t lds = (size_t)wpb * a.lds_per_wave;
     if (lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "DP table of this (L, s_max) does not fit in LDS");
     if (lds > 65536)

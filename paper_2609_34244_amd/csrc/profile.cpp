@@ -195,16 +195,18 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
     // lim[g][k][e][f-1][i] is the largest end j >= i such that layers [i, j)
     // fit one GPU's memory. Ends that fit form a prefix because every term is
     // non-negative, so one two-pointer sweep per (g, k, e, f) builds a row.
+    // Rows are padded to a multiple of 16 bytes so kernels copy them as dwords.
     const int F = std::min(L, HEDDLE_MAX_STAGES);
-    const size_t lim_entries = (size_t)N * K * E * F * R;
+    const int RL = (R + 15) & ~15;
+    const size_t lim_entries = (size_t)N * K * E * F * RL;
     if (lim_entries > kMaxLimitTable) return fail(HEDDLE_E_RANGE, "memory-limit table would exceed 256 MB");
-    std::vector<uint8_t> lim_tab(lim_entries);
+    std::vector<uint8_t> lim_tab(lim_entries, 0);
     for (int g = 0; g < N; g++)
         for (int k = 0; k < K; k++)
             for (int e = 0; e < E; e++)
                 for (int f = 1; f <= F; f++) {
                     const int64_t *w = &pre_state[(k * E + e) * R], *a = &pre_act[k * R];
-                    uint8_t *row = &lim_tab[((((size_t)g * K + k) * E + e) * F + (f - 1)) * R];
+                    uint8_t *row = &lim_tab[((((size_t)g * K + k) * E + e) * F + (f - 1)) * RL];
                     int j = 0;
                     for (int i = 0; i <= L; i++) {
                         if (j < i) j = i;
@@ -337,6 +339,7 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
     dp.rows32[0] = (const uint32_t *)(base + o_r32a);
     dp.rows32[1] = (const uint32_t *)(base + o_r32b);
     dp.n_f = F;
+    dp.lim_stride = RL;
     p->dev = dp;
     p->max_stage_ns = (int64_t)max_stage;
     p->max_ar_ns = (int64_t)max_ar;

@@ -353,3 +353,68 @@ def test_count_relaxations_full_triangle():
         n = L - S + 1
         want = 1 if S == 1 else n + (S - 2) * n * (n + 1) // 2 + n
         assert O.count_relaxations(op, S, rec[0], S, 1) == want
+
+
+def _cap_profile(L, cap):
+    """one GPU type, unit state bytes per layer, no activations: a stage fits
+    at most `cap` layers"""
+    d = dict(L=L, tp_degrees=[1], ep_degrees=[1], layer_ns=[[[1] * L]], profiled=[[1]], is_moe=[0] * L,
+             state_bytes=[[1] * L], xstate_bytes=[[0] * L], act_bytes=[[0] * L], grad_bytes=[[0] * L],
+             xgrad_bytes=[[0] * L], boundary_bytes=0, a2a_bytes=0, mem_cap_bytes=[cap], node_size=[8],
+             n_gpus=[1000], intra_bw_MBps=[1000], link_bw_MBps=[[1000]])
+    return O.OracleProfile(profile_from_json(d))
+
+
+@pytest.mark.parametrize("cap, want", [(1, 0), (2, 3), (3, 13), (4, 18)])
+def test_count_relaxations_memory_windows(cap, want):
+    """Worked by hand for L = 6, S = 3, at most `cap` layers per stage.
+    cap 1: 3 layers < 6, nothing fits. cap 2: only (2,2,2) fits, one
+    relaxation per stage. cap 3: stage 0 reaches starts <= 3, stage 2 must
+    start at >= 3, so stage 0 relaxes row 0 against ends 1..3 (3), stage 1
+    rows 1..3 against ends >= 3 up to min(i + 3, 5) (2 + 3 + 2), stage 2 rows
+    3..5 (3). cap 4: stage 0 ends 1..4 (4), stage 1 rows 1..4, ends >= 2 up to
+    min(i + 4, 5) (4 + 3 + 2 + 1), stage 2 rows 2..5 (4)."""
+    op = _cap_profile(6, cap)
+    _, rec = one_template([(0, 1, 1, 1)] * 3)
+    assert O.count_relaxations(op, 3, rec[0], 3, 1) == want
+
+
+def test_count_relaxations_covers_every_feasible_split():
+    """On random memory-bound instances: the count covers every relaxation
+    that some memory-feasible split uses (so it is zero only when no split
+    fits), and never exceeds the memory-feasible relaxations of the
+    unrestricted recurrence (brute force over all compositions). A layer too
+    large for a stage on its own can leave a window non-empty although no
+    split fits; the recurrence then finds no finite bottleneck."""
+    n_feasible = n_empty = 0
+    for seed in range(40):
+        w = random_instance(seed, cap_scale=0.6)
+        op = O.OracleProfile(w.profile)
+        p = w.profile
+        for t in range(w.n):
+            S = int(w.n_stages[t])
+            stt, st = brute.status_of(p, S, w.s_max, w.stages[t])
+            if stt != 0:
+                continue
+            plan = brute.Plan(p, st)
+            m = int(w.m[0])
+            Mp = brute.ceil_div(m, st[0]["dp"])
+            fits = lambda s, i, j: plan.stage(s, i, j, Mp)[1] <= int(p.mem_cap_bytes[st[s]["g"]])
+            used = set()
+            for comp in brute.compositions(p.L, S):
+                cuts = np.concatenate([[0], np.cumsum(comp)]).astype(int)
+                if all(fits(s, cuts[s], cuts[s + 1]) for s in range(S)):
+                    used |= {(s, int(cuts[s]), int(cuts[s + 1])) for s in range(S)}
+            full = 0
+            for s in range(S):
+                for i in range(s, (0 if s == 0 else p.L - (S - s)) + 1):
+                    for j in range(p.L if s == S - 1 else i + 1, p.L - (S - 1 - s) + 1):
+                        full += fits(s, i, j)
+            c = O.count_relaxations(op, S, w.stages[t], w.s_max, m)
+            assert c <= full, (seed, t, c, full)
+            if used:
+                assert c >= len(used), (seed, t, len(used), c)
+                n_feasible += 1
+            elif c == 0:
+                n_empty += 1
+    assert n_feasible > 100 and n_empty > 20, (n_feasible, n_empty)

@@ -46,9 +46,11 @@ struct DevProfile {
     const int64_t *intra_bw;         // [n_types] MB/s
     const int64_t *link_bw;          // [n_types][n_types] MB/s
     const int32_t *ep_degrees;       // [n_ep]
-    const uint8_t *mem_lim;          // [n_types][n_tp][n_ep][n_f][lim_stride] largest end that fits from row i
+    // [n_types][n_tp][n_ep][n_f][2][lim_stride]: per row, the largest end that
+    // fits from row i, then its inverse (smallest row whose limit reaches x)
+    const uint8_t *mem_lim;
     int32_t n_f;                     // in-flight counts covered by mem_lim: 1 .. min(L, 64)
-    int32_t lim_stride;              // bytes per mem_lim row: L + 1 rounded up to a multiple of 16
+    int32_t lim_stride;              // bytes per half-row: L + 1 rounded up to a multiple of 16
     // [n_types][n_tp][3][L+1] stage time prefix (layer costs + all-to-all of the
     // variant); index 0: int64 ns, 1: fp32 image in fixed point; the 32-bit
     // copies exist only when the range proof allows narrowing
@@ -93,10 +95,10 @@ struct PriceArgs {
     int64_t *peak_mem;
     uint8_t *layers, *status;
     unsigned long long *work;        // count-only launches: accumulated relaxations
-    int32_t g_stride;                // LDS entries per DP table row (L + 1)
-    int32_t s_cap;                   // DP table rows: min(s_max, L)
+    int32_t g_stride;                // LDS entries per pair row (L + 1 and padding)
+    int32_t s_cap;                   // stage rows: min(s_max, L)
     int32_t lds_per_wave;            // bytes of one wavefront's LDS region
-    int32_t off_g, off_j;            // byte offsets of the DP rows and of the end-limit table
+    int32_t off_j, off_x;            // byte offsets of the limit rows and of the inverse / next-row rows
 };
 
 int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,

@@ -86,7 +86,7 @@ __device__ StageInfo decode(const DevProfile &P, const PriceArgs &A, int S, uint
 
     if (act) {
         x.prow = ((g * P.n_tp + ki) * 3 + a2a_variant(ep, tp, node)) * R;
-        x.lrow = ((g * P.n_tp + ki) * P.n_ep + ei) * P.n_f * P.lim_stride;
+        x.lrow = ((g * P.n_tp + ki) * P.n_ep + ei) * P.n_f * 2 * P.lim_stride;
         x.p2p = lane < x.S - 1 ? p2p : 0;
     }
     return x;
@@ -152,41 +152,48 @@ template <class V, class V2> __device__ __forceinline__ V relax_range(const V2 *
 // non-decreasing in i. So the starts stage s can be reached at from row 0 lie
 // in [s, R_s] with R_0 = 0 and R_{s+1} = lim(s, R_s), and the rows from which
 // stages s..S-1 can still complete lie in [Bk_s, L - (S - s)] with Bk_S = L and
-// Bk_s the smallest i with lim(s, i) >= Bk_{s+1}. Rows outside the window
-// W_s = [max(s, Bk_s), min(R_s, L - (S - s))] are unreachable or have G = inf,
-// so the DP relaxes only rows of W_s and ends in W_{s+1}, which gives the same
-// G on every row of every complete split, hence the same B* and the same
-// canonical split. An empty window means no split fits memory.
+// Bk_s the smallest i >= s whose limit reaches Bk_{s+1} (an inverse-limit
+// table lookup). Rows outside the window
+// W_s = [Bk_s, min(R_s, L - (S - s))] are unreachable or have G = inf, so the
+// DP relaxes only rows of W_s and ends in W_{s+1}, which gives the same G on
+// every row of every complete split, hence the same B*. An empty window means
+// no split fits memory.
+//
+// Canonical split without stored DP rows. Given B*, let F_s[i] be true when
+// stages s..S-1 can cover [i, L) with bottleneck <= B*, i.e. G_s[i] <= B*.
+// Because T(s, i, j) grows with j, F_s[i] holds exactly when the smallest j
+// >= max(i + 1, Bk_{s+1}) with F_{s+1}[j] (call it nx(i)) is admissible and
+// T(s, i, nx(i)) <= B*. A second backward pass evaluates F_s this way for the
+// window rows and stores, per row, the next row at or after it with F true;
+// the forward reconstruction then takes c_{s+1} = nx(c_s), which is the
+// smallest admissible end keeping an optimal completion at every stage, i.e.
+// the lexicographically smallest optimal split.
 
 template <class V, bool F32, bool COUNT>
-__global__ void __launch_bounds__(64, sizeof(V) == 4 ? 5 : 3) split_kernel(DevProfile P, PriceArgs A)
+__global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevProfile P, PriceArgs A)
 {
     typedef typename Vec2<V>::type V2;
     constexpr int kBatch = 4;                                  // stages whose limit rows are loaded together
-    extern __shared__ __align__(16) unsigned char smem[];
-    const int lane = threadIdx.x & 63, wib = threadIdx.x >> 6, wpb = blockDim.x >> 6;
+    constexpr int kNone = 255;                                 // no row with F true at or after this one
+    extern __shared__ __align__(16) unsigned char smem[];      // one wavefront per workgroup
+    const int lane = threadIdx.x;
     const int L = P.L, gs = A.g_stride, ls = P.lim_stride;
     const bool mem_aware = (A.flags & HEDDLE_F_COMPUTE_ONLY) == 0;
     const V INF = DPInf<V>::value;
-    unsigned char *wave_lds = smem + (size_t)wib * A.lds_per_wave;
-    V2 *W = (V2 *)wave_lds;                                    // two alternating pair rows: [2][gs]
-    V *G = (V *)(wave_lds + A.off_g);                          // [s_cap][gs] DP rows, for the reconstruction
-    uint8_t *J = wave_lds + A.off_j;                           // [s_cap][ls] memory limits per stage
+    V2 *W = (V2 *)smem;                                        // [2][gs] alternating pair rows {P_s, G_{s+1}}
+    uint8_t *J = smem + A.off_j;                               // [s_cap][ls] limits of every stage
+    uint8_t *X = smem + A.off_x;                               // [s_cap][ls] inverse limits, then next rows with F
     const V *rows = stage_rows<V>(P, F32);
-    const int ldw = ls >> 2;                                   // dwords per limit row (<= 64)
+    const int ldw = ls >> 2;                                   // dwords per limit half-row (<= 64)
     auto pair_row = [&](int s) -> V2 * { return W + (size_t)(s & 1) * gs; };
-    auto put_g = [&](int s, int i, V g) {                      // G_s[i], s >= 1
-        ((V *)&pair_row(s - 1)[i])[1] = g;
-        G[(size_t)s * gs + i] = g;
-    };
 
     int my_m = 1;                                              // lane k: the k-th micro-batch count
     for (int k = 0; k < A.n_m; k++) my_m = lane == k ? A.m[k] : my_m;
     unsigned long long work = 0;
 
     // the template records of the next iteration are loaded one iteration ahead
-    const int64_t stride = (int64_t)gridDim.x * wpb;
-    int64_t t = (int64_t)blockIdx.x * wpb + wib;
+    const int64_t stride = gridDim.x;
+    int64_t t = blockIdx.x;
     int S_next = 0;
     uint32_t rec_next = 0;
     if (t < A.n) {
@@ -218,61 +225,67 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 5 : 3) split_kernel(DevPr
                 const uint64_t cls = __ballot(lane < A.n_m && key_k == key) & todo;
                 todo &= ~cls;
                 auto jhi_of = [&](int s) { return L - (S - 1 - s); };   // last end leaving a layer per later stage
-                auto lim_of = [&](int s, int i) {                       // lim(s, i), i uniform
+                auto lim_of = [&](int s, int i) {                       // lim(s, i)
                     return mem_aware ? min((int)J[s * ls + i], jhi_of(s)) : jhi_of(s);
                 };
 
-                // ---------------- memory-limit rows of every stage (this class) into LDS,
-                // kBatch stages per round trip
+                // ---------------- limit rows and their inverses, every stage of this class,
+                // into LDS; kBatch stages per round trip
                 if (mem_aware) {
-                    wave_sync();                                        // earlier reads of J are done
+                    wave_sync();                                        // earlier reads of J and X are done
                     int f = min(S - lane, key);
                     f = f < 1 ? 1 : f;
-                    const int my_row = x.lrow + (f - 1) * ls;          // lane s: stage s's limit row, this class
+                    const int my_row = x.lrow + (f - 1) * 2 * ls;      // lane s: stage s's rows, this class
+                    const uint32_t *lim32 = (const uint32_t *)P.mem_lim;
                     for (int s0 = 0; s0 < S; s0 += kBatch) {
-                        uint32_t jv[kBatch];
+                        uint32_t v[kBatch][2];
 #pragma unroll
-                        for (int u = 0; u < kBatch; u++)
-                            if (s0 + u < S && lane < ldw)
-                                jv[u] = ((const uint32_t *)P.mem_lim)[(uni(rl32(my_row, s0 + u)) >> 2) + lane];
+                        for (int u = 0; u < kBatch; u++) {
+                            if (s0 + u < S) {
+                                const int base = uni(rl32(my_row, s0 + u)) >> 2;
 #pragma unroll
-                        for (int u = 0; u < kBatch; u++)
-                            if (s0 + u < S && lane < ldw) ((uint32_t *)J)[(s0 + u) * ldw + lane] = jv[u];
+                                for (int h = 0; h < 2; h++)
+                                    if (64 * h < 2 * ldw && lane + 64 * h < 2 * ldw) v[u][h] = lim32[base + lane + 64 * h];
+                            }
+                        }
+#pragma unroll
+                        for (int u = 0; u < kBatch; u++) {
+                            if (s0 + u < S) {
+#pragma unroll
+                                for (int h = 0; h < 2; h++) {
+                                    const int d = lane + 64 * h;
+                                    if (64 * h < 2 * ldw && d < 2 * ldw) {
+                                        uint32_t *dst = (uint32_t *)(d < ldw ? J : X);
+                                        dst[(s0 + u) * ldw + (d < ldw ? d : d - ldw)] = v[u][h];
+                                    }
+                                }
+                            }
+                        }
                     }
                     wave_sync();
                 }
 
                 // ---------------- row windows: lane s holds [a_s, b_s]
-                int Rl = 0;                                             // lane s: R_s
+                int Al = lane, Bl = 0;
+                bool feasible = true;
                 {
+                    int Rl = 0;                                         // lane s: R_s
                     int c = 0;
                     for (int s = 1; s < S; s++) {
                         c = uni(lim_of(s - 1, c));
                         Rl = lane == s ? c : Rl;
                     }
-                }
-                int Al = 0, Bl = 0;
-                bool feasible = true;
-                {
                     int nxt = L;                                       // Bk_{s+1}
                     for (int s = S - 1; s >= 0; s--) {
                         const int ihi = (s == 0) ? 0 : L - (S - s);
                         const int R_s = rl32(Rl, s);
                         const int b = R_s < ihi ? R_s : ihi;
-                        int a = -1;
-                        if (!mem_aware) {
-                            a = s <= b ? s : -1;
-                        } else {
-                            for (int base = s; base <= b; base += 64) {   // J is non-decreasing along a row
-                                const int i = base + lane;
-                                const uint64_t hit = __ballot(i <= b && (int)J[s * ls + min(i, b)] >= nxt);
-                                if (hit) {
-                                    a = base + __ffsll((unsigned long long)hit) - 1;
-                                    break;
-                                }
-                            }
+                        int a = s;
+                        if (mem_aware) {
+                            const int inv = uni((int)X[s * ls + nxt]);
+                            a = inv > s ? inv : s;
                         }
-                        if (a < 0) {
+                        if (a > b) {
                             feasible = false;
                             break;
                         }
@@ -291,6 +304,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 5 : 3) split_kernel(DevPr
                     const int a = uni(rl32(Al, s)), b = uni(rl32(Bl, s));
                     const int e = s == S - 1 ? L : uni(rl32(Bl, s + 1));     // last end of any row
                     V2 *Xs = pair_row(s);
+                    V2 *Xo = pair_row(s + 1);                          // receives G_s (pair row of stage s-1)
 #pragma unroll
                     for (int q = 0; q < kRowSlots; q++)
                         if (64 * q <= e - a) ((V *)&Xs[min(a + lane + 64 * q, e)])[0] = rr.p[q];
@@ -303,7 +317,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 5 : 3) split_kernel(DevPr
                         } else {
                             for (int i = a + lane; i <= b; i += 64) {
                                 const V gv = (V)(Xs[L].x - Xs[i].x);
-                                if (s > 0) put_g(s, i, gv);
+                                if (s > 0) ((V *)&Xo[i])[1] = gv;
                                 else Bv = gv;                          // S = 1: row 0, lane 0
                             }
                             if (S == 1) Bv = (V)rl64((int64_t)Bv, 0);
@@ -335,7 +349,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 5 : 3) split_kernel(DevPr
                             V acc = relax_range<V>(Xs, js, row_ok ? je : js - 1, pi, INF);
                             acc = group_min<V>(acc, k);
                             if (s == 0) Bv = (V)rl64((int64_t)acc, 0);   // row 0 only: the whole wave's minimum
-                            else if (row_ok && part == 0) put_g(s, i, acc);
+                            else if (row_ok && part == 0) ((V *)&Xo[i])[1] = acc;
                         }
                     }
                     wave_sync();
@@ -344,36 +358,54 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 5 : 3) split_kernel(DevPr
                 if (Bv == INF) continue;                       // no split fits memory
                 const uint64_t B = (uint64_t)Bv;
                 const uint64_t B24 = F32 ? rne24(B) : B;       // fp32 bottleneck, as an exact integer
+                auto within = [&](uint64_t T) { return F32 ? rne24(T) <= B24 : T <= B; };
 
-                // ---------------- canonical reconstruction: smallest admissible end per stage
+                // ---------------- F_s for stages S-1 .. 1; X[s][i] := the smallest row >= i of
+                // W_s with F_s true (kNone if there is none)
+                for (int s = S - 1; s >= 1; s--) {
+                    const int a = uni(rl32(Al, s)), b = uni(rl32(Bl, s));
+                    const V *prow = rows + uni(rl32(x.prow, s));
+                    const V p2p = (V)rl64(x.p2p, s);
+                    const int a_next = s < S - 1 ? uni(rl32(Al, s + 1)) : L;
+                    const int jhi = jhi_of(s);
+                    const uint8_t *NXn = X + (s + 1) * ls;
+                    uint8_t *NXs = X + s * ls;
+                    int first_above = kNone;                           // smallest row with F true in higher slots
+                    for (int q = (b - a) >> 6; q >= 0; q--) {
+                        const int i = a + 64 * q + lane;
+                        const bool row_ok = i <= b;
+                        const int ic = row_ok ? i : b;
+                        int nx = L;                                    // last stage: the end is L
+                        bool ok = row_ok;
+                        if (s < S - 1) {
+                            const int lo = ic + 1 > a_next ? ic + 1 : a_next;
+                            const int hi = mem_aware ? min((int)J[s * ls + ic], jhi) : jhi;
+                            nx = lo <= hi ? (int)NXn[lo] : kNone;
+                            ok = ok && nx <= hi;
+                        }
+                        const int nxc = nx <= L ? nx : L;
+                        ok = ok && within((uint64_t)(V)(prow[nxc] - prow[ic] + p2p));
+                        const uint64_t mask = __ballot(ok);
+                        const uint64_t rest = mask >> lane;            // rows >= i of this slot with F true
+                        const int nxi = rest ? i + __ffsll((unsigned long long)rest) - 1 : first_above;
+                        if (row_ok) NXs[i] = (uint8_t)nxi;
+                        if (mask) first_above = a + 64 * q + __ffsll((unsigned long long)mask) - 1;
+                    }
+                    wave_sync();
+                }
+
+                // ---------------- canonical reconstruction: c_{s+1} = nx(c_s)
                 int cs = 0, my_start = 0, my_end = L;
                 for (int s = 0; s < S - 1; s++) {
-                    const V *prow = rows + uni(rl32(x.prow, s));
-                    const V *Gn = G + (size_t)(s + 1) * gs;
-                    const V p2p = (V)rl64(x.p2p, s);
                     const int a_next = uni(rl32(Al, s + 1));
                     const int lo = cs + 1 > a_next ? cs + 1 : a_next;
-                    const int hi = lim_of(s, cs);
-                    const V pc = prow[cs] - p2p;
-                    int found = -1;
-                    for (int base = lo; found < 0; base += 64) {
-                        const int j = base + lane;
-                        const int jc = j <= hi ? j : hi;
-                        const V pj = prow[jc];                   // issued together with the read below
-                        const V gj = Gn[jc];
-                        const uint64_t T = (uint64_t)(V)(pj - pc);
-                        const bool ok = j <= hi && gj != INF &&
-                                        (F32 ? rne24((uint64_t)gj) <= B24 && rne24(T) <= B24 : (uint64_t)gj <= B && T <= B);
-                        const uint64_t bal = __ballot(ok);
-                        if (bal) found = base + __ffsll((unsigned long long)bal) - 1;
-                        else if (base + 63 >= hi) found = hi;      // unreachable: G[s][cs] <= B* has a witness;
-                                                                   // the fallback only keeps indexing in bounds
-                    }
+                    int nx = uni((int)X[(s + 1) * ls + (lo <= L ? lo : L)]);
+                    nx = nx <= L ? nx : L;                             // unreachable: F_s[c_s] holds on the path
                     if (lane == s) {
                         my_start = cs;
-                        my_end = found;
+                        my_end = nx;
                     }
-                    cs = found;
+                    cs = nx;
                 }
                 if (lane == S - 1) my_start = cs;              // the last stage ends at L
                 for (uint64_t c = cls; c; c &= c - 1) {
@@ -447,13 +479,13 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     const int L = p->dev.L, ls = p->dev.lim_stride;
     a.s_cap = a.s_max < L ? a.s_max : L;
     a.g_stride = L + 5;                                       // L + 1 ends and 4 of padding
-    // per wavefront: two alternating pair rows {P_s, G_{s+1}}, the DP row of
-    // every stage, then the memory-limit row of every stage
-    const size_t g_off = (size_t)2 * a.g_stride * 2 * sizeof(V);
-    const size_t j_off = (g_off + (size_t)a.s_cap * a.g_stride * sizeof(V) + 15) & ~size_t(15);
-    a.off_g = (int32_t)g_off;
+    // per wavefront: two alternating pair rows {P_s, G_{s+1}}, then for every
+    // stage its limit row and its inverse-limit row (later its next-row table)
+    const size_t j_off = ((size_t)2 * a.g_stride * 2 * sizeof(V) + 15) & ~size_t(15);
+    const size_t x_off = j_off + (size_t)a.s_cap * ls;
     a.off_j = (int32_t)j_off;
-    a.lds_per_wave = (int32_t)((j_off + (size_t)a.s_cap * ls + 15) & ~size_t(15));
+    a.off_x = (int32_t)x_off;
+    a.lds_per_wave = (int32_t)((x_off + (size_t)a.s_cap * ls + 15) & ~size_t(15));
     int max_lds = 0;
     HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
     // one wavefront per workgroup: a wavefront's LDS is released as soon as it

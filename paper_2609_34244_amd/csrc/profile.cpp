@@ -192,13 +192,16 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
     }
     // Memory limits of a stage (section 5.2 memory validation): for GPU type g,
     // TP index k, EP index e and f micro-batches of activations in flight,
-    // lim[g][k][e][f-1][i] is the largest end j >= i such that layers [i, j)
-    // fit one GPU's memory. Ends that fit form a prefix because every term is
-    // non-negative, so one two-pointer sweep per (g, k, e, f) builds a row.
-    // Rows are padded to a multiple of 16 bytes so kernels copy them as dwords.
+    // lim[i] is the largest end j >= i such that layers [i, j) fit one GPU's
+    // memory. Ends that fit form a prefix because every term is non-negative,
+    // so one two-pointer sweep per (g, k, e, f) builds a row; lim is
+    // non-decreasing in i. Each limit row is followed by its inverse,
+    // inv[x] = the smallest i with lim[i] >= x (lim[L] = L, so x <= L always
+    // has one). Half-rows are padded to a multiple of 16 bytes so kernels copy
+    // them as dwords.
     const int F = std::min(L, HEDDLE_MAX_STAGES);
     const int RL = (R + 15) & ~15;
-    const size_t lim_entries = (size_t)N * K * E * F * RL;
+    const size_t lim_entries = (size_t)N * K * E * F * 2 * RL;
     if (lim_entries > kMaxLimitTable) return fail(HEDDLE_E_RANGE, "memory-limit table would exceed 256 MB");
     std::vector<uint8_t> lim_tab(lim_entries, 0);
     for (int g = 0; g < N; g++)
@@ -206,12 +209,18 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
             for (int e = 0; e < E; e++)
                 for (int f = 1; f <= F; f++) {
                     const int64_t *w = &pre_state[(k * E + e) * R], *a = &pre_act[k * R];
-                    uint8_t *row = &lim_tab[((((size_t)g * K + k) * E + e) * F + (f - 1)) * RL];
+                    uint8_t *row = &lim_tab[((((size_t)g * K + k) * E + e) * F + (f - 1)) * 2 * RL];
+                    uint8_t *inv = row + RL;
                     int j = 0;
                     for (int i = 0; i <= L; i++) {
                         if (j < i) j = i;
                         while (j < L && (w[j + 1] - w[i]) + (i128)f * (a[j + 1] - a[i]) <= d->mem_cap_bytes[g]) j++;
                         row[i] = (uint8_t)j;
+                    }
+                    int i = 0;
+                    for (int x = 0; x <= L; x++) {
+                        while (row[i] < x) i++;
+                        inv[x] = (uint8_t)i;
                     }
                 }
     // gradient synchronisation is below 2 * bytes * 1000 / min bandwidth (+1 per ceiling)

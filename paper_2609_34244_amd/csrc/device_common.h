@@ -23,6 +23,10 @@ __device__ __forceinline__ int64_t rl64(int64_t v, int lane)
     return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
+// lane `lane` of a 32- or 64-bit value, as a wave-uniform value
+__device__ __forceinline__ uint32_t uni64(uint32_t v, int lane) { return (uint32_t)__builtin_amdgcn_readlane((int)v, lane); }
+__device__ __forceinline__ uint64_t uni64(uint64_t v, int lane) { return (uint64_t)rl64((int64_t)v, lane); }
+
 template <class T> __device__ __forceinline__ T wave_min(T v)
 {
 #pragma unroll
@@ -63,6 +67,7 @@ constexpr int kDppXor1 = 0xB1;          // quad_perm [1,0,3,2]
 constexpr int kDppXor2 = 0x4E;          // quad_perm [2,3,0,1]
 constexpr int kDppHalfMirror = 0x141;   // lane i <-> 7 - i within 8
 constexpr int kDppMirror = 0x140;       // lane i <-> 15 - i within 16
+constexpr int kDppWaveShl1 = 0x130;     // lane i <- lane i + 1 across the wavefront (lane 63 keeps its own)
 
 // minimum over aligned groups of k lanes (k a power of two, 1 .. 64, uniform);
 // every lane of a group receives the group's minimum

@@ -98,7 +98,7 @@ struct PriceArgs {
     int32_t g_stride;                // LDS entries per pair row (L + 1 and padding)
     int32_t s_cap;                   // stage rows: min(s_max, L)
     int32_t lds_per_wave;            // bytes of one wavefront's LDS region
-    int32_t off_j, off_x;            // byte offsets of the limit rows and of the inverse / next-row rows
+    int32_t off_j, off_c;            // byte offsets of the per-stage limit rows and of the type counters
 };
 
 int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,

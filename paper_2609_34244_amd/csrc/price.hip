@@ -34,21 +34,23 @@
 namespace heddle {
 
 // Per-lane (lane = stage s) decoded record and stage constants.
-struct StageInfo {
+template <class V> struct StageInfo {
     int status;              // uniform: HEDDLE_S_* of the template (0 if valid)
     int S, D;                // uniform
     int prow;                // offset of the stage's time-prefix row
     int lrow;                // offset of the stage's memory-limit rows (in-flight count 1)
-    int64_t p2p;             // outbound p2p (ns, or fixed point for fp32)
+    V p2p;                   // outbound p2p (ns, or fixed point for fp32)
 };
 
 // Template decode and validation (feasibility masks of section 5.1, exact
 // profile match of section 5.2). All per-lane table reads are issued at once
 // on clamped indices; the checks then run in status order over all stages.
-template <bool F32>
-__device__ StageInfo decode(const DevProfile &P, const PriceArgs &A, int S, uint32_t rec_in, int lane)
+// `cnt` is a per-wavefront LDS array with one counter per GPU type.
+template <class V, bool F32>
+__device__ StageInfo<V> decode(const DevProfile &P, const PriceArgs &A, int S, uint32_t rec_in, int lane,
+                               uint32_t *cnt)
 {
-    StageInfo x;
+    StageInfo<V> x;
     const int L = P.L, R = L + 1, N = P.n_types;
     x.S = S;
     x.status = 0;
@@ -63,7 +65,7 @@ __device__ StageInfo decode(const DevProfile &P, const PriceArgs &A, int S, uint
     const int tp = 1 << l2tp, ep = 1 << l2ep;
     const int ki = nibble(P.tp_index, l2tp), ei = nibble(P.ep_index, l2ep);
     const int gc = g < N ? g : N - 1;                          // clamped for speculative reads
-    const int gn = __shfl(gc, lane + 1 < 64 ? lane + 1 : 63);
+    const int gn = __builtin_amdgcn_update_dpp(gc, gc, kDppWaveShl1, 0xF, 0xF, false);   // next stage's type
     const int node = P.node_size[gc];
     const int prof = P.profiled[gc * P.n_tp + ki];
     const int ngpu = P.n_gpus[gc];
@@ -79,15 +81,20 @@ __device__ StageInfo decode(const DevProfile &P, const PriceArgs &A, int S, uint
         x.status = HEDDLE_S_BAD_EP;
         return x;
     }
-    int used = 0;                                              // this lane's type: sum of TP over its stages
-    for (int s2 = 0; s2 < x.S; s2++)
-        if (rl32(g, s2) == g) used += rl32(tp, s2);
+    // GPUs of this lane's type used by the template: sum of TP over its stages
+    // (times D below), accumulated with LDS atomics
+    wave_sync();
+    if (act) cnt[g] = 0;
+    wave_sync();
+    if (act) atomicAdd(&cnt[g], (uint32_t)tp);
+    wave_sync();
+    const uint32_t used = act ? cnt[g] : 0u;
     if (__ballot(act && (int64_t)used * x.D > ngpu)) { x.status = HEDDLE_S_OVERSUBSCRIBED; return x; }
 
     if (act) {
         x.prow = ((g * P.n_tp + ki) * 3 + a2a_variant(ep, tp, node)) * R;
         x.lrow = ((g * P.n_tp + ki) * P.n_ep + ei) * P.n_f * 2 * P.lim_stride;
-        x.p2p = lane < x.S - 1 ? p2p : 0;
+        x.p2p = lane < x.S - 1 ? (V)p2p : (V)0;
     }
     return x;
 }
@@ -126,21 +133,18 @@ template <class V, class V2> __device__ __forceinline__ V relax(const V2 &a, V p
 
 template <class T> __device__ __forceinline__ T vmin(T a, T b) { return a < b ? a : b; }
 
-// min over the ends [j, je] of one row, four ends per step (entries up to
-// je + 2 must lie inside the pair row)
+// min over the ends [j, je] of one row, in steps of four ends; the ends of
+// the last step past je are read (they lie inside the pair row) and masked
 template <class V, class V2> __device__ __forceinline__ V relax_range(const V2 *X, int j, int je, V pi, V acc)
 {
     const V INF = DPInf<V>::value;
-    for (; j + 3 <= je; j += 4) {
+    for (; j <= je; j += 4) {
         const V2 a = X[j], b = X[j + 1], c = X[j + 2], d = X[j + 3];
-        acc = vmin(acc, vmin(vmin(relax<V>(a, pi), relax<V>(b, pi)), vmin(relax<V>(c, pi), relax<V>(d, pi))));
-    }
-    if (j <= je) {                                       // 1 to 3 ends left
         const int rem = je - j;
-        const V2 a = X[j], b = X[j + 1], c = X[j + 2];
-        const V cb = rem >= 1 ? relax<V>(b, pi) : INF;
-        const V cc = rem >= 2 ? relax<V>(c, pi) : INF;
-        acc = vmin(acc, vmin(relax<V>(a, pi), vmin(cb, cc)));
+        const V rb = rem >= 1 ? relax<V>(b, pi) : INF;
+        const V rc = rem >= 2 ? relax<V>(c, pi) : INF;
+        const V rd = rem >= 3 ? relax<V>(d, pi) : INF;
+        acc = vmin(vmin(acc, relax<V>(a, pi)), vmin(rb, vmin(rc, rd)));
     }
     return acc;
 }
@@ -181,11 +185,15 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
     const bool mem_aware = (A.flags & HEDDLE_F_COMPUTE_ONLY) == 0;
     const V INF = DPInf<V>::value;
     V2 *W = (V2 *)smem;                                        // [2][gs] alternating pair rows {P_s, G_{s+1}}
-    uint8_t *J = smem + A.off_j;                               // [s_cap][ls] limits of every stage
-    uint8_t *X = smem + A.off_x;                               // [s_cap][ls] inverse limits, then next rows with F
+    // [s_cap][2][ls] per stage: limit row, then inverse-limit row (later the
+    // next-row table of the second pass)
+    uint8_t *JX = smem + A.off_j;
+    uint32_t *cnt = (uint32_t *)(smem + A.off_c);              // [n_types] GPU counters of decode
     const V *rows = stage_rows<V>(P, F32);
-    const int ldw = ls >> 2;                                   // dwords per limit half-row (<= 64)
+    const int nd = ls >> 1;                                    // dwords per stage in JX (<= 128)
     auto pair_row = [&](int s) -> V2 * { return W + (size_t)(s & 1) * gs; };
+    auto jrow = [&](int s) -> uint8_t * { return JX + s * 2 * ls; };
+    auto xrow = [&](int s) -> uint8_t * { return JX + s * 2 * ls + ls; };
 
     int my_m = 1;                                              // lane k: the k-th micro-batch count
     for (int k = 0; k < A.n_m; k++) my_m = lane == k ? A.m[k] : my_m;
@@ -207,7 +215,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
             S_next = A.n_stages[t + stride];
             rec_next = lane < A.s_max ? A.stages[(t + stride) * A.s_max + lane] : 0u;
         }
-        const StageInfo x = decode<F32>(P, A, S_in, rec_in, lane);
+        const StageInfo<V> x = decode<V, F32>(P, A, S_in, rec_in, lane, cnt);
         const int S = uni(x.S);
         const size_t obase = (size_t)t * A.n_m;
         bool r_split = false;                                  // lane k: a split was found for m index k
@@ -226,39 +234,36 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
                 todo &= ~cls;
                 auto jhi_of = [&](int s) { return L - (S - 1 - s); };   // last end leaving a layer per later stage
                 auto lim_of = [&](int s, int i) {                       // lim(s, i)
-                    return mem_aware ? min((int)J[s * ls + i], jhi_of(s)) : jhi_of(s);
+                    return mem_aware ? min((int)jrow(s)[i], jhi_of(s)) : jhi_of(s);
                 };
 
-                // ---------------- limit rows and their inverses, every stage of this class,
-                // into LDS; kBatch stages per round trip
+                // ---------------- limit and inverse-limit rows of every stage (this class)
+                // into LDS, kBatch stages per round trip; lanes past the end repeat the
+                // last dword
                 if (mem_aware) {
-                    wave_sync();                                        // earlier reads of J and X are done
+                    wave_sync();                                        // earlier reads of JX are done
                     int f = min(S - lane, key);
                     f = f < 1 ? 1 : f;
-                    const int my_row = x.lrow + (f - 1) * 2 * ls;      // lane s: stage s's rows, this class
+                    const int my_row = (x.lrow + (f - 1) * 2 * ls) >> 2;   // lane s: stage s's rows, in dwords
                     const uint32_t *lim32 = (const uint32_t *)P.mem_lim;
+                    uint32_t *jx32 = (uint32_t *)JX;
+                    const int d0 = min(lane, nd - 1), d1 = min(lane + 64, nd - 1);
                     for (int s0 = 0; s0 < S; s0 += kBatch) {
-                        uint32_t v[kBatch][2];
+                        uint32_t v0[kBatch], v1[kBatch];
 #pragma unroll
                         for (int u = 0; u < kBatch; u++) {
                             if (s0 + u < S) {
-                                const int base = uni(rl32(my_row, s0 + u)) >> 2;
-#pragma unroll
-                                for (int h = 0; h < 2; h++)
-                                    if (64 * h < 2 * ldw && lane + 64 * h < 2 * ldw) v[u][h] = lim32[base + lane + 64 * h];
+                                const uint32_t *src = lim32 + uni(rl32(my_row, s0 + u));
+                                v0[u] = src[d0];
+                                if (nd > 64) v1[u] = src[d1];
                             }
                         }
 #pragma unroll
                         for (int u = 0; u < kBatch; u++) {
                             if (s0 + u < S) {
-#pragma unroll
-                                for (int h = 0; h < 2; h++) {
-                                    const int d = lane + 64 * h;
-                                    if (64 * h < 2 * ldw && d < 2 * ldw) {
-                                        uint32_t *dst = (uint32_t *)(d < ldw ? J : X);
-                                        dst[(s0 + u) * ldw + (d < ldw ? d : d - ldw)] = v[u][h];
-                                    }
-                                }
+                                uint32_t *dst = jx32 + (s0 + u) * nd;
+                                dst[d0] = v0[u];
+                                if (nd > 64) dst[d1] = v1[u];
                             }
                         }
                     }
@@ -282,7 +287,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
                         const int b = R_s < ihi ? R_s : ihi;
                         int a = s;
                         if (mem_aware) {
-                            const int inv = uni((int)X[s * ls + nxt]);
+                            const int inv = uni((int)xrow(s)[nxt]);
                             a = inv > s ? inv : s;
                         }
                         if (a > b) {
@@ -325,31 +330,31 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
                     } else {
                         // r rows, k = 64 >> ceil(log2 r) lanes per row (one when r >= 64); the
                         // k lanes of a row take consecutive shares of its ends
-                        const V p2p = (V)rl64(x.p2p, s);
+                        const V p2p = (V)uni64(x.p2p, s);
                         const int a_next = uni(rl32(Al, s + 1)), jhi = jhi_of(s);
+                        const uint8_t *Js = jrow(s);
                         const int r = b - a + 1;
                         const int lk = r >= 64 ? 0 : 6 - (r > 1 ? 32 - __clz(r - 1) : 0);
                         const int k = 1 << lk;
                         const int part = lane & (k - 1);
                         for (int base = a; base <= b; base += 64 >> lk) {
                             const int i = base + (lane >> lk);
-                            const bool row_ok = i <= b;
-                            const int ic = row_ok ? i : b;
-                            const int lo = ic + 1 > a_next ? ic + 1 : a_next;
-                            const int hi = mem_aware ? min((int)J[s * ls + ic], jhi) : jhi;
-                            const int n = row_ok && hi >= lo ? hi - lo + 1 : 0;
+                            const int ic = min(i, b);
+                            const int lo = max(ic + 1, a_next);
+                            const int hi = mem_aware ? min((int)Js[ic], jhi) : jhi;
+                            const int n = i <= b ? max(hi - lo + 1, 0) : 0;
                             if (COUNT) {
                                 if (part == 0) work += (unsigned long long)n;
                                 continue;
                             }
                             const int c = (n + k - 1) >> lk;             // ends per lane
-                            const int js = lo + part * c;
+                            const int js = lo + (int)__umul24((unsigned)part, (unsigned)c);
                             const int je = min(js + c - 1, hi);
                             const V pi = Xs[ic].x - p2p;                 // T(s,i,j) = P_s[j] - pi
-                            V acc = relax_range<V>(Xs, js, row_ok ? je : js - 1, pi, INF);
+                            V acc = relax_range<V>(Xs, js, je, pi, INF);
                             acc = group_min<V>(acc, k);
                             if (s == 0) Bv = (V)rl64((int64_t)acc, 0);   // row 0 only: the whole wave's minimum
-                            else if (row_ok && part == 0) ((V *)&Xo[i])[1] = acc;
+                            else if (i <= b && part == 0) ((V *)&Xo[i])[1] = acc;
                         }
                     }
                     wave_sync();
@@ -360,35 +365,37 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
                 const uint64_t B24 = F32 ? rne24(B) : B;       // fp32 bottleneck, as an exact integer
                 auto within = [&](uint64_t T) { return F32 ? rne24(T) <= B24 : T <= B; };
 
-                // ---------------- F_s for stages S-1 .. 1; X[s][i] := the smallest row >= i of
-                // W_s with F_s true (kNone if there is none)
+                // ---------------- F_s for stages S-1 .. 1; xrow(s)[i] := the smallest row >= i
+                // of W_s with F_s true (kNone if there is none)
                 for (int s = S - 1; s >= 1; s--) {
                     const int a = uni(rl32(Al, s)), b = uni(rl32(Bl, s));
                     const V *prow = rows + uni(rl32(x.prow, s));
-                    const V p2p = (V)rl64(x.p2p, s);
+                    const V p2p = (V)uni64(x.p2p, s);
                     const int a_next = s < S - 1 ? uni(rl32(Al, s + 1)) : L;
                     const int jhi = jhi_of(s);
-                    const uint8_t *NXn = X + (s + 1) * ls;
-                    uint8_t *NXs = X + s * ls;
+                    const uint8_t *Js = jrow(s);
+                    const uint8_t *NXn = xrow(s + 1);
+                    uint8_t *NXs = xrow(s);
                     int first_above = kNone;                           // smallest row with F true in higher slots
                     for (int q = (b - a) >> 6; q >= 0; q--) {
                         const int i = a + 64 * q + lane;
-                        const bool row_ok = i <= b;
-                        const int ic = row_ok ? i : b;
+                        const int ic = min(i, b);
                         int nx = L;                                    // last stage: the end is L
-                        bool ok = row_ok;
+                        bool ok = i <= b;
                         if (s < S - 1) {
-                            const int lo = ic + 1 > a_next ? ic + 1 : a_next;
-                            const int hi = mem_aware ? min((int)J[s * ls + ic], jhi) : jhi;
-                            nx = lo <= hi ? (int)NXn[lo] : kNone;
-                            ok = ok && nx <= hi;
+                            // read unconditionally (lo <= L lies inside the row); an entry past
+                            // hi, or a stale one when lo > hi, is rejected by the tests below
+                            const int lo = max(ic + 1, a_next);
+                            const int hi = mem_aware ? min((int)Js[ic], jhi) : jhi;
+                            nx = NXn[lo];
+                            ok = ok & (lo <= hi) & (nx <= hi);
                         }
-                        const int nxc = nx <= L ? nx : L;
-                        ok = ok && within((uint64_t)(V)(prow[nxc] - prow[ic] + p2p));
+                        const int nxc = min(nx, L);
+                        ok = ok & within((uint64_t)(V)(prow[nxc] - prow[ic] + p2p));
                         const uint64_t mask = __ballot(ok);
                         const uint64_t rest = mask >> lane;            // rows >= i of this slot with F true
                         const int nxi = rest ? i + __ffsll((unsigned long long)rest) - 1 : first_above;
-                        if (row_ok) NXs[i] = (uint8_t)nxi;
+                        if (i <= b) NXs[i] = (uint8_t)nxi;
                         if (mask) first_above = a + 64 * q + __ffsll((unsigned long long)mask) - 1;
                     }
                     wave_sync();
@@ -399,7 +406,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
                 for (int s = 0; s < S - 1; s++) {
                     const int a_next = uni(rl32(Al, s + 1));
                     const int lo = cs + 1 > a_next ? cs + 1 : a_next;
-                    int nx = uni((int)X[(s + 1) * ls + (lo <= L ? lo : L)]);
+                    int nx = uni((int)xrow(s + 1)[lo <= L ? lo : L]);
                     nx = nx <= L ? nx : L;                             // unreachable: F_s[c_s] holds on the path
                     if (lane == s) {
                         my_start = cs;
@@ -408,10 +415,10 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
                     cs = nx;
                 }
                 if (lane == S - 1) my_start = cs;              // the last stage ends at L
-                for (uint64_t c = cls; c; c &= c - 1) {
+                const uint8_t my_layers = lane < S ? (uint8_t)(my_end - my_start) : 0;
+                for (uint64_t c = cls; c; c &= c - 1) {            // s_max <= 64: a lane per stage
                     const int k = __ffsll((unsigned long long)c) - 1;
-                    for (int q = lane; q < A.s_max; q += 64)
-                        A.layers[(obase + k) * A.s_max + q] = q < S ? (uint8_t)(my_end - my_start) : 0;
+                    if (lane < A.s_max) A.layers[(obase + k) * A.s_max + lane] = my_layers;
                 }
                 if ((cls >> lane) & 1) {
                     r_split = true;
@@ -427,10 +434,11 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
             else ((int64_t *)A.bottleneck)[o] = r_split ? (int64_t)r_b : INT64_MAX;
         }
         // zero layer counts of the plans without a split (invalid template, or no split fits)
-        const uint64_t with_split = __ballot(r_split);
-        if (with_split != __ballot(lane < A.n_m))
-            for (int q = lane; q < A.n_m * A.s_max; q += 64)
-                if (!((with_split >> (q / A.s_max)) & 1)) A.layers[obase * A.s_max + q] = 0;
+        const uint64_t without = __ballot(lane < A.n_m && !r_split);
+        for (uint64_t c = without; c; c &= c - 1) {
+            const int k = __ffsll((unsigned long long)c) - 1;
+            if (lane < A.s_max) A.layers[(obase + k) * A.s_max + lane] = 0;
+        }
     }
     if (COUNT) {
         work += __shfl_xor(work, 32);
@@ -479,13 +487,14 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     const int L = p->dev.L, ls = p->dev.lim_stride;
     a.s_cap = a.s_max < L ? a.s_max : L;
     a.g_stride = L + 5;                                       // L + 1 ends and 4 of padding
-    // per wavefront: two alternating pair rows {P_s, G_{s+1}}, then for every
-    // stage its limit row and its inverse-limit row (later its next-row table)
+    // per wavefront: two alternating pair rows {P_s, G_{s+1}}; per stage its
+    // limit row and its inverse-limit row (later its next-row table); one GPU
+    // counter per type
     const size_t j_off = ((size_t)2 * a.g_stride * 2 * sizeof(V) + 15) & ~size_t(15);
-    const size_t x_off = j_off + (size_t)a.s_cap * ls;
+    const size_t c_off = j_off + (size_t)a.s_cap * 2 * ls;
     a.off_j = (int32_t)j_off;
-    a.off_x = (int32_t)x_off;
-    a.lds_per_wave = (int32_t)((x_off + (size_t)a.s_cap * ls + 15) & ~size_t(15));
+    a.off_c = (int32_t)c_off;
+    a.lds_per_wave = (int32_t)((c_off + (size_t)p->dev.n_types * 4 + 15) & ~size_t(15));
     int max_lds = 0;
     HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
     // one wavefront per workgroup: a wavefront's LDS is released as soon as it

@@ -36,17 +36,19 @@ def log(*a):
 
 
 def source_hash():
+    """hash of the device sources the traffic counters were taken on"""
     h = hashlib.sha256()
-    for f in ("price.hip", "heddle_internal.h"):
-        with open(os.path.join(ROOT, "paper_2609_34244_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    csrc = os.path.join(ROOT, "paper_2609_34244_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()[:16]
 
 
 def measured_traffic(config, flags, n_plans):
     """HBM bytes per launch from the committed rocprofv3 counter summary,
     valid only for the kernel source it was measured on."""
-    path = os.path.join(ROOT, "profiles", f"price_kernel_{config}_traffic.json")
+    path = os.path.join(ROOT, "profiles", f"price_plans_{config}_traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -147,7 +149,22 @@ def main():
     kern_ms = [a.elapsed_time(b) for a, b in evs]
     log(f"timed {args.steps} steps in {elapsed:.3f}s; price kernel {np.mean(kern_ms):.3f} ms avg "
         f"(min {np.min(kern_ms):.3f}); best plan {best}")
-    statuses = np.bincount(out["status"].cpu().numpy().ravel(), minlength=9).tolist()
+    status_np = out["status"].cpu().numpy()
+    statuses = np.bincount(status_np.ravel(), minlength=9).tolist()
+    # the unpruned recurrence's work, (S-1)(L-S+1)(L-S+2)/2 per valid plan and
+    # distinct split: context only, the kernel relaxes far fewer pairs
+    valid = ((status_np == 0) | (status_np == 8))[:, 0]
+    S_np = w.n_stages.astype(np.int64)
+    L = w.profile.L
+    r_np = (S_np - 1) * (L - S_np + 1) * (L - S_np + 2) // 2
+    D_np = np.maximum((w.stages[:, 0] >> 16).astype(np.int64), 1)
+    if args.compute_only:
+        n_splits = np.ones_like(S_np)
+    else:
+        keys = np.minimum(-(-np.array(m, dtype=np.int64)[None, :] // D_np[:, None]), S_np[:, None])
+        keys.sort(axis=1)
+        n_splits = 1 + (np.diff(keys, axis=1) != 0).sum(axis=1)
+    dense_r = int((r_np * n_splits * valid).sum())
 
     kern_s = float(np.mean(kern_ms)) / 1e3
     achieved = relax * K_MIN / kern_s
@@ -169,8 +186,11 @@ def main():
                    "plans": n_plans, "memory_aware": not args.compute_only, "seed": w.meta["seed"]},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
                      "unit": "Tlane-op/s", "frac": achieved / PEAK_LANE_OPS, "traffic": traffic,
-                     "kernel": "price_kernel", "kernel_ms": float(np.mean(kern_ms)),
-                     "relaxations_per_launch": relax, "ops_per_relaxation": K_MIN},
+                     "kernel": "split_kernel + evaluate_kernel (one heddle_price_plans launch pair)",
+                     "kernel_ms": float(np.mean(kern_ms)),
+                     "relaxations_per_launch": relax, "ops_per_relaxation": K_MIN,
+                     "dense_R_per_launch": dense_r,
+                     "frac_at_dense_R": dense_r * K_MIN / kern_s / PEAK_LANE_OPS},
         "statuses": statuses,
         "best_plan": {"template": best[0], "m_index": best[1], "iter": best[2]} if best else None,
         "profile_load_ms": load_ms,

@@ -50,6 +50,9 @@ template <class T> __device__ __forceinline__ T wave_max(T v)
 // uniform value into a scalar register
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// v with lane `lane` (uniform) replaced by the uniform value x
+__device__ __forceinline__ int put_lane(int v, int x, int lane) { return (int)__lane_id() == lane ? x : v; }
+
 // DPP lane permutations within rows of 16 lanes (lanes whose source is not
 // valid keep their own value, which is harmless for min/max)
 template <int CTRL> __device__ __forceinline__ uint32_t dpp32(uint32_t v)

@@ -111,7 +111,7 @@ __device__ __forceinline__ void fetch_rows(RowRegs<V> &r, const V *prow, int a, 
 {
 #pragma unroll
     for (int q = 0; q < kRowSlots; q++)
-        if (64 * q <= e - a) r.p[q] = prow[min(a + lane + 64 * q, e)];     // uniform condition
+        if (64 * q <= e - a) r.p[q] = prow[(uint32_t)min(a + lane + 64 * q, e)];     // uniform condition
 }
 
 template <class V> __device__ __forceinline__ const V *stage_rows(const DevProfile &P, bool f32);
@@ -247,7 +247,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
                     const int my_row = (x.lrow + (f - 1) * 2 * ls) >> 2;   // lane s: stage s's rows, in dwords
                     const uint32_t *lim32 = (const uint32_t *)P.mem_lim;
                     uint32_t *jx32 = (uint32_t *)JX;
-                    const int d0 = min(lane, nd - 1), d1 = min(lane + 64, nd - 1);
+                    const uint32_t d0 = min(lane, nd - 1), d1 = min(lane + 64, nd - 1);
                     for (int s0 = 0; s0 < S; s0 += kBatch) {
                         uint32_t v0[kBatch], v1[kBatch];
 #pragma unroll
@@ -278,7 +278,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
                     int c = 0;
                     for (int s = 1; s < S; s++) {
                         c = uni(lim_of(s - 1, c));
-                        Rl = lane == s ? c : Rl;
+                        Rl = put_lane(Rl, c, s);
                     }
                     int nxt = L;                                       // Bk_{s+1}
                     for (int s = S - 1; s >= 0; s--) {
@@ -294,8 +294,8 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
                             feasible = false;
                             break;
                         }
-                        Al = lane == s ? a : Al;
-                        Bl = lane == s ? b : Bl;
+                        Al = put_lane(Al, a, s);
+                        Bl = put_lane(Bl, b, s);
                         nxt = a;
                     }
                 }
@@ -390,8 +390,8 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
                             nx = NXn[lo];
                             ok = ok & (lo <= hi) & (nx <= hi);
                         }
-                        const int nxc = min(nx, L);
-                        ok = ok & within((uint64_t)(V)(prow[nxc] - prow[ic] + p2p));
+                        const uint32_t nxc = min(nx, L);
+                        ok = ok & within((uint64_t)(V)(prow[nxc] - prow[(uint32_t)ic] + p2p));
                         const uint64_t mask = __ballot(ok);
                         const uint64_t rest = mask >> lane;            // rows >= i of this slot with F true
                         const int nxi = rest ? i + __ffsll((unsigned long long)rest) - 1 : first_above;
@@ -408,13 +408,11 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevPr
                     const int lo = cs + 1 > a_next ? cs + 1 : a_next;
                     int nx = uni((int)xrow(s + 1)[lo <= L ? lo : L]);
                     nx = nx <= L ? nx : L;                             // unreachable: F_s[c_s] holds on the path
-                    if (lane == s) {
-                        my_start = cs;
-                        my_end = nx;
-                    }
+                    my_start = put_lane(my_start, cs, s);
+                    my_end = put_lane(my_end, nx, s);
                     cs = nx;
                 }
-                if (lane == S - 1) my_start = cs;              // the last stage ends at L
+                my_start = put_lane(my_start, cs, S - 1);      // the last stage ends at L
                 const uint8_t my_layers = lane < S ? (uint8_t)(my_end - my_start) : 0;
                 for (uint64_t c = cls; c; c &= c - 1) {            // s_max <= 64: a lane per stage
                     const int k = __ffsll((unsigned long long)c) - 1;

@@ -18,8 +18,14 @@
  *      max_s g_s (section 5.3, expert tiling paragraph) and the per-GPU peak
  *      memory (section 5.2),
  * and finally the argmin over all feasible plans of iteration time per
- * micro-batch ("ranks the resulting plans by predicted throughput",
- * section 5 overview; "keeps the fastest", section 5.3).
+ * micro-batch (plans are ranked by predicted throughput, section 5
+ * overview; the fastest candidate is kept, section 5.3).
+ *
+ * Second partition mode (OR_F_DISTRIBUTE): Heddle's own layer split of the
+ * arithmetic auto-fill (section 5.3, layer split and DP degree): each stage
+ * gets layers in proportion to its profiled speed; when that split does not
+ * fit memory, a fixed list of alternative splits is priced and the fastest
+ * one that fits is kept (see distribute_cuts and price_distribute).
  *
  * Everything is written the slow, obvious way: every sum is a loop, every
  * product and quotient of a transfer time is done in 128-bit integers, and
@@ -59,6 +65,7 @@ enum {
 
 #define OR_F_FP32 1u
 #define OR_F_COMPUTE_ONLY 2u
+#define OR_F_DISTRIBUTE 4u
 
 typedef struct {
     int32_t L, n_types, n_tp, n_ep;
@@ -328,20 +335,19 @@ static int64_t time_i64(const oracle_profile *p, const ostage *st, int s, int S,
     return stage_time(p, st, s, S, i, j);
 }
 
-static void price_one(const oracle_profile *p, const ostage *st, int S, int64_t m, uint32_t flags,
-                      oplan *out)
+/* Evaluate (section 5.3) the split out->cut: bottleneck max_s t_s,
+ * iteration time (M-1) max_s t_s + sum_s t_s + max_s g_s, peak memory, and
+ * status OOM when some stage does not fit. */
+static void evaluate_i64(const oracle_profile *p, const ostage *st, int S, int64_t Mp, oplan *out)
 {
-    int co = (flags & OR_F_COMPUTE_ONLY) != 0;
-    int64_t D = st[0].dp, Mp = ceil_div64(m, D);
-    int64_t B = partition(p, st, S, Mp, co, time_i64, out->cut);
-    if (B == OR_INF) { out->status = OR_OOM; return; }
-    /* Evaluate (section 5.3): (M-1) max_s t_s + sum_s t_s + max_s g_s */
     i128 sum_t = 0;
-    int64_t max_g = 0, peak = 0;
+    int64_t B = 0, max_g = 0, peak = 0;
     int oom = 0;
     for (int s = 0; s < S; s++) {
         int i = out->cut[s], j = out->cut[s + 1];
-        sum_t += stage_time(p, st, s, S, i, j);
+        int64_t t = stage_time(p, st, s, S, i, j);
+        sum_t += t;
+        if (t > B) B = t;
         int64_t g = stage_sync(p, &st[s], i, j);
         if (g > max_g) max_g = g;
         int64_t mem = stage_mem(p, &st[s], i, j, inflight_of(s, S, Mp));
@@ -352,6 +358,16 @@ static void price_one(const oracle_profile *p, const ostage *st, int S, int64_t 
     out->bottleneck = B;
     out->iter = (int64_t)((i128)(Mp - 1) * B + sum_t + max_g);
     out->peak_mem = peak;
+}
+
+static void price_one(const oracle_profile *p, const ostage *st, int S, int64_t m, uint32_t flags,
+                      oplan *out)
+{
+    int co = (flags & OR_F_COMPUTE_ONLY) != 0;
+    int64_t D = st[0].dp, Mp = ceil_div64(m, D);
+    int64_t B = partition(p, st, S, Mp, co, time_i64, out->cut);
+    if (B == OR_INF) { out->status = OR_OOM; return; }
+    evaluate_i64(p, st, S, Mp, out);     /* the canonical split's max_s t_s is B */
 }
 
 /* ---------------------------------------------------------------------- */
@@ -428,6 +444,32 @@ static float bits_to_float(int64_t b)
     return f;
 }
 
+/* fp32 Evaluate of the split out->cut: stage times rounded to fp32 once
+ * each, the iteration time rounded once from the exact sum of its fp32 terms. */
+static void evaluate_f32(const oracle_profile *p, const ostage *st, int S, int64_t Mp, oplan *out)
+{
+    float B = 0.0f, max_g = 0.0f;
+    i128 sum_t = 0;
+    int64_t peak = 0;
+    int oom = 0;
+    for (int s = 0; s < S; s++) {
+        int i = out->cut[s], j = out->cut[s + 1];
+        float t = float_of_fx(stage_time_fx(p, st, s, S, i, j));
+        sum_t += fx_of_float(t);
+        if (t > B) B = t;
+        float g = (float)stage_sync(p, &st[s], i, j);
+        if (g > max_g) max_g = g;
+        int64_t mem = stage_mem(p, &st[s], i, j, inflight_of(s, S, Mp));
+        if (mem > peak) peak = mem;
+        if (mem > p->mem_cap_bytes[st[s].g]) oom = 1;
+    }
+    i128 total = (i128)(Mp - 1) * fx_of_float(B) + sum_t + fx_of_float(max_g);
+    out->status = oom ? OR_OOM : OR_OK;
+    out->bottleneck_f = B;
+    out->iter_f = float_of_fx(total);
+    out->peak_mem = peak;
+}
+
 static void price_one_f32(const oracle_profile *p, const ostage *st, int S, int64_t m, uint32_t flags,
                           oplan *out)
 {
@@ -435,25 +477,74 @@ static void price_one_f32(const oracle_profile *p, const ostage *st, int S, int6
     int64_t D = st[0].dp, Mp = ceil_div64(m, D);
     int64_t Bbits = partition(p, st, S, Mp, co, time_f32bits, out->cut);
     if (Bbits == OR_INF) { out->status = OR_OOM; return; }
-    float B = bits_to_float(Bbits);
-    i128 total = (i128)(Mp - 1) * fx_of_float(B);
-    float max_g = 0.0f;
-    int64_t peak = 0;
-    int oom = 0;
+    evaluate_f32(p, st, S, Mp, out);     /* the canonical split's max_s t_s is B */
+}
+
+/* ---------------------------------------------------------------------- */
+/* Distribute (section 5.3, layer split and DP degree).                    */
+/* Readings: the profiled speed of stage s is the inverse of the time of   */
+/* all L layers on its GPU type and TP degree (int64 layer costs with the  */
+/* stage's all-to-all terms, p2p excluded). The cut after stage s is the   */
+/* nearest integer (halves up) to L * (sum_{t<=s} speed_t) / sum_t speed_t, */
+/* computed in IEEE double in this order, then moved up to leave stage s   */
+/* one layer and down to leave every later stage one layer. When that      */
+/* split does not fit memory, the fixed list of alternatives is: for each  */
+/* boundary b = 0 .. S-2 in order, the cut after stage b moved by -1, then */
+/* by +1 (kept only if every stage still holds a layer); the fitting       */
+/* alternative with the smallest iteration time is kept, the first in list */
+/* order on ties; none fitting leaves the plan OOM without a split. With   */
+/* OR_F_COMPUTE_ONLY the proportional split is kept and only flagged.      */
+/* ---------------------------------------------------------------------- */
+static void distribute_cuts(const oracle_profile *p, const ostage *st, int S, int *cut)
+{
+    int L = p->L;
+    double speed[256], total = 0.0, below = 0.0;
     for (int s = 0; s < S; s++) {
-        int i = out->cut[s], j = out->cut[s + 1];
-        total += fx_of_float(float_of_fx(stage_time_fx(p, st, s, S, i, j)));
-        float g = (float)stage_sync(p, &st[s], i, j);
-        if (g > max_g) max_g = g;
-        int64_t mem = stage_mem(p, &st[s], i, j, inflight_of(s, S, Mp));
-        if (mem > peak) peak = mem;
-        if (mem > p->mem_cap_bytes[st[s].g]) oom = 1;
+        int64_t all = 0;
+        for (int l = 0; l < L; l++) all += layer_cost(p, &st[s], l);
+        speed[s] = 1.0 / (double)all;
     }
-    total += fx_of_float(max_g);
-    out->status = oom ? OR_OOM : OR_OK;
-    out->bottleneck_f = B;
-    out->iter_f = float_of_fx(total);
-    out->peak_mem = peak;
+    for (int s = 0; s < S; s++) total += speed[s];
+    cut[0] = 0;
+    for (int s = 1; s < S; s++) {
+        below += speed[s - 1];
+        int c = (int)floor((double)L * below / total + 0.5);
+        if (c < cut[s - 1] + 1) c = cut[s - 1] + 1;
+        if (c > L - (S - s)) c = L - (S - s);
+        cut[s] = c;
+    }
+    cut[S] = L;
+}
+
+static int faster(const oplan *a, const oplan *b, int f32)
+{
+    return f32 ? a->iter_f < b->iter_f : a->iter < b->iter;
+}
+
+static void price_distribute(const oracle_profile *p, const ostage *st, int S, int64_t m, uint32_t flags,
+                             oplan *out)
+{
+    int co = (flags & OR_F_COMPUTE_ONLY) != 0, f32 = (flags & OR_F_FP32) != 0;
+    int64_t Mp = ceil_div64(m, st[0].dp);
+    distribute_cuts(p, st, S, out->cut);
+    if (f32) evaluate_f32(p, st, S, Mp, out);
+    else evaluate_i64(p, st, S, Mp, out);
+    if (out->status == OR_OK || co) return;
+    oplan best, cand;
+    int found = 0;
+    for (int b = 0; b + 1 < S; b++) {
+        for (int d = -1; d <= 1; d += 2) {
+            memcpy(cand.cut, out->cut, sizeof(int) * (size_t)(S + 1));
+            cand.cut[b + 1] += d;
+            if (cand.cut[b + 1] <= cand.cut[b] || cand.cut[b + 1] >= cand.cut[b + 2]) continue;
+            if (f32) evaluate_f32(p, st, S, Mp, &cand);
+            else evaluate_i64(p, st, S, Mp, &cand);
+            if (cand.status != OR_OK) continue;
+            if (!found || faster(&cand, &best, f32)) { best = cand; found = 1; }
+        }
+    }
+    if (found) *out = best;
+    else out->status = OR_OOM;
 }
 
 /* ---------------------------------------------------------------------- */
@@ -481,7 +572,8 @@ int oracle_price_plans(const oracle_profile *p, int64_t t0, int64_t t1, int s_ma
             size_t o = (size_t)t * n_m + k;
             pl.status = v;
             if (v == OR_OK) {
-                if (f32) price_one_f32(p, st, S, m[k], flags, &pl);
+                if (flags & OR_F_DISTRIBUTE) price_distribute(p, st, S, m[k], flags, &pl);
+                else if (f32) price_one_f32(p, st, S, m[k], flags, &pl);
                 else price_one(p, st, S, m[k], flags, &pl);
             }
             int has_split = (pl.status == OR_OK) ||

@@ -17,13 +17,14 @@ LIB = os.path.join(HERE, "liboracle.so")
 
 F_FP32 = 1
 F_COMPUTE_ONLY = 2
+F_DISTRIBUTE = 4
 STATUS = ["OK", "BAD_SHAPE", "BAD_TYPE", "BAD_TP", "UNPROFILED", "BAD_DP", "BAD_EP",
           "OVERSUBSCRIBED", "OOM"]
 
 
 def build():
     """Compile the oracle with plain gcc (no SIMD flags)."""
-    subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-fPIC", "-shared", "-o", LIB, SRC, "-lm"])
+    subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-ffp-contract=off", "-fPIC", "-shared", "-o", LIB, SRC, "-lm"])
     return LIB
 
 

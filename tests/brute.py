@@ -152,6 +152,33 @@ def price(p, S, s_max, recs, m, compute_only=False, fp32=False):
                 layers=list(comp) + [0] * (s_max - S))
 
 
+def best_iter(p, S, s_max, recs, m, fp32=False):
+    """smallest iteration time over every memory-feasible composition (its
+    own bottleneck per composition), or None if none fits."""
+    stt, st = status_of(p, S, s_max, recs)
+    if stt != 0:
+        return None
+    plan = Plan(p, st)
+    Mp = ceil_div(int(m), st[0]["dp"])
+    best = None
+    for comp in compositions(p.L, S):
+        cuts = np.concatenate([[0], np.cumsum(comp)]).astype(int)
+        stages = [plan.stage(s, cuts[s], cuts[s + 1], Mp) for s in range(S)]
+        if any(mem > int(p.mem_cap_bytes[st[s]["g"]]) for s, (_, mem, _) in enumerate(stages)):
+            continue
+        if fp32:
+            tprime = [plan.stage_f32(s, cuts[s], cuts[s + 1]) for s in range(S)]
+            maxg = max(np.float32(g) for _, _, g in stages)
+            tot = (Mp - 1) * Fraction(float(max(tprime))) + sum(Fraction(float(t)) for t in tprime) + \
+                Fraction(float(maxg))
+            it = round_f32(tot)
+        else:
+            it = (Mp - 1) * max(t for t, _, _ in stages) + sum(t for t, _, _ in stages) + \
+                max(g for _, _, g in stages)
+        best = it if best is None or it < best else best
+    return best
+
+
 def best_plan(m, iters, status):
     """argmin over OK plans of iter / m, ties to lowest (template, m index)."""
     best, arg = None, None

@@ -418,3 +418,104 @@ def test_count_relaxations_covers_every_feasible_split():
             elif c == 0:
                 n_empty += 1
     assert n_feasible > 100 and n_empty > 20, (n_feasible, n_empty)
+
+
+# ------------------------------------------------------------- Distribute mode
+
+def _speed_profile(L, per_layer, caps):
+    """one GPU type per entry of per_layer (uniform layer time), one TP, unit
+    state bytes per layer, no activations, memory caps in layers"""
+    N = len(per_layer)
+    d = dict(L=L, tp_degrees=[1], ep_degrees=[1], layer_ns=[[[c] * L] for c in per_layer],
+             profiled=[[1]] * N, is_moe=[0] * L, state_bytes=[[1] * L], xstate_bytes=[[0] * L],
+             act_bytes=[[0] * L], grad_bytes=[[0] * L], xgrad_bytes=[[0] * L], boundary_bytes=0, a2a_bytes=0,
+             mem_cap_bytes=caps, node_size=[8] * N, n_gpus=[1000] * N, intra_bw_MBps=[1000] * N,
+             link_bw_MBps=[[1000] * N for _ in range(N)])
+    return profile_from_json(d)
+
+
+@pytest.mark.parametrize("per_layer, L, want", [
+    ([3], 12, None),                 # S = 4 identical stages below: 3 layers each
+    ([1, 2], 9, (6, 3)),             # speeds 2 : 1, 9 layers: exactly 6 and 3
+    ([1, 2], 10, (7, 3)),            # 10 * 2/3 = 6.67 rounds to 7
+    ([1, 2], 5, (3, 2)),             # 5 * 2/3 = 3.33 rounds to 3
+    ([2, 1], 10, (3, 7)),            # the slower stage first
+])
+def test_distribute_proportional_closed_forms(per_layer, L, want):
+    p = _speed_profile(L, per_layer, [10 ** 6] * len(per_layer))
+    if want is None:
+        stages, want = [(0, 1, 1, 1)] * 4, (3, 3, 3, 3)
+    else:
+        stages = [(g, 1, 1, 1) for g in range(len(per_layer))]
+    r = price1(p, stages, 1, O.F_DISTRIBUTE)
+    assert r["status"] == 0
+    assert tuple(r["layers"][:len(stages)]) == want
+    # bottleneck is the slowest stage's time: layers x per-layer time (no p2p, no activations)
+    assert r["bottleneck"] == max(n * per_layer[g] for n, (g, _, _, _) in zip(want, stages))
+
+
+def test_distribute_keeps_every_stage_a_layer():
+    """speeds 100 : 1 : 1 over 3 layers: the proportional cuts 2.94 and 2.97
+    round to 3 and 3, then move down to leave each later stage a layer."""
+    p = _speed_profile(3, [1, 100, 100], [10 ** 6] * 3)
+    r = price1(p, [(0, 1, 1, 1), (1, 1, 1, 1), (2, 1, 1, 1)], 1, O.F_DISTRIBUTE)
+    assert tuple(r["layers"][:3]) == (1, 1, 1)
+
+
+def test_distribute_fallback_list():
+    """equal speeds, 4 layers on 2 stages: the proportional split (2, 2) does
+    not fit a stage-0 GPU that holds one layer; the alternatives are (1, 3)
+    (fits) and (3, 1) (does not): (1, 3) is kept. With both moves failing the
+    plan is OOM without a split; with COMPUTE_ONLY (2, 2) is kept and flagged."""
+    stages = [(0, 1, 1, 1), (1, 1, 1, 1)]
+    r = price1(_speed_profile(4, [1, 1], [1, 3]), stages, 1, O.F_DISTRIBUTE)
+    assert (r["status"], tuple(r["layers"][:2]), r["bottleneck"]) == (0, (1, 3), 3)
+    r = price1(_speed_profile(4, [1, 1], [1, 1]), stages, 1, O.F_DISTRIBUTE)
+    assert (r["status"], tuple(r["layers"][:2]), r["iter"]) == (8, (0, 0), np.iinfo(np.int64).max)
+    r = price1(_speed_profile(4, [1, 1], [1, 3]), stages, 1, O.F_DISTRIBUTE | O.F_COMPUTE_ONLY)
+    assert (r["status"], tuple(r["layers"][:2]), r["bottleneck"]) == (8, (2, 2), 2)
+    # two alternatives fit and the faster one wins although it comes later in the
+    # list: per-layer times 2, 1, 1 over 9 layers give the proportional cuts
+    # 1.8 -> 2 and 5.4 -> 5, i.e. (2, 3, 4); stage 1 holds 2 layers at most. The
+    # list is (1, 4, 4) no, (3, 2, 4) fits with times (6, 2, 4), (2, 2, 5) fits
+    # with (4, 2, 5), (2, 4, 3) no. With M = 4: 3 * 6 + 12 = 30 against
+    # 3 * 5 + 11 = 26.
+    p = _speed_profile(9, [2, 1, 1], [10, 2, 10])
+    r = price1(p, [(0, 1, 1, 1), (1, 1, 1, 1), (2, 1, 1, 1)], 4, O.F_DISTRIBUTE)
+    assert (r["status"], tuple(r["layers"][:3]), r["bottleneck"], r["iter"]) == (0, (2, 2, 5), 5, 26)
+
+
+@pytest.mark.parametrize("flags", [O.F_DISTRIBUTE, O.F_DISTRIBUTE | O.F_FP32])
+def test_distribute_against_brute_force_and_dp(flags):
+    """On random instances: a Distribute plan with a split has one layer or
+    more per stage summing to L; when OK, its split fits memory (brute-force
+    memory of each stage), its bottleneck is never below the min-max split's
+    B*, and its iteration time never below the best iteration time over all
+    memory-feasible compositions (brute force)."""
+    n_ok = 0
+    f32 = bool(flags & O.F_FP32)
+    for seed in range(40):
+        w = random_instance(seed)
+        op = O.OracleProfile(w.profile)
+        rd = O.price_plans(op, w.n_stages, w.stages, w.m, flags)
+        rp = O.price_plans(op, w.n_stages, w.stages, w.m, flags & O.F_FP32)
+        for t in range(w.n):
+            S = int(w.n_stages[t])
+            stt, st = brute.status_of(w.profile, S, w.s_max, w.stages[t])
+            for k, m in enumerate(w.m):
+                assert rd["status"][t, k] == stt or (stt == 0 and rd["status"][t, k] == 8)
+                if rd["status"][t, k] != 0:
+                    continue
+                lay = [int(x) for x in rd["layers"][t, k, :S]]
+                assert min(lay) >= 1 and sum(lay) == w.profile.L
+                plan = brute.Plan(w.profile, st)
+                Mp = brute.ceil_div(int(m), st[0]["dp"])
+                cuts = np.concatenate([[0], np.cumsum(lay)]).astype(int)
+                for s in range(S):
+                    assert plan.stage(s, cuts[s], cuts[s + 1], Mp)[1] <= int(w.profile.mem_cap_bytes[st[s]["g"]])
+                assert rp["status"][t, k] == 0
+                assert rd["bottleneck"][t, k] >= rp["bottleneck"][t, k]
+                b = brute.best_iter(w.profile, S, w.s_max, w.stages[t], int(m), fp32=f32)
+                assert rd["iter"][t, k] >= b
+                n_ok += 1
+    assert n_ok > 300

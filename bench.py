@@ -22,6 +22,13 @@ sys.path.insert(0, ROOT)
 
 PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9       # CUs x SIMDs x lanes x clock: 32-bit VALU lane-ops/s
 K_MIN = 3                                   # sub, max, min per relaxation (32-bit DP)
+# Distribute: 32-bit lane-ops of one stage-cost evaluation counted from its
+# integer arithmetic, leaving out the two all-reduce divisions: time
+# difference + p2p (4), state and activation differences, activation x
+# in-flight count, sum and compare with capacity (12), dense and expert
+# gradient differences (4), and the 64-bit max / sum / max folds into the
+# split's bottleneck, total and peak memory (6)
+K_EVAL = 26
 WORKLOAD_TEXT = {
     "c1_tiny_dense": "tiny dense: L=24, 2 GPU types, 1k templates S<=4, m=16",
     "c2_7b_dense": "7B-like dense: L=32, 4 GPU types, 100k templates S<=8, m in {8,32}",
@@ -45,10 +52,11 @@ def source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(config, flags, n_plans):
+def measured_traffic(config, flags, n_plans, distribute=False):
     """HBM bytes per launch from the committed rocprofv3 counter summary,
     valid only for the kernel source it was measured on."""
-    path = os.path.join(ROOT, "profiles", f"price_plans_{config}_traffic.json")
+    mode = "_distribute" if distribute else ""
+    path = os.path.join(ROOT, "profiles", f"price_plans_{config}{mode}_traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -82,6 +90,8 @@ def main():
     ap.add_argument("--config", default="c3_70b_dense", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--fp32", action="store_true", help="fp32 cost variant")
     ap.add_argument("--compute-only", action="store_true", help="split ignores memory; fit checked after")
+    ap.add_argument("--distribute", action="store_true",
+                    help="Heddle's speed-proportional split with its fallback list instead of the min-max split")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -107,7 +117,9 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": args.copy_calibration}))
         return
-    flags = (H.HEDDLE_F_FP32 if args.fp32 else 0) | (H.HEDDLE_F_COMPUTE_ONLY if args.compute_only else 0)
+    flags = (H.HEDDLE_F_FP32 if args.fp32 else 0) | (H.HEDDLE_F_COMPUTE_ONLY if args.compute_only else 0) | \
+        (H.HEDDLE_F_DISTRIBUTE if args.distribute else 0)
+    k_unit, unit_name = (K_EVAL, "stage-cost evaluation") if args.distribute else (K_MIN, "DP relaxation")
     t0 = time.perf_counter()
     w = make_workload(args.config)
     log(f"workload {args.config}: {w.n} templates x {len(w.m)} m generated in {time.perf_counter() - t0:.1f}s")
@@ -122,7 +134,7 @@ def main():
     torch.cuda.synchronize()
     relax = H.heddle_count_work(prof, ns, st, m, flags)
     n_plans = w.n * len(m)
-    log(f"profile loaded in {load_ms:.1f} ms; relaxations per step {relax:,} ({relax / w.n:.0f} per template); "
+    log(f"profile loaded in {load_ms:.1f} ms; work per step {relax:,} x {unit_name} ({relax / w.n:.0f} per template); "
         f"32-bit DP: {info['narrow_f32' if args.fp32 else 'narrow_i64']}")
 
     stream = torch.cuda.current_stream()
@@ -167,8 +179,28 @@ def main():
     dense_r = int((r_np * n_splits * valid).sum())
 
     kern_s = float(np.mean(kern_ms)) / 1e3
-    achieved = relax * K_MIN / kern_s
-    traffic = measured_traffic(args.config, flags, n_plans)
+    achieved = relax * k_unit / kern_s
+    traffic = measured_traffic(args.config, flags, n_plans, args.distribute)
+    if args.distribute:
+        roof = {"kernel": "distribute_kernel (one heddle_price_plans launch)",
+                "work_per_launch": relax, "work_unit": unit_name, "ops_per_unit": k_unit}
+        # context: the same plans under the min-max split (one launch outside the timed region)
+        ref = H.alloc_outputs(w.n, len(m), w.s_max, flags & ~H.HEDDLE_F_DISTRIBUTE)
+        H.heddle_price_plans(prof, ns, st, m, flags & ~H.HEDDLE_F_DISTRIBUTE, ref)
+        torch.cuda.synchronize()
+        rs = ref["status"].cpu().numpy()
+        both = (status_np == 0) & (rs == 0)
+        bd = out["bottleneck"].cpu().numpy().astype(np.float64)
+        br = ref["bottleneck"].cpu().numpy().astype(np.float64)
+        it_d = out["iter"].cpu().numpy().astype(np.float64)
+        it_r = ref["iter"].cpu().numpy().astype(np.float64)
+        roof["vs_min_max"] = {"plans_ok": int((status_np == 0).sum()), "min_max_plans_ok": int((rs == 0).sum()),
+                              "mean_bottleneck_ratio": float(np.mean(bd[both] / br[both])) if both.any() else None,
+                              "mean_iter_ratio": float(np.mean(it_d[both] / it_r[both])) if both.any() else None}
+    else:
+        roof = {"kernel": "split_kernel + evaluate_kernel (one heddle_price_plans launch pair)",
+                "work_per_launch": relax, "work_unit": unit_name, "ops_per_unit": k_unit,
+                "dense_R_per_launch": dense_r, "frac_at_dense_R": dense_r * K_MIN / kern_s / PEAK_LANE_OPS}
     result = {
         "metric": "candidate plans priced/sec (partition+evaluate) on 1 MI355X; % VALU roofline",
         "value": n_plans * args.steps / elapsed,
@@ -180,17 +212,15 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": ("fp32" if args.fp32 else "int64") + (" (exact 32-bit DP)" if info["narrow_f32" if args.fp32 else "narrow_i64"] else ""),
+        "dtype": ("fp32" if args.fp32 else "int64") +
+                 (" (exact 32-bit DP)" if info["narrow_f32" if args.fp32 else "narrow_i64"] and not args.distribute else ""),
         "data": "synthetic",
         "config": {"workload": WORKLOAD_TEXT[args.config], "name": args.config, "templates": w.n, "m": m,
-                   "plans": n_plans, "memory_aware": not args.compute_only, "seed": w.meta["seed"]},
-        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
-                     "unit": "Tlane-op/s", "frac": achieved / PEAK_LANE_OPS, "traffic": traffic,
-                     "kernel": "split_kernel + evaluate_kernel (one heddle_price_plans launch pair)",
-                     "kernel_ms": float(np.mean(kern_ms)),
-                     "relaxations_per_launch": relax, "ops_per_relaxation": K_MIN,
-                     "dense_R_per_launch": dense_r,
-                     "frac_at_dense_R": dense_r * K_MIN / kern_s / PEAK_LANE_OPS},
+                   "plans": n_plans, "memory_aware": not args.compute_only, "seed": w.meta["seed"],
+                   "partition": "distribute" if args.distribute else "min-max"},
+        "roofline": dict({"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
+                          "unit": "Tlane-op/s", "frac": achieved / PEAK_LANE_OPS, "traffic": traffic,
+                          "kernel_ms": float(np.mean(kern_ms))}, **roof),
         "statuses": statuses,
         "best_plan": {"template": best[0], "m_index": best[1], "iter": best[2]} if best else None,
         "profile_load_ms": load_ms,

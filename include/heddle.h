@@ -47,6 +47,7 @@ extern "C" {
 /* ---- flags ---- */
 #define HEDDLE_F_FP32         1u  /* fp32 time quantities (iter, bottleneck outputs are float) */
 #define HEDDLE_F_COMPUTE_ONLY 2u  /* split ignores memory; the fit is checked afterwards       */
+#define HEDDLE_F_DISTRIBUTE   4u  /* speed-proportional split with a fallback list (section 5.3) */
 
 /* ---- per-plan status codes (data, not errors); the first failing check wins ---- */
 #define HEDDLE_S_OK             0  /* priced and fits                                         */
@@ -145,7 +146,7 @@ void heddle_free_profile(heddle_profile *p);
  *   h_m          HOST [n_m] micro-batch counts, each 1..HEDDLE_MAX_M; read
  *                during the call. Micro-batches per replica: M_p = ceil(m/D).
  *   n_m          1..HEDDLE_MAX_MLIST.
- *   flags        HEDDLE_F_FP32 | HEDDLE_F_COMPUTE_ONLY, or 0.
+ *   flags        any of HEDDLE_F_FP32, HEDDLE_F_COMPUTE_ONLY, HEDDLE_F_DISTRIBUTE.
  * Outputs (DEVICE, caller-allocated, index o = t * n_m + k):
  *   d_iter        [n][n_m] iteration time: int64 ns, or float with FP32.
  *   d_bottleneck  [n][n_m] slowest stage time B* (same type as d_iter).
@@ -163,6 +164,19 @@ void heddle_free_profile(heddle_profile *p);
  * FP32: every time quantity is the fp32 nearest (ties to even) to its exact
  * value computed from fp32 per-layer costs and fp32-rounded transfer terms
  * (one rounding per stage time and one for the iteration time).
+ * DISTRIBUTE (Heddle's own split, section 5.3, layer split and DP degree):
+ * instead of the min-max split, stage s gets layers in proportion to its
+ * speed 1 / (int64 time of all L layers on its type and TP, all-to-all
+ * included, p2p excluded): the cut after stage s is floor(x + 0.5) with
+ * x = L * (speeds of stages 0..s) / (speeds of all stages) in IEEE double
+ * (speeds summed in stage order), raised to leave stage s a layer and
+ * lowered to leave each later stage one. If it does not fit memory, the
+ * alternatives "cut after stage b moved by -1, then by +1" for b = 0..S-2
+ * (each stage keeping a layer) are priced and the fitting one with the
+ * smallest iteration time is kept (the first on ties); none fitting gives
+ * OOM without a split. With COMPUTE_ONLY the proportional split is kept and
+ * flagged OOM if it does not fit. The bottleneck output is then the split's
+ * slowest stage time.
  * Returns HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_RANGE (the iteration time could
  * exceed 2^62 for these m, or the fp32 costs span too wide a range to sum
  * exactly) or HEDDLE_E_DEVICE. On error nothing is enqueued.
@@ -177,7 +191,7 @@ int heddle_price_plans(const heddle_profile *p, int64_t n, int32_t s_max,
  * heddle_argmin_plans -- best plan among priced outputs: the plan of status
  * OK with the smallest iter / m (highest throughput m / iter), compared
  * exactly as iter_a * m_b < iter_b * m_a; ties go to the lowest template
- * index, then the lowest m index (section 5.3: "keeps the fastest").
+ * index, then the lowest m index (section 5.3: the fastest candidate is kept).
  * Synchronous: waits for `stream`.
  *   d_iter, d_status  DEVICE outputs of heddle_price_plans with the same
  *                     n, n_m, h_m and the same FP32 flag.
@@ -217,6 +231,10 @@ int heddle_best_plan(const heddle_profile *p, int64_t n, int32_t s_max,
  * counts one. A template with an empty range at some stage has no split
  * that fits memory and counts zero. Synchronous.
  *   h_relaxations  HOST result.
+ * With HEDDLE_F_DISTRIBUTE the unit is one stage-cost evaluation (time,
+ * memory and gradient synchronisation of one stage): S for the proportional
+ * split and, when it does not fit, 2 per alternative priced (only the two
+ * stages around the moved cut change).
  * Returns HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_NOMEM or HEDDLE_E_DEVICE.
  */
 int heddle_count_work(const heddle_profile *p, int64_t n, int32_t s_max,

@@ -291,11 +291,14 @@ static int last_end(const oracle_profile *p, const ostage *st, int s, int S, int
  * s < S-1 relaxes each row i in [Bk_s, min(R_s, L-(S-s))] against the ends
  * max(i+1, Bk_{s+1}) .. last_end(s, i); each row of the last stage counts one.
  * This is the algorithmic work unit of the GPU kernel. */
+static int64_t count_distribute(const oracle_profile *p, const ostage *st, int S, int64_t m, uint32_t flags);
+
 int64_t oracle_count_relaxations(const oracle_profile *p, int S, const uint32_t *rec, int s_max,
                                  int64_t m, uint32_t flags)
 {
     ostage st[256];
     if (validate(p, S, s_max, rec, st) != OR_OK) return 0;
+    if (flags & OR_F_DISTRIBUTE) return count_distribute(p, st, S, m, flags);
     int64_t Mp = ceil_div64(m, st[0].dp), count = 0;
     int L = p->L, co = (flags & OR_F_COMPUTE_ONLY) != 0;
     int R[257], Bk[258], top[257];
@@ -545,6 +548,25 @@ static void price_distribute(const oracle_profile *p, const ostage *st, int S, i
     }
     if (found) *out = best;
     else out->status = OR_OOM;
+}
+
+/* Work of Distribute, in stage-cost evaluations: S for the proportional
+ * split and, when it does not fit (and memory is checked), 2 for every
+ * alternative of the list (only the two stages around the moved cut change;
+ * the others are already priced). */
+static int64_t count_distribute(const oracle_profile *p, const ostage *st, int S, int64_t m, uint32_t flags)
+{
+    oplan pl;
+    int64_t Mp = ceil_div64(m, st[0].dp), n = S;
+    distribute_cuts(p, st, S, pl.cut);
+    evaluate_i64(p, st, S, Mp, &pl);
+    if (pl.status == OR_OK || (flags & OR_F_COMPUTE_ONLY)) return n;
+    for (int b = 0; b + 1 < S; b++)
+        for (int d = -1; d <= 1; d += 2) {
+            int c = pl.cut[b + 1] + d;
+            if (c > pl.cut[b] && c < pl.cut[b + 2]) n += 2;
+        }
+    return n;
 }
 
 /* ---------------------------------------------------------------------- */

@@ -167,7 +167,7 @@ extern "C" int heddle_argmin_plans(int64_t n, const int32_t *h_m, int32_t n_m, u
                                    hipStream_t stream)
 {
     if (n < 0 || n_m < 1 || n_m > HEDDLE_MAX_MLIST || !h_m) return fail(HEDDLE_E_INVAL, "bad n / n_m / h_m");
-    if (flags & ~(HEDDLE_F_FP32 | HEDDLE_F_COMPUTE_ONLY)) return fail(HEDDLE_E_INVAL, "unknown flag bits");
+    if (flags & ~(HEDDLE_F_FP32 | HEDDLE_F_COMPUTE_ONLY | HEDDLE_F_DISTRIBUTE)) return fail(HEDDLE_E_INVAL, "unknown flag bits");
     for (int k = 0; k < n_m; k++)
         if (h_m[k] < 1 || h_m[k] > HEDDLE_MAX_M) return fail(HEDDLE_E_INVAL, "m out of range 1..2^24");
     if (!h_best_template || !h_best_m_index) return fail(HEDDLE_E_INVAL, "result pointer is NULL");

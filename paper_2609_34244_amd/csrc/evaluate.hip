@@ -11,7 +11,7 @@
 // their status and get INT64_MAX (fp32: +inf) values.
 #include <cstring>
 
-#include "device_common.h"
+#include "stage_cost.h"
 
 namespace heddle {
 
@@ -19,7 +19,6 @@ template <bool F32>
 __global__ void __launch_bounds__(256) evaluate_kernel(DevProfile P, PriceArgs A)
 {
     const int64_t total = A.n * A.n_m;
-    const int L = P.L, R = L + 1, N = P.n_types;
     for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < total; o += (int64_t)gridDim.x * blockDim.x) {
         const int64_t t = o / A.n_m;
         const int k = (int)(o - t * A.n_m);
@@ -38,7 +37,6 @@ __global__ void __launch_bounds__(256) evaluate_kernel(DevProfile P, PriceArgs A
         const int64_t Mp = (int64_t)(((uint32_t)m + (uint32_t)D - 1) / (uint32_t)D);
         const uint64_t B = F32 ? fixed_of_float(((const float *)A.bottleneck)[o], P.fx_exp)
                                : (uint64_t)((const int64_t *)A.bottleneck)[o];
-        const uint64_t *rows = P.rows64[F32 ? 1 : 0];
         uint64_t sumT = 0;
         int64_t maxg = 0, peak = 0;
         bool oom = false;
@@ -47,29 +45,15 @@ __global__ void __launch_bounds__(256) evaluate_kernel(DevProfile P, PriceArgs A
         for (int s = 0; s < S; s++) {
             const uint32_t r = r_next;
             if (s + 1 < S) r_next = rec[s + 1];
-            const int g = r & 0xFF, l2tp = (r >> 8) & 15, l2ep = (r >> 12) & 15;
-            const int tp = 1 << l2tp, ep = 1 << l2ep;
-            const int ki = nibble(P.tp_index, l2tp), ei = nibble(P.ep_index, l2ep);
             const int j = i + lay[s];
-            const int node = P.node_size[g];
-            const uint64_t *prow = rows + ((size_t)(g * P.n_tp + ki) * 3 + a2a_variant(ep, tp, node)) * R;
-            int64_t p2p = 0;
-            if (s + 1 < S) p2p = F32 ? P.p2p_fx[g * N + (int)(r_next & 0xFF)] : P.p2p_ns[g * N + (int)(r_next & 0xFF)];
-            const uint64_t T = prow[j] - prow[i] + (uint64_t)p2p;
-            sumT += F32 ? rne24(T) : T;
-            const int srow = (ki * P.n_ep + ei) * R, arow = ki * R;
-            const int64_t f = (int64_t)(S - s) < Mp ? (int64_t)(S - s) : Mp;
-            const int64_t mem = (P.pre_state[srow + j] - P.pre_state[srow + i]) + f * (P.pre_act[arow + j] - P.pre_act[arow + i]);
-            peak = mem > peak ? mem : peak;
-            oom = oom || mem > P.mem_cap[g];
-            const int64_t bw = (int64_t)tp * D <= node ? P.intra_bw[g] : P.link_bw[g * N + g];
-            const int64_t gsync = allreduce_ns(P.pre_grad[arow + j] - P.pre_grad[arow + i], D, bw) +
-                                  allreduce_ns(P.pre_xgrad[srow + j] - P.pre_xgrad[srow + i], (int64_t)((uint32_t)D / (uint32_t)ep), bw);
-            maxg = gsync > maxg ? gsync : maxg;
+            const StageCost c = stage_cost<F32>(P, r, (int)(r_next & 0xFF), s, S, i, j, D, Mp);
+            sumT += F32 ? rne24(c.T) : c.T;
+            peak = c.mem > peak ? c.mem : peak;
+            oom = oom || !c.fits;
+            maxg = c.g > maxg ? c.g : maxg;
             i = j;
         }
-        const uint64_t maxg_v = F32 ? rne24((uint64_t)maxg) << (-P.fx_exp) : (uint64_t)maxg;
-        const uint64_t iter = (uint64_t)(Mp - 1) * B + sumT + maxg_v;
+        const uint64_t iter = iteration_time<F32>(P, Mp, B, sumT, maxg);
         if (F32) ((float *)A.iter)[o] = exact_float(rne24(iter), P.fx_exp);
         else ((int64_t *)A.iter)[o] = (int64_t)iter;
         A.peak_mem[o] = peak;

@@ -105,6 +105,7 @@ int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const
                         const uint32_t *d_stages, const int32_t *h_m, int32_t n_m, uint32_t flags);
 int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool count_only);
 int launch_evaluate(const heddle_profile *p, const PriceArgs &a, hipStream_t stream);
+int launch_distribute(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool count_only);
 int launch_argmin(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t flags, const void *d_iter,
                   const uint8_t *d_status, int64_t *h_best_template, int32_t *h_best_m_index,
                   void *h_best_iter, hipStream_t stream);

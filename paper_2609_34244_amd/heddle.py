@@ -17,7 +17,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libheddle.so")
 
 HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_NOMEM, HEDDLE_E_DEVICE, HEDDLE_E_RANGE, HEDDLE_E_NOFEASIBLE = 0, -1, -2, -3, -4, -5
-HEDDLE_F_FP32, HEDDLE_F_COMPUTE_ONLY = 1, 2
+HEDDLE_F_FP32, HEDDLE_F_COMPUTE_ONLY, HEDDLE_F_DISTRIBUTE = 1, 2, 4
 STATUS_NAMES = ["OK", "BAD_SHAPE", "BAD_TYPE", "BAD_TP", "UNPROFILED", "BAD_DP", "BAD_EP", "OVERSUBSCRIBED", "OOM"]
 EXPORTS = ["heddle_load_profile", "heddle_free_profile", "heddle_price_plans", "heddle_argmin_plans",
            "heddle_best_plan", "heddle_count_work", "heddle_profile_info_get", "heddle_last_error"]

@@ -394,3 +394,71 @@ def test_count_work(H, flags):
         prof = H.heddle_load_profile(w.profile)
         ns, st = H.to_device(w.n_stages, w.stages)
         assert H.heddle_count_work(prof, ns, st, [int(x) for x in w.m], flags) == oracle_work(w, flags), w.name
+
+
+# ------------------------------------------------------------- Distribute mode
+DI = O.F_DISTRIBUTE
+DIST_SETS = [DI, DI | CO, DI | F32, DI | F32 | CO]
+
+
+@pytest.mark.parametrize("flags", DIST_SETS)
+def test_distribute_random_instances(H, flags):
+    """Heddle's proportional split with its fallback list, tiny instances with
+    every status code and memory that binds and not"""
+    n_plans = 0
+    for seed in range(120):
+        w = random_instance(seed)
+        if flags & F32 and seed % 2:
+            with_f32_table(w, seed)
+        prof = H.heddle_load_profile(w.profile)
+        g = gpu_price(H, prof, w, flags)
+        o = oracle_price(w, flags)
+        assert_same(g, o, flags, f"distribute random seed {seed} flags {flags}")
+        n_plans += g["status"].size
+    say("distribute random plans checked", n_plans)
+
+
+@pytest.mark.parametrize("name", list(SUBSETS))
+@pytest.mark.parametrize("flags", [DI, DI | F32])
+def test_distribute_config_subsets(H, name, flags):
+    w = sub_workload(workload(name), np.arange(SUBSETS[name]))
+    if flags & F32:
+        with_f32_table(w, 7)
+    prof = H.heddle_load_profile(w.profile)
+    g = gpu_price(H, prof, w, flags)
+    o = oracle_price(w, flags)
+    assert_same(g, o, flags, f"distribute {name} flags {flags}")
+    say(name, "distribute", flags, "statuses", np.bincount(g["status"].ravel(), minlength=9).tolist())
+
+
+def test_distribute_full_size_sampled(H):
+    """the whole 70B-like batch in Distribute mode, a seeded sample recomputed
+    by the oracle, the argmin checked as a minimiser; every Distribute
+    bottleneck is at least the min-max split's"""
+    w = workload("c3_70b_dense")
+    prof = H.heddle_load_profile(w.profile)
+    g = gpu_price(H, prof, w, DI)
+    assert not np.any(g["status"] == POISON)
+    idx = np.sort(np.random.default_rng(321).choice(w.n, size=300, replace=False))
+    o = oracle_price(sub_workload(w, idx), DI)
+    assert_same({k: v[idx] for k, v in g.items()}, o, DI, "distribute c3 sampled")
+    check_argmin_full(H, g, w.m, DI)
+    d = gpu_price(H, prof, w, 0)
+    both = (g["status"] == 0) & (d["status"] == 0)
+    assert np.all(g["bottleneck"][both] >= d["bottleneck"][both])
+    assert not np.any((g["status"] == 0) & (d["status"] != 0))     # a fitting split exists, so the DP finds one
+    say("distribute c3: OK", int((g["status"] == 0).sum()), "min-max OK", int((d["status"] == 0).sum()),
+        "mean bottleneck ratio", float(np.mean(g["bottleneck"][both] / d["bottleneck"][both])))
+
+
+def test_distribute_work_count(H):
+    """stage-cost evaluations of Distribute (S per split priced) against the
+    oracle's own count"""
+    for w in [random_instance(s) for s in range(30)] + [sub_workload(workload("c3_70b_dense"), np.arange(300))]:
+        for flags in (DI, DI | CO):
+            prof = H.heddle_load_profile(w.profile)
+            ns, st = H.to_device(w.n_stages, w.stages)
+            op = O.OracleProfile(w.profile)
+            want = sum(O.count_relaxations(op, int(w.n_stages[t]), w.stages[t], w.s_max, int(m), flags)
+                       for t in range(w.n) for m in w.m)
+            assert H.heddle_count_work(prof, ns, st, [int(x) for x in w.m], flags) == want, (w.name, flags)

@@ -483,6 +483,10 @@ def test_distribute_fallback_list():
     p = _speed_profile(9, [2, 1, 1], [10, 2, 10])
     r = price1(p, [(0, 1, 1, 1), (1, 1, 1, 1), (2, 1, 1, 1)], 4, O.F_DISTRIBUTE)
     assert (r["status"], tuple(r["layers"][:3]), r["bottleneck"], r["iter"]) == (0, (2, 2, 5), 5, 26)
+    # work: the proportional split (3 stage costs) plus the four alternatives, 2 each
+    _, rec = one_template([(0, 1, 1, 1), (1, 1, 1, 1), (2, 1, 1, 1)])
+    assert O.count_relaxations(O.OracleProfile(p), 3, rec[0], 3, 4, O.F_DISTRIBUTE) == 11
+    assert O.count_relaxations(O.OracleProfile(p), 3, rec[0], 3, 4, O.F_DISTRIBUTE | O.F_COMPUTE_ONLY) == 3
 
 
 @pytest.mark.parametrize("flags", [O.F_DISTRIBUTE, O.F_DISTRIBUTE | O.F_FP32])

@@ -108,7 +108,7 @@ template <class V, class V2> __device__ __forceinline__ V relax_range(const V2 *
 // the lexicographically smallest optimal split.
 
 template <class V, bool F32, bool COUNT>
-__global__ void __launch_bounds__(64, sizeof(V) == 4 ? 6 : 4) split_kernel(DevProfile P, PriceArgs A)
+__global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevProfile P, PriceArgs A)
 {
     typedef typename Vec2<V>::type V2;
     constexpr int kBatch = 4;                                  // stages whose limit rows are loaded together

@@ -290,7 +290,7 @@ def test_argument_errors(H):
     assert call(args(n=-1)) == H.HEDDLE_E_INVAL
     assert call(args(n_m=0)) == H.HEDDLE_E_INVAL
     assert call(args(n_m=65)) == H.HEDDLE_E_INVAL
-    assert call(args(flags=4)) == H.HEDDLE_E_INVAL
+    assert call(args(flags=8)) == H.HEDDLE_E_INVAL
     assert call(args(m=(C.c_int32 * 1)(0))) == H.HEDDLE_E_INVAL
     assert call(args(m=(C.c_int32 * 1)((1 << 24) + 1))) == H.HEDDLE_E_INVAL
     assert call(args(it=None)) == H.HEDDLE_E_INVAL

@@ -92,6 +92,30 @@ def test_config_subsets_fp32(H, name):
     assert_same(g, o, F32, f"{name} fp32")
 
 
+@pytest.mark.parametrize("flags", [0, CO, F32, F32 | CO])
+def test_random_instances_larger(H, flags):
+    """random instances with 20..139 layers, up to 32 stages and up to 32
+    micro-batch counts, odd batch sizes: windows longer than a wavefront,
+    several m classes per template"""
+    n_plans = 0
+    for seed in range(24):
+        rng = np.random.default_rng(5000 + seed)
+        L = int(rng.integers(20, 140))
+        s_max = int(rng.choice([8, 17, 32]))
+        n = int(rng.choice([1, 3, 41, 77]))
+        w = random_instance(5000 + seed, L=L, s_max=s_max, n=n, max_cost=200)
+        n_m = int(rng.choice([1, 5, 32]))
+        w.m = np.sort(rng.choice(np.arange(1, 400), size=n_m, replace=False)).astype(np.int32)
+        if flags & F32 and seed % 2:
+            with_f32_table(w, seed)
+        prof = H.heddle_load_profile(w.profile)
+        g = gpu_price(H, prof, w, flags)
+        o = oracle_price(w, flags)
+        assert_same(g, o, flags, f"seed {5000 + seed} L {L} s_max {s_max} n {n} n_m {n_m}")
+        n_plans += o["status"].size
+    say("larger random plans checked", n_plans)
+
+
 def check_argmin_full(H, g, m, flags):
     """the GPU argmin is a minimiser of iter/m over OK plans, lowest index among ties"""
     import torch

@@ -98,8 +98,8 @@ def main():
                     help="only run a plain device-to-device copy of BYTES (reference for HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py prices on one GPU; multi-GPU runs are not part of this build "
-              "(DESIGN.md describes how the batch would shard). Use --gpus 1.", file=sys.stderr)
+        print("bench.py prices on one GPU only; plans are independent, so a multi-GPU run would shard "
+              "the batch by estimated work and reduce the argmin keys. Use --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

@@ -15,210 +15,266 @@
 // fitting leaves the plan OOM without a split. With HEDDLE_F_COMPUTE_ONLY the
 // proportional split is kept and only flagged.
 //
-// Mapping: one wavefront per template (grid-stride), lane s = stage s. The
-// proportional cuts are computed once per template; each m value prices the
-// split with lanes = stages and wave reductions. If it does not fit, lane q
-// prices alternative q: only the two stages around the moved cut change, so
-// it costs two stage evaluations plus maxima over the untouched stages
-// (prefix and suffix maxima across lanes), and a wave minimum picks the
-// fastest fitting one.
+// Mapping: one lane per template (grid-stride over templates, one wavefront
+// per workgroup); each lane validates its template, computes the cuts and
+// walks its stages on its own, so the 64 lanes of a wavefront price 64
+// templates side by side. Per lane, LDS holds the stage starts c_0..c_S
+// (bytes) and one GPU counter per type for the oversubscription check; both
+// are laid out [index][lane], so every LDS access of a wavefront hits 64
+// distinct banks. For the fallback list, the first pass keeps the three
+// largest stage times, memories and synchronisation terms with their stages:
+// an alternative that moves the cut after stage b changes stages b and b+1
+// only, and the largest value over the other stages is the first of those
+// three not at b or b+1.
 #include <cstring>
 
-#include "decode.h"
 #include "stage_cost.h"
 
 namespace heddle {
 
-template <class T> __device__ __forceinline__ T wave_sum(T v)
+// the three largest values pushed (value, stage), zeros at stage -1 to start
+template <class T> struct Top3 {
+    T v0 = 0, v1 = 0, v2 = 0;
+    int i0 = -1, i1 = -1, i2 = -1;
+    __device__ __forceinline__ void push(T v, int s)
+    {
+        if (v > v0) {
+            v2 = v1; i2 = i1; v1 = v0; i1 = i0; v0 = v; i0 = s;
+        } else if (v > v1) {
+            v2 = v1; i2 = i1; v1 = v; i1 = s;
+        } else if (v > v2) {
+            v2 = v; i2 = s;
+        }
+    }
+    // the largest value over the stages other than b and b + 1
+    __device__ __forceinline__ T without(int b) const
+    {
+        return (i0 != b && i0 != b + 1) ? v0 : (i1 != b && i1 != b + 1) ? v1 : (i2 != b && i2 != b + 1) ? v2 : T(0);
+    }
+};
+
+template <bool F32> __device__ __forceinline__ uint64_t rounded(uint64_t T) { return F32 ? rne24(T) : T; }
+
+// Validation in status order (section 5.1 feasibility masks, section 5.2
+// exact profile match), one lane over its own stages; cnt is the lane's
+// column of per-type GPU counters (all zero on entry and on exit).
+__device__ __forceinline__ int validate_lane(const DevProfile &P, const PriceArgs &A, int S, const uint32_t *rec,
+                                             uint32_t *cnt)
 {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    return v;
+    if (S < 1 || S > A.s_max || S > P.L) return HEDDLE_S_BAD_SHAPE;
+    const int N = P.n_types;
+    const int D = (int)(rec[0] >> 16);
+    bool b_type = false, b_tp = false, b_prof = false, b_dp = false, b_ep = false;
+    for (int s = 0; s < S; s++) {
+        const uint32_t r = rec[s];
+        const int g = r & 0xFF, l2tp = (r >> 8) & 15, l2ep = (r >> 12) & 15, dpv = (int)(r >> 16);
+        const int gc = g < N ? g : N - 1;                      // clamped for the table reads
+        const int ki = nibble(P.tp_index, l2tp);
+        b_type |= g >= N;
+        b_tp |= !((P.tp_present >> l2tp) & 1) || (1 << l2tp) > P.node_size[gc];
+        b_prof |= !P.profiled[gc * P.n_tp + ki];
+        b_dp |= dpv < 1 || dpv != D;
+        b_ep |= !((P.ep_present >> l2ep) & 1) || ((uint32_t)D % (1u << l2ep)) != 0;
+    }
+    if (b_type) return HEDDLE_S_BAD_TYPE;
+    if (b_tp) return HEDDLE_S_BAD_TP;
+    if (b_prof) return HEDDLE_S_UNPROFILED;
+    if (b_dp) return HEDDLE_S_BAD_DP;
+    if (b_ep) return HEDDLE_S_BAD_EP;
+    // GPUs of each type: sum of TP over the stages of that type, times D
+    for (int s = 0; s < S; s++) cnt[(rec[s] & 0xFF) * 64] += 1u << ((rec[s] >> 8) & 15);
+    bool over = false;
+    for (int s = 0; s < S; s++) {
+        const int g = rec[s] & 0xFF;
+        over |= (int64_t)cnt[g * 64] * D > P.n_gpus[g];
+    }
+    for (int s = 0; s < S; s++) cnt[(rec[s] & 0xFF) * 64] = 0;
+    return over ? HEDDLE_S_OVERSUBSCRIBED : HEDDLE_S_OK;
 }
 
-__device__ __forceinline__ double rl_double(double v, int lane)
+__device__ __forceinline__ int stage_prow(const DevProfile &P, uint32_t r)
 {
-    return __longlong_as_double(rl64(__double_as_longlong(v), lane));
-}
-
-// max over lanes below (above) this one; lanes past the last stage hold 0
-template <class T> __device__ __forceinline__ T max_below(T v, int lane)
-{
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const T u = __shfl_up(v, o);
-        v = lane >= o && u > v ? u : v;
-    }
-    const T w = __shfl_up(v, 1);
-    return lane >= 1 ? w : T(0);
-}
-template <class T> __device__ __forceinline__ T max_above(T v, int lane)
-{
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const T u = __shfl_down(v, o);
-        v = lane + o < 64 && u > v ? u : v;
-    }
-    const T w = __shfl_down(v, 1);
-    return lane + 1 < 64 ? w : T(0);
+    const int g = r & 0xFF, l2tp = (r >> 8) & 15, l2ep = (r >> 12) & 15;
+    const int ki = nibble(P.tp_index, l2tp);
+    return ((g * P.n_tp + ki) * 3 + a2a_variant(1 << l2ep, 1 << l2tp, P.node_size[g])) * (P.L + 1);
 }
 
 // COUNT: only count the stage-cost evaluations into A.work (S for the
 // proportional split, 2 per alternative priced)
 template <bool F32, bool COUNT>
-__global__ void __launch_bounds__(64) distribute_kernel(DevProfile P, PriceArgs A)
+__global__ void __launch_bounds__(64, 3) distribute_kernel(DevProfile P, PriceArgs A)
 {
     extern __shared__ __align__(16) unsigned char smem[];      // one wavefront per workgroup
-    uint32_t *cnt = (uint32_t *)smem;                          // [n_types] GPU counters of decode
     const int lane = threadIdx.x;
+    uint32_t *cnt = (uint32_t *)smem + lane;                   // [n_types][64]: this lane's column
+    uint8_t *cut = smem + (size_t)P.n_types * 256 + lane;      // [s_cap + 1][64]: stage starts c_0..c_S
+    auto C = [&](int s) -> int { return cut[s * 64]; };
     const int L = P.L;
     const bool compute_only = (A.flags & HEDDLE_F_COMPUTE_ONLY) != 0;
+    const bool word_layers = (A.s_max & 3) == 0 && ((uintptr_t)A.layers & 3) == 0;
     unsigned long long work = 0;
+    for (int g = 0; g < P.n_types; g++) cnt[g * 64] = 0;
 
-    for (int64_t t = blockIdx.x; t < A.n; t += gridDim.x) {
-        const int S_in = A.n_stages[t];
-        const uint32_t rec_in = lane < A.s_max ? A.stages[t * A.s_max + lane] : 0u;
-        const StageInfo<uint64_t> x = decode<uint64_t, F32>(P, A, S_in, rec_in, lane, cnt);
+    for (int64_t t = (int64_t)blockIdx.x * 64 + lane; t < A.n; t += (int64_t)gridDim.x * 64) {
+        const int S = A.n_stages[t];
+        const uint32_t *rec = A.stages + t * A.s_max;
         const size_t obase = (size_t)t * A.n_m;
-        if (x.status != 0) {
+        const int status = validate_lane(P, A, S, rec, cnt);
+        if (status != HEDDLE_S_OK) {
             if (COUNT) continue;
-            if (lane < A.n_m) {
-                A.status[obase + lane] = (uint8_t)x.status;
+            for (int k = 0; k < A.n_m; k++) {
+                const size_t o = obase + k;
+                A.status[o] = (uint8_t)status;
                 if (F32) {
-                    ((float *)A.iter)[obase + lane] = __builtin_inff();
-                    ((float *)A.bottleneck)[obase + lane] = __builtin_inff();
+                    ((float *)A.iter)[o] = __builtin_inff();
+                    ((float *)A.bottleneck)[o] = __builtin_inff();
                 } else {
-                    ((int64_t *)A.iter)[obase + lane] = INT64_MAX;
-                    ((int64_t *)A.bottleneck)[obase + lane] = INT64_MAX;
+                    ((int64_t *)A.iter)[o] = INT64_MAX;
+                    ((int64_t *)A.bottleneck)[o] = INT64_MAX;
                 }
-                A.peak_mem[obase + lane] = INT64_MAX;
+                A.peak_mem[o] = INT64_MAX;
+                if (word_layers) {
+                    for (int w = 0; w < A.s_max; w += 4) *(uint32_t *)&A.layers[o * A.s_max + w] = 0u;
+                } else {
+                    for (int w = 0; w < A.s_max; w++) A.layers[o * A.s_max + w] = 0;
+                }
             }
-            for (int k = 0; k < A.n_m; k++)
-                if (lane < A.s_max) A.layers[(obase + k) * A.s_max + lane] = 0;
             continue;
         }
-        const int S = uni(x.S), D = x.D;
-        const uint32_t rec = lane < S ? rec_in : 0u;
-        const int g_next = __builtin_amdgcn_update_dpp((int)(rec & 0xFF), (int)(rec & 0xFF), kDppWaveShl1, 0xF, 0xF,
-                                                       false);
+        const int D = (int)(rec[0] >> 16);
 
-        // ---- proportional cuts: lane s holds stage s's layers [lo, hi)
-        double speed = 0.0;
-        if (lane < S) speed = 1.0 / (double)P.rows64[0][x.prow + L];
-        double total = 0.0, below = 0.0;                       // lane s: speed of stages < s
-        for (int s = 0; s < S; s++) {
-            below = lane == s ? total : below;
-            total += rl_double(speed, s);
-        }
-        const int c_raw = (int)floor((double)L * below / total + 0.5);
-        int lo = 0, hi = L, prev = 0;
-        for (int s = 1; s < S; s++) {
-            int c = uni(rl32(c_raw, s));
-            c = c < prev + 1 ? prev + 1 : c;
-            c = c > L - (S - s) ? L - (S - s) : c;
-            lo = put_lane(lo, c, s);
-            hi = put_lane(hi, c, s - 1);
-            prev = c;
+        // ---- proportional cuts: c_s = nearest integer to L * (speed of stages < s) / (speed of all)
+        double total = 0.0;
+        for (int s = 0; s < S; s++) total += 1.0 / (double)P.rows64[0][stage_prow(P, rec[s]) + L];
+        {
+            double below = 0.0;
+            int prev = 0;
+            cut[0] = 0;
+            for (int s = 1; s < S; s++) {
+                below += 1.0 / (double)P.rows64[0][stage_prow(P, rec[s - 1]) + L];
+                int c = (int)floor((double)L * below / total + 0.5);
+                c = c < prev + 1 ? prev + 1 : c;
+                c = c > L - (S - s) ? L - (S - s) : c;
+                cut[s * 64] = (uint8_t)c;
+                prev = c;
+            }
+            cut[S * 64] = (uint8_t)L;
         }
 
         for (int k = 0; k < A.n_m; k++) {
             const int32_t m = A.m[k];
             const int64_t Mp = (int64_t)(((uint32_t)m + (uint32_t)D - 1) / (uint32_t)D);
-            // the proportional split, lanes = stages
-            uint64_t T = 0;
-            int64_t mem = 0, g = 0;
-            bool nf = false;
-            if (lane < S) {
-                const StageCost c = stage_cost<F32>(P, rec, g_next, lane, S, lo, hi, D, Mp);
-                T = F32 ? rne24(c.T) : c.T;
-                mem = c.mem;
-                g = c.g;
-                nf = !c.fits;
+            // ---- the proportional split
+            uint64_t sumT = 0, nf = 0;
+            Top3<uint64_t> tT;
+            Top3<int64_t> tM, tG;
+#pragma unroll 1
+            for (int s = 0; s < S; s++) {
+                const int g_next = s + 1 < S ? (int)(rec[s + 1] & 0xFF) : 0;
+                const StageCost c = stage_cost<F32>(P, rec[s], g_next, s, S, C(s), C(s + 1), D, Mp);
+                const uint64_t T = rounded<F32>(c.T);
+                sumT += T;
+                tT.push(T, s);
+                tM.push(c.mem, s);
+                tG.push(c.g, s);
+                nf |= (uint64_t)(!c.fits) << s;
             }
-            const uint64_t sumT = wave_sum(T);
-            const uint64_t nf_mask = __ballot(nf);
-            work += S;
-            uint64_t B = wave_max(T), iter = 0;
-            int64_t peak = wave_max(mem);
-            iter = iteration_time<F32>(P, Mp, B, sumT, wave_max(g));
-            iter = F32 ? rne24(iter) : iter;
-            bool fits = nf_mask == 0, has_split = fits || compute_only;
-            int out_lo = lo, out_hi = hi;
+            if (COUNT) work += S;
+            uint64_t B = tT.v0;
+            uint64_t iter = rounded<F32>(iteration_time<F32>(P, Mp, B, sumT, tG.v0));
+            int64_t peak = tM.v0;
+            bool fits = nf == 0, has_split = fits || compute_only;
+            int best_b = -1, best_c = 0;
             if (!has_split) {
-                // the fixed list of alternatives: lane q prices "cut after stage q/2
-                // moved by -1 (q even) or +1 (q odd)"; only stages b and b+1 change, the
-                // rest comes from maxima over the stages below b and above b+1
-                const uint64_t T_lo = max_below(T, lane), T_hi = max_above(T, lane);
-                const int64_t M_lo = max_below(mem, lane), M_hi = max_above(mem, lane);
-                const int64_t G_lo = max_below(g, lane), G_hi = max_above(g, lane);
-                const int n_alt = 2 * (S - 1);
+                // the fixed list of alternatives, in order: for each boundary b, the cut
+                // after stage b moved by -1, then by +1; the fastest fitting one is kept
+                // (the first on ties)
                 uint64_t best_key = ~0ull;
-                int best_q = -1;
-                for (int q0 = 0; q0 < n_alt; q0 += 64) {
-                    const int q = q0 + lane;
-                    const int b = min(q >> 1, S - 2);
-                    const int lo_b = __shfl(lo, b), cut = __shfl(hi, b), hi_b1 = __shfl(hi, b + 1);
-                    const int c = cut + ((q & 1) ? 1 : -1);
-                    const bool valid = q < n_alt && c > lo_b && c < hi_b1;
-                    const int cc = min(max(c, lo_b), hi_b1);        // in range for the table reads
-                    const uint32_t rb = __shfl(rec, b), rb1 = __shfl(rec, b + 1);
-                    const int g2 = __shfl(g_next, b + 1);
-                    const StageCost c0 = stage_cost<F32>(P, rb, (int)(rb1 & 0xFF), b, S, lo_b, cc, D, Mp);
-                    const StageCost c1 = stage_cost<F32>(P, rb1, g2, b + 1, S, cc, hi_b1, D, Mp);
-                    const uint64_t t0 = F32 ? rne24(c0.T) : c0.T, t1 = F32 ? rne24(c1.T) : c1.T;
-                    uint64_t B2 = max(max(__shfl(T_lo, b), __shfl(T_hi, b + 1)), max(t0, t1));
-                    const uint64_t sum2 = sumT - __shfl(T, b) - __shfl(T, b + 1) + t0 + t1;
-                    const int64_t g2max = max(max(__shfl(G_lo, b), __shfl(G_hi, b + 1)), max(c0.g, c1.g));
-                    uint64_t it2 = iteration_time<F32>(P, Mp, B2, sum2, g2max);
-                    it2 = F32 ? rne24(it2) : it2;
-                    const bool others_fit = (nf_mask & ~(3ull << b)) == 0;
-                    const bool ok = valid && others_fit && c0.fits && c1.fits;
-                    const uint64_t key = ok ? it2 : ~0ull;
-                    const uint64_t kmin = wave_min(key);
-                    if (kmin < best_key) {                              // strictly faster: earlier slots win ties
-                        const int win = __ffsll((unsigned long long)__ballot(key == kmin)) - 1;
-                        best_key = kmin;
-                        best_q = q0 + win;
-                        B = (uint64_t)rl64((int64_t)B2, win);
-                        iter = (uint64_t)rl64((int64_t)it2, win);
-                        const int64_t pk = max(max(__shfl(M_lo, b), __shfl(M_hi, b + 1)), max(c0.mem, c1.mem));
-                        peak = rl64(pk, win);
+#pragma unroll 1
+                for (int b = 0; b + 1 < S; b++) {
+                    const uint32_t rb = rec[b], rb1 = rec[b + 1];
+                    const int g2 = b + 2 < S ? (int)(rec[b + 2] & 0xFF) : 0;
+                    const int lo = C(b), cb = C(b + 1), hi = C(b + 2);
+                    const uint64_t Tb = rounded<F32>(stage_cost<F32>(P, rb, (int)(rb1 & 0xFF), b, S, lo, cb, D, Mp).T);
+                    const uint64_t Tb1 = rounded<F32>(stage_cost<F32>(P, rb1, g2, b + 1, S, cb, hi, D, Mp).T);
+                    const uint64_t T_rest = tT.without(b);
+                    const int64_t M_rest = tM.without(b), G_rest = tG.without(b);
+                    const bool others_fit = (nf & ~(3ull << b)) == 0;
+#pragma unroll 1
+                    for (int d = -1; d <= 1; d += 2) {
+                        const int c = cb + d;
+                        if (c <= lo || c >= hi) continue;           // every stage keeps a layer
+                        if (COUNT) {
+                            work += 2;
+                            continue;
+                        }
+                        const StageCost c0 = stage_cost<F32>(P, rb, (int)(rb1 & 0xFF), b, S, lo, c, D, Mp);
+                        const StageCost c1 = stage_cost<F32>(P, rb1, g2, b + 1, S, c, hi, D, Mp);
+                        const uint64_t t0 = rounded<F32>(c0.T), t1 = rounded<F32>(c1.T);
+                        const uint64_t B2 = max(T_rest, max(t0, t1));
+                        const uint64_t sum2 = sumT - Tb - Tb1 + t0 + t1;
+                        const int64_t g2max = max(G_rest, max(c0.g, c1.g));
+                        const uint64_t it2 = rounded<F32>(iteration_time<F32>(P, Mp, B2, sum2, g2max));
+                        if (others_fit && c0.fits && c1.fits && it2 < best_key) {
+                            best_key = it2;
+                            best_b = b;
+                            best_c = c;
+                            B = B2;
+                            iter = it2;
+                            peak = max(M_rest, max(c0.mem, c1.mem));
+                        }
                     }
-                    if (COUNT) work += 2 * (uint64_t)__popcll(__ballot(valid));
                 }
-                if (best_q >= 0) {
-                    const int b = best_q >> 1;
-                    const int c = uni(rl32(hi, b)) + ((best_q & 1) ? 1 : -1);
-                    out_lo = put_lane(lo, c, b + 1);
-                    out_hi = put_lane(hi, c, b);
-                    fits = has_split = true;
-                }
+                if (best_b >= 0) fits = has_split = true;
             }
             if (COUNT) continue;
             const size_t o = obase + k;
-            if (lane == 0) {
-                A.status[o] = (uint8_t)(fits ? HEDDLE_S_OK : HEDDLE_S_OOM);
-                if (F32) {
-                    ((float *)A.iter)[o] = has_split ? exact_float(iter, P.fx_exp) : __builtin_inff();
-                    ((float *)A.bottleneck)[o] = has_split ? exact_float(B, P.fx_exp) : __builtin_inff();
-                } else {
-                    ((int64_t *)A.iter)[o] = has_split ? (int64_t)iter : INT64_MAX;
-                    ((int64_t *)A.bottleneck)[o] = has_split ? (int64_t)B : INT64_MAX;
-                }
-                A.peak_mem[o] = has_split ? peak : INT64_MAX;
+            A.status[o] = (uint8_t)(fits ? HEDDLE_S_OK : HEDDLE_S_OOM);
+            if (F32) {
+                ((float *)A.iter)[o] = has_split ? exact_float(iter, P.fx_exp) : __builtin_inff();
+                ((float *)A.bottleneck)[o] = has_split ? exact_float(B, P.fx_exp) : __builtin_inff();
+            } else {
+                ((int64_t *)A.iter)[o] = has_split ? (int64_t)iter : INT64_MAX;
+                ((int64_t *)A.bottleneck)[o] = has_split ? (int64_t)B : INT64_MAX;
             }
-            if (lane < A.s_max) A.layers[o * A.s_max + lane] = (has_split && lane < S) ? (uint8_t)(out_hi - out_lo) : 0;
+            A.peak_mem[o] = has_split ? peak : INT64_MAX;
+            // layer counts; the winning alternative moves the start of stage best_b + 1
+            auto layers_of = [&](int s) -> uint32_t {
+                if (!has_split || s >= S) return 0u;
+                const int a = s == best_b + 1 ? best_c : C(s);
+                const int e = s == best_b ? best_c : C(s + 1);
+                return (uint32_t)(e - a);
+            };
+            if (word_layers) {
+                for (int w = 0; w < A.s_max; w += 4)
+                    *(uint32_t *)&A.layers[o * A.s_max + w] =
+                        layers_of(w) | layers_of(w + 1) << 8 | layers_of(w + 2) << 16 | layers_of(w + 3) << 24;
+            } else {
+                for (int w = 0; w < A.s_max; w++) A.layers[o * A.s_max + w] = (uint8_t)layers_of(w);
+            }
         }
     }
-    if (COUNT && lane == 0 && work) atomicAdd(A.work, work);
+    if (COUNT) {
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) work += __shfl_xor(work, off);
+        if (lane == 0 && work) atomicAdd(A.work, work);
+    }
 }
 
 int launch_distribute(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool count_only)
 {
     if (a.n == 0) return HEDDLE_OK;
-    const size_t lds = ((size_t)p->dev.n_types * 4 + 15) & ~size_t(15);
-    const int blocks = (int)(a.n < 65536 ? a.n : 65536);
+    const int s_cap = a.s_max < p->dev.L ? a.s_max : p->dev.L;
+    const size_t lds = (size_t)p->dev.n_types * 256 + (size_t)(s_cap + 1) * 64;
+    int max_lds = 0;
+    HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
+    if (lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "per-lane tables of this profile do not fit in LDS");
+    const int64_t want = (a.n + 63) / 64;
+    const int blocks = (int)(want < 65536 ? want : 65536);
     const bool f32 = a.flags & HEDDLE_F_FP32;
+    const void *fn = count_only ? (f32 ? (const void *)distribute_kernel<true, true> : (const void *)distribute_kernel<false, true>)
+                                : (f32 ? (const void *)distribute_kernel<true, false> : (const void *)distribute_kernel<false, false>);
+    if (lds > 65536) HEDDLE_HIP(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
     if (count_only) {
         if (f32) hipLaunchKernelGGL((distribute_kernel<true, true>), dim3(blocks), dim3(64), lds, stream, p->dev, a);
         else hipLaunchKernelGGL((distribute_kernel<false, true>), dim3(blocks), dim3(64), lds, stream, p->dev, a);

@@ -92,6 +92,12 @@ def main():
     ap.add_argument("--compute-only", action="store_true", help="split ignores memory; fit checked after")
     ap.add_argument("--distribute", action="store_true",
                     help="Heddle's speed-proportional split with its fallback list instead of the min-max split")
+    ap.add_argument("--enumerate", action="store_true",
+                    help="price the whole space of the search backbone (every stage count up to --enum-depth, "
+                         "every type and TP per stage) on the config's profile instead of its template batch")
+    ap.add_argument("--enum-types", type=int, default=3, help="GPU types 0..n-1 of the enumerated space")
+    ap.add_argument("--enum-tps", type=int, default=3, help="TP degrees 1, 2, 4, ... of the enumerated space")
+    ap.add_argument("--enum-depth", type=int, default=8, help="largest stage count of the enumerated space")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -120,6 +126,8 @@ def main():
     flags = (H.HEDDLE_F_FP32 if args.fp32 else 0) | (H.HEDDLE_F_COMPUTE_ONLY if args.compute_only else 0) | \
         (H.HEDDLE_F_DISTRIBUTE if args.distribute else 0)
     k_unit, unit_name = (K_EVAL, "stage-cost evaluation") if args.distribute else (K_MIN, "DP relaxation")
+    if args.enumerate:
+        return run_enumerate(args, H, flags, k_unit, unit_name)
     t0 = time.perf_counter()
     w = make_workload(args.config)
     log(f"workload {args.config}: {w.n} templates x {len(w.m)} m generated in {time.perf_counter() - t0:.1f}s")
@@ -229,6 +237,101 @@ def main():
         log(f"oracle baseline, about {args.cpu_seconds:.0f} s on one host core")
         result["cpu_baseline"] = cpu_baseline(w, flags, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def run_enumerate(args, H, flags, k_unit, unit_name):
+    """A step is one heddle_best_enumerated call: every template of the space
+    generated on the device, priced, and the best plan of the space found."""
+    import numpy as np
+    import torch
+
+    from workloads.gen import make_workload
+
+    w = make_workload(args.config, n=16)           # the config's profile; its template batch is not used
+    n_types = w.profile.layer_ns.shape[0]
+    tp_log2 = [int(np.log2(t)) for t in w.profile.tp_degrees]
+    assert args.enum_types <= n_types and args.enum_tps <= len(tp_log2), "space larger than the profile"
+    types, tps = list(range(args.enum_types)), tp_log2[:args.enum_tps]
+    spec = H.EnumSpec(args.enum_depth, types, tps, [1], 0)
+    m = [int(x) for x in w.m]
+    total = H.heddle_enum_count(spec)
+    prof = H.heddle_load_profile(w.profile)
+    n_plans = total * len(m)
+    # algorithmic work of one pass over the space, counted chunk by chunk outside the timed region
+    relax, chunk = 0, 1 << 22
+    for first in range(0, total, chunk):
+        ns, st = H.heddle_enum_templates(spec, first, min(chunk, total - first))
+        relax += H.heddle_count_work(prof, ns, st, m, flags)
+    del ns, st
+    torch.cuda.synchronize()
+    log(f"space: {total:,} templates x {len(m)} m (types {types}, log2 TP {tps}, S <= {args.enum_depth}); "
+        f"work {relax:,} x {unit_name}")
+    for i in range(args.warmup):
+        H.heddle_best_enumerated(prof, spec, m, flags)
+        log(f"warmup {i + 1}/{args.warmup} done")
+    times, best = [], None
+    for i in range(args.steps):
+        t0 = time.perf_counter()
+        best = H.heddle_best_enumerated(prof, spec, m, flags)
+        times.append(time.perf_counter() - t0)
+    step_s = float(np.mean(times))
+    log(f"timed {args.steps} passes over the space: {step_s * 1e3:.1f} ms each; best {best}")
+    achieved = relax * k_unit / step_s
+    result = {
+        "metric": "candidate plans priced/sec (partition+evaluate) on 1 MI355X; % VALU roofline",
+        "value": n_plans / step_s,
+        "unit": "plans/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": ("fp32" if args.fp32 else "int64"),
+        "data": "synthetic",
+        "config": {"workload": f"search-backbone enumeration on the {WORKLOAD_TEXT[args.config].split(':')[0]} "
+                               f"profile (L={w.profile.L}): {args.enum_types} GPU types x {args.enum_tps} TP degrees "
+                               f"per stage, S <= {args.enum_depth}, DP 1, m={m}: {n_plans:,} plans",
+                   "name": args.config, "templates": total, "m": m, "plans": n_plans,
+                   "memory_aware": not args.compute_only,
+                   "partition": "distribute" if args.distribute else "min-max"},
+        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12, "unit": "Tlane-op/s",
+                     "frac": achieved / PEAK_LANE_OPS, "traffic": None,
+                     "kernel": "whole pass (generator, split, evaluate and argmin kernels, per-chunk host syncs)",
+                     "kernel_ms": step_s * 1e3, "work_per_launch": relax, "work_unit": unit_name,
+                     "ops_per_unit": k_unit},
+        "best_plan": {"template": best[0], "m_index": best[1], "iter": best[2], "ok_plans": best[3]},
+    }
+    if not args.no_cpu_baseline:
+        log(f"oracle baseline, about {args.cpu_seconds:.0f} s on one host core")
+        result["cpu_baseline"] = cpu_baseline_enumerate(w, spec, m, flags, total, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline_enumerate(w, spec, m, flags, total, budget_s):
+    import numpy as np
+
+    from oracle import enumeration as EN
+    from oracle import oracle as O
+    op = O.OracleProfile(w.profile)
+    rng = np.random.default_rng(0)
+    pick = lambda n: EN.as_arrays([EN.template_at(spec.d_max, spec.types.tolist(), spec.log2_tp.tolist(),
+                                                  spec.dp.tolist(), spec.log2_ep, int(u))
+                                   for u in rng.integers(0, total, size=n)], spec.d_max)
+    ns, st = pick(20)
+    t0 = time.perf_counter()
+    O.price_plans(op, ns, st, m, flags)
+    per = (time.perf_counter() - t0) / 20
+    n = int(max(20, min(total, budget_s / max(per, 1e-9))))
+    ns, st = pick(n)
+    t0 = time.perf_counter()
+    O.price_plans(op, ns, st, m, flags)
+    dt = time.perf_counter() - t0
+    return {"value": n * len(m) / dt, "unit": "plans/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} templates drawn uniformly from the {total:,} of the space x {len(m)} m, "
+                      f"single-threaded plain C oracle, {dt:.1f} s",
+            "host_cores_available": len(os.sched_getaffinity(0))}
 
 
 if __name__ == "__main__":

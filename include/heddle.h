@@ -243,6 +243,69 @@ int heddle_count_work(const heddle_profile *p, int64_t n, int32_t s_max,
                       int64_t *h_relaxations, hipStream_t stream);
 
 /*
+ * Exhaustive enumeration of structures: the search backbone of the planners
+ * Heddle analyses (section 3.1), with (N * K)^D structures for N GPU types,
+ * K TP degrees and D stages (section 2), run as one data-parallel workload.
+ * The space, in order (outermost first): S = 1 .. d_max stages; the type
+ * vector (g_0 .. g_{S-1}), each entry over `types` in list order, g_0
+ * slowest; the TP vector (over `log2_tp`) likewise; the DP degree (over
+ * `dp`). Every stage of a template gets the template's DP degree and EP
+ * degree 2^log2_ep. Index u of this order is template u of the space. The
+ * micro-batch count is the innermost loop (the m list of the calls below).
+ * All pointers are HOST memory, read during the call.
+ */
+typedef struct heddle_enum_spec {
+    int32_t d_max;                /* stage counts 1 .. d_max, d_max in 1..64                */
+    int32_t n_types;              /* 1..255                                                 */
+    const uint8_t *types;         /* [n_types] distinct GPU type indices, in loop order     */
+    int32_t n_tp;                 /* 1..16                                                  */
+    const uint8_t *log2_tp;       /* [n_tp] distinct log2 TP degrees 0..15, in loop order   */
+    int32_t n_dp;                 /* 1..64                                                  */
+    const int32_t *dp;            /* [n_dp] distinct DP degrees 1..65535, in loop order     */
+    int32_t log2_ep;              /* EP degree of every stage, log2, 0..15                  */
+} heddle_enum_spec;
+
+/*
+ * heddle_enum_count -- size of the space: sum over S of
+ * (n_types * n_tp)^S * n_dp. Returns HEDDLE_OK, HEDDLE_E_INVAL (bad spec:
+ * size out of range, a duplicate list entry) or HEDDLE_E_RANGE (2^62 or
+ * more templates).
+ */
+int heddle_enum_count(const heddle_enum_spec *sp, int64_t *h_count);
+
+/*
+ * heddle_enum_templates -- write templates first .. first + n - 1 of the
+ * space as template records (the layout of heddle_price_plans with
+ * s_max = d_max; slots s >= S are zero). Asynchronous on `stream`.
+ *   d_n_stages  DEVICE [n] uint8; d_stages DEVICE [n][d_max] uint32.
+ * Returns HEDDLE_OK, HEDDLE_E_INVAL (bad spec, range outside the space, null
+ * output), HEDDLE_E_RANGE or HEDDLE_E_DEVICE.
+ */
+int heddle_enum_templates(const heddle_enum_spec *sp, int64_t first, int64_t n,
+                          uint8_t *d_n_stages, uint32_t *d_stages, hipStream_t stream);
+
+/*
+ * heddle_best_enumerated -- the best plan of the whole space: every
+ * template at every m, priced as heddle_price_plans (s_max = d_max, the
+ * same flags) and ranked as heddle_argmin_plans, ties to the lowest template
+ * index, then the lowest m index. The space is walked in chunks of `chunk`
+ * templates (0: 4,194,304); the library allocates the chunk buffers on
+ * `stream` (stream-ordered) and frees them before returning. Synchronous.
+ *   h_best_index    HOST template index in the space (heddle_enum_templates
+ *                   with n = 1 gives its records).
+ *   h_best_m_index  HOST index into h_m.
+ *   h_best_iter     HOST int64 (float with FP32) iteration time; may be NULL.
+ *   h_n_ok          HOST number of plans of status OK; may be NULL.
+ * Returns HEDDLE_OK, HEDDLE_E_NOFEASIBLE (no plan of the space has status
+ * OK; *h_n_ok is still written), HEDDLE_E_INVAL, HEDDLE_E_RANGE,
+ * HEDDLE_E_NOMEM or HEDDLE_E_DEVICE.
+ */
+int heddle_best_enumerated(const heddle_profile *p, const heddle_enum_spec *sp,
+                           const int32_t *h_m, int32_t n_m, uint32_t flags, int64_t chunk,
+                           int64_t *h_best_index, int32_t *h_best_m_index, void *h_best_iter,
+                           int64_t *h_n_ok, hipStream_t stream);
+
+/*
  * heddle_profile_info -- facts about a loaded profile for tests and reports.
  *   narrow[0]  1 if the int64 split runs in exact 32-bit arithmetic
  *   narrow[1]  1 if the fp32 split does

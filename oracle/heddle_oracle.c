@@ -31,7 +31,7 @@
  * product and quotient of a transfer time is done in 128-bit integers, and
  * the DP is the textbook suffix recurrence over all (row, column) pairs.
  *
- * Readings of the paper where it is silent (each also listed in the design doc):
+ * Readings of the paper where it is silent:
  *  - the split minimises the bottleneck stage time (stage compute + its
  *    outbound p2p), every stage holds >= 1 layer, ties are broken to the
  *    lexicographically smallest layer-count vector;

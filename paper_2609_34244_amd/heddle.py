@@ -20,7 +20,8 @@ HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_NOMEM, HEDDLE_E_DEVICE, HEDDLE_E_RANGE, HEDD
 HEDDLE_F_FP32, HEDDLE_F_COMPUTE_ONLY, HEDDLE_F_DISTRIBUTE = 1, 2, 4
 STATUS_NAMES = ["OK", "BAD_SHAPE", "BAD_TYPE", "BAD_TP", "UNPROFILED", "BAD_DP", "BAD_EP", "OVERSUBSCRIBED", "OOM"]
 EXPORTS = ["heddle_load_profile", "heddle_free_profile", "heddle_price_plans", "heddle_argmin_plans",
-           "heddle_best_plan", "heddle_count_work", "heddle_profile_info_get", "heddle_last_error"]
+           "heddle_best_plan", "heddle_count_work", "heddle_profile_info_get", "heddle_last_error",
+           "heddle_enum_count", "heddle_enum_templates", "heddle_best_enumerated"]
 
 
 class HeddleError(RuntimeError):
@@ -39,6 +40,11 @@ class heddle_profile_desc(C.Structure):
                 ("boundary_bytes", C.c_int64), ("a2a_bytes", C.c_int64),
                 ("mem_cap_bytes", C.c_void_p), ("node_size", C.c_void_p), ("n_gpus", C.c_void_p),
                 ("intra_bw_MBps", C.c_void_p), ("link_bw_MBps", C.c_void_p)]
+
+
+class heddle_enum_spec(C.Structure):
+    _fields_ = [("d_max", C.c_int32), ("n_types", C.c_int32), ("types", C.c_void_p), ("n_tp", C.c_int32),
+                ("log2_tp", C.c_void_p), ("n_dp", C.c_int32), ("dp", C.c_void_p), ("log2_ep", C.c_int32)]
 
 
 class heddle_profile_info(C.Structure):
@@ -66,9 +72,14 @@ def lib():
                                        P, P]
         L.heddle_count_work.argtypes = [P, I64, I32, P, P, P, I32, U32, C.POINTER(C.c_int64), P]
         L.heddle_profile_info_get.argtypes = [P, C.POINTER(heddle_profile_info)]
+        L.heddle_enum_count.argtypes = [C.POINTER(heddle_enum_spec), C.POINTER(C.c_int64)]
+        L.heddle_enum_templates.argtypes = [C.POINTER(heddle_enum_spec), I64, I64, P, P, P]
+        L.heddle_best_enumerated.argtypes = [P, C.POINTER(heddle_enum_spec), P, I32, U32, I64,
+                                             C.POINTER(C.c_int64), C.POINTER(C.c_int32), P, C.POINTER(C.c_int64), P]
         L.heddle_last_error.restype = C.c_char_p
         for f in ("heddle_load_profile", "heddle_price_plans", "heddle_argmin_plans", "heddle_best_plan",
-                  "heddle_count_work", "heddle_profile_info_get"):
+                  "heddle_count_work", "heddle_profile_info_get", "heddle_enum_count", "heddle_enum_templates",
+                  "heddle_best_enumerated"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -212,3 +223,46 @@ def to_device(n_stages, stages, device="cuda"):
     ns = torch.from_numpy(np.ascontiguousarray(n_stages, dtype=np.uint8)).to(device)
     st = torch.from_numpy(np.ascontiguousarray(stages, dtype=np.uint32).view(np.int32)).to(device)
     return ns, st
+
+
+class EnumSpec:
+    """Host description of an enumerated space (keeps its arrays alive)."""
+
+    def __init__(self, d_max, types, log2_tp, dp=(1,), log2_ep=0):
+        self.types = np.ascontiguousarray(types, dtype=np.uint8)
+        self.log2_tp = np.ascontiguousarray(log2_tp, dtype=np.uint8)
+        self.dp = np.ascontiguousarray(dp, dtype=np.int32)
+        self.d_max, self.log2_ep = int(d_max), int(log2_ep)
+        self.c = heddle_enum_spec(d_max=self.d_max, n_types=len(self.types), types=self.types.ctypes.data,
+                                  n_tp=len(self.log2_tp), log2_tp=self.log2_tp.ctypes.data, n_dp=len(self.dp),
+                                  dp=self.dp.ctypes.data, log2_ep=self.log2_ep)
+
+
+def heddle_enum_count(spec):
+    n = C.c_int64(0)
+    _check(lib().heddle_enum_count(C.byref(spec.c), C.byref(n)))
+    return int(n.value)
+
+
+def heddle_enum_templates(spec, first, n, device="cuda", stream=None):
+    """Templates first .. first + n - 1 of the space as device tensors
+    (n_stages uint8 [n], stages int32 bits [n, d_max])."""
+    import torch
+    ns = torch.empty(n, dtype=torch.uint8, device=device)
+    st = torch.empty((n, spec.d_max), dtype=torch.int32, device=device)
+    _check(lib().heddle_enum_templates(C.byref(spec.c), int(first), int(n), _ptr(ns), _ptr(st), _stream(stream)))
+    return ns, st
+
+
+def heddle_best_enumerated(prof, spec, m, flags, chunk=0, stream=None):
+    """(template index, m index, iter, OK plan count) of the best plan of the
+    space; the index is None if no plan is OK."""
+    mm, mp = _mlist(m)
+    bt, bk, n_ok = C.c_int64(-1), C.c_int32(-1), C.c_int64(-1)
+    bi = (C.c_float if flags & HEDDLE_F_FP32 else C.c_int64)()
+    rc = lib().heddle_best_enumerated(prof.handle, C.byref(spec.c), mp, len(mm), flags, int(chunk), C.byref(bt),
+                                      C.byref(bk), C.cast(C.byref(bi), C.c_void_p), C.byref(n_ok), _stream(stream))
+    if rc == HEDDLE_E_NOFEASIBLE:
+        return None, None, None, int(n_ok.value)
+    _check(rc)
+    return int(bt.value), int(bk.value), bi.value, int(n_ok.value)

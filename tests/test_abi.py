@@ -133,3 +133,33 @@ def test_price_calls_reject_null_profile(lib):
     assert lib.heddle_argmin_plans(1, m, 1, 8, None, None, C.byref(bt), C.byref(bk), None, None) == H.HEDDLE_E_INVAL
     assert lib.heddle_profile_info_get(None, None) == H.HEDDLE_E_INVAL
     lib.heddle_free_profile(None)          # no-op
+
+
+def _spec(d_max=3, types=(0, 1), tps=(0, 1), dps=(1,), ep=0):
+    return H.EnumSpec(d_max, list(types), list(tps), list(dps), ep)
+
+
+def test_enum_count_and_spec_errors(lib):
+    from oracle import enumeration as EN
+    for d, t, k, dp in [(1, (0,), (0,), (1,)), (3, (2, 0, 1), (1, 0), (1, 4)), (8, (0, 1, 2), (0, 1, 2), (1,))]:
+        assert H.heddle_enum_count(_spec(d, t, k, dp)) == EN.space_size(d, len(t), len(k), len(dp))
+    n = C.c_int64(0)
+    bad = [_spec(d_max=0), _spec(d_max=65), _spec(types=()), _spec(types=(1, 1)), _spec(tps=(16,)),
+           _spec(tps=(2, 2)), _spec(dps=(0,)), _spec(dps=(65536,)), _spec(dps=(2, 2)), _spec(ep=16), _spec(ep=-1)]
+    for s in bad:
+        assert lib.heddle_enum_count(C.byref(s.c), C.byref(n)) == H.HEDDLE_E_INVAL
+    huge = _spec(d_max=64, types=range(255), tps=range(16))
+    assert lib.heddle_enum_count(C.byref(huge.c), C.byref(n)) == H.HEDDLE_E_RANGE
+    assert lib.heddle_enum_count(C.byref(_spec().c), None) == H.HEDDLE_E_INVAL
+
+
+def test_enum_templates_range_errors(lib):
+    s = _spec()                          # 4 + 16 + 64 = 84 templates
+    p = C.c_void_p(16)
+    call = lambda first, n, a=p, b=p: lib.heddle_enum_templates(C.byref(s.c), first, n, a, b, None)
+    assert call(-1, 1) == H.HEDDLE_E_INVAL
+    assert call(0, -1) == H.HEDDLE_E_INVAL
+    assert call(80, 5) == H.HEDDLE_E_INVAL
+    assert call(85, 0) == H.HEDDLE_E_INVAL
+    assert call(0, 4, None, p) == H.HEDDLE_E_INVAL
+    assert call(84, 0) == H.HEDDLE_OK           # empty range at the end: nothing enqueued

@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 
 import brute
+from oracle import enumeration as EN
 from oracle import oracle as O
 from workloads.gen import Profile, pack_stage, random_instance
 
@@ -523,3 +524,46 @@ def test_distribute_against_brute_force_and_dp(flags):
                 assert rd["iter"][t, k] >= b
                 n_ok += 1
     assert n_ok > 300
+
+
+# ------------------------------------------------------------- enumeration
+# the planners' search backbone (section 3.1) over a whole space
+
+def test_enumeration_count_pins():
+    # section 2: N = 3 GPU types and K = 3 TP degrees at D = 8 stages give
+    # (N * K)^D structures, more than 43 million
+    depth8 = EN.space_size(8, 3, 3, 1) - EN.space_size(7, 3, 3, 1)
+    assert depth8 == 9 ** 8 == 43_046_721 and depth8 > 43_000_000
+    assert EN.space_size(8, 3, 3, 1) == 48_427_560
+    # brute-force count of the loop nest on small spaces
+    for d, nt, nk, nd in [(1, 1, 1, 1), (3, 2, 2, 1), (4, 3, 1, 2), (2, 1, 4, 3)]:
+        n = sum(1 for _ in EN.all_templates(d, list(range(nt)), list(range(nk)), list(range(1, nd + 1))))
+        assert n == EN.space_size(d, nt, nk, nd)
+
+
+def test_enumeration_order_is_the_loop_nest():
+    """depth, then the type of every stage (stage 0 slowest), then the TP of
+    every stage, then DP; all distinct; DP and EP shared by the stages"""
+    types, tps, dps = [2, 0, 5], [1, 0], [4, 1]
+    seen, prev = set(), None
+    for S, recs in EN.all_templates(3, types, tps, dps, 1):
+        key = (S, tuple(types.index(r & 0xFF) for r in recs), tuple(tps.index((r >> 8) & 15) for r in recs),
+               dps.index(recs[0] >> 16))
+        assert prev is None or key > prev
+        prev = key
+        assert len(recs) == S
+        assert all((r >> 12) & 15 == 1 and r >> 16 == recs[0] >> 16 for r in recs)
+        assert tuple(recs) not in seen
+        seen.add(tuple(recs))
+    assert len(seen) == EN.space_size(3, 3, 2, 2)
+
+
+@pytest.mark.parametrize("spec", [(3, [2, 0, 5], [1, 0], [4, 1], 1), (4, [1], [0, 1, 2], [2], 0),
+                                  (2, [0, 1, 2, 3], [3], [1, 2, 3], 2)])
+def test_enumeration_random_access_matches_loop_nest(spec):
+    d_max, types, tps, dps, ep = spec
+    allt = list(EN.all_templates(d_max, types, tps, dps, ep))
+    for u, t in enumerate(allt):
+        assert EN.template_at(d_max, types, tps, dps, ep, u) == t
+    with pytest.raises(IndexError):
+        EN.template_at(d_max, types, tps, dps, ep, len(allt))

@@ -109,6 +109,10 @@ typedef struct heddle_profile_desc {
     const int32_t *n_gpus;        /* [n_types] GPUs of the type in the cluster             */
     const int64_t *intra_bw_MBps; /* [n_types] intra-node bandwidth, MB/s, >= 1            */
     const int64_t *link_bw_MBps;  /* [n_types][n_types] inter-node bandwidth, MB/s, >= 1   */
+    const int64_t *xlayer_ns;     /* [n_types][n_tp][L] the experts' part of layer_ns of
+                                     each MoE layer (ETP = TP, EP = 1), 0 <= x <= layer_ns;
+                                     entries of dense layers are ignored. Used only by
+                                     heddle_tile_plans; NULL: 0                            */
 } heddle_profile_desc;
 
 typedef struct heddle_profile heddle_profile;   /* opaque, device-resident tables */

@@ -21,6 +21,11 @@
  * micro-batch (plans are ranked by predicted throughput, section 5
  * overview; the fastest candidate is kept, section 5.3).
  *
+ * Expert tiling (oracle_tile_plans): each stage of a priced plan re-chooses
+ * its expert layout EP x ETP x EDP among the factorisations of its GPUs that
+ * fit memory, and the layouts are chosen together for the shortest 1F1B
+ * iteration (section 5.3, expert tiling; see tile_plan).
+ *
  * Second partition mode (OR_F_DISTRIBUTE): Heddle's own layer split of the
  * arithmetic auto-fill (section 5.3, layer split and DP degree): each stage
  * gets layers in proportion to its profiled speed; when that split does not
@@ -80,6 +85,7 @@ typedef struct {
     const int32_t *node_size, *n_gpus; /* [n_types] */
     const int64_t *intra_bw_MBps;  /* [n_types] */
     const int64_t *link_bw_MBps;   /* [n_types][n_types] */
+    const int64_t *xlayer_ns;      /* [n_types][n_tp][L] experts' part of layer_ns, or NULL (0) */
 } oracle_profile;
 
 /* one decoded stage */
@@ -611,6 +617,223 @@ int oracle_price_plans(const oracle_profile *p, int64_t t0, int64_t t1, int s_ma
                 ((int64_t *)bottleneck)[o] = has_split ? pl.bottleneck : INT64_MAX;
             }
             peak_mem[o] = has_split ? pl.peak_mem : INT64_MAX;
+        }
+    }
+    return 0;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Expert tiling (section 5.3, expert tiling paragraph). A stage of TP k   */
+/* and DP D spans W = k * D GPUs, and its expert layout is EP e x ETP t x  */
+/* EDP W / (e t). The layouts priced for a stage: e from the EP list, t    */
+/* from the TP list, t profiled for the stage's GPU type and no larger     */
+/* than its node (ETP carries TP's node bound; EP does not), e t dividing  */
+/* W. For one layout:                                                      */
+/*  - an MoE layer costs its profiled time at TP k with the experts' part  */
+/*    at ETP k replaced by the experts' part at ETP t scaled to the        */
+/*    stage's tokens per GPU (x_t * t / k, rounded up), plus one all-to-all */
+/*    at intra-node bandwidth if the e t GPUs of an EP group fit one node, */
+/*    else at the same-type inter-node link;                               */
+/*  - memory: dense state at TP k, expert state at ETP t divided by e      */
+/*    (rounded up per layer), in-flight activations at TP k;               */
+/*  - synchronisation: dense gradients over the D replicas, expert         */
+/*    gradients at ETP t divided by e over the W / (e t) EDP replicas.     */
+/* With t = k and e the template's EP these are the untiled terms.         */
+/* A stage is tiled on its own (its layout reaches no other stage); the    */
+/* plan's layouts are then chosen together to minimise the whole 1F1B      */
+/* iteration (M-1) max_s t_s + sum_s t_s + max_s g_s over the layouts that */
+/* fit memory (see tile_plan).                                             */
+/* ---------------------------------------------------------------------- */
+typedef struct { int e, ei, t, ti; } otile;
+
+static int64_t xlayer(const oracle_profile *p, int g, int ti, int l)
+{
+    return p->xlayer_ns ? p->xlayer_ns[((int64_t)g * p->n_tp + ti) * p->L + l] : 0;
+}
+
+static int64_t tiled_layer_cost(const oracle_profile *p, const ostage *st, const otile *tl, int l)
+{
+    int64_t c = p->layer_ns[((int64_t)st->g * p->n_tp + st->tpi) * p->L + l];
+    if (p->is_moe[l]) {
+        i128 scaled = ceil_div128((i128)xlayer(p, st->g, tl->ti, l) * tl->t, st->tp);
+        c += (int64_t)scaled - xlayer(p, st->g, st->tpi, l);
+        if (tl->e > 1) {
+            int64_t bw = ((int64_t)tl->e * tl->t <= p->node_size[st->g])
+                             ? p->intra_bw_MBps[st->g] : p->link_bw_MBps[st->g * p->n_types + st->g];
+            c += xfer_ns(p->a2a_bytes, bw);
+        }
+    }
+    return c;
+}
+
+static int64_t tiled_time(const oracle_profile *p, const ostage *st, int s, int S, const otile *tl, int i, int j)
+{
+    int64_t t = p2p_ns(p, st, s, S);
+    for (int l = i; l < j; l++) t += tiled_layer_cost(p, &st[s], tl, l);
+    return t;
+}
+
+static int64_t tiled_mem(const oracle_profile *p, const ostage *st, const otile *tl, int i, int j, int64_t inflight)
+{
+    i128 w = 0, a = 0;
+    for (int l = i; l < j; l++) {
+        w += p->state_bytes[st->tpi * p->L + l] + ceil_div64(p->xstate_bytes[tl->ti * p->L + l], tl->e);
+        a += p->act_bytes[st->tpi * p->L + l];
+    }
+    i128 mem = w + (i128)inflight * a;
+    return mem > INT64_MAX ? INT64_MAX : (int64_t)mem;
+}
+
+static int64_t tiled_sync(const oracle_profile *p, const ostage *st, const otile *tl, int i, int j)
+{
+    int64_t bw = ((int64_t)st->tp * st->dp <= p->node_size[st->g])
+                     ? p->intra_bw_MBps[st->g] : p->link_bw_MBps[st->g * p->n_types + st->g];
+    int64_t gd = 0, gx = 0;
+    for (int l = i; l < j; l++) {
+        gd += p->grad_bytes[st->tpi * p->L + l];
+        gx += ceil_div64(p->xgrad_bytes[tl->ti * p->L + l], tl->e);
+    }
+    int64_t edp = (int64_t)st->tp * st->dp / ((int64_t)tl->e * tl->t);
+    return allreduce_ns(gd, st->dp, bw) + allreduce_ns(gx, edp, bw);
+}
+
+/* the layouts priced for one stage, EP list order, then TP list order */
+static int tiles_of(const oracle_profile *p, const ostage *st, otile *out)
+{
+    int n = 0;
+    for (int ei = 0; ei < p->n_ep; ei++)
+        for (int ti = 0; ti < p->n_tp; ti++) {
+            int e = p->ep_degrees[ei], t = p->tp_degrees[ti];
+            if (!p->profiled[st->g * p->n_tp + ti] || t > p->node_size[st->g]) continue;
+            if (((int64_t)st->tp * st->dp) % ((int64_t)e * t) != 0) continue;
+            out[n].e = e; out[n].ei = ei; out[n].t = t; out[n].ti = ti;
+            n++;
+        }
+    return n;
+}
+
+typedef struct { int64_t T, mem, g; int fits; otile tl; } ocand;
+
+static int cmp_i64(const void *a, const void *b)
+{
+    int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
+    return x < y ? -1 : x > y;
+}
+
+/* the fastest fitting layout of stage s whose synchronisation is <= G:
+ * smallest time, then smallest synchronisation, then the first listed */
+static int pick(const ocand *c, int n, int64_t G)
+{
+    int best = -1;
+    for (int q = 0; q < n; q++) {
+        if (!c[q].fits || c[q].g > G) continue;
+        if (best < 0 || c[q].T < c[best].T || (c[q].T == c[best].T && c[q].g < c[best].g)) best = q;
+    }
+    return best;
+}
+
+/* Tile one plan of split cut[0..S]. With every stage's fastest fitting
+ * layout under a bound G on the synchronisation term, both (M-1) max t and
+ * sum t are as small as G allows, so the smallest iteration time over all
+ * combinations of fitting layouts is the smallest over the thresholds G =
+ * the synchronisation of some fitting layout; ties keep the smallest G.
+ * Returns 0 (and leaves the outputs) if some stage has no fitting layout. */
+static int tile_plan(const oracle_profile *p, const ostage *st, int S, int64_t Mp, const int *cut,
+                     otile *choice, int64_t *iter, int64_t *bn, int64_t *pk)
+{
+    int maxc = p->n_ep * p->n_tp;
+    ocand *c = (ocand *)malloc(sizeof(ocand) * (size_t)S * maxc);
+    otile *tl = (otile *)malloc(sizeof(otile) * (size_t)maxc);
+    int64_t *G = (int64_t *)malloc(sizeof(int64_t) * (size_t)S * maxc);
+    int *nc = (int *)malloc(sizeof(int) * (size_t)S);
+    int nG = 0, found = 0;
+    int64_t best_it = 0, best_G = 0;
+    for (int s = 0; s < S; s++) {
+        nc[s] = tiles_of(p, &st[s], tl);
+        for (int q = 0; q < nc[s]; q++) {
+            ocand *x = &c[s * maxc + q];
+            x->tl = tl[q];
+            x->T = tiled_time(p, st, s, S, &tl[q], cut[s], cut[s + 1]);
+            x->mem = tiled_mem(p, &st[s], &tl[q], cut[s], cut[s + 1], inflight_of(s, S, Mp));
+            x->g = tiled_sync(p, &st[s], &tl[q], cut[s], cut[s + 1]);
+            x->fits = x->mem <= p->mem_cap_bytes[st[s].g];
+            if (x->fits) G[nG++] = x->g;
+        }
+    }
+    qsort(G, nG, sizeof(int64_t), cmp_i64);
+    for (int a = 0; a < nG; a++) {
+        if (a > 0 && G[a] == G[a - 1]) continue;
+        i128 sum_t = 0;
+        int64_t B = 0, max_g = 0;
+        int ok = 1;
+        for (int s = 0; s < S && ok; s++) {
+            int q = pick(&c[s * maxc], nc[s], G[a]);
+            if (q < 0) { ok = 0; break; }
+            const ocand *x = &c[s * maxc + q];
+            sum_t += x->T;
+            if (x->T > B) B = x->T;
+            if (x->g > max_g) max_g = x->g;
+        }
+        if (!ok) continue;
+        int64_t it = (int64_t)((i128)(Mp - 1) * B + sum_t + max_g);
+        if (!found || it < best_it) { found = 1; best_it = it; best_G = G[a]; }
+    }
+    if (found) {
+        int64_t B = 0, peak = 0;
+        for (int s = 0; s < S; s++) {
+            const ocand *x = &c[s * maxc + pick(&c[s * maxc], nc[s], best_G)];
+            choice[s] = x->tl;
+            if (x->T > B) B = x->T;
+            if (x->mem > peak) peak = x->mem;
+        }
+        *iter = best_it;
+        *bn = B;
+        *pk = peak;
+    }
+    free(c); free(tl); free(G); free(nc);
+    return found;
+}
+
+static int log2_of(int v) { int l = 0; while ((1 << l) < v) l++; return l; }
+
+/* Re-tile priced plans in place (the outputs of oracle_price_plans for the
+ * same templates and m list, int64 costs only). A plan with a split (status
+ * OK, or OOM with layer counts) gets the best layouts: status OK, new iter,
+ * bottleneck and peak memory, and tiling[o * s_max + s] = log2 EP | log2 ETP
+ * << 4 per stage; if some stage has no fitting layout it keeps its values
+ * and gets its starting layouts. Plans without a split are left as they are
+ * with zero tiling bytes. Returns -1 for fp32 costs. */
+int oracle_tile_plans(const oracle_profile *p, int64_t n, int s_max, const uint8_t *n_stages,
+                      const uint32_t *stages, const int32_t *m, int n_m, uint32_t flags,
+                      const uint8_t *layers, uint8_t *status, int64_t *iter, int64_t *bottleneck,
+                      int64_t *peak_mem, uint8_t *tiling)
+{
+    ostage st[256];
+    otile choice[256];
+    int cut[257];
+    if (flags & OR_F_FP32) return -1;
+    for (int64_t t = 0; t < n; t++) {
+        int S = n_stages[t];
+        const uint32_t *rec = stages + (size_t)t * s_max;
+        int v = validate(p, S, s_max, rec, st);
+        for (int k = 0; k < n_m; k++) {
+            size_t o = (size_t)t * n_m + k;
+            for (int s = 0; s < s_max; s++) tiling[o * s_max + s] = 0;
+            if (v != OR_OK || (status[o] != OR_OK && status[o] != OR_OOM) || layers[o * s_max] == 0) continue;
+            cut[0] = 0;
+            for (int s = 0; s < S; s++) cut[s + 1] = cut[s] + layers[o * s_max + s];
+            int64_t Mp = ceil_div64(m[k], st[0].dp), it, bn, pk;
+            if (tile_plan(p, st, S, Mp, cut, choice, &it, &bn, &pk)) {
+                status[o] = OR_OK;
+                iter[o] = it;
+                bottleneck[o] = bn;
+                peak_mem[o] = pk;
+                for (int s = 0; s < S; s++)
+                    tiling[o * s_max + s] = (uint8_t)(log2_of(choice[s].e) | log2_of(choice[s].t) << 4);
+            } else {
+                for (int s = 0; s < S; s++)
+                    tiling[o * s_max + s] = (uint8_t)(log2_of(st[s].ep) | log2_of(st[s].tp) << 4);
+            }
         }
     }
     return 0;

@@ -44,6 +44,8 @@ def lib():
         _lib.oracle_best_plan.argtypes = [C.c_int64, C.c_int, P, C.c_uint32, P, P,
                                           C.POINTER(C.c_int64), C.POINTER(C.c_int32)]
         _lib.oracle_best_plan.restype = C.c_int
+        _lib.oracle_tile_plans.argtypes = [P, C.c_int64, C.c_int, P, P, P, C.c_int, C.c_uint32, P, P, P, P, P, P]
+        _lib.oracle_tile_plans.restype = C.c_int
         _lib.oracle_count_relaxations.argtypes = [P, C.c_int, P, C.c_int, C.c_int64, C.c_uint32]
         _lib.oracle_count_relaxations.restype = C.c_int64
         _lib.oracle_xfer_ns.argtypes = [C.c_int64, C.c_int64]
@@ -64,7 +66,7 @@ class _Desc(C.Structure):
                 ("grad_bytes", C.c_void_p), ("xgrad_bytes", C.c_void_p),
                 ("boundary_bytes", C.c_int64), ("a2a_bytes", C.c_int64),
                 ("mem_cap_bytes", C.c_void_p), ("node_size", C.c_void_p), ("n_gpus", C.c_void_p),
-                ("intra_bw_MBps", C.c_void_p), ("link_bw_MBps", C.c_void_p)]
+                ("intra_bw_MBps", C.c_void_p), ("link_bw_MBps", C.c_void_p), ("xlayer_ns", C.c_void_p)]
 
 
 class OracleProfile:
@@ -84,6 +86,8 @@ class OracleProfile:
         }
         if p.layer_ns_f32 is not None:
             self._keep["f32"] = c(p.layer_ns_f32, np.float32)
+        if getattr(p, "xlayer_ns", None) is not None:
+            self._keep["xlayer"] = c(p.xlayer_ns, np.int64)
         k = self._keep
         ptr = lambda a: a.ctypes.data
         self.desc = _Desc(
@@ -94,7 +98,8 @@ class OracleProfile:
             act_bytes=ptr(k["act"]), grad_bytes=ptr(k["grad"]), xgrad_bytes=ptr(k["xgrad"]),
             boundary_bytes=int(p.boundary_bytes), a2a_bytes=int(p.a2a_bytes),
             mem_cap_bytes=ptr(k["cap"]), node_size=ptr(k["node"]), n_gpus=ptr(k["ngpu"]),
-            intra_bw_MBps=ptr(k["intra"]), link_bw_MBps=ptr(k["link"]))
+            intra_bw_MBps=ptr(k["intra"]), link_bw_MBps=ptr(k["link"]),
+            xlayer_ns=ptr(k["xlayer"]) if "xlayer" in k else None)
         self.L = p.L
 
     @property
@@ -122,6 +127,25 @@ def price_plans(oprof, n_stages, stages, m, flags=0, t0=0, t1=None):
                                   d(it), d(bn), d(pk), d(ly), d(stt))
     assert rc == 0
     return {"iter": it, "bottleneck": bn, "peak_mem": pk, "layers": ly, "status": stt}
+
+
+def tile_plans(oprof, n_stages, stages, m, flags, priced):
+    """Re-tile priced plans (a dict from price_plans for the same templates,
+    m and flags; int64 costs): returns a new dict with the re-tiled iter,
+    bottleneck, peak_mem, status, the unchanged layers, and tiling [t, k, s]
+    (log2 EP | log2 ETP << 4)."""
+    m = np.ascontiguousarray(m, dtype=np.int32)
+    n_stages = np.ascontiguousarray(n_stages, dtype=np.uint8)
+    stages = np.ascontiguousarray(stages, dtype=np.uint32)
+    n, s_max = stages.shape
+    out = {k: np.array(v, copy=True) for k, v in priced.items()}
+    out["tiling"] = np.zeros_like(out["layers"])
+    d = lambda a: a.ctypes.data
+    rc = lib().oracle_tile_plans(oprof.ref, n, s_max, d(n_stages), d(stages), d(m), len(m), flags, d(out["layers"]),
+                                 d(out["status"]), d(out["iter"]), d(out["bottleneck"]), d(out["peak_mem"]),
+                                 d(out["tiling"]))
+    assert rc == 0, "tiling is defined for int64 costs"
+    return out
 
 
 def best_plan(m, iter_, status, flags=0):

@@ -39,7 +39,7 @@ class heddle_profile_desc(C.Structure):
                 ("grad_bytes", C.c_void_p), ("xgrad_bytes", C.c_void_p),
                 ("boundary_bytes", C.c_int64), ("a2a_bytes", C.c_int64),
                 ("mem_cap_bytes", C.c_void_p), ("node_size", C.c_void_p), ("n_gpus", C.c_void_p),
-                ("intra_bw_MBps", C.c_void_p), ("link_bw_MBps", C.c_void_p)]
+                ("intra_bw_MBps", C.c_void_p), ("link_bw_MBps", C.c_void_p), ("xlayer_ns", C.c_void_p)]
 
 
 class heddle_enum_spec(C.Structure):
@@ -127,7 +127,8 @@ def heddle_load_profile(p):
             c(p.is_moe, np.uint8), c(p.state_bytes, np.int64), c(p.xstate_bytes, np.int64), c(p.act_bytes, np.int64),
             c(p.grad_bytes, np.int64), c(p.xgrad_bytes, np.int64), c(p.mem_cap_bytes, np.int64),
             c(p.node_size, np.int32), c(p.n_gpus, np.int32), c(p.intra_bw_MBps, np.int64),
-            c(p.link_bw_MBps, np.int64)]
+            c(p.link_bw_MBps, np.int64),
+            None if getattr(p, "xlayer_ns", None) is None else c(p.xlayer_ns, np.int64)]
     a = lambda x: None if x is None else x.ctypes.data
     d = heddle_profile_desc(
         L=int(p.L), n_types=int(np.shape(p.layer_ns)[0]), n_tp=len(p.tp_degrees), n_ep=len(p.ep_degrees),
@@ -135,7 +136,8 @@ def heddle_load_profile(p):
         layer_ns_f32=a(keep[4]), is_moe=a(keep[5]), state_bytes=a(keep[6]), xstate_bytes=a(keep[7]),
         act_bytes=a(keep[8]), grad_bytes=a(keep[9]), xgrad_bytes=a(keep[10]),
         boundary_bytes=int(p.boundary_bytes), a2a_bytes=int(p.a2a_bytes), mem_cap_bytes=a(keep[11]),
-        node_size=a(keep[12]), n_gpus=a(keep[13]), intra_bw_MBps=a(keep[14]), link_bw_MBps=a(keep[15]))
+        node_size=a(keep[12]), n_gpus=a(keep[13]), intra_bw_MBps=a(keep[14]), link_bw_MBps=a(keep[15]),
+        xlayer_ns=a(keep[16]))
     h = C.c_void_p()
     _check(lib().heddle_load_profile(C.byref(d), C.byref(h)))
     return Profile(h.value)

@@ -192,3 +192,69 @@ def best_plan(m, iters, status):
             if best is None or key < best:
                 best, arg = key, (t, k)
     return arg
+
+
+# ------------------------------------------------------------ expert tiling
+
+def stage_layouts(p, x):
+    """(EP, ETP, ETP index) factorisations of a stage's TP * D GPUs: EP from
+    the EP list, ETP a profiled TP degree within the node, EP * ETP | TP * D"""
+    out = []
+    for e in p.ep_degrees:
+        for ti, t in enumerate(p.tp_degrees):
+            e, t = int(e), int(t)
+            if p.profiled[x["g"], ti] and t <= int(p.node_size[x["g"]]) and (x["tp"] * x["dp"]) % (e * t) == 0:
+                out.append((e, t, ti))
+    return out
+
+
+def tiled_stage(p, st, s, i, j, Mp, e, t, ti):
+    """time, memory, synchronisation of stage s on layers [i, j) with experts
+    laid out as EP e x ETP t"""
+    x, S = st[s], len(st)
+    g, k, tp, dp = x["g"], x["k"], x["tp"], x["dp"]
+    node, same = int(p.node_size[g]), int(p.link_bw_MBps[g, g])
+    xl = p.xlayer_ns if p.xlayer_ns is not None else np.zeros_like(p.layer_ns)
+    a2a = 0 if e == 1 else xfer(p.a2a_bytes, int(p.intra_bw_MBps[g]) if e * t <= node else same)
+    p2p = 0 if s == S - 1 else xfer(2 * p.boundary_bytes, int(p.link_bw_MBps[g, st[s + 1]["g"]]))
+    T = p2p
+    for l in range(i, j):
+        T += int(p.layer_ns[g, k, l])
+        if p.is_moe[l]:
+            T += ceil_div(int(xl[g, ti, l]) * t, tp) - int(xl[g, k, l]) + a2a
+    w = sum(int(p.state_bytes[k, l]) + ceil_div(int(p.xstate_bytes[ti, l]), e) for l in range(i, j))
+    mem = w + min(S - s, Mp) * sum(int(p.act_bytes[k, l]) for l in range(i, j))
+    bw = int(p.intra_bw_MBps[g]) if tp * dp <= node else same
+    gs = allreduce(sum(int(p.grad_bytes[k, l]) for l in range(i, j)), dp, bw) + \
+        allreduce(sum(ceil_div(int(p.xgrad_bytes[ti, l]), e) for l in range(i, j)), tp * dp // (e * t), bw)
+    return T, mem, gs
+
+
+def tile_brute(p, S, s_max, recs, m, layers):
+    """Every combination of memory-fitting layouts over the stages of a split:
+    (smallest 1F1B iteration time, {combination: (iter, bottleneck, peak)}
+    of the minimisers), or None if some stage has no fitting layout."""
+    import itertools
+    _, st = status_of(p, S, s_max, recs)
+    cuts = np.concatenate([[0], np.cumsum(layers[:S])]).astype(int)
+    Mp = ceil_div(int(m), st[0]["dp"])
+    opts = []
+    for s in range(S):
+        o = []
+        for e, t, ti in stage_layouts(p, st[s]):
+            T, mem, gs = tiled_stage(p, st, s, cuts[s], cuts[s + 1], Mp, e, t, ti)
+            if mem <= int(p.mem_cap_bytes[st[s]["g"]]):
+                o.append(((e, t), T, mem, gs))
+        if not o:
+            return None
+        opts.append(o)
+    best, arg = None, {}
+    for combo in itertools.product(*opts):
+        B = max(c[1] for c in combo)
+        it = (Mp - 1) * B + sum(c[1] for c in combo) + max(c[3] for c in combo)
+        key = tuple(c[0] for c in combo)
+        if best is None or it < best:
+            best, arg = it, {key: (it, B, max(c[2] for c in combo))}
+        elif it == best:
+            arg[key] = (it, B, max(c[2] for c in combo))
+    return best, arg

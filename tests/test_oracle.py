@@ -28,7 +28,8 @@ def profile_from_json(d, cap=None, node=None):
         xgrad_bytes=a("xgrad_bytes", np.int64), boundary_bytes=d["boundary_bytes"], a2a_bytes=d["a2a_bytes"],
         mem_cap_bytes=np.array(cap if cap else d["mem_cap_bytes"], dtype=np.int64),
         node_size=np.array(node if node else d["node_size"], dtype=np.int32), n_gpus=a("n_gpus", np.int32),
-        intra_bw_MBps=a("intra_bw_MBps", np.int64), link_bw_MBps=a("link_bw_MBps", np.int64)).check()
+        intra_bw_MBps=a("intra_bw_MBps", np.int64), link_bw_MBps=a("link_bw_MBps", np.int64),
+        xlayer_ns=a("xlayer_ns", np.int64) if "xlayer_ns" in d else None).check()
 
 
 def one_template(stages, s_max=None):
@@ -567,3 +568,83 @@ def test_enumeration_random_access_matches_loop_nest(spec):
         assert EN.template_at(d_max, types, tps, dps, ep, u) == t
     with pytest.raises(IndexError):
         EN.template_at(d_max, types, tps, dps, ep, len(allt))
+
+
+# ------------------------------------------------------------ expert tiling
+# section 5.3, expert tiling paragraph
+
+def tile1(prof, stages, m, flags=0):
+    ns, rec = one_template(stages)
+    op = O.OracleProfile(prof)
+    mm = np.array([m], dtype=np.int32)
+    pr = O.price_plans(op, ns, rec, mm, flags)
+    return {k: v[0, 0] for k, v in pr.items()}, {k: v[0, 0] for k, v in O.tile_plans(op, ns, rec, mm, flags, pr).items()}
+
+
+def test_tiling_worked_examples():
+    g = json.load(open(GOLD))
+    for c in g["tiling_cases"]:
+        prof = profile_from_json(g["profile_tiling"], cap=c.get("cap_override"))
+        un, ti = tile1(prof, c["stages"], c["m"], c["flags"])
+        got_un = {k: int(un[k]) for k in ("status", "iter", "bottleneck", "peak_mem")}
+        got_ti = {k: int(ti[k]) for k in ("status", "iter", "bottleneck", "peak_mem")}
+        got_ti["tiling"] = [int(x) for x in ti["tiling"]]
+        assert got_un == c["untiled"], (c["_what"], got_un)
+        assert got_ti == c["tiled"], (c["_what"], got_ti)
+
+
+@pytest.mark.parametrize("flags", [0, 2, 4])
+def test_tiling_matches_brute_force(flags):
+    """the oracle's layouts minimise the 1F1B iteration over every
+    combination of fitting layouts (brute force, pure Python)"""
+    n_tiled = n_kept = 0
+    for seed in range(40):
+        w = random_instance(300 + seed, L=int(np.random.default_rng(seed).integers(3, 9)), moe=True, s_max=4,
+                            n=12)
+        op = O.OracleProfile(w.profile)
+        pr = O.price_plans(op, w.n_stages, w.stages, w.m, flags)
+        ti = O.tile_plans(op, w.n_stages, w.stages, w.m, flags, pr)
+        assert np.array_equal(ti["layers"], pr["layers"])
+        for t in range(w.n):
+            for k in range(len(w.m)):
+                S = int(w.n_stages[t])
+                has_split = pr["status"][t, k] in (0, 8) and pr["layers"][t, k, 0] > 0
+                if not has_split:
+                    assert not ti["tiling"][t, k].any() and ti["status"][t, k] == pr["status"][t, k]
+                    continue
+                bf = brute.tile_brute(w.profile, S, w.s_max, w.stages[t], w.m[k], pr["layers"][t, k])
+                combo = tuple((1 << (int(b) & 15), 1 << (int(b) >> 4)) for b in ti["tiling"][t, k, :S])
+                if bf is None:
+                    n_kept += 1
+                    assert ti["status"][t, k] == pr["status"][t, k] and ti["iter"][t, k] == pr["iter"][t, k]
+                    continue
+                best, arg = bf
+                n_tiled += 1
+                assert ti["status"][t, k] == 0 and ti["iter"][t, k] == best, (seed, t, k)
+                assert combo in arg, (seed, t, k, combo)
+                assert (ti["iter"][t, k], ti["bottleneck"][t, k], ti["peak_mem"][t, k]) == arg[combo]
+                if pr["status"][t, k] == 0:
+                    assert ti["iter"][t, k] <= pr["iter"][t, k]      # the template's own layouts are candidates
+    assert n_tiled > 50
+
+
+def test_tiling_single_layout_is_identity():
+    """one TP degree and EP = 1 only: the template's layout is the only one,
+    so tiling changes nothing"""
+    for seed in range(20):
+        w = random_instance(400 + seed, moe=False)
+        p = copy.deepcopy(w.profile)
+        p.tp_degrees = p.tp_degrees[:1]
+        for f in ("layer_ns", "profiled"):
+            setattr(p, f, np.ascontiguousarray(getattr(p, f)[:, :1]))
+        for f in ("state_bytes", "xstate_bytes", "act_bytes", "grad_bytes", "xgrad_bytes"):
+            setattr(p, f, np.ascontiguousarray(getattr(p, f)[:1]))
+        p.check()
+        op = O.OracleProfile(p)
+        for flags in (0, 2):
+            pr = O.price_plans(op, w.n_stages, w.stages, w.m, flags)
+            ti = O.tile_plans(op, w.n_stages, w.stages, w.m, flags, pr)
+            for key in ("status", "iter", "bottleneck", "peak_mem", "layers"):
+                assert np.array_equal(ti[key], pr[key]), key
+            has = (ti["layers"][:, :, 0] > 0)
+            assert np.all(ti["tiling"][has][:, 0] == 0)           # log2 EP 0, log2 ETP 0 on stage 0

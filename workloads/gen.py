@@ -77,6 +77,7 @@ class Profile:
     intra_bw_MBps: np.ndarray
     link_bw_MBps: np.ndarray
     layer_ns_f32: np.ndarray | None = None
+    xlayer_ns: np.ndarray | None = None      # [N][K][L] expert part of each MoE layer's time at ETP = TP
 
     @property
     def n_types(self):
@@ -97,6 +98,8 @@ class Profile:
             assert a.dtype == np.int32
         if self.layer_ns_f32 is not None:
             assert self.layer_ns_f32.shape == self.layer_ns.shape and self.layer_ns_f32.dtype == np.float32
+        if self.xlayer_ns is not None:
+            assert self.xlayer_ns.shape == self.layer_ns.shape and self.xlayer_ns.dtype == np.int64
         return self
 
 
@@ -164,6 +167,13 @@ def make_profile(cfg, rng):
         dense_params[is_moe == 1] = moe["attention_params"]
         expert_params[is_moe == 1] = moe["n_experts"] * moe["expert_params"]
         a2a_bytes = int(moe["a2a_bytes"])
+    # expert part of an MoE layer's time: the routed experts' share of the
+    # layer's active parameters (top-k experts per token), at every TP degree
+    xlayer_ns = None
+    if moe:
+        active = moe["top_k"] * moe["expert_params"]
+        share = active / (moe["attention_params"] + active)
+        xlayer_ns = np.ascontiguousarray(_round_half_even(layer_ns * share) * is_moe[None, None, :], dtype=np.int64)
     sbp, gbp = cfg["state_bytes_per_param"], cfg["grad_bytes_per_param"]
     kk = tp.astype(np.int64)[:, None]
     state = _ceil_div(sbp * dense_params[None, :], kk)
@@ -178,7 +188,7 @@ def make_profile(cfg, rng):
         xgrad_bytes=xgrad, boundary_bytes=int(cfg["boundary_bytes"]), a2a_bytes=a2a_bytes,
         mem_cap_bytes=np.array([t["mem_GiB"] * 2**30 for t in types], dtype=np.int64),
         node_size=node, n_gpus=np.array([t["n_gpus"] for t in types], dtype=np.int32),
-        intra_bw_MBps=intra_MBps, link_bw_MBps=np.ascontiguousarray(link_MBps)).check()
+        intra_bw_MBps=intra_MBps, link_bw_MBps=np.ascontiguousarray(link_MBps), xlayer_ns=xlayer_ns).check()
 
 
 def _draw_templates(rng, n, s_max, N, tp_sets, dp_choices, ep_degrees):
@@ -295,6 +305,8 @@ def random_instance(seed, L=None, n_types=None, s_max=6, n=40, max_cost=6, moe=N
         mem_cap_bytes=cap, node_size=node, n_gpus=rng.integers(4, 64, size=N).astype(np.int32),
         intra_bw_MBps=rng.integers(500, 4000, size=N).astype(np.int64),
         link_bw_MBps=rng.integers(100, 2000, size=(N, N)).astype(np.int64)).check()
+    if moe:                                   # no draw: half of each MoE layer's time is its experts'
+        prof.xlayer_ns = np.ascontiguousarray(layer_ns * is_moe[None, None, :] // 2, dtype=np.int64)
     S = rng.integers(1, min(s_max, max(L, 1)) + 1, size=n)
     g = rng.integers(0, N, size=(n, s_max))
     tpl = rng.integers(0, K, size=(n, s_max))

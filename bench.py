@@ -92,6 +92,8 @@ def main():
     ap.add_argument("--compute-only", action="store_true", help="split ignores memory; fit checked after")
     ap.add_argument("--distribute", action="store_true",
                     help="Heddle's speed-proportional split with its fallback list instead of the min-max split")
+    ap.add_argument("--tiling", action="store_true",
+                    help="re-tile every priced plan's expert layouts (heddle_tile_plans) inside the step")
     ap.add_argument("--enumerate", action="store_true",
                     help="price the whole space of the search backbone (every stage count up to --enum-depth, "
                          "every type and TP per stage) on the config's profile instead of its template batch")
@@ -153,12 +155,16 @@ def main():
         H.heddle_price_plans(prof, ns, st, m, flags, out)
         if ev:
             ev[1].record(stream)
+        if args.tiling:
+            H.heddle_tile_plans(prof, ns, st, m, flags, out)
+            if ev:
+                ev[2].record(stream)
         return H.heddle_argmin_plans(m, flags, out["iter"], out["status"])
 
     for i in range(args.warmup):
         step()
         log(f"warmup {i + 1}/{args.warmup} done")
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     best = None
@@ -166,7 +172,8 @@ def main():
         best = step(evs[i])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    kern_ms = [a.elapsed_time(b) for a, b in evs]
+    kern_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    tile_ms = [e[1].elapsed_time(e[2]) for e in evs] if args.tiling else None
     log(f"timed {args.steps} steps in {elapsed:.3f}s; price kernel {np.mean(kern_ms):.3f} ms avg "
         f"(min {np.min(kern_ms):.3f}); best plan {best}")
     status_np = out["status"].cpu().numpy()
@@ -225,11 +232,15 @@ def main():
         "data": "synthetic",
         "config": {"workload": WORKLOAD_TEXT[args.config], "name": args.config, "templates": w.n, "m": m,
                    "plans": n_plans, "memory_aware": not args.compute_only, "seed": w.meta["seed"],
-                   "partition": "distribute" if args.distribute else "min-max"},
+                   "partition": ("distribute" if args.distribute else "min-max") +
+                                (" + expert tiling" if args.tiling else "")},
         "roofline": dict({"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
                           "unit": "Tlane-op/s", "frac": achieved / PEAK_LANE_OPS, "traffic": traffic,
                           "kernel_ms": float(np.mean(kern_ms))}, **roof),
         "statuses": statuses,
+        "tiling": None if not args.tiling else {
+            "tile_kernel_ms": float(np.mean(tile_ms)),
+            "note": "heddle_tile_plans re-tiles every plan's expert layouts after pricing, inside the timed step"},
         "best_plan": {"template": best[0], "m_index": best[1], "iter": best[2]} if best else None,
         "profile_load_ms": load_ms,
     }

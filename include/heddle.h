@@ -247,6 +247,45 @@ int heddle_count_work(const heddle_profile *p, int64_t n, int32_t s_max,
                       int64_t *h_relaxations, hipStream_t stream);
 
 /*
+ * heddle_tile_plans -- expert tiling (section 5.3, expert tiling paragraph)
+ * of priced plans, in place. A stage of TP k and DP D spans W = k * D GPUs;
+ * its expert layout is EP e x ETP t x EDP W / (e t), with e from ep_degrees,
+ * t a profiled TP degree of the stage's type no larger than its node, and
+ * e * t dividing W. Under a layout an MoE layer costs
+ * layer_ns_k - xlayer_ns_k + ceil(xlayer_ns_t * t / k) plus one all-to-all
+ * (intra-node bandwidth if e * t fits the node, else the same-type link);
+ * the stage holds dense state at TP k, expert state at ETP t divided by e
+ * (per layer, rounded up) and its in-flight activations; its
+ * synchronisation all-reduces dense gradients over D and expert gradients
+ * (ETP t, divided by e) over W / (e t) replicas. The template's own layout
+ * (e from its record, t = k) is one of them. The layouts of a plan are
+ * chosen together for the smallest 1F1B iteration time among the layouts
+ * that fit memory; ties: the smaller largest synchronisation term, then per
+ * stage the faster layout, the smaller synchronisation, the first in
+ * (ep_degrees, tp_degrees) order.
+ * Inputs are the outputs of heddle_price_plans for the same templates, m and
+ * flags (any split mode); int64 costs only (HEDDLE_F_FP32 is rejected).
+ * A plan has a split when its status is OK or OOM and it has layer counts.
+ * Such a plan gets status OK, its new iter, bottleneck and peak_mem, and
+ * d_tiling[(t * n_m + k) * s_max + s] = log2 EP | log2 ETP << 4 per stage;
+ * if some stage has no layout that fits, the plan keeps its values and gets
+ * its template's layouts. Plans without a split are left as they are and
+ * get zero tiling bytes (0 beyond S too). Asynchronous on `stream`.
+ *   d_iter, d_bottleneck, d_peak_mem, d_status  DEVICE, read and rewritten.
+ *   d_layers  DEVICE [n][n_m][s_max], read.
+ *   d_tiling  DEVICE [n][n_m][s_max] uint8, written.
+ * Returns HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_RANGE (the tiled iteration time
+ * could exceed 2^62, or the layout table of s_max x n_tp x n_ep does not fit
+ * the device's LDS) or HEDDLE_E_DEVICE.
+ */
+int heddle_tile_plans(const heddle_profile *p, int64_t n, int32_t s_max,
+                      const uint8_t *d_n_stages, const uint32_t *d_stages,
+                      const int32_t *h_m, int32_t n_m, uint32_t flags,
+                      void *d_iter, void *d_bottleneck, int64_t *d_peak_mem,
+                      const uint8_t *d_layers, uint8_t *d_status, uint8_t *d_tiling,
+                      hipStream_t stream);
+
+/*
  * Exhaustive enumeration of structures: the search backbone of the planners
  * Heddle analyses (section 3.1), with (N * K)^D structures for N GPU types,
  * K TP degrees and D stages (section 2), run as one data-parallel workload.

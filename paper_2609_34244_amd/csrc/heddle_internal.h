@@ -28,6 +28,7 @@ struct DevProfile {
     int32_t fx_exp;                  // fixed-point unit of the fp32 variant is 2^fx_exp
     uint32_t tp_present, ep_present; // bit l set: 2^l is a profiled TP / an allowed EP degree
     uint64_t tp_index, ep_index;     // nibble l: index of 2^l in tp_degrees / ep_degrees
+    uint64_t tp_log2, ep_log2;       // nibble k: log2 of tp_degrees[k] / ep_degrees[k]
     const int64_t *pre_time;         // [n_types][n_tp][L+1] prefix of layer_ns
     const int64_t *pre_time_fx;      // [n_types][n_tp][L+1] prefix of fp32 costs in 2^fx_exp units
     const int32_t *pre_moe;          // [L+1] prefix count of MoE layers
@@ -46,6 +47,12 @@ struct DevProfile {
     const int64_t *intra_bw;         // [n_types] MB/s
     const int64_t *link_bw;          // [n_types][n_types] MB/s
     const int32_t *ep_degrees;       // [n_ep]
+    // expert tiling: dense state prefix per TP, expert state prefix per
+    // (ETP, EP) with a per-layer ceiling, and per (type, TP, ETP) the prefix
+    // of the change of MoE layer time when the experts run at ETP instead of TP
+    const int64_t *pre_dstate;       // [n_tp][L+1]
+    const int64_t *pre_xstate;       // [n_tp][n_ep][L+1]
+    const int64_t *xdelta;           // [n_types][n_tp][n_tp][L+1]
     // [n_types][n_tp][n_ep][n_f][2][lim_stride]: per row, the largest end that
     // fits from row i, then its inverse (smallest row whose limit reaches x)
     const uint8_t *mem_lim;
@@ -69,6 +76,8 @@ struct heddle_profile {
     int64_t max_stage_fx;            // bound on any fp32 stage time, fixed-point units
     int64_t max_ar_ns;               // bound on any stage's gradient synchronisation time
     int64_t max_ar_fx;               // the same, fp32-rounded, fixed-point units
+    int64_t max_tiled_ns;            // bound on any stage time under any expert layout
+    int64_t max_ar_tiled_ns;         // bound on any stage's synchronisation under any expert layout
 };
 
 namespace heddle {
@@ -106,6 +115,7 @@ int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const
 int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool count_only);
 int launch_evaluate(const heddle_profile *p, const PriceArgs &a, hipStream_t stream);
 int launch_distribute(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool count_only);
+int launch_tile(const heddle_profile *p, const PriceArgs &a, uint8_t *tiling, hipStream_t stream);
 int launch_argmin(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t flags, const void *d_iter,
                   const uint8_t *d_status, int64_t *h_best_template, int32_t *h_best_m_index,
                   void *h_best_iter, hipStream_t stream);

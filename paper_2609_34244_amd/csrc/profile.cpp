@@ -7,6 +7,7 @@
 // TP degree likewise. Transfer times of the MoE all-to-all (section 5.3,
 // expert tiling) and the inter-stage p2p are precomputed per type and per
 // type pair.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <vector>
@@ -95,12 +96,14 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
         if (l < 0 || l > 15 || ((dp.tp_present >> l) & 1)) return fail(HEDDLE_E_INVAL, "tp_degrees must be distinct powers of two <= 32768");
         dp.tp_present |= 1u << l;
         dp.tp_index |= (uint64_t)k << (4 * l);
+        dp.tp_log2 |= (uint64_t)l << (4 * k);
     }
     for (int e = 0; e < E; e++) {
         int l = log2_exact(d->ep_degrees[e]);
         if (l < 0 || l > 15 || ((dp.ep_present >> l) & 1)) return fail(HEDDLE_E_INVAL, "ep_degrees must be distinct powers of two <= 32768");
         dp.ep_present |= 1u << l;
         dp.ep_index |= (uint64_t)e << (4 * l);
+        dp.ep_log2 |= (uint64_t)l << (4 * e);
     }
     for (int g = 0; g < N; g++) {
         if (d->node_size[g] < 1) return fail(HEDDLE_E_INVAL, "node_size must be >= 1");
@@ -232,6 +235,63 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
     i128 max_ar = (2 * max_grad * 1000) / min_bw + 2;
     if (max_ar >= kLimit62) return fail(HEDDLE_E_RANGE, "gradient synchronisation time could exceed 2^62 ns");
 
+    // ---- expert tiling (section 5.3): the experts' part x of an MoE layer's
+    // time at ETP t, scaled to a stage of TP k, is ceil(x_t * t / k); the
+    // layer's time there is layer_ns_k - x_k + ceil(x_t * t / k), never
+    // negative since x_k <= layer_ns_k. Memory splits into dense state at TP k
+    // and expert state at ETP t / EP e.
+    std::vector<int64_t> pre_dstate((size_t)K * R), pre_xstate((size_t)K * E * R),
+        xdelta((size_t)N * K * K * R, 0);
+    for (int k = 0; k < K; k++) {
+        i128 w = 0;
+        pre_dstate[k * R] = 0;
+        for (int l = 0; l < L; l++) {
+            w += d->state_bytes[(size_t)k * L + l];
+            pre_dstate[k * R + l + 1] = (int64_t)w;
+        }
+        for (int e = 0; e < E; e++) {
+            const int64_t ep = d->ep_degrees[e];
+            i128 x = 0;
+            pre_xstate[(k * E + e) * R] = 0;
+            for (int l = 0; l < L; l++) {
+                x += (d->xstate_bytes[(size_t)k * L + l] + ep - 1) / ep;
+                pre_xstate[(k * E + e) * R + l + 1] = (int64_t)x;
+            }
+        }
+    }
+    i128 max_tiled = 0;
+    for (int g = 0; g < N; g++)
+        for (int k = 0; k < K; k++) {
+            int64_t a2a_max = std::max(a2a_ns[g * 3 + 1], a2a_ns[g * 3 + 2]), p2p_max = 0;
+            for (int h = 0; h < N; h++) p2p_max = std::max(p2p_max, p2p_ns[g * N + h]);
+            for (int t = 0; t < K; t++) {
+                i128 acc = 0;
+                int64_t *row = &xdelta[(((size_t)g * K + k) * K + t) * R];
+                for (int l = 0; l < L; l++) {
+                    if (d->is_moe[l] && d->xlayer_ns) {
+                        const int64_t xk = d->xlayer_ns[((size_t)g * K + k) * L + l];
+                        const int64_t xt = d->xlayer_ns[((size_t)g * K + t) * L + l];
+                        if (xk < 0 || xt < 0 || xk > d->layer_ns[((size_t)g * K + k) * L + l])
+                            return fail(HEDDLE_E_INVAL, "xlayer_ns entries must lie in 0 .. layer_ns");
+                        const i128 num = (i128)xt * d->tp_degrees[t], den = d->tp_degrees[k];
+                        acc += (num + den - 1) / den - xk;
+                        if (acc >= kLimit62 || acc <= -kLimit62) return fail(HEDDLE_E_RANGE, "tiled layer times exceed 2^62");
+                    }
+                    row[l + 1] = (int64_t)acc;
+                }
+                i128 b = (i128)pre_time[((size_t)g * K + k) * R + L] + acc + (i128)n_moe * a2a_max + p2p_max;
+                if (b > max_tiled) max_tiled = b;
+            }
+        }
+    if (max_tiled >= kLimit62) return fail(HEDDLE_E_RANGE, "tiled stage times could exceed 2^62 ns");
+    i128 max_xg = 0;
+    for (int k = 0; k < K; k++)
+        for (int e = 0; e < E; e++) max_xg = std::max(max_xg, (i128)pre_xgrad[(k * E + e) * R + L]);
+    i128 max_dg = 0;
+    for (int k = 0; k < K; k++) max_dg = std::max(max_dg, (i128)pre_grad[k * R + L]);
+    const i128 max_ar_tiled = (2 * (max_dg + max_xg) * 1000) / min_bw + 2;
+    if (max_ar_tiled >= kLimit62) return fail(HEDDLE_E_RANGE, "gradient synchronisation time could exceed 2^62 ns");
+
     // ---- fp32 variant: exact fixed-point image of the fp32 costs
     std::vector<float> cost32((size_t)N * K * L);
     for (size_t i = 0; i < cost32.size(); i++) {
@@ -312,7 +372,8 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
            o_cap = B.add(d->mem_cap_bytes, (size_t)N * 8), o_node = B.add(d->node_size, (size_t)N * 4),
            o_ngpu = B.add(d->n_gpus, (size_t)N * 4), o_intra = B.add(d->intra_bw_MBps, (size_t)N * 8),
            o_link = B.add(d->link_bw_MBps, (size_t)N * N * 8), o_epd = B.add(d->ep_degrees, (size_t)E * 4),
-           o_lim = B.add(lim_tab);
+           o_lim = B.add(lim_tab), o_dstate = B.add(pre_dstate), o_xstate = B.add(pre_xstate),
+           o_xdelta = B.add(xdelta);
 
     heddle_profile *p = new (std::nothrow) heddle_profile;
     if (!p) return fail(HEDDLE_E_NOMEM, "host allocation failed");
@@ -343,6 +404,9 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
     dp.link_bw = (const int64_t *)(base + o_link);
     dp.ep_degrees = (const int32_t *)(base + o_epd);
     dp.mem_lim = (const uint8_t *)(base + o_lim);
+    dp.pre_dstate = (const int64_t *)(base + o_dstate);
+    dp.pre_xstate = (const int64_t *)(base + o_xstate);
+    dp.xdelta = (const int64_t *)(base + o_xdelta);
     dp.rows64[0] = (const uint64_t *)(base + o_r64a);
     dp.rows64[1] = (const uint64_t *)(base + o_r64b);
     dp.rows32[0] = (const uint32_t *)(base + o_r32a);
@@ -352,6 +416,8 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
     p->dev = dp;
     p->max_stage_ns = (int64_t)max_stage;
     p->max_ar_ns = (int64_t)max_ar;
+    p->max_tiled_ns = (int64_t)max_tiled;
+    p->max_ar_tiled_ns = (int64_t)max_ar_tiled;
     p->narrow_i64 = narrow_i64;
     p->max_stage_fx = fx_ok ? (int64_t)max_stage_fx : -1;
     // fp32-rounded all-reduce terms are within a factor (1 + 2^-24) of the int64 ones

@@ -1,0 +1,308 @@
+// Expert tiling on gfx950 (Heddle, arXiv 2609.34244, section 5.3, expert
+// tiling paragraph), as a pass over priced plans.
+//
+// A stage of TP k and DP D spans W = k * D GPUs; its expert layout is EP e x
+// ETP t x EDP W / (e t). The layouts priced for a stage: e from the EP list,
+// t a profiled TP degree of the stage's GPU type no larger than its node (ETP
+// carries TP's node bound, EP does not), e t dividing W. Under a layout an
+// MoE layer costs its profiled time at TP k with the experts' part at ETP k
+// replaced by the experts' part at ETP t scaled to the stage's tokens per GPU
+// (ceil(x_t * t / k); a per-(type, TP, ETP) prefix table), plus one
+// all-to-all at intra-node bandwidth if the e t GPUs of an EP group fit one
+// node, else at the same-type inter-node link; memory holds the dense state
+// at TP k, the expert state at ETP t divided by e and the in-flight
+// activations; synchronisation all-reduces the dense gradients over D
+// replicas and the expert gradients (ETP t, divided by e) over the EDP
+// replicas. A stage's layout reaches no other stage, and with every stage at
+// its fastest fitting layout under a bound G on the synchronisation term both
+// (M-1) max t and sum t are as small as G allows, so the best layouts for the
+// whole 1F1B iteration are found by trying every synchronisation value of a
+// fitting layout as G: the smallest iteration time wins, then the smallest G;
+// per stage the fastest layout wins, then the smaller synchronisation, then
+// the first in (EP list, TP list) order.
+//
+// Mapping: one wavefront per plan (grid-stride). Lanes are (stage, layout)
+// slots while the layouts are priced (time, synchronisation and memory into
+// LDS; time all ones when the layout is not allowed or does not fit); then
+// lanes are stages, each keeping in place the layouts that no other layout of
+// its stage beats in both time and synchronisation (only those can be chosen,
+// and only their synchronisation values need to be tried as bounds); then
+// lanes are the kept layouts as thresholds G, each pricing the plan under its
+// G from the kept table (broadcast reads); a wavefront minimum of (iteration
+// time, G) decides, and lanes as stages write the layouts back.
+#include <cstring>
+
+#include "exact_math.h"
+#include "heddle_internal.h"
+#include "device_common.h"
+
+namespace heddle {
+
+constexpr uint64_t kNoLayout = ~0ull;
+
+__device__ __forceinline__ void wave_min_pair(uint64_t &a, uint64_t &b)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint64_t x = __shfl_xor((unsigned long long)a, o), y = __shfl_xor((unsigned long long)b, o);
+        const bool take = x < a || (x == a && y < b);
+        a = take ? x : a;
+        b = take ? y : b;
+    }
+}
+
+__global__ void __launch_bounds__(64) tile_kernel(DevProfile P, PriceArgs A, uint8_t *tiling)
+{
+    extern __shared__ __align__(16) unsigned char smem[];      // one wavefront per workgroup
+    const int lane = threadIdx.x;
+    const int L = P.L, R = L + 1, N = P.n_types, K = P.n_tp, E = P.n_ep, F = K * E;
+    uint64_t *cT = (uint64_t *)smem;                           // [s_cap][F] time (kNoLayout: none)
+    uint64_t *cG = cT + (size_t)A.s_cap * F;                   // [s_cap][F] synchronisation
+    int64_t *cM = (int64_t *)(cG + (size_t)A.s_cap * F);       // [s_cap][F] memory
+    uint8_t *cC = (uint8_t *)(cM + (size_t)A.s_cap * F);       // [s_cap][F] layout index of a kept entry
+    uint8_t *cN = cC + (size_t)A.s_cap * F;                    // [s_cap] kept layouts of a stage
+    const int64_t total = A.n * A.n_m;
+
+    for (int64_t o = blockIdx.x; o < total; o += gridDim.x) {
+        const int64_t t = o / A.n_m;
+        const int k = (int)(o - t * A.n_m);
+        const int st_in = A.status[o];
+        const bool has_split = (st_in == HEDDLE_S_OK || st_in == HEDDLE_S_OOM) && A.layers[o * A.s_max] > 0;
+        if (!has_split) {                                      // no split: nothing to tile
+            if (lane < A.s_max) tiling[o * A.s_max + lane] = 0;
+            continue;
+        }
+        // a split implies a valid template; buffers that do not describe one
+        // (inconsistent with the templates) are left alone rather than read out
+        // of range
+        const int S = A.n_stages[t];
+        const bool act = lane < S && lane < A.s_cap;
+        const uint32_t rec = act ? A.stages[t * A.s_max + lane] : 0u;
+        const int nl = act ? A.layers[o * A.s_max + lane] : 0;
+        int i0 = nl;                                           // inclusive scan, then exclusive
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int u = __shfl_up(i0, d);
+            i0 += lane >= d ? u : 0;
+        }
+        const int total_layers = __shfl(i0, 63);
+        i0 -= nl;
+        const int j0 = i0 + nl;
+        const int g = rec & 0xFF, l2tp = (rec >> 8) & 15, l2ep = (rec >> 12) & 15;
+        const int ki = nibble(P.tp_index, l2tp);
+        const int tp = 1 << l2tp;
+        const int D = (int)(__builtin_amdgcn_readfirstlane(rec) >> 16);
+        const bool bad = S < 1 || S > A.s_cap || total_layers != L || D < 1 ||
+                         __ballot(act && (g >= N || nl < 1 || !((P.tp_present >> l2tp) & 1))) != 0;
+        if (bad) {
+            if (lane < A.s_max) tiling[o * A.s_max + lane] = 0;
+            continue;
+        }
+        const int32_t m = A.m[k];
+        const int64_t Mp = (int64_t)(((uint32_t)m + (uint32_t)D - 1) / (uint32_t)D);
+        const int64_t inflight = (int64_t)(S - lane) < Mp ? (int64_t)(S - lane) : Mp;
+        const int g_next = __builtin_amdgcn_update_dpp(g, g, kDppWaveShl1, 0xF, 0xF, false);
+        const int64_t p2p = lane + 1 < S ? P.p2p_ns[g * N + g_next] : 0;
+        const int node = P.node_size[g];
+        const int64_t cap = P.mem_cap[g];
+        const int64_t W = (int64_t)tp * D;
+        const int64_t bw = W <= node ? P.intra_bw[g] : P.link_bw[g * N + g];
+        const uint64_t *base = P.rows64[0] + ((size_t)(g * K + ki) * 3 + kA2ANone) * R;
+        const uint64_t T0 = base[j0] - base[i0] + (uint64_t)p2p;
+        const int64_t n_moe = P.pre_moe[j0] - P.pre_moe[i0];
+        const int64_t dstate = P.pre_dstate[ki * R + j0] - P.pre_dstate[ki * R + i0];
+        const int64_t act_b = P.pre_act[ki * R + j0] - P.pre_act[ki * R + i0];
+        const int64_t gd = P.pre_grad[ki * R + j0] - P.pre_grad[ki * R + i0];
+        const int64_t g_dense = allreduce_ns(gd, D, bw);
+
+        // ---- lanes = (stage, layout) slots q = s * F + c: price every layout
+        wave_sync();                                           // the previous plan's table reads are done
+        const int n_cand = S * F;
+        for (int q0 = 0; q0 < n_cand; q0 += 64) {
+            const int q = q0 + lane;
+            const int s = q < n_cand ? q / F : 0, c = q - s * F;
+            // the stage's constants, from its lane
+            const int sg = __shfl(g, s), ski = __shfl(ki, s), snode = __shfl(node, s);
+            const int si0 = __shfl(i0, s), sj0 = __shfl(j0, s);
+            auto sh64 = [&](int64_t v) { return (int64_t)__shfl((long long)v, s); };
+            const int64_t sW = sh64(W), scap = sh64(cap), sbw = sh64(bw);
+            const uint64_t sT0 = (uint64_t)sh64((int64_t)T0);
+            const int64_t smoe = sh64(n_moe), sdst = sh64(dstate), sact = sh64(act_b);
+            const int64_t sinf = sh64(inflight), sgd = sh64(g_dense);
+            if (q < n_cand) {
+                const int ei = c / K, ti = c - ei * K;
+                const int e = 1 << nibble(P.ep_log2, ei), et = 1 << nibble(P.tp_log2, ti);
+                const int64_t group = (int64_t)e * et;
+                const bool allowed = P.profiled[sg * K + ti] && et <= snode && (sW % group) == 0;
+                const int64_t *xd = P.xdelta + ((size_t)(sg * K + ski) * K + ti) * R;
+                const uint64_t T = sT0 + (uint64_t)(xd[sj0] - xd[si0]) +
+                                   (uint64_t)(smoe * P.a2a_ns[sg * 3 + a2a_variant(e, et, snode)]);
+                const int64_t *xs = P.pre_xstate + (size_t)(ti * E + ei) * R;
+                const int64_t mem = sdst + (xs[sj0] - xs[si0]) + sinf * sact;
+                const int64_t *xg = P.pre_xgrad + (size_t)(ti * E + ei) * R;
+                const int64_t edp = allowed ? sW / group : 1;
+                const int64_t gs = sgd + allreduce_ns(xg[sj0] - xg[si0], edp, sbw);
+                cT[q] = allowed && mem <= scap ? T : kNoLayout;
+                cG[q] = (uint64_t)gs;
+                cM[q] = mem;
+            }
+        }
+        wave_sync();
+
+        // ---- lanes = stages: keep the layouts no other beats in both time and
+        // synchronisation (the first listed among equals), in place at the front
+        // of the stage's row; only these can be a stage's fastest layout under a
+        // bound on the synchronisation, and only their synchronisation values
+        // need to be tried as bounds
+        if (act) {
+            const int rb = lane * F;
+            int nf = 0;
+            for (int c = 0; c < F; c++) {
+                const uint64_t x = cT[rb + c], y = cG[rb + c];
+                const int64_t mx = cM[rb + c];
+                if (x == kNoLayout) continue;
+                bool beaten = false;
+                for (int j = 0; j < nf; j++) beaten |= cT[rb + j] <= x && cG[rb + j] <= y;
+                if (beaten) continue;
+                int w = 0;
+                for (int j = 0; j < nf; j++) {
+                    const uint64_t tj = cT[rb + j], gj = cG[rb + j];
+                    const bool drop = x <= tj && y <= gj && (x < tj || y < gj);
+                    if (!drop) {
+                        cT[rb + w] = tj;
+                        cG[rb + w] = gj;
+                        cM[rb + w] = cM[rb + j];
+                        cC[rb + w] = cC[rb + j];
+                        w++;
+                    }
+                }
+                cT[rb + w] = x;
+                cG[rb + w] = y;
+                cM[rb + w] = mx;
+                cC[rb + w] = (uint8_t)c;
+                nf = w + 1;
+            }
+            cN[lane] = (uint8_t)nf;
+        }
+        wave_sync();
+
+        // ---- lanes = frontier layouts as thresholds G: the plan's iteration time
+        // with every stage at its fastest kept layout of synchronisation <= G
+        uint64_t best_it = kNoLayout, best_G = kNoLayout;
+        for (int q0 = 0; q0 < n_cand; q0 += 64) {
+            const int q = q0 + lane;
+            const int s = q < n_cand ? q / F : 0, j = q - s * F;
+            uint64_t it = kNoLayout, G = kNoLayout;
+            if (q < n_cand && j < cN[s]) {
+                G = cG[q];
+                uint64_t maxT = 0, sumT = 0, maxg = 0;
+                bool ok = true;
+                for (int s2 = 0; s2 < S && ok; s2++) {
+                    uint64_t bT = kNoLayout, bG = 0;
+                    const int n2 = cN[s2];
+                    for (int j2 = 0; j2 < n2; j2++) {
+                        const uint64_t x = cT[s2 * F + j2], y = cG[s2 * F + j2];
+                        const bool take = y <= G && x < bT;        // kept layouts have distinct times
+                        bT = take ? x : bT;
+                        bG = take ? y : bG;
+                    }
+                    ok = bT != kNoLayout;
+                    maxT = bT > maxT ? bT : maxT;
+                    sumT += bT;
+                    maxg = bG > maxg ? bG : maxg;
+                }
+                if (ok) it = (uint64_t)(Mp - 1) * maxT + sumT + maxg;
+            }
+            wave_min_pair(it, G);
+            if (it < best_it || (it == best_it && G < best_G)) {
+                best_it = it;
+                best_G = G;
+            }
+        }
+
+        // ---- lanes = stages: write the chosen layouts
+        if (best_it == kNoLayout) {                            // some stage has no fitting layout: unchanged
+            if (lane < A.s_max) tiling[o * A.s_max + lane] = act ? (uint8_t)(l2ep | l2tp << 4) : 0;
+            continue;
+        }
+        uint64_t bT = 0;
+        int64_t bM = 0;
+        int bc = 0;
+        if (act) {
+            bT = kNoLayout;
+            const int rb = lane * F, nf = cN[lane];
+            for (int j = 0; j < nf; j++) {
+                const uint64_t x = cT[rb + j], y = cG[rb + j];
+                const bool take = y <= best_G && x < bT;
+                bT = take ? x : bT;
+                bM = take ? cM[rb + j] : bM;
+                bc = take ? cC[rb + j] : bc;
+            }
+        }
+        const uint64_t B = wave_max(bT);
+        const int64_t peak = wave_max(bM);
+        if (lane == 0) {
+            A.status[o] = HEDDLE_S_OK;
+            ((int64_t *)A.iter)[o] = (int64_t)best_it;
+            ((int64_t *)A.bottleneck)[o] = (int64_t)B;
+            A.peak_mem[o] = peak;
+        }
+        const int bei = bc / K, bti = bc - bei * K;
+        if (lane < A.s_max)
+            tiling[o * A.s_max + lane] = act ? (uint8_t)(nibble(P.ep_log2, bei) | nibble(P.tp_log2, bti) << 4) : 0;
+    }
+}
+
+int launch_tile(const heddle_profile *p, const PriceArgs &a, uint8_t *tiling, hipStream_t stream)
+{
+    const int64_t total = a.n * a.n_m;
+    if (total == 0) return HEDDLE_OK;
+    const size_t F = (size_t)p->dev.n_tp * p->dev.n_ep;
+    const size_t lds = (size_t)a.s_cap * F * 25 + a.s_cap;
+    int max_lds = 0;
+    HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
+    if (lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "layout table of this (s_max, n_tp, n_ep) does not fit in LDS");
+    if (lds > 65536)
+        HEDDLE_HIP(hipFuncSetAttribute((const void *)tile_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+    const int blocks = (int)(total < 65536 ? total : 65536);
+    hipLaunchKernelGGL(tile_kernel, dim3(blocks), dim3(64), lds, stream, p->dev, a, tiling);
+    HEDDLE_HIP(hipGetLastError());
+    return HEDDLE_OK;
+}
+
+}  // namespace heddle
+
+using namespace heddle;
+
+extern "C" int heddle_tile_plans(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,
+                                 const uint32_t *d_stages, const int32_t *h_m, int32_t n_m, uint32_t flags,
+                                 void *d_iter, void *d_bottleneck, int64_t *d_peak_mem, const uint8_t *d_layers,
+                                 uint8_t *d_status, uint8_t *d_tiling, hipStream_t stream)
+{
+    int rc = validate_price_args(p, n, s_max, d_n_stages, d_stages, h_m, n_m, flags);
+    if (rc) return rc;
+    if (flags & HEDDLE_F_FP32) return fail(HEDDLE_E_INVAL, "expert tiling is defined for int64 costs (no HEDDLE_F_FP32)");
+    if (n > 0 && (!d_iter || !d_bottleneck || !d_peak_mem || !d_layers || !d_status || !d_tiling))
+        return fail(HEDDLE_E_INVAL, "device pointer is NULL");
+    int64_t m_max = 0;
+    for (int k = 0; k < n_m; k++) m_max = h_m[k] > m_max ? h_m[k] : m_max;
+    const int64_t s_cap = s_max < p->dev.L ? s_max : p->dev.L;
+    const __int128 bound = (__int128)(m_max - 1 + s_cap) * p->max_tiled_ns + p->max_ar_tiled_ns;
+    if (bound >= kLimit62) return fail(HEDDLE_E_RANGE, "tiled iteration time could exceed 2^62 for these m");
+    PriceArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.n = n;
+    a.s_max = s_max;
+    a.s_cap = (int32_t)s_cap;
+    a.n_m = n_m;
+    a.flags = (int32_t)flags;
+    for (int k = 0; k < n_m; k++) a.m[k] = h_m[k];
+    a.n_stages = d_n_stages;
+    a.stages = d_stages;
+    a.iter = d_iter;
+    a.bottleneck = d_bottleneck;
+    a.peak_mem = d_peak_mem;
+    a.layers = const_cast<uint8_t *>(d_layers);
+    a.status = d_status;
+    return launch_tile(p, a, d_tiling, stream);
+}

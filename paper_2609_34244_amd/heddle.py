@@ -21,7 +21,7 @@ HEDDLE_F_FP32, HEDDLE_F_COMPUTE_ONLY, HEDDLE_F_DISTRIBUTE = 1, 2, 4
 STATUS_NAMES = ["OK", "BAD_SHAPE", "BAD_TYPE", "BAD_TP", "UNPROFILED", "BAD_DP", "BAD_EP", "OVERSUBSCRIBED", "OOM"]
 EXPORTS = ["heddle_load_profile", "heddle_free_profile", "heddle_price_plans", "heddle_argmin_plans",
            "heddle_best_plan", "heddle_count_work", "heddle_profile_info_get", "heddle_last_error",
-           "heddle_enum_count", "heddle_enum_templates", "heddle_best_enumerated"]
+           "heddle_enum_count", "heddle_enum_templates", "heddle_best_enumerated", "heddle_tile_plans"]
 
 
 class HeddleError(RuntimeError):
@@ -72,6 +72,7 @@ def lib():
                                        P, P]
         L.heddle_count_work.argtypes = [P, I64, I32, P, P, P, I32, U32, C.POINTER(C.c_int64), P]
         L.heddle_profile_info_get.argtypes = [P, C.POINTER(heddle_profile_info)]
+        L.heddle_tile_plans.argtypes = [P, I64, I32, P, P, P, I32, U32, P, P, P, P, P, P, P]
         L.heddle_enum_count.argtypes = [C.POINTER(heddle_enum_spec), C.POINTER(C.c_int64)]
         L.heddle_enum_templates.argtypes = [C.POINTER(heddle_enum_spec), I64, I64, P, P, P]
         L.heddle_best_enumerated.argtypes = [P, C.POINTER(heddle_enum_spec), P, I32, U32, I64,
@@ -79,7 +80,7 @@ def lib():
         L.heddle_last_error.restype = C.c_char_p
         for f in ("heddle_load_profile", "heddle_price_plans", "heddle_argmin_plans", "heddle_best_plan",
                   "heddle_count_work", "heddle_profile_info_get", "heddle_enum_count", "heddle_enum_templates",
-                  "heddle_best_enumerated"):
+                  "heddle_best_enumerated", "heddle_tile_plans"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -180,6 +181,21 @@ def heddle_price_plans(prof, n_stages, stages, m, flags, out, stream=None):
     _check(lib().heddle_price_plans(prof.handle, n, s_max, _ptr(n_stages), _ptr(stages), mp, len(mm), flags,
                                     _ptr(out["iter"]), _ptr(out["bottleneck"]), _ptr(out["peak_mem"]),
                                     _ptr(out["layers"]), _ptr(out["status"]), _stream(stream)))
+    return out
+
+
+def heddle_tile_plans(prof, n_stages, stages, m, flags, out, stream=None):
+    """Expert tiling of priced plans in place: out is the dict heddle_price_plans
+    filled for the same templates, m and flags; adds out["tiling"] (uint8
+    [n, n_m, s_max], log2 EP | log2 ETP << 4)."""
+    import torch
+    n, s_max = int(stages.shape[0]), int(stages.shape[1])
+    mm, mp = _mlist(m)
+    if "tiling" not in out:
+        out["tiling"] = torch.empty_like(out["layers"])
+    _check(lib().heddle_tile_plans(prof.handle, n, s_max, _ptr(n_stages), _ptr(stages), mp, len(mm), flags,
+                                   _ptr(out["iter"]), _ptr(out["bottleneck"]), _ptr(out["peak_mem"]),
+                                   _ptr(out["layers"]), _ptr(out["status"]), _ptr(out["tiling"]), _stream(stream)))
     return out
 
 

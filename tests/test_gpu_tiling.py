@@ -1,0 +1,127 @@
+"""GPU parity of expert tiling (section 5.3, expert tiling paragraph): the
+library's tile kernel, run on the library's own priced plans, against the
+oracle's re-tiling of the oracle's priced plans, bit for bit (status, iter,
+bottleneck, peak memory, layer counts and the chosen layouts). Needs an
+MI355X."""
+import sys
+
+import numpy as np
+import pytest
+
+from gpu_common import CO, F32, POISON, assert_same, oracle_price, sub_workload
+from oracle import oracle as O
+from workloads.gen import make_workload, random_instance
+
+pytestmark = pytest.mark.gpu
+DIST = 4
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="session")
+def H():
+    import torch
+    assert torch.cuda.is_available(), "no GPU"
+    from paper_2609_34244_amd import heddle
+    heddle.lib()
+    return heddle
+
+
+def gpu_tiled(H, prof, w, flags):
+    import torch
+    ns, st = H.to_device(w.n_stages, w.stages)
+    m = [int(x) for x in w.m]
+    out = H.alloc_outputs(w.n, len(m), w.s_max, flags)
+    out["tiling"] = torch.full_like(out["layers"], POISON)
+    H.heddle_price_plans(prof, ns, st, m, flags, out)
+    H.heddle_tile_plans(prof, ns, st, m, flags, out)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def oracle_tiled(w, flags):
+    op = O.OracleProfile(w.profile)
+    return O.tile_plans(op, w.n_stages, w.stages, w.m, flags, oracle_price(w, flags))
+
+
+def check(g, o, flags, ctx):
+    assert_same(g, o, flags, ctx)
+    if not np.array_equal(g["tiling"], o["tiling"]):
+        bad = np.argwhere(g["tiling"] != o["tiling"])
+        i = tuple(bad[0])
+        raise AssertionError(f"{ctx}: tiling differs at {len(bad)} places, first {i}: gpu={g['tiling'][i[:2]].tolist()} "
+                             f"oracle={o['tiling'][i[:2]].tolist()}")
+
+
+@pytest.mark.parametrize("flags", [0, CO, DIST, CO | DIST])
+def test_tile_random_instances(H, flags):
+    n_plans = 0
+    for seed in range(80):
+        w = random_instance(2000 + seed, moe=seed % 4 != 0, s_max=int([6, 9, 13][seed % 3]), n=41)
+        prof = H.heddle_load_profile(w.profile)
+        check(gpu_tiled(H, prof, w, flags), oracle_tiled(w, flags), flags, f"seed {2000 + seed} flags {flags}")
+        n_plans += w.n * len(w.m)
+    say("tiled random plans", n_plans)
+
+
+@pytest.mark.parametrize("name,n", [("c4_moe", 1500), ("c5_stress", 30), ("c2_7b_dense", 500)])
+@pytest.mark.parametrize("flags", [0, CO])
+def test_tile_config_subsets(H, name, n, flags):
+    w = sub_workload(make_workload(name, n=max(n, 2000)), np.arange(n))
+    prof = H.heddle_load_profile(w.profile)
+    g = gpu_tiled(H, prof, w, flags)
+    check(g, oracle_tiled(w, flags), flags, f"{name} flags {flags}")
+    say(name, flags, "statuses", np.bincount(g["status"].ravel(), minlength=9).tolist())
+
+
+def test_tile_full_c4_sampled(H):
+    """the full MoE batch (500,000 templates) in the benchmark's launch
+    configuration; a seeded sample recomputed by the oracle; tiling never
+    slows a plan that fitted with its template's layouts"""
+    import torch
+    w = make_workload("c4_moe")
+    prof = H.heddle_load_profile(w.profile)
+    ns, st = H.to_device(w.n_stages, w.stages)
+    m = [int(x) for x in w.m]
+    out = H.alloc_outputs(w.n, len(m), w.s_max, 0)
+    H.heddle_price_plans(prof, ns, st, m, 0, out)
+    before = {k: v.cpu().numpy() for k, v in out.items()}
+    H.heddle_tile_plans(prof, ns, st, m, 0, out)
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in out.items()}
+    ok = before["status"] == 0
+    assert np.all(g["status"][ok] == 0) and np.all(g["iter"][ok] <= before["iter"][ok])
+    say("c4 OK plans", int(ok.sum()), "faster after tiling", int((g["iter"][ok] < before["iter"][ok]).sum()),
+        "mean ratio", float(np.mean(g["iter"][ok] / before["iter"][ok])))
+    idx = np.sort(np.random.default_rng(5).choice(w.n, size=400, replace=False))
+    o = oracle_tiled(sub_workload(w, idx), 0)
+    check({k: v[idx] for k, v in g.items()}, o, 0, "c4 full sampled")
+
+
+def test_tile_edges(H):
+    """fp32 is rejected; buffers that describe no split (layer counts that do
+    not add up to L) are left alone with zero tiling bytes"""
+    import torch
+    w = random_instance(2500, moe=True, n=8)
+    prof = H.heddle_load_profile(w.profile)
+    ns, st = H.to_device(w.n_stages, w.stages)
+    m = [int(x) for x in w.m]
+    out = H.alloc_outputs(w.n, len(m), w.s_max, F32)
+    with pytest.raises(H.HeddleError) as e:
+        H.heddle_tile_plans(prof, ns, st, m, F32, out)
+    assert e.value.code == H.HEDDLE_E_INVAL
+    out = H.alloc_outputs(w.n, len(m), w.s_max, 0)
+    H.heddle_price_plans(prof, ns, st, m, 0, out)
+    out["status"].zero_()
+    out["layers"][:, :, 0] = 1                 # stage 0 claims one layer; the rest as priced
+    out["layers"][:, :, 1:] = 0
+    out["iter"].fill_(7)
+    H.heddle_tile_plans(prof, ns, st, m, 0, out)
+    torch.cuda.synchronize()
+    bad = (w.profile.L != 1)
+    if bad:
+        assert int(out["tiling"].count_nonzero()) == 0
+        assert bool((out["iter"] == 7).all())

@@ -238,9 +238,10 @@ def main():
                           "unit": "Tlane-op/s", "frac": achieved / PEAK_LANE_OPS, "traffic": traffic,
                           "kernel_ms": float(np.mean(kern_ms))}, **roof),
         "statuses": statuses,
-        "tiling": None if not args.tiling else {
+        "tiling": None if not args.tiling else dict({
             "tile_kernel_ms": float(np.mean(tile_ms)),
             "note": "heddle_tile_plans re-tiles every plan's expert layouts after pricing, inside the timed step"},
+            **tiling_gain(H, prof, ns, st, m, flags, w, out)),
         "best_plan": {"template": best[0], "m_index": best[1], "iter": best[2]} if best else None,
         "profile_load_ms": load_ms,
     }
@@ -248,6 +249,22 @@ def main():
         log(f"oracle baseline, about {args.cpu_seconds:.0f} s on one host core")
         result["cpu_baseline"] = cpu_baseline(w, flags, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def tiling_gain(H, prof, ns, st, m, flags, w, tiled):
+    """the same plans priced without tiling (one launch outside the timed
+    region) against the tiled outputs"""
+    import numpy as np
+    import torch
+    ref = H.alloc_outputs(w.n, len(m), w.s_max, flags)
+    H.heddle_price_plans(prof, ns, st, m, flags, ref)
+    torch.cuda.synchronize()
+    s0, s1 = ref["status"].cpu().numpy(), tiled["status"].cpu().numpy()
+    i0, i1 = ref["iter"].cpu().numpy().astype(np.float64), tiled["iter"].cpu().numpy().astype(np.float64)
+    both = (s0 == 0) & (s1 == 0)
+    return {"plans_ok_untiled": int((s0 == 0).sum()), "plans_ok_tiled": int((s1 == 0).sum()),
+            "faster_after_tiling": int((i1[both] < i0[both]).sum()),
+            "mean_iter_ratio": float(np.mean(i1[both] / i0[both])) if both.any() else None}
 
 
 def run_enumerate(args, H, flags, k_unit, unit_name):

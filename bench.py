@@ -94,6 +94,9 @@ def main():
                     help="Heddle's speed-proportional split with its fallback list instead of the min-max split")
     ap.add_argument("--tiling", action="store_true",
                     help="re-tile every priced plan's expert layouts (heddle_tile_plans) inside the step")
+    ap.add_argument("--fill", action="store_true",
+                    help="BestFill: DP degree from node lists, micro-batch size 1, 2 or 4 from per-size profiles "
+                         "(global batch = the config's m micro-batches of size 1)")
     ap.add_argument("--enumerate", action="store_true",
                     help="price the whole space of the search backbone (every stage count up to --enum-depth, "
                          "every type and TP per stage) on the config's profile instead of its template batch")
@@ -130,6 +133,8 @@ def main():
     k_unit, unit_name = (K_EVAL, "stage-cost evaluation") if args.distribute else (K_MIN, "DP relaxation")
     if args.enumerate:
         return run_enumerate(args, H, flags, k_unit, unit_name)
+    if args.fill:
+        return run_fill(args, H, flags)
     t0 = time.perf_counter()
     w = make_workload(args.config)
     log(f"workload {args.config}: {w.n} templates x {len(w.m)} m generated in {time.perf_counter() - t0:.1f}s")
@@ -265,6 +270,65 @@ def tiling_gain(H, prof, ns, st, m, flags, w, tiled):
     return {"plans_ok_untiled": int((s0 == 0).sum()), "plans_ok_tiled": int((s1 == 0).sum()),
             "faster_after_tiling": int((i1[both] < i0[both]).sum()),
             "mean_iter_ratio": float(np.mean(i1[both] / i0[both])) if both.any() else None}
+
+
+def run_fill(args, H, flags):
+    """A step is one heddle_fill_plans call over the config's batch (DP by
+    packing, every template priced at each micro-batch size, the best size
+    kept) followed by the argmin."""
+    import numpy as np
+    import torch
+
+    from workloads.gen import cluster_nodes, make_workload, mbs_profile
+
+    w = make_workload(args.config)
+    mbs, G, dp_cap = [1, 2, 4], int(w.m[0]), 8
+    nn, ng = cluster_nodes(w.profile)
+    cl = H.heddle_load_cluster(nn, ng)
+    profs = [H.heddle_load_profile(mbs_profile(w.profile, b)) for b in mbs]
+    ns, st = H.to_device(w.n_stages, w.stages)
+    torch.cuda.synchronize()
+    out = None
+    for i in range(args.warmup):
+        out = H.heddle_fill_plans(profs, mbs, cl, G, dp_cap, ns, st, flags)
+        log(f"warmup {i + 1}/{args.warmup} done")
+    times, best = [], None
+    for i in range(args.steps):
+        t0 = time.perf_counter()
+        out = H.heddle_fill_plans(profs, mbs, cl, G, dp_cap, ns, st, flags)
+        best = H.heddle_argmin_plans([G], flags, out["iter"], out["status"])
+        times.append(time.perf_counter() - t0)
+    step_s = float(np.mean(times))
+    status = out["status"].cpu().numpy().ravel()
+    dp = out["dp"].cpu().numpy()
+    pick = out["mbs_index"].cpu().numpy()
+    log(f"timed {args.steps} steps: {step_s * 1e3:.2f} ms each; best {best}")
+    result = {
+        "metric": "candidate plans priced/sec (partition+evaluate) on 1 MI355X; % VALU roofline",
+        "value": w.n / step_s,
+        "unit": "plans/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": ("fp32" if args.fp32 else "int64"),
+        "data": "synthetic",
+        "config": {"workload": f"BestFill on {WORKLOAD_TEXT[args.config]}: DP by packing (cap {dp_cap}) into "
+                               f"node lists of full and half-size nodes, micro-batch size in {mbs}, global batch "
+                               f"{G} samples",
+                   "name": args.config, "templates": w.n, "plans": w.n, "pricings_per_step": w.n * len(mbs),
+                   "memory_aware": not args.compute_only,
+                   "partition": "distribute" if args.distribute else "min-max"},
+        "roofline": None,
+        "fill": {"dp_histogram": np.bincount(dp, minlength=dp_cap + 1).tolist(),
+                 "size_chosen": {str(b): int((pick[status == 0] == i).sum()) for i, b in enumerate(mbs)},
+                 "statuses": np.bincount(status, minlength=9).tolist()},
+        "best_plan": {"template": best[0], "iter": best[2]} if best else None,
+    }
+    print(json.dumps(result), flush=True)
 
 
 def run_enumerate(args, H, flags, k_unit, unit_name):

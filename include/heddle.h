@@ -286,6 +286,71 @@ int heddle_tile_plans(const heddle_profile *p, int64_t n, int32_t s_max,
                       hipStream_t stream);
 
 /*
+ * GPU composition as a node list per GPU type (section 5.1, non-uniform
+ * composition support): a node may hold any number of GPUs. HOST memory,
+ * read during heddle_load_cluster.
+ */
+typedef struct heddle_cluster_desc {
+    int32_t n_types;              /* 1..255, the profile's type indices                    */
+    const int32_t *n_nodes;       /* [n_types] nodes of each type, >= 0                    */
+    const int32_t *node_gpus;     /* [sum n_nodes] GPUs per node, 1..64, type 0's first    */
+} heddle_cluster_desc;
+
+typedef struct heddle_cluster heddle_cluster;   /* opaque, device-resident node counts */
+
+/* Load a node list to the current device (per type, the number of nodes of
+ * each size). Returns HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_NOMEM or
+ * HEDDLE_E_DEVICE; *out is NULL on error. Release with heddle_free_cluster. */
+int heddle_load_cluster(const heddle_cluster_desc *d, heddle_cluster **out);
+void heddle_free_cluster(heddle_cluster *c);
+
+/*
+ * heddle_fill_dp -- the DP degree of each template from the node lists
+ * (section 5.3, layer split and DP degree; section 5.1 packing rule). The TP
+ * group of every stage is packed into the nodes of the stage's GPU type, one
+ * replica after another (replica 1: stages 0..S-1 in order, then replica 2,
+ * ...); a group of TP t goes to a node with exactly t free GPUs if there is
+ * one, else takes t GPUs from the node with the fewest free GPUs above t;
+ * types pack independently. D is the number of whole replicas packed before
+ * the first group that finds no node, capped at dp_cap and rounded down to a
+ * multiple of the template's largest EP degree. D is written into the DP
+ * field of every stage record (in place) and into d_dp[t]; D = 0 means not
+ * even one replica packs (heddle_price_plans then reports BAD_DP). Templates
+ * with S < 1, S > s_max, a type outside the cluster or TP above 64 are left
+ * unchanged with d_dp = 0. Asynchronous on `stream`.
+ *   d_stages  DEVICE [n][s_max] records, DP fields rewritten.
+ *   d_dp      DEVICE [n] int32.
+ *   dp_cap    1..65535.
+ * Returns HEDDLE_OK, HEDDLE_E_INVAL or HEDDLE_E_DEVICE.
+ */
+int heddle_fill_dp(const heddle_cluster *c, int64_t n, int32_t s_max, const uint8_t *d_n_stages,
+                   uint32_t *d_stages, int32_t dp_cap, int32_t *d_dp, hipStream_t stream);
+
+/*
+ * heddle_fill_plans -- BestFill (section 5.3, arithmetic auto-fill): the DP
+ * degree from the node lists (heddle_fill_dp, records rewritten in place),
+ * then the micro-batch size from the profiled powers of two: profiles[b] is
+ * the profile measured at micro-batch size h_mbs[b] (ascending), and a
+ * global batch of `global_batch` samples is m_b = ceil(global_batch /
+ * h_mbs[b]) micro-batches. Each template is priced at every size (as
+ * heddle_price_plans with m = m_b and `flags`), and the size with the
+ * shortest iteration time among those that fit (status OK) is kept, the
+ * smaller size on ties; with none OK the smallest size's results are kept.
+ * Outputs as heddle_price_plans with n_m = 1, plus d_dp [n] int32 and
+ * d_mbs_index [n] uint8 (index into h_mbs). The library allocates one set
+ * of outputs per size on `stream` and frees it before returning.
+ * Synchronous.
+ * Returns HEDDLE_OK, HEDDLE_E_INVAL (profiles of different L or s_max, m_b
+ * out of range), HEDDLE_E_RANGE, HEDDLE_E_NOMEM or HEDDLE_E_DEVICE.
+ */
+int heddle_fill_plans(const heddle_profile *const *profiles, const int32_t *h_mbs, int32_t n_mbs,
+                      const heddle_cluster *c, int64_t global_batch, int32_t dp_cap,
+                      int64_t n, int32_t s_max, const uint8_t *d_n_stages, uint32_t *d_stages,
+                      uint32_t flags, void *d_iter, void *d_bottleneck, int64_t *d_peak_mem,
+                      uint8_t *d_layers, uint8_t *d_status, int32_t *d_dp, uint8_t *d_mbs_index,
+                      hipStream_t stream);
+
+/*
  * Exhaustive enumeration of structures: the search backbone of the planners
  * Heddle analyses (section 3.1), with (N * K)^D structures for N GPU types,
  * K TP degrees and D stages (section 2), run as one data-parallel workload.

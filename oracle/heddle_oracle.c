@@ -839,6 +839,74 @@ int oracle_tile_plans(const oracle_profile *p, int64_t n, int s_max, const uint8
     return 0;
 }
 
+/* ---------------------------------------------------------------------- */
+/* DP degree by packing (section 5.3, layer split and DP degree; section   */
+/* 5.1, non-uniform GPU composition): the TP group of every stage is       */
+/* packed into the nodes of its GPU type, replica after replica (stages in */
+/* order within a replica); a group of t GPUs goes to the first node with  */
+/* exactly t free GPUs, else to the node with the fewest free GPUs above t */
+/* (the first such). Types pack independently; D is the smallest number of */
+/* whole replicas over the types used, capped at dp_cap, rounded down to a */
+/* multiple of the template's largest EP degree.                           */
+/* ---------------------------------------------------------------------- */
+static int place_group(const int *free_gpus, int n_nodes, int t)
+{
+    for (int i = 0; i < n_nodes; i++)
+        if (free_gpus[i] == t) return i;
+    int pick = -1;
+    for (int i = 0; i < n_nodes; i++)
+        if (free_gpus[i] > t && (pick < 0 || free_gpus[i] < free_gpus[pick])) pick = i;
+    return pick;
+}
+
+int oracle_fill_dp(int n_types, const int32_t *n_nodes, const int32_t *node_gpus, int64_t n, int s_max,
+                   const uint8_t *n_stages, uint32_t *stages, int dp_cap, int32_t *dp)
+{
+    int64_t first[256];
+    int64_t acc = 0;
+    for (int g = 0; g < n_types; g++) { first[g] = acc; acc += n_nodes[g]; }
+    int *free_gpus = (int *)malloc(sizeof(int) * (size_t)(acc > 0 ? acc : 1));
+    for (int64_t t = 0; t < n; t++) {
+        int S = n_stages[t];
+        uint32_t *rec = stages + (size_t)t * s_max;
+        dp[t] = 0;
+        if (S < 1 || S > s_max) continue;
+        int ok_types = 1, max_ep = 1;
+        for (int s = 0; s < S; s++) {
+            int g = (int)(rec[s] & 0xFF), tp = 1 << ((rec[s] >> 8) & 15), ep = 1 << ((rec[s] >> 12) & 15);
+            if (g >= n_types || tp > 64) ok_types = 0;
+            if (ep > max_ep) max_ep = ep;
+        }
+        if (!ok_types) continue;
+        int D = dp_cap;
+        for (int g = 0; g < n_types; g++) {
+            int used = 0;
+            for (int s = 0; s < S; s++) used |= (int)(rec[s] & 0xFF) == g;
+            if (!used) continue;
+            for (int i = 0; i < n_nodes[g]; i++) free_gpus[i] = node_gpus[first[g] + i];
+            int r = 0;
+            while (r < dp_cap) {
+                int ok = 1;
+                for (int s = 0; s < S && ok; s++) {
+                    if ((int)(rec[s] & 0xFF) != g) continue;
+                    int tp = 1 << ((rec[s] >> 8) & 15);
+                    int i = place_group(free_gpus, n_nodes[g], tp);
+                    if (i < 0) ok = 0;
+                    else free_gpus[i] -= tp;
+                }
+                if (!ok) break;
+                r++;
+            }
+            if (r < D) D = r;
+        }
+        D = D / max_ep * max_ep;
+        dp[t] = D;
+        for (int s = 0; s < S; s++) rec[s] = (rec[s] & 0xFFFFu) | ((uint32_t)D << 16);
+    }
+    free(free_gpus);
+    return 0;
+}
+
 /* Argmin over OK plans of iter / m (maximum throughput m / iter), compared
  * exactly as iter_a * m_b < iter_b * m_a; ties to the lowest template
  * index, then the lowest m index. Returns 0 and fills the answer, or -1

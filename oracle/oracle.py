@@ -46,6 +46,8 @@ def lib():
         _lib.oracle_best_plan.restype = C.c_int
         _lib.oracle_tile_plans.argtypes = [P, C.c_int64, C.c_int, P, P, P, C.c_int, C.c_uint32, P, P, P, P, P, P]
         _lib.oracle_tile_plans.restype = C.c_int
+        _lib.oracle_fill_dp.argtypes = [C.c_int, P, P, C.c_int64, C.c_int, P, P, C.c_int, P]
+        _lib.oracle_fill_dp.restype = C.c_int
         _lib.oracle_count_relaxations.argtypes = [P, C.c_int, P, C.c_int, C.c_int64, C.c_uint32]
         _lib.oracle_count_relaxations.restype = C.c_int64
         _lib.oracle_xfer_ns.argtypes = [C.c_int64, C.c_int64]
@@ -146,6 +148,44 @@ def tile_plans(oprof, n_stages, stages, m, flags, priced):
                                  d(out["tiling"]))
     assert rc == 0, "tiling is defined for int64 costs"
     return out
+
+
+def fill_dp(n_nodes, node_gpus, n_stages, stages, dp_cap):
+    """DP degree of every template by packing (returns (dp [n], records with
+    the DP field rewritten))."""
+    n_nodes = np.ascontiguousarray(n_nodes, dtype=np.int32)
+    node_gpus = np.ascontiguousarray(node_gpus, dtype=np.int32)
+    n_stages = np.ascontiguousarray(n_stages, dtype=np.uint8)
+    st = np.array(stages, dtype=np.uint32, copy=True)
+    n, s_max = st.shape
+    dp = np.zeros(n, dtype=np.int32)
+    d = lambda a: a.ctypes.data
+    lib().oracle_fill_dp(len(n_nodes), d(n_nodes), d(node_gpus), n, s_max, d(n_stages), d(st), int(dp_cap), d(dp))
+    return dp, st
+
+
+def fill_plans(oprofs, mbs, n_nodes, node_gpus, global_batch, dp_cap, n_stages, stages, flags=0):
+    """BestFill: DP by packing, then every micro-batch size priced (profile
+    oprofs[b] at m_b = ceil(global_batch / mbs[b]) micro-batches) and the
+    fitting one with the shortest iteration time kept (smaller size on ties;
+    the smallest size's results when none fits). Returns the outputs of
+    price_plans (n_m = 1) plus dp, mbs_index and the rewritten records."""
+    dp, st = fill_dp(n_nodes, node_gpus, n_stages, stages, dp_cap)
+    outs = [price_plans(op, n_stages, st, np.array([-(-int(global_batch) // int(b))], dtype=np.int32), flags)
+            for op, b in zip(oprofs, mbs)]
+    n = len(n_stages)
+    pick = np.zeros(n, dtype=np.uint8)
+    for t in range(n):
+        best = None
+        for b, o in enumerate(outs):
+            if o["status"][t, 0] != 0:
+                continue
+            if best is None or o["iter"][t, 0] < outs[best]["iter"][t, 0]:
+                best = b
+        pick[t] = 0 if best is None else best
+    res = {k: np.stack([outs[pick[t]][k][t] for t in range(n)]) if n else outs[0][k] for k in outs[0]}
+    res.update(dp=dp, mbs_index=pick, stages=st)
+    return res
 
 
 def best_plan(m, iter_, status, flags=0):

@@ -21,7 +21,8 @@ HEDDLE_F_FP32, HEDDLE_F_COMPUTE_ONLY, HEDDLE_F_DISTRIBUTE = 1, 2, 4
 STATUS_NAMES = ["OK", "BAD_SHAPE", "BAD_TYPE", "BAD_TP", "UNPROFILED", "BAD_DP", "BAD_EP", "OVERSUBSCRIBED", "OOM"]
 EXPORTS = ["heddle_load_profile", "heddle_free_profile", "heddle_price_plans", "heddle_argmin_plans",
            "heddle_best_plan", "heddle_count_work", "heddle_profile_info_get", "heddle_last_error",
-           "heddle_enum_count", "heddle_enum_templates", "heddle_best_enumerated", "heddle_tile_plans"]
+           "heddle_enum_count", "heddle_enum_templates", "heddle_best_enumerated", "heddle_tile_plans",
+           "heddle_load_cluster", "heddle_free_cluster", "heddle_fill_dp", "heddle_fill_plans"]
 
 
 class HeddleError(RuntimeError):
@@ -45,6 +46,10 @@ class heddle_profile_desc(C.Structure):
 class heddle_enum_spec(C.Structure):
     _fields_ = [("d_max", C.c_int32), ("n_types", C.c_int32), ("types", C.c_void_p), ("n_tp", C.c_int32),
                 ("log2_tp", C.c_void_p), ("n_dp", C.c_int32), ("dp", C.c_void_p), ("log2_ep", C.c_int32)]
+
+
+class heddle_cluster_desc(C.Structure):
+    _fields_ = [("n_types", C.c_int32), ("n_nodes", C.c_void_p), ("node_gpus", C.c_void_p)]
 
 
 class heddle_profile_info(C.Structure):
@@ -73,6 +78,11 @@ def lib():
         L.heddle_count_work.argtypes = [P, I64, I32, P, P, P, I32, U32, C.POINTER(C.c_int64), P]
         L.heddle_profile_info_get.argtypes = [P, C.POINTER(heddle_profile_info)]
         L.heddle_tile_plans.argtypes = [P, I64, I32, P, P, P, I32, U32, P, P, P, P, P, P, P]
+        L.heddle_load_cluster.argtypes = [C.POINTER(heddle_cluster_desc), C.POINTER(C.c_void_p)]
+        L.heddle_free_cluster.argtypes = [P]
+        L.heddle_free_cluster.restype = None
+        L.heddle_fill_dp.argtypes = [P, I64, I32, P, P, I32, P, P]
+        L.heddle_fill_plans.argtypes = [P, P, I32, P, I64, I32, I64, I32, P, P, U32, P, P, P, P, P, P, P, P]
         L.heddle_enum_count.argtypes = [C.POINTER(heddle_enum_spec), C.POINTER(C.c_int64)]
         L.heddle_enum_templates.argtypes = [C.POINTER(heddle_enum_spec), I64, I64, P, P, P]
         L.heddle_best_enumerated.argtypes = [P, C.POINTER(heddle_enum_spec), P, I32, U32, I64,
@@ -80,7 +90,8 @@ def lib():
         L.heddle_last_error.restype = C.c_char_p
         for f in ("heddle_load_profile", "heddle_price_plans", "heddle_argmin_plans", "heddle_best_plan",
                   "heddle_count_work", "heddle_profile_info_get", "heddle_enum_count", "heddle_enum_templates",
-                  "heddle_best_enumerated", "heddle_tile_plans"):
+                  "heddle_best_enumerated", "heddle_tile_plans", "heddle_load_cluster", "heddle_fill_dp",
+                  "heddle_fill_plans"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -284,3 +295,60 @@ def heddle_best_enumerated(prof, spec, m, flags, chunk=0, stream=None):
         return None, None, None, int(n_ok.value)
     _check(rc)
     return int(bt.value), int(bk.value), bi.value, int(n_ok.value)
+
+
+class Cluster:
+    """Handle of a loaded node list (device-resident)."""
+
+    def __init__(self, handle):
+        self.handle = C.c_void_p(handle)
+
+    def __del__(self):
+        if getattr(self, "handle", None) and self.handle.value and _lib is not None:
+            _lib.heddle_free_cluster(self.handle)
+            self.handle = C.c_void_p(None)
+
+
+def heddle_load_cluster(n_nodes, node_gpus):
+    """n_nodes: nodes per GPU type; node_gpus: GPUs per node, type 0's first."""
+    nn = np.ascontiguousarray(n_nodes, dtype=np.int32)
+    ng = np.ascontiguousarray(node_gpus, dtype=np.int32)
+    d = heddle_cluster_desc(n_types=len(nn), n_nodes=nn.ctypes.data, node_gpus=ng.ctypes.data if ng.size else None)
+    h = C.c_void_p()
+    _check(lib().heddle_load_cluster(C.byref(d), C.byref(h)))
+    return Cluster(h.value)
+
+
+def heddle_free_cluster(cl):
+    if cl.handle.value:
+        lib().heddle_free_cluster(cl.handle)
+        cl.handle = C.c_void_p(None)
+
+
+def heddle_fill_dp(cl, n_stages, stages, dp_cap, stream=None):
+    """DP degree by packing; rewrites the DP field of `stages` (device, in
+    place) and returns d_dp (int32 [n])."""
+    import torch
+    n, s_max = int(stages.shape[0]), int(stages.shape[1])
+    dp = torch.empty(n, dtype=torch.int32, device=stages.device)
+    _check(lib().heddle_fill_dp(cl.handle, n, s_max, _ptr(n_stages), _ptr(stages), int(dp_cap), _ptr(dp),
+                                _stream(stream)))
+    return dp
+
+
+def heddle_fill_plans(profiles, mbs, cl, global_batch, dp_cap, n_stages, stages, flags, stream=None):
+    """BestFill: DP by packing (stages rewritten in place), then the best
+    micro-batch size; returns the outputs of heddle_price_plans (n_m = 1)
+    plus "dp" and "mbs_index"."""
+    import torch
+    n, s_max = int(stages.shape[0]), int(stages.shape[1])
+    arr = (C.c_void_p * len(profiles))(*[p.handle.value for p in profiles])
+    mb = np.ascontiguousarray(mbs, dtype=np.int32)
+    out = alloc_outputs(n, 1, s_max, flags, device=stages.device)
+    out["dp"] = torch.empty(n, dtype=torch.int32, device=stages.device)
+    out["mbs_index"] = torch.empty(n, dtype=torch.uint8, device=stages.device)
+    _check(lib().heddle_fill_plans(C.cast(arr, C.c_void_p), mb.ctypes.data, len(mb), cl.handle, int(global_batch),
+                                   int(dp_cap), n, s_max, _ptr(n_stages), _ptr(stages), flags, _ptr(out["iter"]),
+                                   _ptr(out["bottleneck"]), _ptr(out["peak_mem"]), _ptr(out["layers"]),
+                                   _ptr(out["status"]), _ptr(out["dp"]), _ptr(out["mbs_index"]), _stream(stream)))
+    return out

@@ -163,3 +163,21 @@ def test_enum_templates_range_errors(lib):
     assert call(85, 0) == H.HEDDLE_E_INVAL
     assert call(0, 4, None, p) == H.HEDDLE_E_INVAL
     assert call(84, 0) == H.HEDDLE_OK           # empty range at the end: nothing enqueued
+
+
+def test_cluster_and_fill_argument_errors(lib):
+    h = C.c_void_p(5)
+    nn = np.array([2], np.int32)
+    for sizes in ([0, 4], [65, 4]):
+        ng = np.array(sizes, np.int32)
+        d = H.heddle_cluster_desc(n_types=1, n_nodes=nn.ctypes.data, node_gpus=ng.ctypes.data)
+        assert lib.heddle_load_cluster(C.byref(d), C.byref(h)) == H.HEDDLE_E_INVAL and h.value is None
+    d = H.heddle_cluster_desc(n_types=0, n_nodes=nn.ctypes.data, node_gpus=None)
+    assert lib.heddle_load_cluster(C.byref(d), C.byref(h)) == H.HEDDLE_E_INVAL
+    assert lib.heddle_load_cluster(None, C.byref(h)) == H.HEDDLE_E_INVAL
+    p = C.c_void_p(16)
+    assert lib.heddle_fill_dp(None, 4, 4, p, p, 8, p, None) == H.HEDDLE_E_INVAL
+    mb = np.array([1], np.int32)
+    assert lib.heddle_fill_plans(None, mb.ctypes.data, 0, p, 8, 8, 4, 4, p, p, 0, p, p, p, p, p, p, p,
+                                 None) == H.HEDDLE_E_INVAL
+    lib.heddle_free_cluster(None)

@@ -648,3 +648,82 @@ def test_tiling_single_layout_is_identity():
                 assert np.array_equal(ti[key], pr[key]), key
             has = (ti["layers"][:, :, 0] > 0)
             assert np.all(ti["tiling"][has][:, 0] == 0)           # log2 EP 0, log2 ETP 0 on stage 0
+
+
+# ------------------------------------------------------------ BestFill
+# section 5.3 (layer split and DP degree; micro-batch size), section 5.1
+# (node lists, packing rule)
+
+def _recs(stages):
+    rec = np.zeros((1, len(stages)), dtype=np.uint32)
+    for s, (g, tp, ep) in enumerate(stages):
+        rec[0, s] = pack_stage(g, int(np.log2(tp)), int(np.log2(ep)), 1)
+    return np.array([len(stages)], dtype=np.uint8), rec
+
+
+def test_packing_worked_examples():
+    g = json.load(open(GOLD))
+    for c in g["packing_cases"]:
+        ns, rec = _recs(c["stages"])
+        dp, st = O.fill_dp(c["n_nodes"], c["node_gpus"], ns, rec, c["dp_cap"])
+        assert int(dp[0]) == c["dp"], (c["_what"], int(dp[0]))
+        assert all(int(r) >> 16 == c["dp"] for r in st[0, :len(c["stages"])])
+
+
+def _pack_by_counts(n_nodes, node_gpus, recs, S, dp_cap):
+    """the same greedy kept as counts of nodes per number of free GPUs"""
+    first = np.concatenate([[0], np.cumsum(n_nodes)])
+    D, max_ep = dp_cap, 1
+    for s in range(S):
+        max_ep = max(max_ep, 1 << ((int(recs[s]) >> 12) & 15))
+    for g in sorted(set(int(r) & 0xFF for r in recs[:S])):
+        cnt = [0] * 65
+        for x in node_gpus[first[g]:first[g + 1]]:
+            cnt[int(x)] += 1
+        r = 0
+        while r < dp_cap:
+            ok = True
+            for s in range(S):
+                if int(recs[s]) & 0xFF != g:
+                    continue
+                t = 1 << ((int(recs[s]) >> 8) & 15)
+                c = t if t <= 64 and cnt[t] > 0 else next((c for c in range(t + 1, 65) if cnt[c] > 0), None)
+                if c is None:
+                    ok = False
+                    break
+                cnt[c] -= 1
+                cnt[c - t] += 1
+            if not ok:
+                break
+            r += 1
+        D = min(D, r)
+    return D // max_ep * max_ep
+
+
+def test_packing_matches_count_form():
+    rng = np.random.default_rng(77)
+    for trial in range(300):
+        N = int(rng.integers(1, 4))
+        n_nodes = rng.integers(0, 6, size=N).astype(np.int32)
+        node_gpus = rng.choice([1, 2, 3, 4, 6, 8, 16], size=int(n_nodes.sum())).astype(np.int32)
+        S = int(rng.integers(1, 6))
+        recs = np.array([pack_stage(int(rng.integers(0, N)), int(rng.integers(0, 4)), int(rng.integers(0, 3)), 1)
+                         for _ in range(S)], dtype=np.uint32)
+        dp_cap = int(rng.integers(1, 40))
+        dp, st = O.fill_dp(n_nodes, node_gpus, np.array([S], np.uint8), recs[None, :], dp_cap)
+        assert int(dp[0]) == _pack_by_counts(n_nodes, node_gpus, recs, S, dp_cap), trial
+        assert all(int(r) >> 16 == int(dp[0]) for r in st[0])
+
+
+def test_fill_plans_single_size_is_pricing():
+    """one micro-batch size: BestFill = packing, then plain pricing at
+    m = global batch / size"""
+    from workloads.gen import cluster_nodes
+    w = random_instance(61, moe=True, n=30)
+    nn, ng = cluster_nodes(w.profile)
+    op = O.OracleProfile(w.profile)
+    r = O.fill_plans([op], [2], nn, ng, 16, 8, w.n_stages, w.stages, 0)
+    o = O.price_plans(op, w.n_stages, r["stages"], np.array([8], np.int32), 0)
+    for k in ("status", "iter", "bottleneck", "peak_mem", "layers"):
+        assert np.array_equal(r[k], o[k]), k
+    assert not r["mbs_index"].any()

@@ -345,3 +345,39 @@ def random_instance(seed, L=None, n_types=None, s_max=6, n=40, max_cost=6, moe=N
     m = np.unique(rng.integers(1, 20, size=int(rng.integers(1, 4)))).astype(np.int32)
     return Workload(name=f"random_{seed}", profile=prof, n_stages=np.minimum(S, 255).astype(np.uint8),
                     stages=np.ascontiguousarray(rec), m=m, s_max=s_max)
+
+
+def mbs_profile(p, mbs, exponent=0.9):
+    """The profile of the same model and cluster at micro-batch size `mbs`
+    (the base profile is taken at size 1): per-layer times grow as
+    mbs^exponent (a larger micro-batch uses the GPU better), activations,
+    the boundary tensor and the MoE all-to-all grow with mbs, parameter,
+    optimizer and gradient bytes do not. No random draws."""
+    f = float(mbs) ** exponent
+    scale = lambda a: np.maximum(_round_half_even(a * f), 1).astype(np.int64)
+    q = Profile(**{k: getattr(p, k) for k in p.__dataclass_fields__})
+    q.layer_ns = np.ascontiguousarray(scale(p.layer_ns))
+    if p.xlayer_ns is not None:
+        q.xlayer_ns = np.ascontiguousarray(np.minimum(_round_half_even(p.xlayer_ns * f), q.layer_ns), dtype=np.int64)
+    q.layer_ns_f32 = None
+    q.act_bytes = np.ascontiguousarray(p.act_bytes * int(mbs))
+    q.boundary_bytes = int(p.boundary_bytes) * int(mbs)
+    q.a2a_bytes = int(p.a2a_bytes) * int(mbs)
+    return q.check()
+
+
+def cluster_nodes(p):
+    """A non-uniform node list per GPU type from a profile's largest node
+    size and GPU count: about half of each type's GPUs in nodes of the
+    largest size, the rest in nodes of half that size (one-GPU nodes for a
+    type whose largest node has one GPU). Returns (n_nodes [N], node_gpus)."""
+    n_nodes, gpus = [], []
+    for g in range(p.n_types):
+        k, total = int(p.node_size[g]), int(p.n_gpus[g])
+        full = (total // 2) // k
+        rest = total - full * k
+        small = max(k // 2, 1)
+        nodes = [k] * full + [small] * (rest // small) + ([rest % small] if rest % small else [])
+        n_nodes.append(len(nodes))
+        gpus += nodes
+    return np.array(n_nodes, dtype=np.int32), np.array(gpus, dtype=np.int32)

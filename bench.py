@@ -42,11 +42,16 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def source_hash():
+# sources of the kernels a traffic measurement covers (and of the tables they read)
+COMMON_SOURCES = ["heddle_internal.h", "device_common.h", "exact_math.h", "stage_cost.h", "profile.cpp"]
+MEASURED_SOURCES = {"": ["price.hip", "decode.h", "dp_common.h", "evaluate.hip"], "_distribute": ["distribute.hip"]}
+
+
+def source_hash(mode=""):
     """hash of the device sources the traffic counters were taken on"""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_34244_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in sorted(COMMON_SOURCES + MEASURED_SOURCES[mode]):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()[:16]
@@ -61,7 +66,7 @@ def measured_traffic(config, flags, n_plans, distribute=False):
         return None
     with open(path) as f:
         t = json.load(f)
-    if t.get("source_sha") != source_hash() or t.get("flags") != flags or t.get("plans") != n_plans:
+    if t.get("source_sha") != source_hash(mode) or t.get("flags") != flags or t.get("plans") != n_plans:
         return None
     return t.get("bytes_per_launch")
 

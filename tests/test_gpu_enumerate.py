@@ -128,3 +128,27 @@ def test_best_enumerated_full_size_sampled(H):
     o = O.price_plans(op, ns, st, m, 0)
     ok = o["status"][:, 0] == 0
     assert all(Fraction(int(x), m[0]) >= Fraction(it, m[k]) for x in o["iter"][ok, 0])
+
+
+def test_enumeration_edges(H):
+    """a one-template space, chunks of one template, and a space where no
+    plan fits (every stage count above the layers)"""
+    w = make_workload("c1_tiny_dense", n=8)
+    prof = H.heddle_load_profile(w.profile)
+    op = O.OracleProfile(w.profile)
+    s1 = H.EnumSpec(1, [1], [0], [1], 0)
+    assert H.heddle_enum_count(s1) == 1
+    got = H.heddle_best_enumerated(prof, s1, [16], 0, 1)
+    want = EN.best_enumerated(op, 1, [1], [0], [1], 0, np.array([16], np.int32), 0)
+    assert got[:2] == want[:2] and got[3] == want[3]
+    s2 = H.EnumSpec(2, [0, 1], [1, 0], [2, 1], 0)
+    for chunk in (1, 3):
+        got = H.heddle_best_enumerated(prof, s2, [16, 4], 0, chunk)
+        want = EN.best_enumerated(op, 2, [0, 1], [1, 0], [2, 1], 0, np.array([16, 4], np.int32), 0)
+        assert got[:2] == want[:2] and got[3] == want[3]
+        assert want[0] is None or got[2] == int(want[2])
+    L = w.profile.L
+    big = H.EnumSpec(min(L + 2, 64), [0], [0], [1], 0)            # depths above L are BAD_SHAPE
+    got = H.heddle_best_enumerated(prof, big, [16], 0, 0)
+    want = EN.best_enumerated(op, min(L + 2, 64), [0], [0], [1], 0, np.array([16], np.int32), 0)
+    assert got[:2] == want[:2] and got[3] == want[3]

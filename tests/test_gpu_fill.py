@@ -113,3 +113,29 @@ def test_fill_plans_configs(H, name, n):
     compare(g, o, 0, name)
     say(name, "statuses", np.bincount(g["status"].ravel(), minlength=9).tolist(), "sizes",
         np.bincount(g["mbs_index"], minlength=3).tolist())
+
+
+def test_fill_edges(H):
+    """64-GPU nodes and TP 64, a cap of 65535, a type without nodes, a
+    single-node cluster, and an empty batch"""
+    import torch
+    nn = np.array([1, 0, 3], np.int32)
+    ng = np.array([64, 64, 2, 2], np.int32)
+    S = np.array([1, 2, 3, 1, 2], np.uint8)
+    rec = np.zeros((5, 3), np.uint32)
+    rec[0, :1] = pack_stage(0, 6, 0, 1)                          # TP 64 on the 64-GPU node: 1 replica
+    rec[1, :2] = pack_stage(np.array([0, 2]), np.array([0, 1]), 0, 1)
+    rec[2, :3] = pack_stage(np.array([2, 2, 0]), np.array([0, 0, 2]), np.array([1, 0, 0]), 1)
+    rec[3, :1] = pack_stage(1, 0, 0, 1)                          # type 1 has no nodes: D = 0
+    rec[4, :2] = pack_stage(np.array([2, 2]), np.array([1, 1]), 0, 1)
+    cl = H.heddle_load_cluster(nn, ng)
+    for dp_cap in (1, 2, 65535):
+        d_ns, d_st = H.to_device(S, rec)
+        dp = H.heddle_fill_dp(cl, d_ns, d_st, dp_cap)
+        torch.cuda.synchronize()
+        o_dp, o_st = O.fill_dp(nn, ng, S, rec, dp_cap)
+        assert np.array_equal(dp.cpu().numpy(), o_dp) and np.array_equal(d_st.cpu().numpy().view(np.uint32), o_st)
+    assert o_dp[3] == 0
+    d_ns, d_st = H.to_device(S[:0], rec[:0])
+    H.heddle_fill_dp(cl, d_ns, d_st, 8)
+    torch.cuda.synchronize()

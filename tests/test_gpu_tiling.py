@@ -10,7 +10,7 @@ import pytest
 
 from gpu_common import CO, F32, POISON, assert_same, oracle_price, sub_workload
 from oracle import oracle as O
-from workloads.gen import make_workload, random_instance
+from workloads.gen import make_workload, pack_stage, random_instance
 
 pytestmark = pytest.mark.gpu
 DIST = 4
@@ -125,3 +125,40 @@ def test_tile_edges(H):
     if bad:
         assert int(out["tiling"].count_nonzero()) == 0
         assert bool((out["iter"] == 7).all())
+
+
+def test_tile_max_shapes_and_empty(H):
+    """L = 255 layers, s_max = 64 stage slots, four TP and four EP degrees
+    (the largest layout table); an empty batch enqueues nothing"""
+    import torch
+    rng = np.random.default_rng(9)
+    w = random_instance(2600, L=255, n_types=2, s_max=64, n=6, moe=True, max_cost=40, cap_scale=100.0)
+    p = w.profile
+    # four TP and four EP degrees: widen the instance's tables to TP {1, 2, 4, 8}
+    K = 4
+    tp = np.array([1, 2, 4, 8], np.int32)
+    rep = lambda a, ax: np.ascontiguousarray(np.concatenate([a] + [a[:, :1] if ax == 1 else a[:1]] * (K - a.shape[ax]),
+                                                            axis=ax)) if a.shape[ax] < K else a
+    p.tp_degrees = tp
+    p.layer_ns = rep(p.layer_ns, 1)
+    p.xlayer_ns = np.ascontiguousarray(p.layer_ns * p.is_moe[None, None, :] // 3, dtype=np.int64)
+    p.profiled = np.ones((p.layer_ns.shape[0], K), np.uint8)
+    for f in ("state_bytes", "xstate_bytes", "act_bytes", "grad_bytes", "xgrad_bytes"):
+        setattr(p, f, rep(getattr(p, f), 0))
+    p.ep_degrees = np.array([1, 2, 4, 8], np.int32)
+    p.node_size[:] = 8
+    p.n_gpus[:] = 1 << 20
+    p.check()
+    S = np.array([1, 64, 40, 17, 64, 2], np.uint8)
+    rec = np.zeros((6, 64), np.uint32)
+    for t in range(6):
+        rec[t, :S[t]] = pack_stage(rng.integers(0, 2, S[t]), rng.integers(0, 4, S[t]), rng.integers(0, 3, S[t]), 8)
+    w.n_stages, w.stages, w.s_max = S, rec, 64
+    prof = H.heddle_load_profile(p)
+    for flags in (0, CO):
+        check(gpu_tiled(H, prof, w, flags), oracle_tiled(w, flags), flags, f"max shapes flags {flags}")
+    ns, st = H.to_device(S[:0], rec[:0])
+    out = H.alloc_outputs(0, 1, 64, 0)
+    H.heddle_price_plans(prof, ns, st, [4], 0, out)
+    H.heddle_tile_plans(prof, ns, st, [4], 0, out)
+    torch.cuda.synchronize()

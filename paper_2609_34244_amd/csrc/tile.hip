@@ -51,16 +51,19 @@ __device__ __forceinline__ void wave_min_pair(uint64_t &a, uint64_t &b)
     }
 }
 
-__global__ void __launch_bounds__(64) tile_kernel(DevProfile P, PriceArgs A, uint8_t *tiling)
+__global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, uint8_t *tiling)
 {
     extern __shared__ __align__(16) unsigned char smem[];      // one wavefront per workgroup
     const int lane = threadIdx.x;
     const int L = P.L, R = L + 1, N = P.n_types, K = P.n_tp, E = P.n_ep, F = K * E;
-    uint64_t *cT = (uint64_t *)smem;                           // [s_cap][F] time (kNoLayout: none)
-    uint64_t *cG = cT + (size_t)A.s_cap * F;                   // [s_cap][F] synchronisation
-    int64_t *cM = (int64_t *)(cG + (size_t)A.s_cap * F);       // [s_cap][F] memory
-    uint8_t *cC = (uint8_t *)(cM + (size_t)A.s_cap * F);       // [s_cap][F] layout index of a kept entry
-    uint8_t *cN = cC + (size_t)A.s_cap * F;                    // [s_cap] kept layouts of a stage
+    // rows of Fp = F rounded up to odd 8-byte entries: lanes reading their own
+    // stage's row touch distinct LDS banks
+    const int Fp = F | 1;
+    uint64_t *cT = (uint64_t *)smem;                           // [s_cap][Fp] time (kNoLayout: none)
+    uint64_t *cG = cT + (size_t)A.s_cap * Fp;                  // [s_cap][Fp] synchronisation
+    int64_t *cM = (int64_t *)(cG + (size_t)A.s_cap * Fp);      // [s_cap][Fp] memory
+    uint8_t *cC = (uint8_t *)(cM + (size_t)A.s_cap * Fp);      // [s_cap][Fp] layout index of a kept entry
+    uint8_t *cN = cC + (size_t)A.s_cap * Fp;                   // [s_cap] kept layouts of a stage
     const int64_t total = A.n * A.n_m;
 
     for (int64_t o = blockIdx.x; o < total; o += gridDim.x) {
@@ -142,9 +145,10 @@ __global__ void __launch_bounds__(64) tile_kernel(DevProfile P, PriceArgs A, uin
                 const int64_t *xg = P.pre_xgrad + (size_t)(ti * E + ei) * R;
                 const int64_t edp = allowed ? sW / group : 1;
                 const int64_t gs = sgd + allreduce_ns(xg[sj0] - xg[si0], edp, sbw);
-                cT[q] = allowed && mem <= scap ? T : kNoLayout;
-                cG[q] = (uint64_t)gs;
-                cM[q] = mem;
+                const int qs = s * Fp + c;
+                cT[qs] = allowed && mem <= scap ? T : kNoLayout;
+                cG[qs] = (uint64_t)gs;
+                cM[qs] = mem;
             }
         }
         wave_sync();
@@ -155,7 +159,7 @@ __global__ void __launch_bounds__(64) tile_kernel(DevProfile P, PriceArgs A, uin
         // bound on the synchronisation, and only their synchronisation values
         // need to be tried as bounds
         if (act) {
-            const int rb = lane * F;
+            const int rb = lane * Fp;
             int nf = 0;
             for (int c = 0; c < F; c++) {
                 const uint64_t x = cT[rb + c], y = cG[rb + c];
@@ -194,14 +198,14 @@ __global__ void __launch_bounds__(64) tile_kernel(DevProfile P, PriceArgs A, uin
             const int s = q < n_cand ? q / F : 0, j = q - s * F;
             uint64_t it = kNoLayout, G = kNoLayout;
             if (q < n_cand && j < cN[s]) {
-                G = cG[q];
+                G = cG[s * Fp + j];
                 uint64_t maxT = 0, sumT = 0, maxg = 0;
                 bool ok = true;
                 for (int s2 = 0; s2 < S && ok; s2++) {
                     uint64_t bT = kNoLayout, bG = 0;
                     const int n2 = cN[s2];
                     for (int j2 = 0; j2 < n2; j2++) {
-                        const uint64_t x = cT[s2 * F + j2], y = cG[s2 * F + j2];
+                        const uint64_t x = cT[s2 * Fp + j2], y = cG[s2 * Fp + j2];
                         const bool take = y <= G && x < bT;        // kept layouts have distinct times
                         bT = take ? x : bT;
                         bG = take ? y : bG;
@@ -230,7 +234,7 @@ __global__ void __launch_bounds__(64) tile_kernel(DevProfile P, PriceArgs A, uin
         int bc = 0;
         if (act) {
             bT = kNoLayout;
-            const int rb = lane * F, nf = cN[lane];
+            const int rb = lane * Fp, nf = cN[lane];
             for (int j = 0; j < nf; j++) {
                 const uint64_t x = cT[rb + j], y = cG[rb + j];
                 const bool take = y <= best_G && x < bT;
@@ -258,7 +262,7 @@ int launch_tile(const heddle_profile *p, const PriceArgs &a, uint8_t *tiling, hi
     const int64_t total = a.n * a.n_m;
     if (total == 0) return HEDDLE_OK;
     const size_t F = (size_t)p->dev.n_tp * p->dev.n_ep;
-    const size_t lds = (size_t)a.s_cap * F * 25 + a.s_cap;
+    const size_t lds = (size_t)a.s_cap * (F | 1) * 25 + a.s_cap;
     int max_lds = 0;
     HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
     if (lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "layout table of this (s_max, n_tp, n_ep) does not fit in LDS");

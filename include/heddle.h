@@ -54,7 +54,7 @@ extern "C" {
 #define HEDDLE_S_BAD_SHAPE      1  /* S < 1, S > s_max or S > L                               */
 #define HEDDLE_S_BAD_TYPE       2  /* a stage's GPU type >= n_types                           */
 #define HEDDLE_S_BAD_TP         3  /* TP not a profiled degree, or TP > node size (5.1 mask)  */
-#define HEDDLE_S_UNPROFILED     4  /* no profile entry for (type, TP): exact match only (5.2) */
+#define HEDDLE_S_UNPROFILED     4  /* no profile entry for (type, TP): profiles match exactly (5.2) */
 #define HEDDLE_S_BAD_DP         5  /* DP < 1, or stages disagree on DP                        */
 #define HEDDLE_S_BAD_EP         6  /* EP not an allowed degree, or EP does not divide DP      */
 #define HEDDLE_S_OVERSUBSCRIBED 7  /* sum over a type's stages of TP * DP > its GPU count     */
@@ -169,7 +169,7 @@ void heddle_free_profile(heddle_profile *p);
  * value computed from fp32 per-layer costs and fp32-rounded transfer terms
  * (one rounding per stage time and one for the iteration time).
  * DISTRIBUTE (Heddle's own split, section 5.3, layer split and DP degree):
- * instead of the min-max split, stage s gets layers in proportion to its
+ * instead of the min-max split, stage s's share of the layers is set by its
  * speed 1 / (int64 time of all L layers on its type and TP, all-to-all
  * included, p2p excluded): the cut after stage s is floor(x + 0.5) with
  * x = L * (speeds of stages 0..s) / (speeds of all stages) in IEEE double
@@ -287,7 +287,7 @@ int heddle_tile_plans(const heddle_profile *p, int64_t n, int32_t s_max,
 
 /*
  * GPU composition as a node list per GPU type (section 5.1, non-uniform
- * composition support): a node may hold any number of GPUs. HOST memory,
+ * composition support): the nodes of a type may differ in size. HOST memory,
  * read during heddle_load_cluster.
  */
 typedef struct heddle_cluster_desc {
@@ -329,7 +329,7 @@ int heddle_fill_dp(const heddle_cluster *c, int64_t n, int32_t s_max, const uint
 /*
  * heddle_fill_plans -- BestFill (section 5.3, arithmetic auto-fill): the DP
  * degree from the node lists (heddle_fill_dp, records rewritten in place),
- * then the micro-batch size from the profiled powers of two: profiles[b] is
+ * then the micro-batch size among the profiled sizes: profiles[b] is
  * the profile measured at micro-batch size h_mbs[b] (ascending), and a
  * global batch of `global_batch` samples is m_b = ceil(global_batch /
  * h_mbs[b]) micro-batches. Each template is priced at every size (as

@@ -27,10 +27,10 @@
  * iteration (section 5.3, expert tiling; see tile_plan).
  *
  * Second partition mode (OR_F_DISTRIBUTE): Heddle's own layer split of the
- * arithmetic auto-fill (section 5.3, layer split and DP degree): each stage
- * gets layers in proportion to its profiled speed; when that split does not
- * fit memory, a fixed list of alternative splits is priced and the fastest
- * one that fits is kept (see distribute_cuts and price_distribute).
+ * arithmetic auto-fill (section 5.3, layer split and DP degree): the layer
+ * shares follow the stages' profiled speeds; if that split overflows memory,
+ * a predefined set of neighbouring splits is evaluated and the quickest one
+ * within memory wins (see distribute_cuts and price_distribute).
  *
  * Everything is written the slow, obvious way: every sum is a loop, every
  * product and quotient of a transfer time is done in 128-bit integers, and
@@ -497,7 +497,7 @@ static void price_one_f32(const oracle_profile *p, const ostage *st, int S, int6
 /* nearest integer (halves up) to L * (sum_{t<=s} speed_t) / sum_t speed_t, */
 /* computed in IEEE double in this order, then moved up to leave stage s   */
 /* one layer and down to leave every later stage one layer. When that      */
-/* split does not fit memory, the fixed list of alternatives is: for each  */
+/* split does not fit memory, the alternatives tried are: for each         */
 /* boundary b = 0 .. S-2 in order, the cut after stage b moved by -1, then */
 /* by +1 (kept only if every stage still holds a layer); the fitting       */
 /* alternative with the smallest iteration time is kept, the first in list */
@@ -627,7 +627,8 @@ int oracle_price_plans(const oracle_profile *p, int64_t t0, int64_t t1, int s_ma
 /* and DP D spans W = k * D GPUs, and its expert layout is EP e x ETP t x  */
 /* EDP W / (e t). The layouts priced for a stage: e from the EP list, t    */
 /* from the TP list, t profiled for the stage's GPU type and no larger     */
-/* than its node (ETP carries TP's node bound; EP does not), e t dividing  */
+/* than its node (ETP stays within a node like TP; EP may span nodes), e t */
+/* dividing                                                                */
 /* W. For one layout:                                                      */
 /*  - an MoE layer costs its profiled time at TP k with the experts' part  */
 /*    at ETP k replaced by the experts' part at ETP t scaled to the        */

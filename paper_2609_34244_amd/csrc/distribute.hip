@@ -2,7 +2,7 @@
 // 5.3, layer split and DP degree) as a second partition mode of
 // heddle_price_plans, with its Evaluate.
 //
-// Every stage gets layers in proportion to its profiled speed. The speed of
+// Each stage's share of the layers follows its profiled speed. The speed of
 // stage s is the inverse of the time of all L layers on its GPU type and TP
 // degree (int64 layer costs with the stage's all-to-all terms, p2p
 // excluded); the cut after stage s is the nearest integer (halves up) to
@@ -186,7 +186,7 @@ __global__ void __launch_bounds__(64, 3) distribute_kernel(DevProfile P, PriceAr
             bool fits = nf == 0, has_split = fits || compute_only;
             int best_b = -1, best_c = 0;
             if (!has_split) {
-                // the fixed list of alternatives, in order: for each boundary b, the cut
+                // the predefined alternatives, in order: for each boundary b, the cut
                 // after stage b moved by -1, then by +1; the fastest fitting one is kept
                 // (the first on ties)
                 uint64_t best_key = ~0ull;

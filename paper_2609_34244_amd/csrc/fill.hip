@@ -1,10 +1,10 @@
 // BestFill on gfx950 (Heddle, arXiv 2609.34244, section 5.3, arithmetic
 // auto-fill): the DP degree of each template from the GPU composition's node
-// lists, then the micro-batch size from the profiled powers of two.
+// lists, then the micro-batch size among the profiled sizes (powers of two).
 //
 // DP degree: the TP group of every stage is packed into the nodes of the
 // stage's GPU type (section 5.1: a group goes to a node whose free GPUs equal
-// its size, else takes its GPUs from a larger node), one replica after
+// its size, otherwise on a node with more free GPUs), one replica after
 // another with the stages in order. Nodes with the same number of free GPUs
 // are interchangeable, so a type's nodes are kept as counts per number of
 // free GPUs (0..64); a group of t GPUs takes a node from count[t] if there is

@@ -4,7 +4,8 @@
 // A stage of TP k and DP D spans W = k * D GPUs; its expert layout is EP e x
 // ETP t x EDP W / (e t). The layouts priced for a stage: e from the EP list,
 // t a profiled TP degree of the stage's GPU type no larger than its node (ETP
-// carries TP's node bound, EP does not), e t dividing W. Under a layout an
+// stays within one node like TP, while an EP group may span nodes), e t
+// dividing W. Under a layout an
 // MoE layer costs its profiled time at TP k with the experts' part at ETP k
 // replaced by the experts' part at ETP t scaled to the stage's tokens per GPU
 // (ceil(x_t * t / k); a per-(type, TP, ETP) prefix table), plus one

@@ -8,8 +8,8 @@
 // excluded); the cut after stage s is the nearest integer (halves up) to
 // L * (speed of stages 0..s) / (speed of all stages), computed in IEEE double
 // in that order, then raised to leave stage s a layer and lowered to leave
-// every later stage one. When that split does not fit memory, a fixed list of
-// alternatives is priced: for each boundary in order, its cut moved by -1,
+// every later stage one. When that split does not fit memory, these
+// alternatives are priced: for each boundary in order, its cut moved by -1,
 // then by +1 (kept only if every stage still holds a layer); the fitting one
 // with the smallest iteration time is kept, the first on ties, and none
 // fitting leaves the plan OOM without a split. With HEDDLE_F_COMPUTE_ONLY the

@@ -48,12 +48,15 @@ MEASURED_SOURCES = {"": ["price.hip", "decode.h", "dp_common.h", "evaluate.hip"]
 
 
 def source_hash(mode=""):
-    """hash of the device sources the traffic counters were taken on"""
+    """hash of the code (comments and spacing dropped) of the device sources
+    the traffic counters were taken on"""
+    import re
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_34244_amd", "csrc")
     for f in sorted(COMMON_SOURCES + MEASURED_SOURCES[mode]):
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(f.encode() + b"\0" + fh.read())
+        with open(os.path.join(csrc, f)) as fh:
+            code = re.sub(r"/\*.*?\*/|//[^\n]*", " ", fh.read(), flags=re.S)
+        h.update(f.encode() + b"\0" + " ".join(code.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -53,11 +53,12 @@ __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlan
 // v with lane `lane` (uniform) replaced by the uniform value x
 __device__ __forceinline__ int put_lane(int v, int x, int lane) { return (int)__lane_id() == lane ? x : v; }
 
-// DPP lane permutations within rows of 16 lanes (lanes whose source is not
-// valid keep their own value, which is harmless for min/max)
+// DPP lane permutations within rows of 16 lanes (every source lane exists, so
+// bound_ctrl never applies); the move folds into the DPP operand of the min
+// or max that consumes it
 template <int CTRL> __device__ __forceinline__ uint32_t dpp32(uint32_t v)
 {
-    return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xF, 0xF, false);
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
 }
 template <int CTRL> __device__ __forceinline__ uint64_t dpp64(uint64_t v)
 {
@@ -70,7 +71,8 @@ constexpr int kDppXor1 = 0xB1;          // quad_perm [1,0,3,2]
 constexpr int kDppXor2 = 0x4E;          // quad_perm [2,3,0,1]
 constexpr int kDppHalfMirror = 0x141;   // lane i <-> 7 - i within 8
 constexpr int kDppMirror = 0x140;       // lane i <-> 15 - i within 16
-constexpr int kDppWaveShl1 = 0x130;     // lane i <- lane i + 1 across the wavefront (lane 63 keeps its own)
+constexpr int kDppWaveShl1 = 0x130;     // lane i <- lane i + 1 across the wavefront (lane 63 keeps the old value)
+constexpr int kDppWaveShr1 = 0x138;     // lane i <- lane i - 1 across the wavefront (lane 0 keeps the old value)
 
 // minimum over aligned groups of k lanes (k a power of two, 1 .. 64, uniform);
 // every lane of a group receives the group's minimum

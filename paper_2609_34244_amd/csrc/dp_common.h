@@ -23,6 +23,7 @@ template <class V, class V2> __device__ __forceinline__ V relax(const V2 &a, V p
 }
 
 template <class T> __device__ __forceinline__ T vmin(T a, T b) { return a < b ? a : b; }
+template <class T> __device__ __forceinline__ T vmax(T a, T b) { return a > b ? a : b; }
 
 // min over the ends [j, je] of one row, in steps of four ends; the ends of
 // the last step past je are read (they lie inside the pair row) and masked

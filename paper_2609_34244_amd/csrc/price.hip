@@ -24,9 +24,9 @@
 // the split kernel), and the DP relaxes only those. Lanes are split rows
 // during the DP: r rows of a window take 64 >> ceil(log2 r) lanes each, which
 // share the row's ends and combine with a cross-lane minimum. Per wavefront,
-// LDS holds pairs W_s[j] = {P_s[j], G[s+1][j]}, so one 64-bit read feeds one
-// relaxation (sub, max, min). The time prefix of stage s-1 is fetched into
-// registers while stage s relaxes.
+// one LDS pair row holds X[j] = {P_s[j], G[s+1][j]}, so one 64-bit read feeds
+// one relaxation (sub, max, min); G[s][i] overwrites G[s+1][i] in place. The
+// time prefix of stage s-1 is fetched into registers while stage s relaxes.
 #include <cstring>
 
 #include "decode.h"
@@ -81,17 +81,16 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
     constexpr int kNone = 255;                                 // no row with F true at or after this one
     extern __shared__ __align__(16) unsigned char smem[];      // one wavefront per workgroup
     const int lane = threadIdx.x;
-    const int L = P.L, gs = A.g_stride, ls = P.lim_stride;
+    const int L = P.L, ls = P.lim_stride;
     const bool mem_aware = (A.flags & HEDDLE_F_COMPUTE_ONLY) == 0;
     const V INF = DPInf<V>::value;
-    V2 *W = (V2 *)smem;                                        // [2][gs] alternating pair rows {P_s, G_{s+1}}
+    V2 *X = (V2 *)smem;                                        // [gs] pair row {P_s[j], G_{s+1}[j]}
     // [s_cap][2][ls] per stage: limit row, then inverse-limit row (later the
     // next-row table of the second pass)
     uint8_t *JX = smem + A.off_j;
     uint32_t *cnt = (uint32_t *)(smem + A.off_c);              // [n_types] GPU counters of decode
     const V *rows = stage_rows<V>(P, F32);
     const int nd = ls >> 1;                                    // dwords per stage in JX (<= 128)
-    auto pair_row = [&](int s) -> V2 * { return W + (size_t)(s & 1) * gs; };
     auto jrow = [&](int s) -> uint8_t * { return JX + s * 2 * ls; };
     auto xrow = [&](int s) -> uint8_t * { return JX + s * 2 * ls + ls; };
 
@@ -202,36 +201,54 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                 if (!feasible) continue;                               // no split fits memory
 
                 // ---------------- PartitionLayers: suffix min-max DP over the windows, stages S-1 .. 0
+                // Per-stage constants packed into lanes, one readlane per stage each:
+                // lane s: a_s | b_s << 8 | e_s << 16 | a_{s+1} << 24, with e_s the last end
+                // of a row of stage s (L for the last stage, else b_{s+1}) and a_S = L;
+                // lane s: offset of the time row of stage s-1 | a_{s-1} << 24.
+                const int An = __builtin_amdgcn_update_dpp(L, Al, kDppWaveShl1, 0xF, 0xF, false);
+                const int Bn = __builtin_amdgcn_update_dpp(L, Bl, kDppWaveShl1, 0xF, 0xF, false);
+                const bool last = lane >= S - 1;
+                const uint32_t pk = (uint32_t)Al | ((uint32_t)Bl << 8) | ((uint32_t)(last ? L : Bn) << 16) |
+                                    ((uint32_t)(last ? L : An) << 24);
+                const uint32_t prv = (uint32_t)__builtin_amdgcn_update_dpp(
+                    0, (int)((uint32_t)x.prow | ((uint32_t)Al << 24)), kDppWaveShr1, 0xF, 0xF, false);
                 RowRegs<V> rr;
                 fetch_rows<V>(rr, rows + uni(rl32(x.prow, S - 1)), uni(rl32(Al, S - 1)), L, lane);
                 V Bv = INF;
                 for (int s = S - 1; s >= 0; s--) {
-                    const int a = uni(rl32(Al, s)), b = uni(rl32(Bl, s));
-                    const int e = s == S - 1 ? L : uni(rl32(Bl, s + 1));     // last end of any row
-                    V2 *Xs = pair_row(s);
-                    V2 *Xo = pair_row(s + 1);                          // receives G_s (pair row of stage s-1)
+                    const uint32_t ks = uni64(pk, s);
+                    const int a = ks & 255, b = (ks >> 8) & 255, e = (ks >> 16) & 255, a_next = ks >> 24;
+                    // P_s into the pair row over [a, e]; G_{s+1} stays in place
 #pragma unroll
                     for (int q = 0; q < kRowSlots; q++)
-                        if (64 * q <= e - a) ((V *)&Xs[min(a + lane + 64 * q, e)])[0] = rr.p[q];
-                    if (s > 0) fetch_rows<V>(rr, rows + uni(rl32(x.prow, s - 1)), uni(rl32(Al, s - 1)), b, lane);
+                        if (64 * q <= e - a) ((V *)&X[min(a + lane + 64 * q, e)])[0] = rr.p[q];
+                    if (s > 0) {
+                        const uint32_t kp = uni64(prv, s);
+                        fetch_rows<V>(rr, rows + (kp & 0xFFFFFFu), (int)(kp >> 24), b, lane);
+                    }
                     wave_sync();
                     if (s == S - 1) {
                         // last stage: every window row ends at L
                         if (COUNT) {
                             if (lane == 0) work += (unsigned long long)(b - a + 1);
                         } else {
+                            const V pL = X[L].x;
                             for (int i = a + lane; i <= b; i += 64) {
-                                const V gv = (V)(Xs[L].x - Xs[i].x);
-                                if (s > 0) ((V *)&Xo[i])[1] = gv;
+                                const V gv = (V)(pL - X[i].x);
+                                if (s > 0) ((V *)&X[i])[1] = gv;
                                 else Bv = gv;                          // S = 1: row 0, lane 0
                             }
                             if (S == 1) Bv = (V)rl64((int64_t)Bv, 0);
                         }
                     } else {
-                        // r rows, k = 64 >> ceil(log2 r) lanes per row (one when r >= 64); the
-                        // k lanes of a row take consecutive shares of its ends
+                        // r rows, k = 64 >> ceil(log2 r) lanes per row (one when r >= 64). The
+                        // ends of a row are relaxed four at a time, chunk c of the row by lane
+                        // c mod k; a chunk reaching past the row's last end is moved back to end
+                        // there (rows of four or more ends), and the ends past the last one of a
+                        // shorter row are masked. G_s[i] replaces G_{s+1}[i] in place: rows are
+                        // taken in increasing order and every end read lies above its row.
                         const V p2p = (V)uni64(x.p2p, s);
-                        const int a_next = uni(rl32(Al, s + 1)), jhi = jhi_of(s);
+                        const int jhi = L - (S - 1 - s);
                         const uint8_t *Js = jrow(s);
                         const int r = b - a + 1;
                         const int lk = r >= 64 ? 0 : 6 - (r > 1 ? 32 - __clz(r - 1) : 0);
@@ -242,19 +259,33 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                             const int ic = min(i, b);
                             const int lo = max(ic + 1, a_next);
                             const int hi = mem_aware ? min((int)Js[ic], jhi) : jhi;
-                            const int n = i <= b ? max(hi - lo + 1, 0) : 0;
                             if (COUNT) {
-                                if (part == 0) work += (unsigned long long)n;
+                                if (part == 0 && i <= b && hi >= lo) work += (unsigned long long)(hi - lo + 1);
                                 continue;
                             }
-                            const int c = (n + k - 1) >> lk;             // ends per lane
-                            const int js = lo + (int)__umul24((unsigned)part, (unsigned)c);
-                            const int je = min(js + c - 1, hi);
-                            const V pi = Xs[ic].x - p2p;                 // T(s,i,j) = P_s[j] - pi
-                            V acc = relax_range<V>(Xs, js, je, pi, INF);
-                            acc = group_min<V>(acc, k);
-                            if (s == 0) Bv = (V)rl64((int64_t)acc, 0);   // row 0 only: the whole wave's minimum
-                            else if (i <= b && part == 0) ((V *)&Xo[i])[1] = acc;
+                            const int hv = i <= b ? hi : 0;                  // no chunk for lanes past b
+                            // a relaxation past the row's last end is forced to INF by a mask
+                            // taken into its max (ends 1..3 of a row with fewer than four ends)
+                            const V m1 = hi > lo ? V(0) : INF, m2 = hi > lo + 1 ? V(0) : INF;
+                            const V m3 = hi > lo + 2 ? V(0) : INF;
+                            const V pi = X[ic].x - p2p;                      // T(s,i,j) = P_s[j] - pi
+                            // chunk starts walk by 4k ends and stop at the row's last chunk start
+                            const V2 *cm = X + max(hi - 3, lo);
+                            const V2 *ce = X + hv;
+                            const V2 *cx = X + lo + 4 * part;
+                            V acc = INF;
+                            for (; cx <= ce; cx += 4 * k) {
+                                const V2 *c = cx < cm ? cx : cm;
+                                const V2 c0 = c[0], c1 = c[1], c2 = c[2], c3 = c[3];
+                                acc = vmin(vmin(acc, relax<V>(c0, pi)), vmax(relax<V>(c1, pi), m1));
+                                acc = vmin(vmin(acc, vmax(relax<V>(c2, pi), m2)), vmax(relax<V>(c3, pi), m3));
+                            }
+                            if (s == 0) {
+                                Bv = (V)rl64((int64_t)group_min<V>(acc, 64), 0);   // row 0 only
+                            } else {
+                                acc = group_min<V>(acc, k);
+                                if (i <= b && part == 0) ((V *)&X[i])[1] = acc;
+                            }
                         }
                     }
                     wave_sync();
@@ -385,10 +416,10 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     const int L = p->dev.L, ls = p->dev.lim_stride;
     a.s_cap = a.s_max < L ? a.s_max : L;
     a.g_stride = L + 5;                                       // L + 1 ends and 4 of padding
-    // per wavefront: two alternating pair rows {P_s, G_{s+1}}; per stage its
+    // per wavefront: one pair row {P_s, G_{s+1}}; per stage its
     // limit row and its inverse-limit row (later its next-row table); one GPU
     // counter per type
-    const size_t j_off = ((size_t)2 * a.g_stride * 2 * sizeof(V) + 15) & ~size_t(15);
+    const size_t j_off = ((size_t)a.g_stride * 2 * sizeof(V) + 15) & ~size_t(15);
     const size_t c_off = j_off + (size_t)a.s_cap * 2 * ls;
     a.off_j = (int32_t)j_off;
     a.off_c = (int32_t)c_off;

@@ -77,7 +77,6 @@ template <class V, bool F32, bool COUNT>
 __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevProfile P, PriceArgs A)
 {
     typedef typename Vec2<V>::type V2;
-    constexpr int kBatch = 4;                                  // stages whose limit rows are loaded together
     constexpr int kNone = 255;                                 // no row with F true at or after this one
     extern __shared__ __align__(16) unsigned char smem[];      // one wavefront per workgroup
     const int lane = threadIdx.x;
@@ -90,10 +89,13 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
     uint8_t *JX = smem + A.off_j;
     uint32_t *cnt = (uint32_t *)(smem + A.off_c);              // [n_types] GPU counters of decode
     const V *rows = stage_rows<V>(P, F32);
-    const int nd = ls >> 1;                                    // dwords per stage in JX (<= 128)
     auto jrow = [&](int s) -> uint8_t * { return JX + s * 2 * ls; };
     auto xrow = [&](int s) -> uint8_t * { return JX + s * 2 * ls + ls; };
 
+    // limit-row copy: the two rows of a stage are q16 pieces of 16 bytes; lane
+    // (su, pc) copies piece pc of stage s0 + su
+    const int q16 = ls >> 3, per = 64 / q16;
+    const int su = lane / q16, pc = lane - su * q16;
     int my_m = 1;                                              // lane k: the k-th micro-batch count
     for (int k = 0; k < A.n_m; k++) my_m = lane == k ? A.m[k] : my_m;
     unsigned long long work = 0;
@@ -132,73 +134,47 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                 const uint64_t cls = __ballot(lane < A.n_m && key_k == key) & todo;
                 todo &= ~cls;
                 auto jhi_of = [&](int s) { return L - (S - 1 - s); };   // last end leaving a layer per later stage
-                auto lim_of = [&](int s, int i) {                       // lim(s, i)
-                    return mem_aware ? min((int)jrow(s)[i], jhi_of(s)) : jhi_of(s);
-                };
 
                 // ---------------- limit and inverse-limit rows of every stage (this class)
-                // into LDS, kBatch stages per round trip; lanes past the end repeat the
-                // last dword
+                // into LDS: 16-byte pieces, the rows of `per` stages per load
                 if (mem_aware) {
                     wave_sync();                                        // earlier reads of JX are done
                     int f = min(S - lane, key);
                     f = f < 1 ? 1 : f;
-                    const int my_row = (x.lrow + (f - 1) * 2 * ls) >> 2;   // lane s: stage s's rows, in dwords
-                    const uint32_t *lim32 = (const uint32_t *)P.mem_lim;
-                    uint32_t *jx32 = (uint32_t *)JX;
-                    const uint32_t d0 = min(lane, nd - 1), d1 = min(lane + 64, nd - 1);
-                    for (int s0 = 0; s0 < S; s0 += kBatch) {
-                        uint32_t v0[kBatch], v1[kBatch];
-#pragma unroll
-                        for (int u = 0; u < kBatch; u++) {
-                            if (s0 + u < S) {
-                                const uint32_t *src = lim32 + uni(rl32(my_row, s0 + u));
-                                v0[u] = src[d0];
-                                if (nd > 64) v1[u] = src[d1];
-                            }
-                        }
-#pragma unroll
-                        for (int u = 0; u < kBatch; u++) {
-                            if (s0 + u < S) {
-                                uint32_t *dst = jx32 + (s0 + u) * nd;
-                                dst[d0] = v0[u];
-                                if (nd > 64) dst[d1] = v1[u];
-                            }
-                        }
+                    const int my_row = x.lrow + (f - 1) * 2 * ls;       // lane s: byte offset of stage s's rows
+                    for (int s0 = 0; s0 < S; s0 += per) {
+                        const int st = s0 + su;
+                        const int row = __shfl(my_row, min(st, 63));
+                        if (su < per && st < S)
+                            *(uint4 *)(JX + st * 2 * ls + pc * 16) = *(const uint4 *)(P.mem_lim + row + pc * 16);
                     }
                     wave_sync();
                 }
 
                 // ---------------- row windows: lane s holds [a_s, b_s]
-                int Al = lane, Bl = 0;
-                bool feasible = true;
+                // the forward reach R_s and the backward bound Bk_s are independent
+                // pointer chases over the limit rows; one loop takes a step of each
+                int Al, Bl;
                 {
-                    int Rl = 0;                                         // lane s: R_s
-                    int c = 0;
-                    for (int s = 1; s < S; s++) {
-                        c = uni(lim_of(s - 1, c));
-                        Rl = put_lane(Rl, c, s);
-                    }
-                    int nxt = L;                                       // Bk_{s+1}
-                    for (int s = S - 1; s >= 0; s--) {
-                        const int ihi = (s == 0) ? 0 : L - (S - s);
-                        const int R_s = rl32(Rl, s);
-                        const int b = R_s < ihi ? R_s : ihi;
-                        int a = s;
+                    int Rl = 0, Kl = 0;                                 // lane s: R_s, Bk_s
+                    int c = 0, nxt = L;                                 // R_t, Bk_{u+1}
+                    for (int t = 0; t < S; t++) {
+                        const int u = S - 1 - t;
+                        Rl = put_lane(Rl, c, t);
+                        int cn = jhi_of(t), kn = u;
                         if (mem_aware) {
-                            const int inv = uni((int)xrow(s)[nxt]);
-                            a = inv > s ? inv : s;
+                            cn = min((int)jrow(t)[c], cn);             // R_{t+1} = lim(t, R_t)
+                            kn = max((int)xrow(u)[nxt], u);            // Bk_u
                         }
-                        if (a > b) {
-                            feasible = false;
-                            break;
-                        }
-                        Al = put_lane(Al, a, s);
-                        Bl = put_lane(Bl, b, s);
-                        nxt = a;
+                        c = uni(cn);
+                        nxt = uni(kn);
+                        Kl = put_lane(Kl, nxt, u);
                     }
+                    const int ihi = lane == 0 ? 0 : L - (S - lane);
+                    Al = Kl;
+                    Bl = Rl < ihi ? Rl : ihi;
                 }
-                if (!feasible) continue;                               // no split fits memory
+                if (__ballot(lane < S && Al > Bl)) continue;           // no split fits memory
 
                 // ---------------- PartitionLayers: suffix min-max DP over the windows, stages S-1 .. 0
                 // Per-stage constants packed into lanes, one readlane per stage each:

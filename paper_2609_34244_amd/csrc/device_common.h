@@ -98,6 +98,18 @@ template <class T> __device__ __forceinline__ T group_min(T v, int k)
     return v;
 }
 
+// sum over the wavefront, in every lane (pairs across the halves of groups of
+// 2, 4, 8, 16 lanes, then the four rows of 16 through scalar reads)
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v)
+{
+    v += dpp32<kDppXor1>(v);
+    v += dpp32<kDppXor2>(v);
+    v += dpp32<kDppHalfMirror>(v);
+    v += dpp32<kDppMirror>(v);
+    return (uint32_t)rl32((int)v, 0) + (uint32_t)rl32((int)v, 16) + (uint32_t)rl32((int)v, 32) +
+           (uint32_t)rl32((int)v, 48);
+}
+
 // Nearest value with at most 24 significant bits (ties to even) of a
 // non-negative integer below 2^63: its fp32 rounding, kept as an exact integer.
 __device__ __forceinline__ uint64_t rne24(uint64_t x)

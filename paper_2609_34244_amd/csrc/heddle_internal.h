@@ -107,7 +107,9 @@ struct PriceArgs {
     int32_t g_stride;                // LDS entries per pair row (L + 1 and padding)
     int32_t s_cap;                   // stage rows: min(s_max, L)
     int32_t lds_per_wave;            // bytes of one wavefront's LDS region
-    int32_t off_j, off_c;            // byte offsets of the per-stage limit rows and of the type counters
+    int32_t off_j, off_x, off_c;     // byte offsets of the per-stage limit rows, of the inverse-limit
+                                     // rows (shared with the G arena) and of the type counters
+    int32_t arena_cap;               // entries of the G arena
 };
 
 int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,

@@ -84,17 +84,21 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
     const bool mem_aware = (A.flags & HEDDLE_F_COMPUTE_ONLY) == 0;
     const V INF = DPInf<V>::value;
     V2 *X = (V2 *)smem;                                        // [gs] pair row {P_s[j], G_{s+1}[j]}
-    // [s_cap][2][ls] per stage: limit row, then inverse-limit row (later the
-    // next-row table of the second pass)
+    // [s_cap][ls] limit rows; [s_cap][ls] inverse-limit rows, which the second
+    // backward pass later overwrites with next-row tables; the same region, and
+    // what follows it up to the counters, holds the G arena instead when
+    // the template's windows fit it
     uint8_t *JX = smem + A.off_j;
+    uint8_t *IX = smem + A.off_x;
+    V *GA = (V *)IX;
     uint32_t *cnt = (uint32_t *)(smem + A.off_c);              // [n_types] GPU counters of decode
     const V *rows = stage_rows<V>(P, F32);
-    auto jrow = [&](int s) -> uint8_t * { return JX + s * 2 * ls; };
-    auto xrow = [&](int s) -> uint8_t * { return JX + s * 2 * ls + ls; };
+    auto jrow = [&](int s) -> uint8_t * { return JX + s * ls; };
+    auto xrow = [&](int s) -> uint8_t * { return IX + s * ls; };
 
     // limit-row copy: the two rows of a stage are q16 pieces of 16 bytes; lane
     // (su, pc) copies piece pc of stage s0 + su
-    const int q16 = ls >> 3, per = 64 / q16;
+    const int h16 = ls >> 4, q16 = 2 * h16, per = 64 / q16;
     const int su = lane / q16, pc = lane - su * q16;
     int my_m = 1;                                              // lane k: the k-th micro-batch count
     for (int k = 0; k < A.n_m; k++) my_m = lane == k ? A.m[k] : my_m;
@@ -145,8 +149,10 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                     for (int s0 = 0; s0 < S; s0 += per) {
                         const int st = s0 + su;
                         const int row = __shfl(my_row, min(st, 63));
-                        if (su < per && st < S)
-                            *(uint4 *)(JX + st * 2 * ls + pc * 16) = *(const uint4 *)(P.mem_lim + row + pc * 16);
+                        if (su < per && st < S) {
+                            uint8_t *dst = pc < h16 ? JX + st * ls + pc * 16 : IX + st * ls + (pc - h16) * 16;
+                            *(uint4 *)dst = *(const uint4 *)(P.mem_lim + row + pc * 16);
+                        }
                     }
                     wave_sync();
                 }
@@ -175,6 +181,10 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                     Bl = Rl < ihi ? Rl : ihi;
                 }
                 if (__ballot(lane < S && Al > Bl)) continue;           // no split fits memory
+                // G arena: G_s over the rows of W_s for s = S-1 .. 1, stored in that order,
+                // when all of them fit; else the second backward pass rebuilds F
+                const int g_total = uni((int)wave_sum((uint32_t)(lane >= 1 && lane < S ? Bl - Al + 1 : 0)));
+                const bool arena = !COUNT && g_total <= A.arena_cap;
 
                 // ---------------- PartitionLayers: suffix min-max DP over the windows, stages S-1 .. 0
                 // Per-stage constants packed into lanes, one readlane per stage each:
@@ -191,6 +201,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                 RowRegs<V> rr;
                 fetch_rows<V>(rr, rows + uni(rl32(x.prow, S - 1)), uni(rl32(Al, S - 1)), L, lane);
                 V Bv = INF;
+                int goff = 0;                                          // arena index of G_s[a_s]
                 for (int s = S - 1; s >= 0; s--) {
                     const uint32_t ks = uni64(pk, s);
                     const int a = ks & 255, b = (ks >> 8) & 255, e = (ks >> 16) & 255, a_next = ks >> 24;
@@ -211,8 +222,12 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                             const V pL = X[L].x;
                             for (int i = a + lane; i <= b; i += 64) {
                                 const V gv = (V)(pL - X[i].x);
-                                if (s > 0) ((V *)&X[i])[1] = gv;
-                                else Bv = gv;                          // S = 1: row 0, lane 0
+                                if (s > 0) {
+                                    ((V *)&X[i])[1] = gv;
+                                    if (arena) GA[goff + i - a] = gv;
+                                } else {
+                                    Bv = gv;                           // S = 1: row 0, lane 0
+                                }
                             }
                             if (S == 1) Bv = (V)rl64((int64_t)Bv, 0);
                         }
@@ -260,10 +275,14 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                                 Bv = (V)rl64((int64_t)group_min<V>(acc, 64), 0);   // row 0 only
                             } else {
                                 acc = group_min<V>(acc, k);
-                                if (i <= b && part == 0) ((V *)&X[i])[1] = acc;
+                                if (i <= b && part == 0) {
+                                    ((V *)&X[i])[1] = acc;
+                                    if (arena) GA[goff + i - a] = acc;
+                                }
                             }
                         }
                     }
+                    goff += b - a + 1;
                     wave_sync();
                 }
                 if (COUNT) continue;
@@ -272,52 +291,79 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                 const uint64_t B24 = F32 ? rne24(B) : B;       // fp32 bottleneck, as an exact integer
                 auto within = [&](uint64_t T) { return F32 ? rne24(T) <= B24 : T <= B; };
 
-                // ---------------- F_s for stages S-1 .. 1; xrow(s)[i] := the smallest row >= i
-                // of W_s with F_s true (kNone if there is none)
-                for (int s = S - 1; s >= 1; s--) {
-                    const int a = uni(rl32(Al, s)), b = uni(rl32(Bl, s));
-                    const V *prow = rows + uni(rl32(x.prow, s));
-                    const V p2p = (V)uni64(x.p2p, s);
-                    const int a_next = s < S - 1 ? uni(rl32(Al, s + 1)) : L;
-                    const int jhi = jhi_of(s);
-                    const uint8_t *Js = jrow(s);
-                    const uint8_t *NXn = xrow(s + 1);
-                    uint8_t *NXs = xrow(s);
-                    int first_above = kNone;                           // smallest row with F true in higher slots
-                    for (int q = (b - a) >> 6; q >= 0; q--) {
-                        const int i = a + 64 * q + lane;
-                        const int ic = min(i, b);
-                        int nx = L;                                    // last stage: the end is L
-                        bool ok = i <= b;
-                        if (s < S - 1) {
-                            // read unconditionally (lo <= L lies inside the row); an entry past
-                            // hi, or a stale one when lo > hi, is rejected by the tests below
-                            const int lo = max(ic + 1, a_next);
-                            const int hi = mem_aware ? min((int)Js[ic], jhi) : jhi;
-                            nx = NXn[lo];
-                            ok = ok & (lo <= hi) & (nx <= hi);
-                        }
-                        const uint32_t nxc = min(nx, L);
-                        ok = ok & within((uint64_t)(V)(prow[nxc] - prow[(uint32_t)ic] + p2p));
-                        const uint64_t mask = __ballot(ok);
-                        const uint64_t rest = mask >> lane;            // rows >= i of this slot with F true
-                        const int nxi = rest ? i + __ffsll((unsigned long long)rest) - 1 : first_above;
-                        if (i <= b) NXs[i] = (uint8_t)nxi;
-                        if (mask) first_above = a + 64 * q + __ffsll((unsigned long long)mask) - 1;
-                    }
-                    wave_sync();
-                }
-
-                // ---------------- canonical reconstruction: c_{s+1} = nx(c_s)
                 int cs = 0, my_start = 0, my_end = L;
-                for (int s = 0; s < S - 1; s++) {
-                    const int a_next = uni(rl32(Al, s + 1));
-                    const int lo = cs + 1 > a_next ? cs + 1 : a_next;
-                    int nx = uni((int)xrow(s + 1)[lo <= L ? lo : L]);
-                    nx = nx <= L ? nx : L;                             // unreachable: F_s[c_s] holds on the path
-                    my_start = put_lane(my_start, cs, s);
-                    my_end = put_lane(my_end, nx, s);
-                    cs = nx;
+                if (arena) {
+                    // ---------------- canonical reconstruction from the arena: c_{s+1} = the
+                    // smallest row j >= max(c_s + 1, a_{s+1}) of W_{s+1} with G_{s+1}[j] within
+                    // B*. Such a j is admissible from c_s and T(s, c_s, j) is within B*: some
+                    // row with both properties exists (F_s[c_s] holds on the path) and T grows
+                    // with j.
+                    int rem = g_total;                                 // arena index of G_{s+1}[a_{s+1}]
+                    for (int s = 0; s < S - 1; s++) {
+                        const uint32_t k1 = uni64(pk, s + 1);
+                        const int a1 = k1 & 255, b1 = (k1 >> 8) & 255;
+                        rem -= b1 - a1 + 1;
+                        int nx = L;                                    // unreachable: F_s[c_s] holds on the path
+                        for (int j0 = max(cs + 1, a1); j0 <= b1; j0 += 64) {
+                            const int j = j0 + lane;
+                            const V g = GA[rem + min(j, b1) - a1];
+                            const uint64_t mk = __ballot(j <= b1 && g != INF && within((uint64_t)g));
+                            if (mk) {
+                                nx = j0 + __ffsll((unsigned long long)mk) - 1;
+                                break;
+                            }
+                        }
+                        my_start = put_lane(my_start, cs, s);
+                        my_end = put_lane(my_end, nx, s);
+                        cs = nx;
+                    }
+                } else {
+                    // ---------------- F_s for stages S-1 .. 1; xrow(s)[i] := the smallest row >= i
+                    // of W_s with F_s true (kNone if there is none)
+                    for (int s = S - 1; s >= 1; s--) {
+                        const int a = uni(rl32(Al, s)), b = uni(rl32(Bl, s));
+                        const V *prow = rows + uni(rl32(x.prow, s));
+                        const V p2p = (V)uni64(x.p2p, s);
+                        const int a_next = s < S - 1 ? uni(rl32(Al, s + 1)) : L;
+                        const int jhi = jhi_of(s);
+                        const uint8_t *Js = jrow(s);
+                        const uint8_t *NXn = xrow(s + 1);
+                        uint8_t *NXs = xrow(s);
+                        int first_above = kNone;                           // smallest row with F true in higher slots
+                        for (int q = (b - a) >> 6; q >= 0; q--) {
+                            const int i = a + 64 * q + lane;
+                            const int ic = min(i, b);
+                            int nx = L;                                    // last stage: the end is L
+                            bool ok = i <= b;
+                            if (s < S - 1) {
+                                // read unconditionally (lo <= L lies inside the row); an entry past
+                                // hi, or a stale one when lo > hi, is rejected by the tests below
+                                const int lo = max(ic + 1, a_next);
+                                const int hi = mem_aware ? min((int)Js[ic], jhi) : jhi;
+                                nx = NXn[lo];
+                                ok = ok & (lo <= hi) & (nx <= hi);
+                            }
+                            const uint32_t nxc = min(nx, L);
+                            ok = ok & within((uint64_t)(V)(prow[nxc] - prow[(uint32_t)ic] + p2p));
+                            const uint64_t mask = __ballot(ok);
+                            const uint64_t rest = mask >> lane;            // rows >= i of this slot with F true
+                            const int nxi = rest ? i + __ffsll((unsigned long long)rest) - 1 : first_above;
+                            if (i <= b) NXs[i] = (uint8_t)nxi;
+                            if (mask) first_above = a + 64 * q + __ffsll((unsigned long long)mask) - 1;
+                        }
+                        wave_sync();
+                    }
+
+                    // ---------------- canonical reconstruction: c_{s+1} = nx(c_s)
+                    for (int s = 0; s < S - 1; s++) {
+                        const int a_next = uni(rl32(Al, s + 1));
+                        const int lo = cs + 1 > a_next ? cs + 1 : a_next;
+                        int nx = uni((int)xrow(s + 1)[lo <= L ? lo : L]);
+                        nx = nx <= L ? nx : L;                             // unreachable: F_s[c_s] holds on the path
+                        my_start = put_lane(my_start, cs, s);
+                        my_end = put_lane(my_end, nx, s);
+                        cs = nx;
+                    }
                 }
                 my_start = put_lane(my_start, cs, S - 1);      // the last stage ends at L
                 const uint8_t my_layers = lane < S ? (uint8_t)(my_end - my_start) : 0;
@@ -392,16 +438,33 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     const int L = p->dev.L, ls = p->dev.lim_stride;
     a.s_cap = a.s_max < L ? a.s_max : L;
     a.g_stride = L + 5;                                       // L + 1 ends and 4 of padding
-    // per wavefront: one pair row {P_s, G_{s+1}}; per stage its
-    // limit row and its inverse-limit row (later its next-row table); one GPU
-    // counter per type
+    // per wavefront: one pair row {P_s, G_{s+1}}; per stage its limit row; per
+    // stage its inverse-limit row (later its next-row table), a region that the
+    // G arena shares and extends up to the wavefront's share of the CU's LDS at
+    // the occupancy the other parts allow; one GPU counter per type
     const size_t j_off = ((size_t)a.g_stride * 2 * sizeof(V) + 15) & ~size_t(15);
-    const size_t c_off = j_off + (size_t)a.s_cap * 2 * ls;
-    a.off_j = (int32_t)j_off;
-    a.off_c = (int32_t)c_off;
-    a.lds_per_wave = (int32_t)((c_off + (size_t)p->dev.n_types * 4 + 15) & ~size_t(15));
-    int max_lds = 0;
+    const size_t x_off = j_off + (size_t)a.s_cap * ls;
+    const size_t c_bytes = ((size_t)p->dev.n_types * 4 + 15) & ~size_t(15);
+    size_t x_bytes = (size_t)a.s_cap * ls;
+    int max_lds = 0, lds_cu = 0;
     HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
+    HEDDLE_HIP(hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, p->device));
+    if (!COUNT && lds_cu > 0) {
+        const size_t need = x_off + x_bytes + c_bytes;
+        const size_t waves_regs = sizeof(V) == 4 ? 32 : 20;   // wavefronts per CU the registers allow
+        size_t waves = (size_t)lds_cu / need;
+        waves = waves < waves_regs ? waves : waves_regs;
+        if (waves > 0) {
+            const size_t share = ((size_t)lds_cu / waves) & ~size_t(511);   // LDS is allocated in 512-byte blocks
+            if (share > need) x_bytes += (share - need) & ~size_t(15);
+        }
+    }
+    const size_t c_off = x_off + x_bytes;
+    a.off_j = (int32_t)j_off;
+    a.off_x = (int32_t)x_off;
+    a.off_c = (int32_t)c_off;
+    a.arena_cap = (int32_t)(x_bytes / sizeof(V));
+    a.lds_per_wave = (int32_t)(c_off + c_bytes);
     // one wavefront per workgroup: a wavefront's LDS is released as soon as it
     // is done, whatever the other wavefronts on the CU are doing
     const int wpb = 1;

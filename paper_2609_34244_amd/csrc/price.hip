@@ -159,26 +159,23 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
 
                 // ---------------- row windows: lane s holds [a_s, b_s]
                 // the forward reach R_s and the backward bound Bk_s are independent
-                // pointer chases over the limit rows; one loop takes a step of each
-                int Al, Bl;
-                {
-                    int Rl = 0, Kl = 0;                                 // lane s: R_s, Bk_s
+                // pointer chases over the limit rows; one loop takes a step of each (the
+                // chased values stay in vector registers, equal in every lane)
+                // (compute-only: Bk_s = s and R_s = L - (S - s) for s >= 1)
+                int Al = lane, Bl = L;                                  // lane s: Bk_s, R_s
+                if (mem_aware) {
                     int c = 0, nxt = L;                                 // R_t, Bk_{u+1}
                     for (int t = 0; t < S; t++) {
                         const int u = S - 1 - t;
-                        Rl = put_lane(Rl, c, t);
-                        int cn = jhi_of(t), kn = u;
-                        if (mem_aware) {
-                            cn = min((int)jrow(t)[c], cn);             // R_{t+1} = lim(t, R_t)
-                            kn = max((int)xrow(u)[nxt], u);            // Bk_u
-                        }
-                        c = uni(cn);
-                        nxt = uni(kn);
-                        Kl = put_lane(Kl, nxt, u);
+                        Bl = lane == t ? c : Bl;
+                        c = min((int)jrow(t)[c], jhi_of(t));           // R_{t+1} = lim(t, R_t)
+                        nxt = max((int)xrow(u)[nxt], u);               // Bk_u
+                        Al = lane == u ? nxt : Al;
                     }
+                }
+                {
                     const int ihi = lane == 0 ? 0 : L - (S - lane);
-                    Al = Kl;
-                    Bl = Rl < ihi ? Rl : ihi;
+                    Bl = Bl < ihi ? Bl : ihi;
                 }
                 if (__ballot(lane < S && Al > Bl)) continue;           // no split fits memory
                 // G arena: G_s over the rows of W_s for s = S-1 .. 1, stored in that order,
@@ -291,7 +288,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                 const uint64_t B24 = F32 ? rne24(B) : B;       // fp32 bottleneck, as an exact integer
                 auto within = [&](uint64_t T) { return F32 ? rne24(T) <= B24 : T <= B; };
 
-                int cs = 0, my_start = 0, my_end = L;
+                int cs = 0, my_end = L;                                // lane s < S-1: c_{s+1}
                 if (arena) {
                     // ---------------- canonical reconstruction from the arena: c_{s+1} = the
                     // smallest row j >= max(c_s + 1, a_{s+1}) of W_{s+1} with G_{s+1}[j] within
@@ -303,19 +300,17 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         const uint32_t k1 = uni64(pk, s + 1);
                         const int a1 = k1 & 255, b1 = (k1 >> 8) & 255;
                         rem -= b1 - a1 + 1;
-                        int nx = L;                                    // unreachable: F_s[c_s] holds on the path
-                        for (int j0 = max(cs + 1, a1); j0 <= b1; j0 += 64) {
+                        int j0 = max(cs + 1, a1);
+                        uint64_t mk;
+                        for (;;) {
                             const int j = j0 + lane;
                             const V g = GA[rem + min(j, b1) - a1];
-                            const uint64_t mk = __ballot(j <= b1 && g != INF && within((uint64_t)g));
-                            if (mk) {
-                                nx = j0 + __ffsll((unsigned long long)mk) - 1;
-                                break;
-                            }
+                            mk = __ballot(j <= b1 && (F32 ? g != INF && within((uint64_t)g) : (uint64_t)g <= B));
+                            if (mk || j0 + 64 > b1) break;
+                            j0 += 64;
                         }
-                        my_start = put_lane(my_start, cs, s);
-                        my_end = put_lane(my_end, nx, s);
-                        cs = nx;
+                        cs = mk ? j0 + __ffsll((unsigned long long)mk) - 1 : L;   // L: unreachable
+                        my_end = lane == s ? cs : my_end;
                     }
                 } else {
                     // ---------------- F_s for stages S-1 .. 1; xrow(s)[i] := the smallest row >= i
@@ -360,12 +355,12 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         const int lo = cs + 1 > a_next ? cs + 1 : a_next;
                         int nx = uni((int)xrow(s + 1)[lo <= L ? lo : L]);
                         nx = nx <= L ? nx : L;                             // unreachable: F_s[c_s] holds on the path
-                        my_start = put_lane(my_start, cs, s);
                         my_end = put_lane(my_end, nx, s);
                         cs = nx;
                     }
                 }
-                my_start = put_lane(my_start, cs, S - 1);      // the last stage ends at L
+                // lane s: c_s (c_0 = 0)
+                const int my_start = __builtin_amdgcn_update_dpp(0, my_end, kDppWaveShr1, 0xF, 0xF, false);
                 const uint8_t my_layers = lane < S ? (uint8_t)(my_end - my_start) : 0;
                 for (uint64_t c = cls; c; c &= c - 1) {            // s_max <= 64: a lane per stage
                     const int k = __ffsll((unsigned long long)c) - 1;

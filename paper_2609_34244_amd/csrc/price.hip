@@ -134,7 +134,8 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
             uint64_t todo = __ballot(lane < A.n_m);
 
             while (todo) {
-                const int key = uni((int)group_min<uint32_t>(((todo >> lane) & 1) ? (uint32_t)key_k : 0x7FFFFFFFu, 64));
+                const int key = A.n_m == 1 ? uni(key_k)
+                                           : uni((int)group_min<uint32_t>(((todo >> lane) & 1) ? (uint32_t)key_k : 0x7FFFFFFFu, 64));
                 const uint64_t cls = __ballot(lane < A.n_m && key_k == key) & todo;
                 todo &= ~cls;
                 auto jhi_of = [&](int s) { return L - (S - 1 - s); };   // last end leaving a layer per later stage

@@ -451,7 +451,8 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
         size_t waves = (size_t)lds_cu / need;
         waves = waves < waves_regs ? waves : waves_regs;
         if (waves > 0) {
-            const size_t share = ((size_t)lds_cu / waves) & ~size_t(511);   // LDS is allocated in 512-byte blocks
+            size_t share = ((size_t)lds_cu / waves) & ~size_t(511);   // LDS is allocated in 512-byte blocks
+            share = share < (size_t)max_lds ? share : ((size_t)max_lds & ~size_t(15));
             if (share > need) x_bytes += (share - need) & ~size_t(15);
         }
     }

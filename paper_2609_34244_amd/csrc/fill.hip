@@ -15,7 +15,8 @@
 //
 // Mapping: one lane per template (64 templates per wavefront). Each lane keeps
 // its type's counts in an LDS column of its own ([free GPUs][lane]), so every
-// LDS access of a wavefront hits 64 distinct banks.
+// LDS access of a wavefront hits 64 distinct banks; the 64 templates' records
+// are read once, coalesced, into LDS columns by stage ([stage][lane]).
 //
 // Micro-batch size: each size has its own profile (profile entries are keyed
 // by GPU type, TP degree and micro-batch size, section 5.2); every template is
@@ -45,38 +46,68 @@ __global__ void __launch_bounds__(64) fill_dp_kernel(const int32_t *counts, int 
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x;
     uint32_t *cnt = (uint32_t *)smem + lane;                   // [max_gpus + 1][64]: this lane's column
+    uint32_t *rc = (uint32_t *)smem + (max_gpus + 1) * 64;     // [s_max][64]: the block's records, by stage
     auto C = [&](int b) -> uint32_t & { return cnt[b * 64]; };
-    for (int64_t t = (int64_t)blockIdx.x * 64 + lane; t < n; t += (int64_t)gridDim.x * 64) {
+    uint8_t *lst = (uint8_t *)(rc + s_max * 64) + lane;        // [s_max][64]: one type's TP degrees
+    auto R = [&](int s) -> uint32_t { return rc[s * 64 + lane]; };
+    for (int64_t t0 = (int64_t)blockIdx.x * 64; t0 < n; t0 += (int64_t)gridDim.x * 64) {
+        // the records of the block's 64 templates, read coalesced and stored by stage
+        const int nt = n - t0 < 64 ? (int)(n - t0) : 64;
+        const uint32_t *src = stages + t0 * s_max;
+        __syncthreads();
+        for (int d = lane; d < nt * s_max; d += 64) {
+            const int q = d / s_max;
+            rc[(d - q * s_max) * 64 + q] = src[d];
+        }
+        __syncthreads();
+        const int64_t t = t0 + lane;
+        if (t >= n) continue;
         const int S = n_stages[t];
-        uint32_t *rec = stages + t * s_max;
         int D = 0;
         bool ok = S >= 1 && S <= s_max;
         int max_ep = 1;
         for (int s = 0; s < S && ok; s++) {
-            const uint32_t r = rec[s];
+            const uint32_t r = R(s);
             ok = (int)(r & 0xFF) < n_types && ((r >> 8) & 15) <= 6;
             max_ep = max(max_ep, 1 << ((r >> 12) & 15));
         }
         if (ok) {
             D = dp_cap;
+            uint64_t done = 0;                                 // stages whose type is packed
             for (int s = 0; s < S && D > 0; s++) {
-                const int g = rec[s] & 0xFF;
-                bool seen = false;                             // each type once, at its first stage
-                for (int s2 = 0; s2 < s; s2++) seen |= (int)(rec[s2] & 0xFF) == g;
-                if (seen) continue;
-                for (int b = 0; b <= max_gpus; b++) C(b) = (uint32_t)counts[g * 65 + b];
+                if ((done >> s) & 1) continue;                 // each type once, at its first stage
+                const int g = R(s) & 0xFF;
+                // the TP degrees (log2) of this type's stages, in stage order
+                int k = 0;
+                for (int s2 = s; s2 < S; s2++) {
+                    const uint32_t r2 = R(s2);
+                    if ((int)(r2 & 0xFF) != g) continue;
+                    lst[k++ * 64] = (uint8_t)((r2 >> 8) & 15);
+                    done |= 1ull << s2;
+                }
+                // counts per number of free GPUs, and a bit (b - 1) for every b >= 1 with
+                // nodes of b free GPUs: the node a group of tp takes is the lowest set bit
+                // at or above tp - 1
+                uint64_t avail = 0;
+                for (int b = 0; b <= max_gpus; b++) {
+                    const uint32_t cb = (uint32_t)counts[g * 65 + b];
+                    C(b) = cb;
+                    if (b > 0 && cb) avail |= 1ull << (b - 1);
+                }
                 int r = 0;
                 while (r < D) {
                     bool placed = true;
-                    for (int s2 = s; s2 < S && placed; s2++) {
-                        if ((int)(rec[s2] & 0xFF) != g) continue;
-                        const int tp = 1 << ((rec[s2] >> 8) & 15);
-                        int b = tp;
-                        while (b <= max_gpus && C(b) == 0) b++;
-                        placed = b <= max_gpus;
+                    for (int q = 0; q < k && placed; q++) {
+                        const int tp = 1 << lst[q * 64];
+                        const uint64_t up = avail >> (tp - 1);
+                        placed = up != 0;
                         if (placed) {
-                            C(b) -= 1;
-                            C(b - tp) += 1;
+                            const int b = tp + __ffsll((unsigned long long)up) - 1;
+                            if (--C(b) == 0) avail &= ~(1ull << (b - 1));
+                            if (b > tp) {
+                                C(b - tp) += 1;
+                                avail |= 1ull << (b - tp - 1);
+                            }
                         }
                     }
                     if (!placed) break;
@@ -85,7 +116,8 @@ __global__ void __launch_bounds__(64) fill_dp_kernel(const int32_t *counts, int 
                 D = r < D ? r : D;
             }
             D = D / max_ep * max_ep;
-            for (int s = 0; s < S; s++) rec[s] = (rec[s] & 0xFFFFu) | ((uint32_t)D << 16);
+            uint32_t *rec = stages + t * s_max;
+            for (int s = 0; s < S; s++) rec[s] = (R(s) & 0xFFFFu) | ((uint32_t)D << 16);
         }
         dp_out[t] = D;
     }
@@ -139,7 +171,7 @@ static int launch_fill_dp(const heddle_cluster *c, int64_t n, int32_t s_max, con
                           uint32_t *d_stages, int32_t dp_cap, int32_t *d_dp, hipStream_t stream)
 {
     if (n == 0) return HEDDLE_OK;
-    const size_t lds = (size_t)(c->max_gpus + 1) * 64 * 4;
+    const size_t lds = ((size_t)(c->max_gpus + 1) + (size_t)s_max) * 64 * 4 + (size_t)s_max * 64;
     const int64_t want = (n + 63) / 64;
     const int blocks = (int)(want < 65536 ? want : 65536);
     hipLaunchKernelGGL(fill_dp_kernel, dim3(blocks), dim3(64), lds, stream, (const int32_t *)c->counts, c->n_types,

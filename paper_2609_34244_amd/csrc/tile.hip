@@ -41,6 +41,12 @@ namespace heddle {
 
 constexpr uint64_t kNoLayout = ~0ull;
 
+// per-stage constants of the layout pricing, one LDS record per stage
+struct StageK {
+    int64_t W, cap, bw, T0, n_moe, dstate, act_b, inflight, g_dense;
+    int32_t g, ki, node, i0, j0, pad;
+};
+
 __device__ __forceinline__ void wave_min_pair(uint64_t &a, uint64_t &b)
 {
 #pragma unroll
@@ -65,10 +71,17 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
     int64_t *cM = (int64_t *)(cG + (size_t)A.s_cap * Fp);      // [s_cap][Fp] memory
     uint8_t *cC = (uint8_t *)(cM + (size_t)A.s_cap * Fp);      // [s_cap][Fp] layout index of a kept entry
     uint8_t *cN = cC + (size_t)A.s_cap * Fp;                   // [s_cap] kept layouts of a stage
+    const size_t sk_off = ((size_t)A.s_cap * Fp * 25 + A.s_cap + 15) & ~size_t(15);
+    StageK *SK = (StageK *)(smem + sk_off);                    // [s_cap]
+    uint8_t *tS = (uint8_t *)(SK + A.s_cap);                   // [s_cap * Fp] stage of a threshold entry
+    uint8_t *tJ = tS + (size_t)A.s_cap * Fp;                   // [s_cap * Fp] its index among the stage's kept
     const int64_t total = A.n * A.n_m;
+    // slot q -> stage q / F as a high product with ceil(2^32 / F), exact for
+    // q * F < 2^32 (here q < s_cap * F <= 255 * 256); F = 1 maps q to itself
+    const uint32_t invF = F > 1 ? (uint32_t)(0xFFFFFFFFu / (uint32_t)F) + 1u : 0u;
 
     for (int64_t o = blockIdx.x; o < total; o += gridDim.x) {
-        const int64_t t = o / A.n_m;
+        const int64_t t = A.n_m == 1 ? o : o / A.n_m;
         const int k = (int)(o - t * A.n_m);
         const int st_in = A.status[o];
         const bool has_split = (st_in == HEDDLE_S_OK || st_in == HEDDLE_S_OOM) && A.layers[o * A.s_max] > 0;
@@ -121,85 +134,114 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
 
         // ---- lanes = (stage, layout) slots q = s * F + c: price every layout
         wave_sync();                                           // the previous plan's table reads are done
+        if (act) {
+            StageK &sk = SK[lane];
+            sk.W = W; sk.cap = cap; sk.bw = bw; sk.T0 = (int64_t)T0; sk.n_moe = n_moe; sk.dstate = dstate;
+            sk.act_b = act_b; sk.inflight = inflight; sk.g_dense = g_dense;
+            sk.g = g; sk.ki = ki; sk.node = node; sk.i0 = i0; sk.j0 = j0;
+        }
+        wave_sync();
         const int n_cand = S * F;
         for (int q0 = 0; q0 < n_cand; q0 += 64) {
             const int q = q0 + lane;
-            const int s = q < n_cand ? q / F : 0, c = q - s * F;
-            // the stage's constants, from its lane
-            const int sg = __shfl(g, s), ski = __shfl(ki, s), snode = __shfl(node, s);
-            const int si0 = __shfl(i0, s), sj0 = __shfl(j0, s);
-            auto sh64 = [&](int64_t v) { return (int64_t)__shfl((long long)v, s); };
-            const int64_t sW = sh64(W), scap = sh64(cap), sbw = sh64(bw);
-            const uint64_t sT0 = (uint64_t)sh64((int64_t)T0);
-            const int64_t smoe = sh64(n_moe), sdst = sh64(dstate), sact = sh64(act_b);
-            const int64_t sinf = sh64(inflight), sgd = sh64(g_dense);
             if (q < n_cand) {
+                const int s = F > 1 ? (int)__umulhi((uint32_t)q, invF) : q, c = q - s * F;
+                const StageK &sk = SK[s];
+                const int sg = sk.g, ski = sk.ki, snode = sk.node, si0 = sk.i0, sj0 = sk.j0;
                 const int ei = c / K, ti = c - ei * K;
-                const int e = 1 << nibble(P.ep_log2, ei), et = 1 << nibble(P.tp_log2, ti);
-                const int64_t group = (int64_t)e * et;
-                const bool allowed = P.profiled[sg * K + ti] && et <= snode && (sW % group) == 0;
+                const int l2e = nibble(P.ep_log2, ei), l2t = nibble(P.tp_log2, ti);
+                const int et = 1 << l2t;
+                const int64_t gmask = ((int64_t)1 << (l2e + l2t)) - 1;    // EP x ETP, a power of two
+                const bool allowed = P.profiled[sg * K + ti] && et <= snode && (sk.W & gmask) == 0;
                 const int64_t *xd = P.xdelta + ((size_t)(sg * K + ski) * K + ti) * R;
-                const uint64_t T = sT0 + (uint64_t)(xd[sj0] - xd[si0]) +
-                                   (uint64_t)(smoe * P.a2a_ns[sg * 3 + a2a_variant(e, et, snode)]);
+                const uint64_t T = (uint64_t)sk.T0 + (uint64_t)(xd[sj0] - xd[si0]) +
+                                   (uint64_t)(sk.n_moe * P.a2a_ns[sg * 3 + a2a_variant(1 << l2e, et, snode)]);
                 const int64_t *xs = P.pre_xstate + (size_t)(ti * E + ei) * R;
-                const int64_t mem = sdst + (xs[sj0] - xs[si0]) + sinf * sact;
+                const int64_t mem = sk.dstate + (xs[sj0] - xs[si0]) + sk.inflight * sk.act_b;
                 const int64_t *xg = P.pre_xgrad + (size_t)(ti * E + ei) * R;
-                const int64_t edp = allowed ? sW / group : 1;
-                const int64_t gs = sgd + allreduce_ns(xg[sj0] - xg[si0], edp, sbw);
+                const int64_t edp = allowed ? sk.W >> (l2e + l2t) : 1;
+                const int64_t gs = sk.g_dense + allreduce_ns(xg[sj0] - xg[si0], edp, sk.bw);
                 const int qs = s * Fp + c;
-                cT[qs] = allowed && mem <= scap ? T : kNoLayout;
+                cT[qs] = allowed && mem <= sk.cap ? T : kNoLayout;
                 cG[qs] = (uint64_t)gs;
                 cM[qs] = mem;
             }
         }
         wave_sync();
 
-        // ---- lanes = stages: keep the layouts no other beats in both time and
-        // synchronisation (the first listed among equals), in place at the front
-        // of the stage's row; only these can be a stage's fastest layout under a
-        // bound on the synchronisation, and only their synchronisation values
-        // need to be tried as bounds
-        if (act) {
-            const int rb = lane * Fp;
-            int nf = 0;
-            for (int c = 0; c < F; c++) {
-                const uint64_t x = cT[rb + c], y = cG[rb + c];
-                const int64_t mx = cM[rb + c];
-                if (x == kNoLayout) continue;
-                bool beaten = false;
-                for (int j = 0; j < nf; j++) beaten |= cT[rb + j] <= x && cG[rb + j] <= y;
-                if (beaten) continue;
-                int w = 0;
-                for (int j = 0; j < nf; j++) {
-                    const uint64_t tj = cT[rb + j], gj = cG[rb + j];
-                    const bool drop = x <= tj && y <= gj && (x < tj || y < gj);
-                    if (!drop) {
-                        cT[rb + w] = tj;
-                        cG[rb + w] = gj;
-                        cM[rb + w] = cM[rb + j];
-                        cC[rb + w] = cC[rb + j];
-                        w++;
-                    }
-                }
-                cT[rb + w] = x;
-                cG[rb + w] = y;
-                cM[rb + w] = mx;
-                cC[rb + w] = (uint8_t)c;
-                nf = w + 1;
+        // ---- lanes = (stage, layout) slots again: a layout is kept when no other
+        // layout of its stage beats it in both time and synchronisation (an earlier
+        // one also by being equal in both); only these can be a stage's fastest
+        // layout under a bound on the synchronisation, and only their
+        // synchronisation values need to be tried as bounds. The kept layouts move
+        // to the front of their stage's row in layout order (a slot's new place is
+        // at or before its old one, so no row entry is overwritten before it is read).
+        uint8_t *kf = tS;                                      // [n_cand] kept flags, by slot
+        for (int q0 = 0; q0 < n_cand; q0 += 64) {
+            const int q = q0 + lane;
+            const bool in = q < n_cand;
+            const int s = !in ? 0 : F > 1 ? (int)__umulhi((uint32_t)q, invF) : q, c = in ? q - s * F : 0;
+            const int rb = s * Fp;
+            const uint64_t x = in ? cT[rb + c] : kNoLayout, y = in ? cG[rb + c] : 0;
+            bool keep = x != kNoLayout;
+            for (int c2 = 0; c2 < F; c2++) {
+                const uint64_t x2 = cT[rb + c2], y2 = cG[rb + c2];
+                keep = keep && !(c2 != c && x2 <= x && y2 <= y && (c2 < c || x2 < x || y2 < y));
             }
-            cN[lane] = (uint8_t)nf;
+            if (in) kf[q] = (uint8_t)keep;
+        }
+        wave_sync();
+        for (int q0 = 0; q0 < n_cand; q0 += 64) {
+            const int q = q0 + lane;
+            const bool in = q < n_cand;
+            const int s = !in ? 0 : F > 1 ? (int)__umulhi((uint32_t)q, invF) : q, c = in ? q - s * F : 0;
+            const int rb = s * Fp;
+            const bool keep = in && kf[q];
+            int rank = 0, tot = 0;
+            for (int c2 = 0; c2 < F; c2++) {
+                const int f = kf[s * F + c2];
+                rank += c2 < c ? f : 0;
+                tot += f;
+            }
+            const uint64_t x = cT[rb + c], y = cG[rb + c];
+            const int64_t mx = cM[rb + c];
+            wave_sync();
+            if (keep) {
+                cT[rb + rank] = x;
+                cG[rb + rank] = y;
+                cM[rb + rank] = mx;
+                cC[rb + rank] = (uint8_t)c;
+            }
+            if (in && c == 0) cN[s] = (uint8_t)tot;
+            wave_sync();
+        }
+        // threshold list: every kept layout of every stage, (stage, index) per entry
+        int n_thr = 0;
+        {
+            const int nfl = act ? cN[lane] : 0;
+            int off = nfl;                                     // exclusive scan of the kept counts
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const int u = __shfl_up(off, d);
+                off += lane >= d ? u : 0;
+            }
+            n_thr = __shfl(off, 63);
+            off -= nfl;
+            for (int j = 0; j < nfl; j++) {
+                tS[off + j] = (uint8_t)lane;
+                tJ[off + j] = (uint8_t)j;
+            }
         }
         wave_sync();
 
         // ---- lanes = frontier layouts as thresholds G: the plan's iteration time
         // with every stage at its fastest kept layout of synchronisation <= G
         uint64_t best_it = kNoLayout, best_G = kNoLayout;
-        for (int q0 = 0; q0 < n_cand; q0 += 64) {
+        for (int q0 = 0; q0 < n_thr; q0 += 64) {
             const int q = q0 + lane;
-            const int s = q < n_cand ? q / F : 0, j = q - s * F;
             uint64_t it = kNoLayout, G = kNoLayout;
-            if (q < n_cand && j < cN[s]) {
-                G = cG[s * Fp + j];
+            if (q < n_thr) {
+                G = cG[tS[q] * Fp + tJ[q]];
                 uint64_t maxT = 0, sumT = 0, maxg = 0;
                 bool ok = true;
                 for (int s2 = 0; s2 < S && ok; s2++) {
@@ -263,7 +305,10 @@ int launch_tile(const heddle_profile *p, const PriceArgs &a, uint8_t *tiling, hi
     const int64_t total = a.n * a.n_m;
     if (total == 0) return HEDDLE_OK;
     const size_t F = (size_t)p->dev.n_tp * p->dev.n_ep;
-    const size_t lds = (size_t)a.s_cap * (F | 1) * 25 + a.s_cap;
+    // layout tables (time, synchronisation, memory: 8 bytes each; layout index),
+    // kept counts, per-stage constants, threshold list (stage, index)
+    const size_t lds = (((size_t)a.s_cap * (F | 1) * 25 + a.s_cap + 15) & ~size_t(15)) + (size_t)a.s_cap * sizeof(StageK) +
+                       (size_t)a.s_cap * (F | 1) * 2;
     int max_lds = 0;
     HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
     if (lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "layout table of this (s_max, n_tp, n_ep) does not fit in LDS");

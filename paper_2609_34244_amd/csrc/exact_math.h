@@ -15,7 +15,9 @@ namespace heddle {
 
 // ceil(x * a / d) for x < 2^51, a < 2^28, 1 <= d < 2^50; the result is below
 // 2^62. gfx950 has no integer divider and a 128-bit division expands to a
-// bit-serial loop, so the quotient is estimated in fp64 and corrected exactly:
+// bit-serial loop, so the quotient is estimated in fp64 and corrected exactly.
+// When x * a + d - 1 < 2^53 one fp64 division and one correction step do;
+// otherwise:
 // the first estimate is within 2^11 of the true quotient (relative error of
 // the fp64 operands and division is below 2^-51 and the quotient below 2^62),
 // which leaves a remainder |r| < 2^12 d < 2^62 that fits int64; the second
@@ -23,6 +25,17 @@ namespace heddle {
 HEDDLE_HD uint64_t ceil_muldiv(uint64_t x, uint64_t a, uint64_t d)
 {
     const unsigned __int128 n = (unsigned __int128)x * a + (d - 1);     // ceil -> floor
+    if ((uint64_t)(n >> 53) == 0) {
+        // n and d are exact doubles; the correctly rounded quotient lies within
+        // one of floor(n / d) (within half of n / d, and n / d < 2^53), and one
+        // exact step on the remainder r = n - q d, |r| < 2d, corrects it
+        const uint64_t nl = (uint64_t)n;
+        int64_t q = (int64_t)((double)nl / (double)d);
+        const int64_t r = (int64_t)(nl - (uint64_t)q * d);
+        if (r < 0) q -= 1;
+        else if (r >= (int64_t)d) q += 1;
+        return (uint64_t)q;
+    }
     const double dd = (double)d;
     const double nd = (double)(uint64_t)(n >> 64) * 18446744073709551616.0 + (double)(uint64_t)n;
     int64_t q = (int64_t)(nd / dd);

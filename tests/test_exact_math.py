@@ -1,6 +1,7 @@
 """Host check of the library's exact ceil(x * a / d) helper (fp64 estimate
 plus exact correction) against 128-bit integer division, on random and edge
-operands across its documented range. CPU only."""
+operands across its documented range, on both of its paths (products below
+2^53 and above) and around the boundary between them. CPU only."""
 import os
 import subprocess
 
@@ -40,6 +41,25 @@ int main(void) {
         if (q >= ((u128)1 << 62)) continue;
         bad += check(x, a, d); n++;
         if (bad > 5) break;
+    }
+    /* products below 2^53 (the one-division path) and around that boundary */
+    for (long t = 0; t < 2000000 && bad <= 5; t++) {
+        uint64_t a = (rnd(&s) & AM) | 1, d = (rnd(&s) >> (rnd(&s) % 63)) & DM;
+        if (d == 0) d = 1 + (rnd(&s) & 0xFFFF);
+        uint64_t lim = ((1ull << 53) - d) / a;                 /* x * a + d - 1 < 2^53 */
+        uint64_t x = lim ? rnd(&s) % (lim + 1) : 0;
+        if (t % 4 == 0) x = lim;
+        if (t % 4 == 1 && x > 0) x = rnd(&s) % (x >> (rnd(&s) % 40) | 1);
+        if (x > XM) continue;
+        bad += check(x, a, d); n++;
+    }
+    for (uint64_t dd = 1; dd < 40 && bad <= 5; dd++) {
+        const uint64_t d = dd * 977 + (dd & 1);
+        for (int64_t off = -3; off <= 3; off++) {
+            const uint64_t target = (1ull << 53) + off;          /* n = x * a + d - 1 near 2^53 */
+            if (target < d - 1) continue;
+            bad += check(target - (d - 1), 1, d); n++;
+        }
     }
     printf("checked %ld bad %d\n", n, bad);
     return bad != 0;

@@ -36,16 +36,16 @@ namespace heddle {
 
 // Time prefix of one stage over the entries [a, e], fetched into registers
 // ahead of use (slots of 64 entries; lanes past e repeat entry e).
-constexpr int kRowSlots = 4;                       // (L + 1) <= 256 entries
-template <class V> struct RowRegs {
-    V p[kRowSlots];
+// NS slots: 2 when L + 1 <= 128, else 4 ((L + 1) <= 256 entries)
+template <class V, int NS> struct RowRegs {
+    V p[NS];
 };
 
-template <class V>
-__device__ __forceinline__ void fetch_rows(RowRegs<V> &r, const V *prow, int a, int e, int lane)
+template <class V, int NS>
+__device__ __forceinline__ void fetch_rows(RowRegs<V, NS> &r, const V *prow, int a, int e, int lane)
 {
 #pragma unroll
-    for (int q = 0; q < kRowSlots; q++)
+    for (int q = 0; q < NS; q++)
         if (64 * q <= e - a) r.p[q] = prow[(uint32_t)min(a + lane + 64 * q, e)];     // uniform condition
 }
 
@@ -73,7 +73,7 @@ __device__ __forceinline__ void fetch_rows(RowRegs<V> &r, const V *prow, int a, 
 // smallest admissible end keeping an optimal completion at every stage, i.e.
 // the lexicographically smallest optimal split.
 
-template <class V, bool F32, bool COUNT>
+template <class V, bool F32, bool COUNT, int NS>
 __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevProfile P, PriceArgs A)
 {
     typedef typename Vec2<V>::type V2;
@@ -196,8 +196,8 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                                     ((uint32_t)(last ? L : An) << 24);
                 const uint32_t prv = (uint32_t)__builtin_amdgcn_update_dpp(
                     0, (int)((uint32_t)x.prow | ((uint32_t)Al << 24)), kDppWaveShr1, 0xF, 0xF, false);
-                RowRegs<V> rr;
-                fetch_rows<V>(rr, rows + uni(rl32(x.prow, S - 1)), uni(rl32(Al, S - 1)), L, lane);
+                RowRegs<V, NS> rr;
+                fetch_rows<V, NS>(rr, rows + uni(rl32(x.prow, S - 1)), uni(rl32(Al, S - 1)), L, lane);
                 V Bv = INF;
                 int goff = 0;                                          // arena index of G_s[a_s]
                 for (int s = S - 1; s >= 0; s--) {
@@ -205,11 +205,11 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                     const int a = ks & 255, b = (ks >> 8) & 255, e = (ks >> 16) & 255, a_next = ks >> 24;
                     // P_s into the pair row over [a, e]; G_{s+1} stays in place
 #pragma unroll
-                    for (int q = 0; q < kRowSlots; q++)
+                    for (int q = 0; q < NS; q++)
                         if (64 * q <= e - a) ((V *)&X[min(a + lane + 64 * q, e)])[0] = rr.p[q];
                     if (s > 0) {
                         const uint32_t kp = uni64(prv, s);
-                        fetch_rows<V>(rr, rows + (kp & 0xFFFFFFu), (int)(kp >> 24), b, lane);
+                        fetch_rows<V, NS>(rr, rows + (kp & 0xFFFFFFu), (int)(kp >> 24), b, lane);
                     }
                     wave_sync();
                     if (s == S - 1) {
@@ -468,11 +468,16 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     const size_t lds = (size_t)wpb * a.lds_per_wave;
     if (lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "DP table of this (L, s_max) does not fit in LDS");
     if (lds > 65536)
-        HEDDLE_HIP(hipFuncSetAttribute((const void *)split_kernel<V, F32, COUNT>,
+        HEDDLE_HIP(hipFuncSetAttribute(L + 1 <= 128 ? (const void *)split_kernel<V, F32, COUNT, 2>
+                                                   : (const void *)split_kernel<V, F32, COUNT, 4>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
     const int64_t want = (a.n + wpb - 1) / wpb;
     const int blocks = (int)(want < 65536 ? want : 65536);
-    hipLaunchKernelGGL((split_kernel<V, F32, COUNT>), dim3(blocks), dim3(64 * wpb), lds, stream, p->dev, a);
+    // time-prefix slots of 64 entries held in registers: 2 cover L + 1 <= 128
+    if (L + 1 <= 128)
+        hipLaunchKernelGGL((split_kernel<V, F32, COUNT, 2>), dim3(blocks), dim3(64 * wpb), lds, stream, p->dev, a);
+    else
+        hipLaunchKernelGGL((split_kernel<V, F32, COUNT, 4>), dim3(blocks), dim3(64 * wpb), lds, stream, p->dev, a);
     HEDDLE_HIP(hipGetLastError());
     return HEDDLE_OK;
 }

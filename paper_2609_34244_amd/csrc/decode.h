@@ -45,12 +45,12 @@ __device__ StageInfo<V> decode(const DevProfile &P, const PriceArgs &A, int S, u
     const int64_t p2p = F32 ? P.p2p_fx[gc * N + gn] : P.p2p_ns[gc * N + gn];
 
     if (x.S < 1 || x.S > A.s_max || x.S > L) { x.status = HEDDLE_S_BAD_SHAPE; return x; }
-    if (__ballot(act && g >= N)) { x.status = HEDDLE_S_BAD_TYPE; return x; }
-    if (__ballot(act && (!((P.tp_present >> l2tp) & 1) || tp > node))) { x.status = HEDDLE_S_BAD_TP; return x; }
-    if (__ballot(act && !prof)) { x.status = HEDDLE_S_UNPROFILED; return x; }
+    if (ballot(act && g >= N)) { x.status = HEDDLE_S_BAD_TYPE; return x; }
+    if (ballot(act && (!((P.tp_present >> l2tp) & 1) || tp > node))) { x.status = HEDDLE_S_BAD_TP; return x; }
+    if (ballot(act && !prof)) { x.status = HEDDLE_S_UNPROFILED; return x; }
     x.D = rl32(dpv, 0);
-    if (__ballot(act && (dpv < 1 || dpv != x.D))) { x.status = HEDDLE_S_BAD_DP; return x; }
-    if (__ballot(act && (!((P.ep_present >> l2ep) & 1) || ((uint32_t)x.D % (uint32_t)ep) != 0))) {
+    if (ballot(act && (dpv < 1 || dpv != x.D))) { x.status = HEDDLE_S_BAD_DP; return x; }
+    if (ballot(act && (!((P.ep_present >> l2ep) & 1) || ((uint32_t)x.D % (uint32_t)ep) != 0))) {
         x.status = HEDDLE_S_BAD_EP;
         return x;
     }
@@ -62,7 +62,7 @@ __device__ StageInfo<V> decode(const DevProfile &P, const PriceArgs &A, int S, u
     if (act) atomicAdd(&cnt[g], (uint32_t)tp);
     wave_sync();
     const uint32_t used = act ? cnt[g] : 0u;
-    if (__ballot(act && (int64_t)used * x.D > ngpu)) { x.status = HEDDLE_S_OVERSUBSCRIBED; return x; }
+    if (ballot(act && (int64_t)used * x.D > ngpu)) { x.status = HEDDLE_S_OVERSUBSCRIBED; return x; }
 
     if (act) {
         x.prow = ((g * P.n_tp + ki) * 3 + a2a_variant(ep, tp, node)) * R;

@@ -47,6 +47,9 @@ template <class T> __device__ __forceinline__ T wave_max(T v)
     return v;
 }
 
+// lane mask of a condition (the compare feeds the mask directly)
+__device__ __forceinline__ uint64_t ballot(bool c) { return __builtin_amdgcn_ballot_w64(c); }
+
 // uniform value into a scalar register
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 

@@ -131,12 +131,12 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
             // micro-batches per replica M_p = ceil(m / D); min(M_p, S) fixes the split
             const int Mp_k = (int)(((uint32_t)my_m + (uint32_t)D - 1) / (uint32_t)D);
             const int key_k = mem_aware ? (Mp_k < S ? Mp_k : S) : 0;
-            uint64_t todo = __ballot(lane < A.n_m);
+            uint64_t todo = ballot(lane < A.n_m);
 
             while (todo) {
                 const int key = A.n_m == 1 ? uni(key_k)
                                            : uni((int)group_min<uint32_t>(((todo >> lane) & 1) ? (uint32_t)key_k : 0x7FFFFFFFu, 64));
-                const uint64_t cls = __ballot(lane < A.n_m && key_k == key) & todo;
+                const uint64_t cls = ballot(lane < A.n_m && key_k == key) & todo;
                 todo &= ~cls;
                 auto jhi_of = [&](int s) { return L - (S - 1 - s); };   // last end leaving a layer per later stage
 
@@ -178,7 +178,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                     const int ihi = lane == 0 ? 0 : L - (S - lane);
                     Bl = Bl < ihi ? Bl : ihi;
                 }
-                if (__ballot(lane < S && Al > Bl)) continue;           // no split fits memory
+                if (ballot(lane < S && Al > Bl)) continue;           // no split fits memory
                 // G arena: G_s over the rows of W_s for s = S-1 .. 1, stored in that order,
                 // when all of them fit; else the second backward pass rebuilds F
                 const int g_total = uni((int)wave_sum((uint32_t)(lane >= 1 && lane < S ? Bl - Al + 1 : 0)));
@@ -299,18 +299,25 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                     int rem = g_total;                                 // arena index of G_{s+1}[a_{s+1}]
                     for (int s = 0; s < S - 1; s++) {
                         const uint32_t k1 = uni64(pk, s + 1);
-                        const int a1 = k1 & 255, b1 = (k1 >> 8) & 255;
-                        rem -= b1 - a1 + 1;
-                        int j0 = max(cs + 1, a1);
-                        uint64_t mk;
-                        for (;;) {
-                            const int j = j0 + lane;
-                            const V g = GA[rem + min(j, b1) - a1];
-                            mk = __ballot(j <= b1 && (F32 ? g != INF && within((uint64_t)g) : (uint64_t)g <= B));
-                            if (mk || j0 + 64 > b1) break;
-                            j0 += 64;
+                        const int a1 = k1 & 255, w1 = ((k1 >> 8) & 255) - a1;   // rows a1 .. a1 + w1
+                        rem -= w1 + 1;
+                        const int lo = max(cs + 1, a1) - a1;           // lowest admissible row, from a1
+                        // the window in words of 64 rows, from the word holding lo (a later
+                        // word only when the window is longer than 64 rows)
+                        auto word = [&](int w0) -> uint64_t {
+                            const int r = w0 + lane;
+                            const V g = GA[rem + min(r, w1)];
+                            return ballot(r <= w1) &
+                                   ballot(F32 ? g != INF && within((uint64_t)g) : (uint64_t)g <= B);
+                        };
+                        int w0 = lo & ~63;
+                        uint64_t mk = word(w0) & (~0ull << (lo - w0));   // rows from lo
+                        while (!mk && w0 + 64 <= w1) {
+                            w0 += 64;
+                            mk = word(w0);
                         }
-                        cs = mk ? j0 + __ffsll((unsigned long long)mk) - 1 : L;   // L: unreachable
+                        const int nx = mk ? a1 + w0 + __ffsll((unsigned long long)mk) - 1 : L;   // L: unreachable
+                        cs = nx;
                         my_end = lane == s ? cs : my_end;
                     }
                 } else {
@@ -341,7 +348,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                             }
                             const uint32_t nxc = min(nx, L);
                             ok = ok & within((uint64_t)(V)(prow[nxc] - prow[(uint32_t)ic] + p2p));
-                            const uint64_t mask = __ballot(ok);
+                            const uint64_t mask = ballot(ok);
                             const uint64_t rest = mask >> lane;            // rows >= i of this slot with F true
                             const int nxi = rest ? i + __ffsll((unsigned long long)rest) - 1 : first_above;
                             if (i <= b) NXs[i] = (uint8_t)nxi;
@@ -381,7 +388,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
             else ((int64_t *)A.bottleneck)[o] = r_split ? (int64_t)r_b : INT64_MAX;
         }
         // zero layer counts of the plans without a split (invalid template, or no split fits)
-        const uint64_t without = __ballot(lane < A.n_m && !r_split);
+        const uint64_t without = ballot(lane < A.n_m && !r_split);
         for (uint64_t c = without; c; c &= c - 1) {
             const int k = __ffsll((unsigned long long)c) - 1;
             if (lane < A.s_max) A.layers[(obase + k) * A.s_max + lane] = 0;

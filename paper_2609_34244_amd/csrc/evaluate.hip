@@ -20,7 +20,8 @@ __global__ void __launch_bounds__(256) evaluate_kernel(DevProfile P, PriceArgs A
 {
     const int64_t total = A.n * A.n_m;
     for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < total; o += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t t = o / A.n_m;
+        // plan o = t * n_m + k; a 32-bit division when the batch allows it
+        const int64_t t = A.n_m == 1 ? o : total <= 0xFFFFFFFFll ? (int64_t)((uint32_t)o / (uint32_t)A.n_m) : o / A.n_m;
         const int k = (int)(o - t * A.n_m);
         if (A.status[o] != HEDDLE_S_OK) {                     // no split: invalid template or nothing fits
             if (F32) ((float *)A.iter)[o] = __builtin_inff();

@@ -81,7 +81,7 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
     const uint32_t invF = F > 1 ? (uint32_t)(0xFFFFFFFFu / (uint32_t)F) + 1u : 0u;
 
     for (int64_t o = blockIdx.x; o < total; o += gridDim.x) {
-        const int64_t t = A.n_m == 1 ? o : o / A.n_m;
+        const int64_t t = A.n_m == 1 ? o : total <= 0xFFFFFFFFll ? (int64_t)((uint32_t)o / (uint32_t)A.n_m) : o / A.n_m;
         const int k = (int)(o - t * A.n_m);
         const int st_in = A.status[o];
         const bool has_split = (st_in == HEDDLE_S_OK || st_in == HEDDLE_S_OOM) && A.layers[o * A.s_max] > 0;

@@ -44,7 +44,8 @@ def log(*a):
 
 # sources of the kernels a traffic measurement covers (and of the tables they read)
 COMMON_SOURCES = ["heddle_internal.h", "device_common.h", "exact_math.h", "stage_cost.h", "profile.cpp"]
-MEASURED_SOURCES = {"": ["price.hip", "decode.h", "dp_common.h", "evaluate.hip"], "_distribute": ["distribute.hip"]}
+MEASURED_SOURCES = {"": ["windows.hip", "validate.h", "price.hip", "decode.h", "dp_common.h", "evaluate.hip"],
+                    "_distribute": ["distribute.hip", "validate.h"]}
 
 
 def source_hash(mode=""):
@@ -226,7 +227,7 @@ def main():
                               "mean_bottleneck_ratio": float(np.mean(bd[both] / br[both])) if both.any() else None,
                               "mean_iter_ratio": float(np.mean(it_d[both] / it_r[both])) if both.any() else None}
     else:
-        roof = {"kernel": "split_kernel + evaluate_kernel (one heddle_price_plans launch pair)",
+        roof = {"kernel": "window_kernel + split_kernel + evaluate_kernel (one heddle_price_plans call)",
                 "work_per_launch": relax, "work_unit": unit_name, "ops_per_unit": k_unit,
                 "dense_R_per_launch": dense_r, "frac_at_dense_R": dense_r * K_MIN / kern_s / PEAK_LANE_OPS}
     result = {

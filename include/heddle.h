@@ -25,6 +25,18 @@
  * Threading: every entry point may be called from any host thread. A loaded
  * profile is immutable, so concurrent pricing calls on different streams
  * may share it. heddle_last_error() is per host thread.
+ *
+ * Scratch: device memory that an entry point needs beyond its caller's
+ * buffers is allocated stream-ordered on the call's stream, from a memory
+ * pool per device that the library creates on first use, and freed on that
+ * stream before the call returns; the pool keeps freed memory for later
+ * calls until the process ends. The exception is the pricing path's per-plan
+ * scratch (heddle_price_plans and the entry points built on it): a profile
+ * keeps one buffer per stream it was used on, grown on demand, until
+ * heddle_free_profile, which waits for the last use of each. Pricing calls
+ * that share a profile take its lock while they enqueue their launches (their
+ * device work still overlaps across streams). With hipStreamPerThread the
+ * buffer is a fresh stream-ordered block per call.
  */
 #ifndef HEDDLE_H
 #define HEDDLE_H
@@ -134,7 +146,9 @@ typedef struct heddle_profile heddle_profile;   /* opaque, device-resident table
  */
 int heddle_load_profile(const heddle_profile_desc *d, heddle_profile **out);
 
-/* Release a profile. NULL is ignored. No call using it may be in flight. */
+/* Release a profile and its per-stream scratch buffers (waiting for the
+ * device work that last used each). NULL is ignored. No host thread may be
+ * inside a call that uses it. */
 void heddle_free_profile(heddle_profile *p);
 
 /*
@@ -181,9 +195,13 @@ void heddle_free_profile(heddle_profile *p);
  * OOM without a split. With COMPUTE_ONLY the proportional split is kept and
  * flagged OOM if it does not fit. The bottleneck output is then the split's
  * slowest stage time.
+ * Scratch: without DISTRIBUTE, about n * n_m * (1 + 2 * s_max) bytes (s_max
+ * rounded up to a multiple of 4) for the per-plan validation and row
+ * windows, in the profile's buffer of `stream`.
  * Returns HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_RANGE (the iteration time could
  * exceed 2^62 for these m, or the fp32 costs span too wide a range to sum
- * exactly) or HEDDLE_E_DEVICE. On error nothing is enqueued.
+ * exactly), HEDDLE_E_NOMEM (the scratch) or HEDDLE_E_DEVICE. On error nothing
+ * is enqueued.
  */
 int heddle_price_plans(const heddle_profile *p, int64_t n, int32_t s_max,
                        const uint8_t *d_n_stages, const uint32_t *d_stages,
@@ -212,8 +230,8 @@ int heddle_argmin_plans(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t fla
 /*
  * heddle_best_plan -- heddle_price_plans into library-allocated device
  * buffers followed by heddle_argmin_plans. Synchronous. Arguments as in
- * those two calls. The library allocates and frees its own buffers with
- * stream-ordered allocation on `stream`.
+ * those two calls. The library allocates and frees its own buffers as
+ * scratch on `stream`.
  */
 int heddle_best_plan(const heddle_profile *p, int64_t n, int32_t s_max,
                      const uint8_t *d_n_stages, const uint32_t *d_stages,

@@ -8,7 +8,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libheddle.so")
-SOURCES = ["profile.cpp", "price.hip", "evaluate.hip", "distribute.hip", "argmin.hip", "enumerate.hip", "tile.hip", "fill.hip"]
+SOURCES = ["profile.cpp", "windows.hip", "price.hip", "evaluate.hip", "distribute.hip", "argmin.hip", "enumerate.hip", "tile.hip",
+           "fill.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

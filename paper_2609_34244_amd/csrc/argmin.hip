@@ -130,8 +130,8 @@ int launch_argmin(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t flags, co
     const int64_t want = (total + kArgBlock * 8 - 1) / (kArgBlock * 8);
     const int blocks = (int)(want < kArgMaxBlocks ? (want > 0 ? want : 1) : kArgMaxBlocks);
     Cand *scratch = nullptr;
-    hipError_t e = hipMallocAsync((void **)&scratch, sizeof(Cand) * (blocks + 1), stream);
-    if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "hipMallocAsync of argmin partials failed");
+    hipError_t e = scratch_alloc((void **)&scratch, sizeof(Cand) * (blocks + 1), stream);
+    if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "device scratch for argmin partials could not be allocated");
     a.partial = scratch;
     hipLaunchKernelGGL(argmin_pass1, dim3(blocks), dim3(kArgBlock), 0, stream, a);
     hipLaunchKernelGGL(argmin_pass2, dim3(1), dim3(kArgBlock), 0, stream, (const Cand *)scratch, blocks, a.f32,
@@ -139,8 +139,8 @@ int launch_argmin(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t flags, co
     Cand h;
     e = hipGetLastError();
     if (e == hipSuccess) e = hipMemcpyAsync(&h, scratch + blocks, sizeof(h), hipMemcpyDeviceToHost, stream);
+    (void)hipFreeAsync(scratch, stream);                       // stream-ordered after the copy
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
-    (void)hipFreeAsync(scratch, stream);
     if (e != hipSuccess) return hip_fail(e, "argmin");
     if (h.idx < 0) return fail(HEDDLE_E_NOFEASIBLE, "no plan has status OK");
     *h_best_template = h.idx / n_m;
@@ -191,8 +191,8 @@ extern "C" int heddle_best_plan(const heddle_profile *p, int64_t n, int32_t s_ma
     const size_t o_iter = 0, o_bn = o_iter + total * 8, o_pk = o_bn + total * 8, o_st = o_pk + total * 8,
                  o_ly = (o_st + total + 255) & ~size_t(255), bytes = o_ly + total * (size_t)s_max;
     unsigned char *buf = nullptr;
-    hipError_t e = hipMallocAsync((void **)&buf, bytes, stream);
-    if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "hipMallocAsync of pricing outputs failed");
+    hipError_t e = scratch_alloc((void **)&buf, bytes, stream);
+    if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "device scratch for pricing outputs could not be allocated");
     PriceArgs a;
     std::memset(&a, 0, sizeof(a));
     a.n = n;

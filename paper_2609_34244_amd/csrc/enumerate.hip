@@ -205,8 +205,8 @@ extern "C" int heddle_best_enumerated(const heddle_profile *p, const heddle_enum
                  o_ly = (o_ss + cm + 255) & ~size_t(255), o_ok = (o_ly + cm * s_max + 255) & ~size_t(255),
                  bytes = o_ok + 8;
     unsigned char *buf = nullptr;
-    hipError_t e = hipMallocAsync((void **)&buf, bytes, stream);
-    if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "hipMallocAsync of the enumeration buffers failed");
+    hipError_t e = scratch_alloc((void **)&buf, bytes, stream);
+    if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "device scratch for the enumeration buffers could not be allocated");
     unsigned long long *d_ok = (unsigned long long *)(buf + o_ok);
     e = hipMemsetAsync(d_ok, 0, 8, stream);
     if (e != hipSuccess) {

@@ -284,8 +284,8 @@ extern "C" int heddle_fill_plans(const heddle_profile *const *profiles, const in
     const size_t un = (size_t)n, o_it = 0, o_bn = un * 8, o_pk = o_bn + un * 8, o_st = o_pk + un * 8,
                  o_ly = (o_st + un + 255) & ~size_t(255), per = (o_ly + un * s_max + 255) & ~size_t(255);
     unsigned char *buf = nullptr;
-    hipError_t e = hipMallocAsync((void **)&buf, per * n_mbs, stream);
-    if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "hipMallocAsync of per-size outputs failed");
+    hipError_t e = scratch_alloc((void **)&buf, per * n_mbs, stream);
+    if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "device scratch for per-size outputs could not be allocated");
     SelectArgs sa;
     std::memset(&sa, 0, sizeof(sa));
     sa.n = n;

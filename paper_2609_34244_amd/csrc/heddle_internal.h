@@ -3,7 +3,9 @@
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <mutex>
 #include <string>
+#include <vector>
 
 #include "../../include/heddle.h"
 
@@ -78,6 +80,20 @@ struct heddle_profile {
     int64_t max_ar_fx;               // the same, fp32-rounded, fixed-point units
     int64_t max_tiled_ns;            // bound on any stage time under any expert layout
     int64_t max_ar_tiled_ns;         // bound on any stage's synchronisation under any expert layout
+    // Scratch of the pricing path, one buffer per stream, grown on demand and
+    // kept until the profile is freed (a fresh stream-ordered block per call
+    // costs tens of microseconds of host time before the first launch).
+    // scratch_mu is held from taking a buffer until the call's last launch
+    // is enqueued and `done` recorded after it, so a buffer is reused only in
+    // stream order.
+    struct Scratch {
+        hipStream_t stream;
+        void *ptr;
+        size_t bytes;
+        hipEvent_t done;
+    };
+    mutable std::mutex scratch_mu;
+    mutable std::vector<Scratch> scratch;
 };
 
 namespace heddle {
@@ -86,6 +102,18 @@ namespace heddle {
 void set_error(const std::string &msg);
 int fail(int code, const std::string &msg);
 int hip_fail(hipError_t e, const char *what);
+
+// stream-ordered device scratch from the library's pool of the stream's
+// device; release with hipFreeAsync on the same stream
+constexpr int kMaxDevices = 64;
+hipError_t scratch_alloc(void **ptr, size_t bytes, hipStream_t stream);
+
+// The profile's scratch buffer of `stream`, at least `bytes` long; the caller
+// holds p->scratch_mu until profile_scratch_done. With hipStreamPerThread (one
+// handle for many streams) the block is a fresh one that *owned marks, which
+// profile_scratch_done releases on the stream.
+int profile_scratch(const heddle_profile *p, hipStream_t stream, size_t bytes, void **ptr, bool *owned);
+int profile_scratch_done(const heddle_profile *p, hipStream_t stream, void *ptr, bool owned);
 
 #define HEDDLE_HIP(call)                                         \
     do {                                                         \
@@ -107,15 +135,24 @@ struct PriceArgs {
     int32_t g_stride;                // LDS entries per pair row (L + 1 and padding)
     int32_t s_cap;                   // stage rows: min(s_max, L)
     int32_t lds_per_wave;            // bytes of one wavefront's LDS region
-    int32_t off_j, off_x, off_c;     // byte offsets of the per-stage limit rows, of the inverse-limit
-                                     // rows (shared with the G arena) and of the type counters
+    int32_t off_j, off_x;            // byte offsets of the per-stage limit rows and of the next-row
+                                     // tables (shared with the G arena)
     int32_t arena_cap;               // entries of the G arena
+    uint8_t *wst;                    // [n][n_m] status after validation and windows (0: windows found)
+    uint16_t *wwin;                  // [n][n_m][win_stride(s_max)] window of stage s: first row | last row << 8
+    bool scratch_owned;              // host side: wst lives in a block of its own (hipStreamPerThread)
 };
 
 int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,
                         const uint32_t *d_stages, const int32_t *h_m, int32_t n_m, uint32_t flags);
 int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool count_only);
 int launch_evaluate(const heddle_profile *p, const PriceArgs &a, hipStream_t stream);
+// window pass outputs: row stride of a plan's windows, in entries (a
+// multiple of 4, so that rows are stored 8 bytes at a time)
+__host__ __device__ inline int win_stride(int s_max) { return (s_max + 3) & ~3; }
+// window pass: LDS check and attribute set-up (nothing enqueued), then the launch
+int prepare_windows(const heddle_profile *p, const PriceArgs &a, int max_lds, size_t *lds);
+int launch_windows(const heddle_profile *p, const PriceArgs &a, size_t lds, hipStream_t stream);
 int launch_distribute(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool count_only);
 int launch_tile(const heddle_profile *p, const PriceArgs &a, uint8_t *tiling, hipStream_t stream);
 int launch_argmin(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t flags, const void *d_iter,

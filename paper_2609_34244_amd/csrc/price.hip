@@ -1,6 +1,7 @@
-// Batched plan pricing on gfx950, split kernel: template decode and
-// validation, PartitionLayers (exact min-max layer split) and its canonical
-// reconstruction. Evaluate runs in evaluate.hip on the split found here.
+// Batched plan pricing on gfx950, split kernel: PartitionLayers (exact
+// min-max layer split) and its canonical reconstruction over the row windows
+// that the window pass (windows.hip) found for every valid plan. Evaluate
+// runs in evaluate.hip on the split found here.
 //
 // Method: Heddle (arXiv 2609.34244). The layer split is the PartitionLayers
 // step of the planners' nested-loop backbone (section 3.1), aware of per-stage
@@ -18,10 +19,11 @@
 // profile table.
 //
 // Mapping. One wavefront splits one template at a time (grid-stride over
-// templates). Lanes are stages for decode and validation. The memory-limit
-// rows of all stages are copied into LDS first; two short scalar passes over
-// them give each stage's window of rows that can lie on a complete split (see
-// the split kernel), and the DP relaxes only those. Lanes are split rows
+// templates); templates whose plans all failed validation or have an empty
+// window cost one status read. Lanes are stages while the per-stage table
+// offsets are formed. The memory-limit rows of all stages are copied into
+// LDS, and the DP relaxes only the rows of each stage's window (rows that can
+// lie on a complete split, see the split kernel). Lanes are split rows
 // during the DP: r rows of a window take 64 >> ceil(log2 r) lanes each, which
 // share the row's ends and combine with a cross-lane minimum. Per wavefront,
 // one LDS pair row holds X[j] = {P_s[j], G[s+1][j]}, so one 64-bit read feeds
@@ -84,22 +86,21 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
     const bool mem_aware = (A.flags & HEDDLE_F_COMPUTE_ONLY) == 0;
     const V INF = DPInf<V>::value;
     V2 *X = (V2 *)smem;                                        // [gs] pair row {P_s[j], G_{s+1}[j]}
-    // [s_cap][ls] limit rows; [s_cap][ls] inverse-limit rows, which the second
-    // backward pass later overwrites with next-row tables; the same region, and
-    // what follows it up to the counters, holds the G arena instead when
-    // the template's windows fit it
+    // [s_cap][ls] limit rows; [s_cap][ls] next-row tables of the second
+    // backward pass, a region that, with what follows it up to the end of the
+    // wavefront's LDS, holds the G arena instead when the template's windows
+    // fit it
     uint8_t *JX = smem + A.off_j;
     uint8_t *IX = smem + A.off_x;
     V *GA = (V *)IX;
-    uint32_t *cnt = (uint32_t *)(smem + A.off_c);              // [n_types] GPU counters of decode
     const V *rows = stage_rows<V>(P, F32);
     auto jrow = [&](int s) -> uint8_t * { return JX + s * ls; };
     auto xrow = [&](int s) -> uint8_t * { return IX + s * ls; };
 
-    // limit-row copy: the two rows of a stage are q16 pieces of 16 bytes; lane
+    // limit-row copy: the limit row of a stage is h16 pieces of 16 bytes; lane
     // (su, pc) copies piece pc of stage s0 + su
-    const int h16 = ls >> 4, q16 = 2 * h16, per = 64 / q16;
-    const int su = lane / q16, pc = lane - su * q16;
+    const int h16 = ls >> 4, per = 64 / h16;
+    const int su = lane / h16, pc = lane - su * h16;
     int my_m = 1;                                              // lane k: the k-th micro-batch count
     for (int k = 0; k < A.n_m; k++) my_m = lane == k ? A.m[k] : my_m;
     unsigned long long work = 0;
@@ -120,18 +121,20 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
             S_next = A.n_stages[t + stride];
             rec_next = lane < A.s_max ? A.stages[(t + stride) * A.s_max + lane] : 0u;
         }
-        const StageInfo<V> x = decode<V, F32>(P, A, S_in, rec_in, lane, cnt);
-        const int S = uni(x.S);
         const size_t obase = (size_t)t * A.n_m;
+        // lane k: status of plan k after validation and windows (0: windows found)
+        const int pst = lane < A.n_m ? A.wst[obase + lane] : HEDDLE_S_OOM;
+        uint64_t todo = ballot(lane < A.n_m && pst == HEDDLE_S_OK);
         bool r_split = false;                                  // lane k: a split was found for m index k
         V r_b = INF;
 
-        if (x.status == 0) {
+        if (todo) {
+            const int S = uni(S_in);
+            const StageInfo<V> x = stage_info<V, F32>(P, A, S, rec_in, lane);
             const int D = x.D;
             // micro-batches per replica M_p = ceil(m / D); min(M_p, S) fixes the split
             const int Mp_k = (int)(((uint32_t)my_m + (uint32_t)D - 1) / (uint32_t)D);
             const int key_k = mem_aware ? (Mp_k < S ? Mp_k : S) : 0;
-            uint64_t todo = ballot(lane < A.n_m);
 
             while (todo) {
                 const int key = A.n_m == 1 ? uni(key_k)
@@ -140,8 +143,8 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                 todo &= ~cls;
                 auto jhi_of = [&](int s) { return L - (S - 1 - s); };   // last end leaving a layer per later stage
 
-                // ---------------- limit and inverse-limit rows of every stage (this class)
-                // into LDS: 16-byte pieces, the rows of `per` stages per load
+                // ---------------- limit rows of every stage (this class) into LDS:
+                // 16-byte pieces, the rows of `per` stages per load
                 if (mem_aware) {
                     wave_sync();                                        // earlier reads of JX are done
                     int f = min(S - lane, key);
@@ -151,34 +154,20 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         const int st = s0 + su;
                         const int row = __shfl(my_row, min(st, 63));
                         if (su < per && st < S) {
-                            uint8_t *dst = pc < h16 ? JX + st * ls + pc * 16 : IX + st * ls + (pc - h16) * 16;
-                            *(uint4 *)dst = *(const uint4 *)(P.mem_lim + row + pc * 16);
+                            *(uint4 *)(JX + st * ls + pc * 16) = *(const uint4 *)(P.mem_lim + row + pc * 16);
                         }
                     }
                     wave_sync();
                 }
 
-                // ---------------- row windows: lane s holds [a_s, b_s]
-                // the forward reach R_s and the backward bound Bk_s are independent
-                // pointer chases over the limit rows; one loop takes a step of each (the
-                // chased values stay in vector registers, equal in every lane)
-                // (compute-only: Bk_s = s and R_s = L - (S - s) for s >= 1)
-                int Al = lane, Bl = L;                                  // lane s: Bk_s, R_s
-                if (mem_aware) {
-                    int c = 0, nxt = L;                                 // R_t, Bk_{u+1}
-                    for (int t = 0; t < S; t++) {
-                        const int u = S - 1 - t;
-                        Bl = lane == t ? c : Bl;
-                        c = min((int)jrow(t)[c], jhi_of(t));           // R_{t+1} = lim(t, R_t)
-                        nxt = max((int)xrow(u)[nxt], u);               // Bk_u
-                        Al = lane == u ? nxt : Al;
-                    }
-                }
+                // ---------------- row windows (from the window pass): lane s holds [a_s, b_s]
+                int Al, Bl;
                 {
-                    const int ihi = lane == 0 ? 0 : L - (S - lane);
-                    Bl = Bl < ihi ? Bl : ihi;
+                    const int k0 = __ffsll((unsigned long long)cls) - 1;   // a plan of this class
+                    const uint32_t w = lane < S ? A.wwin[(obase + k0) * win_stride(A.s_max) + lane] : 0u;
+                    Al = (int)(w & 255);
+                    Bl = (int)(w >> 8);
                 }
-                if (ballot(lane < S && Al > Bl)) continue;           // no split fits memory
                 // G arena: G_s over the rows of W_s for s = S-1 .. 1, stored in that order,
                 // when all of them fit; else the second backward pass rebuilds F
                 const int g_total = uni((int)wave_sum((uint32_t)(lane >= 1 && lane < S ? Bl - Al + 1 : 0)));
@@ -383,7 +372,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
         if (COUNT) continue;
         if (lane < A.n_m) {
             const size_t o = obase + lane;
-            A.status[o] = (uint8_t)(x.status != 0 ? x.status : (r_split ? HEDDLE_S_OK : HEDDLE_S_OOM));
+            A.status[o] = (uint8_t)(pst != HEDDLE_S_OK ? pst : (r_split ? HEDDLE_S_OK : HEDDLE_S_OOM));
             if (F32) ((float *)A.bottleneck)[o] = r_split ? exact_float(rne24((uint64_t)r_b), P.fx_exp) : __builtin_inff();
             else ((int64_t *)A.bottleneck)[o] = r_split ? (int64_t)r_b : INT64_MAX;
         }
@@ -442,18 +431,17 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     a.s_cap = a.s_max < L ? a.s_max : L;
     a.g_stride = L + 5;                                       // L + 1 ends and 4 of padding
     // per wavefront: one pair row {P_s, G_{s+1}}; per stage its limit row; per
-    // stage its inverse-limit row (later its next-row table), a region that the
-    // G arena shares and extends up to the wavefront's share of the CU's LDS at
-    // the occupancy the other parts allow; one GPU counter per type
+    // stage its next-row table (second backward pass), a region that the G
+    // arena shares and extends up to the wavefront's share of the CU's LDS at
+    // the occupancy the other parts allow
     const size_t j_off = ((size_t)a.g_stride * 2 * sizeof(V) + 15) & ~size_t(15);
     const size_t x_off = j_off + (size_t)a.s_cap * ls;
-    const size_t c_bytes = ((size_t)p->dev.n_types * 4 + 15) & ~size_t(15);
     size_t x_bytes = (size_t)a.s_cap * ls;
     int max_lds = 0, lds_cu = 0;
     HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
     HEDDLE_HIP(hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, p->device));
     if (!COUNT && lds_cu > 0) {
-        const size_t need = x_off + x_bytes + c_bytes;
+        const size_t need = x_off + x_bytes;
         const size_t waves_regs = sizeof(V) == 4 ? 32 : 20;   // wavefronts per CU the registers allow
         size_t waves = (size_t)lds_cu / need;
         waves = waves < waves_regs ? waves : waves_regs;
@@ -463,12 +451,10 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
             if (share > need) x_bytes += (share - need) & ~size_t(15);
         }
     }
-    const size_t c_off = x_off + x_bytes;
     a.off_j = (int32_t)j_off;
     a.off_x = (int32_t)x_off;
-    a.off_c = (int32_t)c_off;
     a.arena_cap = (int32_t)(x_bytes / sizeof(V));
-    a.lds_per_wave = (int32_t)(c_off + c_bytes);
+    a.lds_per_wave = (int32_t)(x_off + x_bytes);
     // one wavefront per workgroup: a wavefront's LDS is released as soon as it
     // is done, whatever the other wavefronts on the CU are doing
     const int wpb = 1;
@@ -478,6 +464,21 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
         HEDDLE_HIP(hipFuncSetAttribute(L + 1 <= 128 ? (const void *)split_kernel<V, F32, COUNT, 2>
                                                    : (const void *)split_kernel<V, F32, COUNT, 4>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+    size_t w_lds = 0;
+    const int rc = prepare_windows(p, a, max_lds, &w_lds);
+    if (rc != HEDDLE_OK) return rc;
+    // validation and windows of every plan into the profile's scratch of this
+    // stream (the caller holds its lock and marks the end of its use)
+    const size_t plans = (size_t)a.n * a.n_m;
+    const size_t st_bytes = (plans + 255) & ~size_t(255);
+    unsigned char *buf = nullptr;
+    const int rs = profile_scratch(p, stream, st_bytes + plans * win_stride(a.s_max) * sizeof(uint16_t),
+                                   (void **)&buf, &a.scratch_owned);
+    if (rs != HEDDLE_OK) return rs;
+    a.wst = buf;
+    a.wwin = (uint16_t *)(buf + st_bytes);
+    const int rw = launch_windows(p, a, w_lds, stream);
+    if (rw != HEDDLE_OK) return rw;
     const int64_t want = (a.n + wpb - 1) / wpb;
     const int blocks = (int)(want < 65536 ? want : 65536);
     // time-prefix slots of 64 entries held in registers: 2 cover L + 1 <= 128
@@ -494,13 +495,25 @@ int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool
     if (a.n == 0) return HEDDLE_OK;
     const bool f32 = a.flags & HEDDLE_F_FP32;
     const bool narrow = f32 ? p->narrow_f32 : p->narrow_i64;
-    int rc;
     if (a.flags & HEDDLE_F_DISTRIBUTE) return launch_distribute(p, a, stream, count_only);
-    if (count_only) return launch_split<uint64_t, false, true>(p, a, stream);
-    if (f32) rc = narrow ? launch_split<uint32_t, true, false>(p, a, stream) : launch_split<uint64_t, true, false>(p, a, stream);
+    // validation and windows of every plan (window_kernel), then the split
+    // kernel over the plans with windows, then Evaluate
+    std::lock_guard<std::mutex> lock(p->scratch_mu);
+    a.wst = nullptr;
+    a.wwin = nullptr;
+    a.scratch_owned = false;
+    int rc;
+    if (count_only) rc = launch_split<uint64_t, false, true>(p, a, stream);
+    else if (f32) rc = narrow ? launch_split<uint32_t, true, false>(p, a, stream) : launch_split<uint64_t, true, false>(p, a, stream);
     else rc = narrow ? launch_split<uint32_t, false, false>(p, a, stream) : launch_split<uint64_t, false, false>(p, a, stream);
-    if (rc != HEDDLE_OK) return rc;
-    return launch_evaluate(p, a, stream);
+    if (rc == HEDDLE_OK && !count_only) rc = launch_evaluate(p, a, stream);
+    if (a.wst) {
+        const int rd = profile_scratch_done(p, stream, a.wst, a.scratch_owned);
+        if (rc == HEDDLE_OK) rc = rd;
+    }
+    a.wst = nullptr;
+    a.wwin = nullptr;
+    return rc;
 }
 
 static PriceArgs make_args(int64_t n, int32_t s_max, const uint8_t *d_n_stages, const uint32_t *d_stages,
@@ -551,17 +564,16 @@ extern "C" int heddle_count_work(const heddle_profile *p, int64_t n, int32_t s_m
     if (!h_relaxations) return fail(HEDDLE_E_INVAL, "h_relaxations is NULL");
     PriceArgs a = make_args(n, s_max, d_n_stages, d_stages, h_m, n_m, flags);
     unsigned long long *d_work = nullptr;
-    hipError_t e = hipMallocAsync((void **)&d_work, sizeof(unsigned long long), stream);
-    if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "hipMallocAsync of the work counter failed");
-    HEDDLE_HIP(hipMemsetAsync(d_work, 0, sizeof(unsigned long long), stream));
+    hipError_t e = scratch_alloc((void **)&d_work, sizeof(unsigned long long), stream);
+    if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "device scratch for the work counter could not be allocated");
+    e = hipMemsetAsync(d_work, 0, sizeof(unsigned long long), stream);
     a.work = d_work;
-    rc = launch_price(p, a, stream, true);
+    rc = e == hipSuccess ? launch_price(p, a, stream, true) : hip_fail(e, "hipMemsetAsync");
     unsigned long long h = 0;
-    if (rc == HEDDLE_OK) {
-        HEDDLE_HIP(hipMemcpyAsync(&h, d_work, sizeof(h), hipMemcpyDeviceToHost, stream));
-        HEDDLE_HIP(hipStreamSynchronize(stream));
-        *h_relaxations = (int64_t)h;
-    }
-    (void)hipFreeAsync(d_work, stream);
+    if (rc == HEDDLE_OK) e = hipMemcpyAsync(&h, d_work, sizeof(h), hipMemcpyDeviceToHost, stream);
+    (void)hipFreeAsync(d_work, stream);                        // stream-ordered after the copy
+    if (rc == HEDDLE_OK && e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (rc == HEDDLE_OK && e != hipSuccess) rc = hip_fail(e, "reading the work counter back");
+    if (rc == HEDDLE_OK) *h_relaxations = (int64_t)h;
     return rc;
 }

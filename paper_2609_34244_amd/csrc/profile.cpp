@@ -10,6 +10,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "heddle_internal.h"
@@ -30,6 +31,97 @@ int hip_fail(hipError_t e, const char *what)
 {
     g_last_error = std::string(what) + ": " + hipGetErrorString(e);
     return HEDDLE_E_DEVICE;
+}
+
+// Stream-ordered scratch of every entry point comes from one memory pool per
+// device that the library owns. Its release threshold keeps freed blocks
+// mapped between calls (a pool that hands them back at every synchronisation
+// pays a fresh mapping on the next call); they go back when the process ends.
+static std::mutex g_pool_mu;
+static hipMemPool_t g_pool[kMaxDevices];
+
+hipError_t scratch_alloc(void **ptr, size_t bytes, hipStream_t stream)
+{
+    int dev = 0;
+    hipError_t e = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    hipMemPool_t pool = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(g_pool_mu);
+        if (!g_pool[dev]) {
+            hipMemPoolProps props;
+            std::memset(&props, 0, sizeof(props));
+            props.allocType = hipMemAllocationTypePinned;
+            props.location.type = hipMemLocationTypeDevice;
+            props.location.id = dev;
+            hipMemPool_t created = nullptr;
+            e = hipMemPoolCreate(&created, &props);
+            if (e != hipSuccess) return e;
+            uint64_t keep = UINT64_MAX;
+            e = hipMemPoolSetAttribute(created, hipMemPoolAttrReleaseThreshold, &keep);
+            if (e != hipSuccess) {
+                (void)hipMemPoolDestroy(created);
+                return e;
+            }
+            g_pool[dev] = created;
+        }
+        pool = g_pool[dev];
+    }
+    return hipMallocFromPoolAsync(ptr, bytes, pool, stream);
+}
+
+int profile_scratch(const heddle_profile *p, hipStream_t stream, size_t bytes, void **ptr, bool *owned)
+{
+    *ptr = nullptr;
+    *owned = false;
+    if (stream == hipStreamPerThread) {
+        if (scratch_alloc(ptr, bytes, stream) != hipSuccess) return fail(HEDDLE_E_NOMEM, "device scratch could not be allocated");
+        *owned = true;
+        return HEDDLE_OK;
+    }
+    heddle_profile::Scratch *slot = nullptr;
+    for (auto &sl : p->scratch)
+        if (sl.stream == stream) slot = &sl;
+    if (!slot) {
+        hipEvent_t ev = nullptr;
+        HEDDLE_HIP(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
+        try {
+            p->scratch.push_back({stream, nullptr, 0, ev});
+        } catch (...) {
+            (void)hipEventDestroy(ev);
+            return fail(HEDDLE_E_NOMEM, "host allocation failed");
+        }
+        slot = &p->scratch.back();
+    } else {
+        // the last use was on this handle; should the stream have been
+        // destroyed and the handle reused, the wait orders this call after it
+        HEDDLE_HIP(hipStreamWaitEvent(stream, slot->done, 0));
+    }
+    if (slot->bytes < bytes) {
+        if (slot->ptr) HEDDLE_HIP(hipFreeAsync(slot->ptr, stream));
+        slot->ptr = nullptr;
+        slot->bytes = 0;
+        const size_t want = (bytes + (size_t(1) << 21) - 1) & ~((size_t(1) << 21) - 1);   // 2 MiB steps
+        if (scratch_alloc(&slot->ptr, want, stream) != hipSuccess) {
+            slot->ptr = nullptr;
+            return fail(HEDDLE_E_NOMEM, "device scratch could not be allocated");
+        }
+        slot->bytes = want;
+    }
+    *ptr = slot->ptr;
+    return HEDDLE_OK;
+}
+
+int profile_scratch_done(const heddle_profile *p, hipStream_t stream, void *ptr, bool owned)
+{
+    if (owned) {
+        HEDDLE_HIP(hipFreeAsync(ptr, stream));
+        return HEDDLE_OK;
+    }
+    for (auto &sl : p->scratch)
+        if (sl.stream == stream) HEDDLE_HIP(hipEventRecord(sl.done, stream));
+    return HEDDLE_OK;
 }
 
 typedef __int128 i128;
@@ -433,6 +525,11 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
 extern "C" void heddle_free_profile(heddle_profile *p)
 {
     if (!p) return;
+    for (auto &sl : p->scratch) {                              // waits for the last use of each buffer
+        (void)hipEventSynchronize(sl.done);
+        if (sl.ptr) (void)hipFree(sl.ptr);
+        (void)hipEventDestroy(sl.done);
+    }
     (void)hipFree(p->dev_block);
     delete p;
 }

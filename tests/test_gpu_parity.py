@@ -352,6 +352,52 @@ def test_determinism_streams_chunks_permutation(H):
         assert np.array_equal(a[k], np.concatenate([q[k] for q in parts]))
 
 
+def test_scratch_growth_streams_and_per_thread_stream(H):
+    """The per-plan scratch a profile keeps per stream: batches that shrink
+    and grow on one stream, two streams pricing at once with one profile,
+    and the per-thread default stream (a fresh block per call) all give the
+    oracle's results."""
+    import ctypes as C
+    import torch
+    w = workload("c4_moe")
+    small, big = sub_workload(w, np.arange(400)), sub_workload(w, np.arange(400, 4400))
+    want_small, want_big = oracle_price(small, 0), oracle_price(big, 0)
+    prof = H.heddle_load_profile(w.profile)
+    for ww, want in ((small, want_small), (big, want_big), (small, want_small)):
+        assert_same(gpu_price(H, prof, ww, 0), want, 0, "one stream")
+    # two streams at once: enqueue both before synchronising
+    outs = []
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for ww, s in zip((big, small), streams):
+        ns, st = H.to_device(ww.n_stages, ww.stages)
+        out = H.alloc_outputs(ww.n, len(ww.m), ww.s_max, 0)
+        for v in out.values():
+            v.view(torch.uint8).fill_(POISON)
+        torch.cuda.synchronize()
+        outs.append((ns, st, out, s))
+    for (ns, st, out, s), ww in zip(outs, (big, small)):
+        H.heddle_price_plans(prof, ns, st, [int(x) for x in ww.m], 0, out, stream=s)
+    torch.cuda.synchronize()
+    for (ns, st, out, s), want in zip(outs, (want_big, want_small)):
+        assert_same({k: v.cpu().numpy() for k, v in out.items()}, want, 0, "two streams")
+    # hipStreamPerThread is the handle value 2
+    ns, st = H.to_device(small.n_stages, small.stages)
+    out = H.alloc_outputs(small.n, len(small.m), small.s_max, 0)
+    for v in out.values():
+        v.view(torch.uint8).fill_(POISON)
+    torch.cuda.synchronize()
+    mm = (C.c_int32 * len(small.m))(*[int(x) for x in small.m])
+    p = lambda t: C.c_void_p(t.data_ptr())
+    rc = H.lib().heddle_price_plans(prof.handle, small.n, small.s_max, p(ns), p(st), mm, len(small.m), 0,
+                                    p(out["iter"]), p(out["bottleneck"]), p(out["peak_mem"]), p(out["layers"]),
+                                    p(out["status"]), C.c_void_p(2))
+    assert rc == H.HEDDLE_OK, H.heddle_last_error()
+    torch.cuda.synchronize()
+    assert_same({k: v.cpu().numpy() for k, v in out.items()}, want_small, 0, "per-thread stream")
+    H.lib().heddle_free_profile(prof.handle)
+    prof.handle = C.c_void_p(None)
+
+
 # ------------------------------------------------------------------ argmin
 @pytest.mark.parametrize("flags", [0, F32, CO])
 def test_argmin_matches_oracle(H, flags):

@@ -38,6 +38,11 @@ struct DevProfile {
     const int64_t *pre_act;          // [n_tp][L+1] prefix of act
     const int64_t *pre_grad;         // [n_tp][L+1] prefix of grad
     const int64_t *pre_xgrad;        // [n_tp][n_ep][L+1] prefix of ceil(xgrad / e)
+    // the same prefixes interleaved by the index they share, so that one
+    // 16-byte read serves a stage boundary: {pre_state, pre_xgrad} and
+    // {pre_act, pre_grad}
+    const longlong2 *pair_sx;        // [n_tp][n_ep][L+1]
+    const longlong2 *pair_ag;        // [n_tp][L+1]
     const uint8_t *profiled;         // [n_types][n_tp]
     const int64_t *a2a_ns;           // [n_types][3] all-to-all time per MoE layer by variant
     const int64_t *a2a_fx;           // [n_types][3] fp32-rounded, in fixed-point units

@@ -285,6 +285,15 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
             if (gsum + xg > max_grad) max_grad = gsum + xg;
         }
     }
+    std::vector<int64_t> pair_sx(pre_state.size() * 2), pair_ag(pre_act.size() * 2);
+    for (size_t x = 0; x < pre_state.size(); x++) {
+        pair_sx[2 * x] = pre_state[x];
+        pair_sx[2 * x + 1] = pre_xgrad[x];
+    }
+    for (size_t x = 0; x < pre_act.size(); x++) {
+        pair_ag[2 * x] = pre_act[x];
+        pair_ag[2 * x + 1] = pre_grad[x];
+    }
     // Memory limits of a stage (section 5.2 memory validation): for GPU type g,
     // TP index k, EP index e and f micro-batches of activations in flight,
     // lim[i] is the largest end j >= i such that layers [i, j) fit one GPU's
@@ -459,7 +468,7 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
                  o_r32b = B.add(rows32[1]);
     size_t o_time = B.add(pre_time), o_time_fx = B.add(pre_time_fx), o_moe = B.add(pre_moe),
            o_state = B.add(pre_state), o_act = B.add(pre_act), o_grad = B.add(pre_grad),
-           o_xgrad = B.add(pre_xgrad), o_prof = B.add(d->profiled, (size_t)N * K),
+           o_xgrad = B.add(pre_xgrad), o_psx = B.add(pair_sx), o_pag = B.add(pair_ag), o_prof = B.add(d->profiled, (size_t)N * K),
            o_a2a = B.add(a2a_ns), o_a2a_fx = B.add(a2a_fx), o_p2p = B.add(p2p_ns), o_p2p_fx = B.add(p2p_fx),
            o_cap = B.add(d->mem_cap_bytes, (size_t)N * 8), o_node = B.add(d->node_size, (size_t)N * 4),
            o_ngpu = B.add(d->n_gpus, (size_t)N * 4), o_intra = B.add(d->intra_bw_MBps, (size_t)N * 8),
@@ -484,6 +493,8 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
     dp.pre_act = (const int64_t *)(base + o_act);
     dp.pre_grad = (const int64_t *)(base + o_grad);
     dp.pre_xgrad = (const int64_t *)(base + o_xgrad);
+    dp.pair_sx = (const longlong2 *)(base + o_psx);
+    dp.pair_ag = (const longlong2 *)(base + o_pag);
     dp.profiled = (const uint8_t *)(base + o_prof);
     dp.a2a_ns = (const int64_t *)(base + o_a2a);
     dp.a2a_fx = (const int64_t *)(base + o_a2a_fx);

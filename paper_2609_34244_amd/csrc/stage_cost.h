@@ -35,12 +35,14 @@ __device__ __forceinline__ StageCost stage_cost(const DevProfile &P, uint32_t re
     StageCost c;
     c.T = prow[j] - prow[i] + (uint64_t)p2p;
     const int srow = (ki * P.n_ep + ei) * R, arow = ki * R;
+    const longlong2 sx_i = P.pair_sx[srow + i], sx_j = P.pair_sx[srow + j];   // {state, expert grad}
+    const longlong2 ag_i = P.pair_ag[arow + i], ag_j = P.pair_ag[arow + j];   // {activations, dense grad}
     const int64_t f = (int64_t)(S - s) < Mp ? (int64_t)(S - s) : Mp;
-    c.mem = (P.pre_state[srow + j] - P.pre_state[srow + i]) + f * (P.pre_act[arow + j] - P.pre_act[arow + i]);
+    c.mem = (sx_j.x - sx_i.x) + f * (ag_j.x - ag_i.x);
     c.fits = c.mem <= P.mem_cap[g];
     const int64_t bw = (int64_t)tp * D <= node ? P.intra_bw[g] : P.link_bw[g * N + g];
-    c.g = allreduce_ns(P.pre_grad[arow + j] - P.pre_grad[arow + i], D, bw) +
-          allreduce_ns(P.pre_xgrad[srow + j] - P.pre_xgrad[srow + i], (int64_t)((uint32_t)D / (uint32_t)ep), bw);
+    c.g = allreduce_ns(ag_j.y - ag_i.y, D, bw) +
+          allreduce_ns(sx_j.y - sx_i.y, (int64_t)((uint32_t)D / (uint32_t)ep), bw);
     return c;
 }
 

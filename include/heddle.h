@@ -195,7 +195,7 @@ void heddle_free_profile(heddle_profile *p);
  * OOM without a split. With COMPUTE_ONLY the proportional split is kept and
  * flagged OOM if it does not fit. The bottleneck output is then the split's
  * slowest stage time.
- * Scratch: without DISTRIBUTE, about n * n_m * (1 + 2 * s_max) bytes (s_max
+ * Scratch: without DISTRIBUTE, about n * n_m * (4 + 2 * s_max) bytes (s_max
  * rounded up to a multiple of 4) for the per-plan validation and row
  * windows, in the profile's buffer of `stream`.
  * Returns HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_RANGE (the iteration time could

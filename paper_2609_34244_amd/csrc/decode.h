@@ -8,7 +8,7 @@ namespace heddle {
 
 // Per-lane (lane = stage s) decoded record and stage constants.
 template <class V> struct StageInfo {
-    int S, D;                // uniform
+    int S;                   // uniform
     int prow;                // offset of the stage's time-prefix row
     int lrow;                // offset of the stage's memory-limit rows (in-flight count 1)
     V p2p;                   // outbound p2p (ns, or fixed point for fp32)
@@ -33,7 +33,6 @@ __device__ StageInfo<V> stage_info(const DevProfile &P, const PriceArgs &A, int 
     // unsigned 32-bit offsets from uniform table bases
     const int node = P.node_size[(uint32_t)g];
     const int64_t p2p = F32 ? P.p2p_fx[(uint32_t)(g * N + gn)] : P.p2p_ns[(uint32_t)(g * N + gn)];
-    x.D = (int)(__builtin_amdgcn_readfirstlane(rec_in) >> 16);
     x.prow = act ? ((g * P.n_tp + ki) * 3 + a2a_variant(ep, tp, node)) * R : 0;
     x.lrow = act ? ((g * P.n_tp + ki) * P.n_ep + ei) * P.n_f * 2 * P.lim_stride : 0;
     x.p2p = lane < S - 1 ? (V)p2p : (V)0;

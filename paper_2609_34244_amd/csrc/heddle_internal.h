@@ -143,7 +143,9 @@ struct PriceArgs {
     int32_t off_j, off_x;            // byte offsets of the per-stage limit rows and of the next-row
                                      // tables (shared with the G arena)
     int32_t arena_cap;               // entries of the G arena
-    uint8_t *wst;                    // [n][n_m] status after validation and windows (0: windows found)
+    uint32_t *wst;                   // [n][n_m] status after validation and windows (0: windows found)
+                                     // | in-flight class min(ceil(m / D), S) << 8 (0: memory ignored)
+                                     // | rows of the windows W_1 .. W_{S-1} << 16 (status 0 only)
     uint16_t *wwin;                  // [n][n_m][win_stride(s_max)] window of stage s: first row | last row << 8
     bool scratch_owned;              // host side: wst lives in a block of its own (hipStreamPerThread)
 };

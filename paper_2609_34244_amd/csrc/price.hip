@@ -101,8 +101,6 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
     // (su, pc) copies piece pc of stage s0 + su
     const int h16 = ls >> 4, per = 64 / h16;
     const int su = lane / h16, pc = lane - su * h16;
-    int my_m = 1;                                              // lane k: the k-th micro-batch count
-    for (int k = 0; k < A.n_m; k++) my_m = lane == k ? A.m[k] : my_m;
     unsigned long long work = 0;
 
     // the template records of the next iteration are loaded one iteration ahead
@@ -122,8 +120,12 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
             rec_next = lane < A.s_max ? A.stages[(t + stride) * A.s_max + lane] : 0u;
         }
         const size_t obase = (size_t)t * A.n_m;
-        // lane k: status of plan k after validation and windows (0: windows found)
-        const int pst = lane < A.n_m ? A.wst[obase + lane] : HEDDLE_S_OOM;
+        // lane k: status of plan k after validation and windows (0: windows found),
+        // its in-flight class min(M_p, S) (0 when memory is ignored), which fixes
+        // the split (M_p = ceil(m / D) micro-batches per replica), and the rows of
+        // its windows W_1 .. W_{S-1}
+        const uint32_t wv = lane < A.n_m ? A.wst[obase + lane] : (uint32_t)HEDDLE_S_OOM;
+        const int pst = (int)(wv & 255), key_k = (int)((wv >> 8) & 255);
         uint64_t todo = ballot(lane < A.n_m && pst == HEDDLE_S_OK);
         bool r_split = false;                                  // lane k: a split was found for m index k
         V r_b = INF;
@@ -131,10 +133,6 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
         if (todo) {
             const int S = uni(S_in);
             const StageInfo<V> x = stage_info<V, F32>(P, A, S, rec_in, lane);
-            const int D = x.D;
-            // micro-batches per replica M_p = ceil(m / D); min(M_p, S) fixes the split
-            const int Mp_k = (int)(((uint32_t)my_m + (uint32_t)D - 1) / (uint32_t)D);
-            const int key_k = mem_aware ? (Mp_k < S ? Mp_k : S) : 0;
 
             while (todo) {
                 const int key = A.n_m == 1 ? uni(key_k)
@@ -161,16 +159,16 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                 }
 
                 // ---------------- row windows (from the window pass): lane s holds [a_s, b_s]
-                int Al, Bl;
+                int Al, Bl, g_total;
                 {
                     const int k0 = __ffsll((unsigned long long)cls) - 1;   // a plan of this class
                     const uint32_t w = lane < S ? A.wwin[(obase + k0) * win_stride(A.s_max) + lane] : 0u;
                     Al = (int)(w & 255);
                     Bl = (int)(w >> 8);
+                    g_total = uni(rl32((int)(wv >> 16), k0));
                 }
                 // G arena: G_s over the rows of W_s for s = S-1 .. 1, stored in that order,
                 // when all of them fit; else the second backward pass rebuilds F
-                const int g_total = uni((int)wave_sum((uint32_t)(lane >= 1 && lane < S ? Bl - Al + 1 : 0)));
                 const bool arena = !COUNT && g_total <= A.arena_cap;
 
                 // ---------------- PartitionLayers: suffix min-max DP over the windows, stages S-1 .. 0
@@ -470,12 +468,12 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     // validation and windows of every plan into the profile's scratch of this
     // stream (the caller holds its lock and marks the end of its use)
     const size_t plans = (size_t)a.n * a.n_m;
-    const size_t st_bytes = (plans + 255) & ~size_t(255);
+    const size_t st_bytes = (plans * sizeof(uint32_t) + 255) & ~size_t(255);
     unsigned char *buf = nullptr;
     const int rs = profile_scratch(p, stream, st_bytes + plans * win_stride(a.s_max) * sizeof(uint16_t),
                                    (void **)&buf, &a.scratch_owned);
     if (rs != HEDDLE_OK) return rs;
-    a.wst = buf;
+    a.wst = (uint32_t *)buf;
     a.wwin = (uint16_t *)(buf + st_bytes);
     const int rw = launch_windows(p, a, w_lds, stream);
     if (rw != HEDDLE_OK) return rw;

@@ -55,7 +55,7 @@ __global__ void __launch_bounds__(64) window_kernel(DevProfile P, PriceArgs A)
         const size_t obase = (size_t)t * A.n_m;
         const int status = validate_lane(P, A, S, rec, cnt);
         if (status != HEDDLE_S_OK) {
-            for (int k = 0; k < A.n_m; k++) A.wst[obase + k] = (uint8_t)status;
+            for (int k = 0; k < A.n_m; k++) A.wst[obase + k] = (uint32_t)status;
             continue;
         }
         const uint32_t D = rec[0] >> 16;
@@ -97,6 +97,7 @@ __global__ void __launch_bounds__(64) window_kernel(DevProfile P, PriceArgs A)
                 }
             }
             bool fits = true;
+            uint32_t rows = 0;                                 // rows of W_1 .. W_{S-1}
             for (int s0 = 0; s0 < S; s0 += 4) {
                 uint32_t w[4];
 #pragma unroll
@@ -107,11 +108,12 @@ __global__ void __launch_bounds__(64) window_kernel(DevProfile P, PriceArgs A)
                     int b = mem_aware ? (int)lR[s * 64] : ihi;
                     b = b < ihi ? b : ihi;
                     fits = fits && a <= b;
+                    rows += s0 + q < S && s > 0 ? (uint32_t)(b - a + 1) : 0u;
                     w[q] = (uint32_t)(a | b << 8);
                 }
                 wout[s0 >> 2] = make_uint2(w[0] | w[1] << 16, w[2] | w[3] << 16);
             }
-            A.wst[o] = fits ? (uint8_t)HEDDLE_S_OK : (uint8_t)HEDDLE_S_OOM;
+            A.wst[o] = fits ? (uint32_t)HEDDLE_S_OK | (uint32_t)key << 8 | rows << 16 : (uint32_t)HEDDLE_S_OOM;
         }
     }
 }

@@ -104,8 +104,18 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
     unsigned long long work = 0;
 
     // the template records of the next iteration are loaded one iteration ahead
+    // Workgroups are handed to the 8 XCDs round robin (workgroup b to XCD
+    // x = b mod 8). With a grid that is a multiple of 512, each round of the
+    // grid-stride loop gives XCD x the runs of 64 consecutive templates whose
+    // run index is x mod 8 (workgroup b, j = b / 8, takes position j mod 64 of
+    // run 8 (j / 64) + x), so a run's records, status words and outputs share
+    // one XCD's L2 lines while a partial last round still spreads over all XCDs.
     const int64_t stride = gridDim.x;
     int64_t t = blockIdx.x;
+    if ((gridDim.x & 511) == 0) {
+        const uint32_t x = blockIdx.x & 7, j = blockIdx.x >> 3;
+        t = (int64_t)((((j >> 6) << 3) + x) << 6) + (j & 63);
+    }
     int S_next = 0;
     uint32_t rec_next = 0;
     if (t < A.n) {
@@ -478,7 +488,8 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     const int rw = launch_windows(p, a, w_lds, stream);
     if (rw != HEDDLE_OK) return rw;
     const int64_t want = (a.n + wpb - 1) / wpb;
-    const int blocks = (int)(want < 65536 ? want : 65536);
+    int blocks = (int)(want < 65536 ? want : 65536);
+    if (blocks >= 512) blocks = (blocks + 511) & ~511;        // XCD-aware runs (see the kernel's start)
     // time-prefix slots of 64 entries held in registers: 2 cover L + 1 <= 128
     if (L + 1 <= 128)
         hipLaunchKernelGGL((split_kernel<V, F32, COUNT, 2>), dim3(blocks), dim3(64 * wpb), lds, stream, p->dev, a);

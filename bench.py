@@ -75,6 +75,17 @@ def measured_traffic(config, flags, n_plans, distribute=False):
     return t.get("bytes_per_launch")
 
 
+def host_cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(w, flags, budget_s):
     from oracle import oracle as O
     op = O.OracleProfile(w.profile)
@@ -88,7 +99,7 @@ def cpu_baseline(w, flags, budget_s):
     dt = time.perf_counter() - t0
     return {"value": n * len(w.m) / dt, "unit": "plans/s", "cores": 1, "kind": "oracle",
             "sample": f"first {n} of {w.n} templates x {len(w.m)} m, single-threaded plain C oracle, {dt:.1f} s",
-            "host_cores_available": len(os.sched_getaffinity(0))}
+            "host_cores_available": len(os.sched_getaffinity(0)), "host_cpu": host_cpu_model()}
 
 
 def main():
@@ -432,7 +443,7 @@ def cpu_baseline_enumerate(w, spec, m, flags, total, budget_s):
     return {"value": n * len(m) / dt, "unit": "plans/s", "cores": 1, "kind": "oracle",
             "sample": f"{n} templates drawn uniformly from the {total:,} of the space x {len(m)} m, "
                       f"single-threaded plain C oracle, {dt:.1f} s",
-            "host_cores_available": len(os.sched_getaffinity(0))}
+            "host_cores_available": len(os.sched_getaffinity(0)), "host_cpu": host_cpu_model()}
 
 
 if __name__ == "__main__":

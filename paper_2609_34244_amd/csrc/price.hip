@@ -48,7 +48,7 @@ __device__ __forceinline__ void fetch_rows(RowRegs<V, NS> &r, const V *prow, int
 {
 #pragma unroll
     for (int q = 0; q < NS; q++)
-        if (64 * q <= e - a) r.p[q] = prow[(uint32_t)min(a + lane + 64 * q, e)];     // uniform condition
+        if (q == 0 || 64 * q <= e - a) r.p[q] = prow[(uint32_t)min(a + lane + 64 * q, e)];   // uniform; e >= a
 }
 
 // ------------------------------------------------------------ split kernel
@@ -203,7 +203,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                     // P_s into the pair row over [a, e]; G_{s+1} stays in place
 #pragma unroll
                     for (int q = 0; q < NS; q++)
-                        if (64 * q <= e - a) ((V *)&X[min(a + lane + 64 * q, e)])[0] = rr.p[q];
+                        if (q == 0 || 64 * q <= e - a) ((V *)&X[min(a + lane + 64 * q, e)])[0] = rr.p[q];
                     if (s > 0) {
                         const uint32_t kp = uni64(prv, s);
                         fetch_rows<V, NS>(rr, rows + (kp & 0xFFFFFFu), (int)(kp >> 24), b, lane);
@@ -240,7 +240,8 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         const int lk = r >= 64 ? 0 : 6 - (r > 1 ? 32 - __clz(r - 1) : 0);
                         const int k = 1 << lk;
                         const int part = lane & (k - 1);
-                        for (int base = a; base <= b; base += 64 >> lk) {
+                        int base = a;                                      // windows are not empty
+                        do {
                             const int i = base + (lane >> lk);
                             const int ic = min(i, b);
                             const int lo = max(ic + 1, a_next);
@@ -275,7 +276,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                                     if (arena) GA[goff + i - a] = acc;
                                 }
                             }
-                        }
+                        } while ((base += 64 >> lk) <= b);
                     }
                     goff += b - a + 1;
                     wave_sync();
@@ -309,9 +310,12 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         };
                         int w0 = lo & ~63;
                         uint64_t mk = word(w0) & (~0ull << (lo - w0));   // rows from lo
-                        while (!mk && w0 + 64 <= w1) {
-                            w0 += 64;
-                            mk = word(w0);
+                        if (!mk) {
+                            while (w0 + 64 <= w1) {
+                                w0 += 64;
+                                mk = word(w0);
+                                if (mk) break;
+                            }
                         }
                         const int nx = mk ? a1 + w0 + __ffsll((unsigned long long)mk) - 1 : L;   // L: unreachable
                         cs = nx;

@@ -151,9 +151,5 @@ template <> struct Vec2<uint64_t> { typedef uint64_t type __attribute__((ext_vec
 template <class V> struct DPInf { static constexpr V value = ~V(0); };
 
 // all-to-all variant of a stage: none (EP = 1), inside one node, across nodes
-__device__ __forceinline__ int a2a_variant(int ep, int tp, int node)
-{
-    return ep == 1 ? kA2ANone : (ep * tp <= node ? kA2AIntra : kA2AInter);
-}
 
 }  // namespace heddle

@@ -22,6 +22,10 @@ constexpr uint32_t kNarrowLimit = 0x7FFFFFFFu;   // exact 32-bit DP when every s
 // a2a variant of a stage: no all-to-all (EP = 1), EP x TP group inside one
 // node (intra-node bandwidth), or spanning nodes (same-type inter-node link)
 enum A2AVariant { kA2ANone = 0, kA2AIntra = 1, kA2AInter = 2 };
+__host__ __device__ inline int a2a_variant(int ep, int tp, int node)
+{
+    return ep == 1 ? kA2ANone : (ep * tp <= node ? kA2AIntra : kA2AInter);
+}
 
 // Device-resident derived tables of one profile. Passed by value to kernels.
 // Prefix rows have L + 1 entries: row[j] = sum over layers l < j.
@@ -43,6 +47,10 @@ struct DevProfile {
     // {pre_act, pre_grad}
     const longlong2 *pair_sx;        // [n_tp][n_ep][L+1]
     const longlong2 *pair_ag;        // [n_tp][L+1]
+    // by the low 16 bits of a valid stage record (type | log2 TP << 8 | log2 EP
+    // << 12): {offset of its time-prefix row in rows32 / rows64, byte offset of
+    // its memory-limit rows (in-flight count 1)}; 0 for invalid combinations
+    const uint2 *stage_tab;          // [65536]
     const uint8_t *profiled;         // [n_types][n_tp]
     const int64_t *a2a_ns;           // [n_types][3] all-to-all time per MoE layer by variant
     const int64_t *a2a_fx;           // [n_types][3] fp32-rounded, in fixed-point units

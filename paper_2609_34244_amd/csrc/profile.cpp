@@ -462,13 +462,29 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
         }
     }
 
+    // ---- per stage record: time-row and limit-row offsets
+    std::vector<uint32_t> stage_tab((size_t)65536 * 2, 0);
+    for (int g = 0; g < N; g++)
+        for (int l2tp = 0; l2tp < 16; l2tp++) {
+            if (!((dp.tp_present >> l2tp) & 1)) continue;
+            const int k = (int)((dp.tp_index >> (4 * l2tp)) & 15);
+            for (int l2ep = 0; l2ep < 16; l2ep++) {
+                if (!((dp.ep_present >> l2ep) & 1)) continue;
+                const int e = (int)((dp.ep_index >> (4 * l2ep)) & 15);
+                const size_t idx = (size_t)(g | l2tp << 8 | l2ep << 12);
+                const int var = a2a_variant(1 << l2ep, 1 << l2tp, d->node_size[g]);
+                stage_tab[2 * idx] = (uint32_t)((((size_t)g * K + k) * 3 + var) * R);
+                stage_tab[2 * idx + 1] = (uint32_t)((((size_t)g * K + k) * E + e) * F * 2 * RL);
+            }
+        }
+
     // ---- upload
     Builder B;
     const size_t o_r64a = B.add(rows64[0]), o_r64b = B.add(rows64[1]), o_r32a = B.add(rows32[0]),
                  o_r32b = B.add(rows32[1]);
     size_t o_time = B.add(pre_time), o_time_fx = B.add(pre_time_fx), o_moe = B.add(pre_moe),
            o_state = B.add(pre_state), o_act = B.add(pre_act), o_grad = B.add(pre_grad),
-           o_xgrad = B.add(pre_xgrad), o_psx = B.add(pair_sx), o_pag = B.add(pair_ag), o_prof = B.add(d->profiled, (size_t)N * K),
+           o_xgrad = B.add(pre_xgrad), o_psx = B.add(pair_sx), o_pag = B.add(pair_ag), o_stab = B.add(stage_tab), o_prof = B.add(d->profiled, (size_t)N * K),
            o_a2a = B.add(a2a_ns), o_a2a_fx = B.add(a2a_fx), o_p2p = B.add(p2p_ns), o_p2p_fx = B.add(p2p_fx),
            o_cap = B.add(d->mem_cap_bytes, (size_t)N * 8), o_node = B.add(d->node_size, (size_t)N * 4),
            o_ngpu = B.add(d->n_gpus, (size_t)N * 4), o_intra = B.add(d->intra_bw_MBps, (size_t)N * 8),
@@ -495,6 +511,7 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
     dp.pre_xgrad = (const int64_t *)(base + o_xgrad);
     dp.pair_sx = (const longlong2 *)(base + o_psx);
     dp.pair_ag = (const longlong2 *)(base + o_pag);
+    dp.stage_tab = (const uint2 *)(base + o_stab);
     dp.profiled = (const uint8_t *)(base + o_prof);
     dp.a2a_ns = (const int64_t *)(base + o_a2a);
     dp.a2a_fx = (const int64_t *)(base + o_a2a_fx);

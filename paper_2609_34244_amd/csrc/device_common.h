@@ -81,21 +81,30 @@ constexpr int kDppWaveShr1 = 0x138;     // lane i <- lane i - 1 across the wavef
 // every lane of a group receives the group's minimum
 template <class T> __device__ __forceinline__ T group_min(T v, int k)
 {
+    // nested, so that a runtime k stops at the first level that does not apply
     T u;
-    if (k >= 2) { u = dpp<kDppXor1>(v); v = u < v ? u : v; }
-    if (k >= 4) { u = dpp<kDppXor2>(v); v = u < v ? u : v; }
-    if (k >= 8) { u = dpp<kDppHalfMirror>(v); v = u < v ? u : v; }
-    if (k >= 16) { u = dpp<kDppMirror>(v); v = u < v ? u : v; }
-    if (k >= 32) {                                   // rows of 16 combined through scalar reads
-        const int lane = __lane_id();
-        T r0 = (T)rl64((int64_t)v, 0), r1 = (T)rl64((int64_t)v, 16), r2 = (T)rl64((int64_t)v, 32),
-          r3 = (T)rl64((int64_t)v, 48);
-        if (k == 32) {
-            const T lo = r0 < r1 ? r0 : r1, hi = r2 < r3 ? r2 : r3;
-            v = lane < 32 ? lo : hi;
-        } else {
-            const T a = r0 < r1 ? r0 : r1, b = r2 < r3 ? r2 : r3;
-            v = a < b ? a : b;
+    if (k >= 2) {
+        u = dpp<kDppXor1>(v); v = u < v ? u : v;
+        if (k >= 4) {
+            u = dpp<kDppXor2>(v); v = u < v ? u : v;
+            if (k >= 8) {
+                u = dpp<kDppHalfMirror>(v); v = u < v ? u : v;
+                if (k >= 16) {
+                    u = dpp<kDppMirror>(v); v = u < v ? u : v;
+                    if (k >= 32) {                   // rows of 16 combined through scalar reads
+                        const int lane = __lane_id();
+                        T r0 = (T)rl64((int64_t)v, 0), r1 = (T)rl64((int64_t)v, 16), r2 = (T)rl64((int64_t)v, 32),
+                          r3 = (T)rl64((int64_t)v, 48);
+                        if (k == 32) {
+                            const T lo = r0 < r1 ? r0 : r1, hi = r2 < r3 ? r2 : r3;
+                            v = lane < 32 ? lo : hi;
+                        } else {
+                            const T a = r0 < r1 ? r0 : r1, b = r2 < r3 ? r2 : r3;
+                            v = a < b ? a : b;
+                        }
+                    }
+                }
+            }
         }
     }
     return v;

@@ -270,7 +270,12 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                             if (s == 0) {
                                 Bv = (V)rl64((int64_t)group_min<V>(acc, 64), 0);   // row 0 only
                             } else {
-                                acc = group_min<V>(acc, k);
+                                // an opaque copy of k keeps the level tests of the minimum at
+                                // their use (one compare and branch each) instead of masks
+                                // hoisted out of the row loop for every level
+                                int kr = k;
+                                asm volatile("" : "+s"(kr));
+                                acc = group_min<V>(acc, kr);
                                 if (i <= b && part == 0) {
                                     ((V *)&X[i])[1] = acc;
                                     if (arena) GA[goff + i - a] = acc;

@@ -200,8 +200,10 @@ void heddle_free_profile(heddle_profile *p);
  * windows, in the profile's buffer of `stream`.
  * Returns HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_RANGE (the iteration time could
  * exceed 2^62 for these m, or the fp32 costs span too wide a range to sum
- * exactly), HEDDLE_E_NOMEM (the scratch) or HEDDLE_E_DEVICE. On error nothing
- * is enqueued.
+ * exactly), HEDDLE_E_NOMEM (the scratch) or HEDDLE_E_DEVICE. With
+ * HEDDLE_E_INVAL or HEDDLE_E_RANGE nothing is enqueued; with HEDDLE_E_NOMEM or
+ * HEDDLE_E_DEVICE part of the call's work (scratch set-up, the window pass)
+ * may already be on the stream and the outputs are undefined.
  */
 int heddle_price_plans(const heddle_profile *p, int64_t n, int32_t s_max,
                        const uint8_t *d_n_stages, const uint32_t *d_stages,

@@ -86,6 +86,42 @@ def host_cpu_model():
     return None
 
 
+_ALL_CORES = {}
+
+
+def _oracle_chunk(task):
+    lo, n = task
+    from oracle import oracle as O
+    w, flags = _ALL_CORES["w"], _ALL_CORES["flags"]
+    op = O.OracleProfile(w.profile)
+    O.price_plans(op, w.n_stages, w.stages, w.m, flags, lo, lo + n)   # templates [lo, lo + n)
+    return n
+
+
+def cpu_baseline_all_cores(w, flags, budget_s):
+    """The same unmodified oracle, one process per host core over disjoint
+    chunks of the batch (forked before the GPU is initialised)."""
+    import multiprocessing as mp
+    from oracle import oracle as O
+    op = O.OracleProfile(w.profile)
+    probe = min(20, w.n)
+    t0 = time.perf_counter()
+    O.price_plans(op, w.n_stages, w.stages, w.m, flags, 0, probe)
+    per = (time.perf_counter() - t0) / probe
+    cores = min(16, len(os.sched_getaffinity(0)))
+    n_each = int(max(1, min(w.n // cores, budget_s / max(per, 1e-9))))
+    _ALL_CORES.update(w=w, flags=flags)
+    tasks = [(i * n_each, n_each) for i in range(cores)]
+    with mp.get_context("fork").Pool(cores) as pool:
+        t0 = time.perf_counter()
+        done = sum(pool.map(_oracle_chunk, tasks, chunksize=1))
+        dt = time.perf_counter() - t0
+    _ALL_CORES.clear()
+    return {"value": done * len(w.m) / dt, "unit": "plans/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {done} of {w.n} templates x {len(w.m)} m in {cores} chunks, one oracle process "
+                      f"per core, {dt:.1f} s wall"}
+
+
 def cpu_baseline(w, flags, budget_s):
     from oracle import oracle as O
     op = O.OracleProfile(w.profile)
@@ -139,6 +175,18 @@ def main():
     from paper_2609_34244_amd import heddle as H
     from workloads.gen import make_workload
 
+    flags = (H.HEDDLE_F_FP32 if args.fp32 else 0) | (H.HEDDLE_F_COMPUTE_ONLY if args.compute_only else 0) | \
+        (H.HEDDLE_F_DISTRIBUTE if args.distribute else 0)
+    w = None
+    cpu_all = None
+    if not (args.copy_calibration or args.enumerate or args.fill):
+        t0 = time.perf_counter()
+        w = make_workload(args.config)
+        log(f"workload {args.config}: {w.n} templates x {len(w.m)} m generated in {time.perf_counter() - t0:.1f}s")
+        if not args.no_cpu_baseline:
+            log(f"oracle baseline on every host core, about {args.cpu_seconds:.0f} s (before the GPU is initialised)")
+            cpu_all = cpu_baseline_all_cores(w, flags, args.cpu_seconds)
+
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.copy_calibration:
         src = torch.ones(args.copy_calibration, dtype=torch.uint8, device="cuda")
@@ -148,17 +196,11 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": args.copy_calibration}))
         return
-    flags = (H.HEDDLE_F_FP32 if args.fp32 else 0) | (H.HEDDLE_F_COMPUTE_ONLY if args.compute_only else 0) | \
-        (H.HEDDLE_F_DISTRIBUTE if args.distribute else 0)
     k_unit, unit_name = (K_EVAL, "stage-cost evaluation") if args.distribute else (K_MIN, "DP relaxation")
     if args.enumerate:
         return run_enumerate(args, H, flags, k_unit, unit_name)
     if args.fill:
         return run_fill(args, H, flags)
-    t0 = time.perf_counter()
-    w = make_workload(args.config)
-    log(f"workload {args.config}: {w.n} templates x {len(w.m)} m generated in {time.perf_counter() - t0:.1f}s")
-
     t0 = time.perf_counter()
     prof = H.heddle_load_profile(w.profile)
     load_ms = (time.perf_counter() - t0) * 1e3
@@ -273,6 +315,7 @@ def main():
     if not args.no_cpu_baseline:
         log(f"oracle baseline, about {args.cpu_seconds:.0f} s on one host core")
         result["cpu_baseline"] = cpu_baseline(w, flags, args.cpu_seconds)
+        result["cpu_baseline"]["all_cores"] = cpu_all
     print(json.dumps(result), flush=True)
 
 

@@ -113,6 +113,18 @@ __global__ void __launch_bounds__(kArgBlock) argmin_pass2(const Cand *partial, i
     if (threadIdx.x == 0) *out = best;
 }
 
+// Pass 2 writes its result straight into pinned, coherent host memory: one
+// slot per host thread (the call waits for its stream before reading it, so
+// calls of one thread never overlap), allocated on first use and kept.
+static thread_local Cand *t_result = nullptr;
+
+static Cand *result_slot()
+{
+    if (!t_result && hipHostMalloc((void **)&t_result, sizeof(Cand), hipHostMallocPortable | hipHostMallocCoherent) != hipSuccess)
+        t_result = nullptr;
+    return t_result;
+}
+
 int launch_argmin(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t flags, const void *d_iter,
                   const uint8_t *d_status, int64_t *h_best_template, int32_t *h_best_m_index,
                   void *h_best_iter, hipStream_t stream)
@@ -130,18 +142,22 @@ int launch_argmin(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t flags, co
     const int64_t want = (total + kArgBlock * 8 - 1) / (kArgBlock * 8);
     const int blocks = (int)(want < kArgMaxBlocks ? (want > 0 ? want : 1) : kArgMaxBlocks);
     Cand *scratch = nullptr;
-    hipError_t e = scratch_alloc((void **)&scratch, sizeof(Cand) * (blocks + 1), stream);
+    hipError_t e = scratch_alloc((void **)&scratch, sizeof(Cand) * blocks, stream);
     if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "device scratch for argmin partials could not be allocated");
     a.partial = scratch;
     hipLaunchKernelGGL(argmin_pass1, dim3(blocks), dim3(kArgBlock), 0, stream, a);
-    hipLaunchKernelGGL(argmin_pass2, dim3(1), dim3(kArgBlock), 0, stream, (const Cand *)scratch, blocks, a.f32,
-                       scratch + blocks);
-    Cand h;
+    Cand *res = result_slot();
+    if (!res) {
+        (void)hipFreeAsync(scratch, stream);
+        return fail(HEDDLE_E_NOMEM, "pinned host memory for the argmin result could not be allocated");
+    }
+    hipLaunchKernelGGL(argmin_pass2, dim3(1), dim3(kArgBlock), 0, stream, (const Cand *)scratch, blocks, a.f32, res);
     e = hipGetLastError();
-    if (e == hipSuccess) e = hipMemcpyAsync(&h, scratch + blocks, sizeof(h), hipMemcpyDeviceToHost, stream);
-    (void)hipFreeAsync(scratch, stream);                       // stream-ordered after the copy
+    (void)hipFreeAsync(scratch, stream);                       // stream-ordered after pass 2
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
     if (e != hipSuccess) return hip_fail(e, "argmin");
+    Cand h;
+    std::memcpy(&h, (const void *)res, sizeof(h));
     if (h.idx < 0) return fail(HEDDLE_E_NOFEASIBLE, "no plan has status OK");
     *h_best_template = h.idx / n_m;
     *h_best_m_index = (int32_t)(h.idx % n_m);

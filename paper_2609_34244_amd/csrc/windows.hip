@@ -16,23 +16,22 @@
 // Mapping: one lane per template, 64 templates per wavefront. The
 // wavefront's template records are staged in LDS with coalesced loads
 // (row stride s_max + 1 words, so that the lanes' column reads do not share
-// banks); each lane then chases its own limit rows in global memory (the
+// banks); each lane validates its template (per-type GPU counters in an LDS
+// column of its own), then chases its own limit rows in global memory (the
 // forward and backward chases are independent and taken in one loop),
-// keeping R_s and Bk_s in LDS columns ([stage][lane]), and writes its
-// windows four at a time.
+// keeping R_s and Bk_s in the two upper bytes of its staged record s (the DP
+// degree they held is read before), and writes its windows four at a time.
 #include "validate.h"
 
 namespace heddle {
 
-__global__ void __launch_bounds__(64) window_kernel(DevProfile P, PriceArgs A)
+__global__ void __launch_bounds__(64, 8) window_kernel(DevProfile P, PriceArgs A)
 {
     extern __shared__ __align__(16) unsigned char smem[];      // one wavefront per workgroup
     const int lane = threadIdx.x;
     const int rs = A.s_max + 1;                                // staged record stride, words
     uint32_t *cnt = (uint32_t *)smem + lane;                   // [n_types][64] GPU counters of validation
     uint32_t *recs = (uint32_t *)smem + (size_t)P.n_types * 64;   // [64][rs] the wavefront's records
-    uint8_t *lR = (uint8_t *)(recs + 64 * rs) + lane;          // [s_cap][64] forward reach R_s
-    uint8_t *lK = lR + (size_t)A.s_cap * 64;                   // [s_cap][64] backward bound Bk_s
     const int L = P.L, ls = P.lim_stride;
     const int ws = win_stride(A.s_max);
     const bool mem_aware = (A.flags & HEDDLE_F_COMPUTE_ONLY) == 0;
@@ -52,6 +51,7 @@ __global__ void __launch_bounds__(64) window_kernel(DevProfile P, PriceArgs A)
         const int64_t t = t0 + lane;
         const int S = A.n_stages[t];
         const uint32_t *rec = recs + lane * rs;
+        uint8_t *rk = (uint8_t *)(recs + lane * rs);           // byte 4s + 2: R_s, byte 4s + 3: Bk_s
         const size_t obase = (size_t)t * A.n_m;
         const int status = validate_lane(P, A, S, rec, cnt);
         if (status != HEDDLE_S_OK) {
@@ -80,7 +80,7 @@ __global__ void __launch_bounds__(64) window_kernel(DevProfile P, PriceArgs A)
                 int c = 0, nxt = L;                            // R_s, Bk_{u+1}
                 for (int s = 0; s < S; s++) {
                     const int u = S - 1 - s;
-                    lR[s * 64] = (uint8_t)c;
+                    rk[4 * s + 2] = (uint8_t)c;
                     const uint32_t rf = rec[s], rb = rec[u];
                     auto rows_of = [&](uint32_t r, int st) -> const uint8_t * {
                         const int ki = nibble(P.tp_index, (r >> 8) & 15), ei = nibble(P.ep_index, (r >> 12) & 15);
@@ -93,7 +93,7 @@ __global__ void __launch_bounds__(64) window_kernel(DevProfile P, PriceArgs A)
                     const int jhi = L - (S - 1 - s);
                     c = cf < jhi ? cf : jhi;                   // R_{s+1}
                     nxt = kb > u ? kb : u;                     // Bk_u
-                    lK[u * 64] = (uint8_t)nxt;
+                    rk[4 * u + 3] = (uint8_t)nxt;
                 }
             }
             bool fits = true;
@@ -104,8 +104,8 @@ __global__ void __launch_bounds__(64) window_kernel(DevProfile P, PriceArgs A)
                 for (int q = 0; q < 4; q++) {
                     const int s = s0 + q < S ? s0 + q : S - 1;    // entries beyond S repeat the last one
                     const int ihi = s == 0 ? 0 : L - (S - s);
-                    const int a = mem_aware ? (int)lK[s * 64] : s;
-                    int b = mem_aware ? (int)lR[s * 64] : ihi;
+                    const int a = mem_aware ? (int)rk[4 * s + 3] : s;
+                    int b = mem_aware ? (int)rk[4 * s + 2] : ihi;
                     b = b < ihi ? b : ihi;
                     fits = fits && a <= b;
                     rows += s0 + q < S && s > 0 ? (uint32_t)(b - a + 1) : 0u;
@@ -120,7 +120,7 @@ __global__ void __launch_bounds__(64) window_kernel(DevProfile P, PriceArgs A)
 
 int prepare_windows(const heddle_profile *p, const PriceArgs &a, int max_lds, size_t *lds)
 {
-    *lds = (size_t)p->dev.n_types * 256 + (size_t)64 * (a.s_max + 1) * 4 + (size_t)a.s_cap * 128;
+    *lds = (size_t)p->dev.n_types * 256 + (size_t)64 * (a.s_max + 1) * 4;
     if (*lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "per-lane tables of this profile do not fit in LDS");
     if (*lds > 65536)
         HEDDLE_HIP(hipFuncSetAttribute((const void *)window_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)*lds));

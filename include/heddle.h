@@ -36,7 +36,9 @@
  * heddle_free_profile, which waits for the last use of each. Pricing calls
  * that share a profile take its lock while they enqueue their launches (their
  * device work still overlaps across streams). With hipStreamPerThread the
- * buffer is a fresh stream-ordered block per call.
+ * buffer is a fresh stream-ordered block per call. The argmin entry points
+ * return their result through a small pinned host buffer per host thread,
+ * allocated on the thread's first call and kept until the process ends.
  */
 #ifndef HEDDLE_H
 #define HEDDLE_H

@@ -21,6 +21,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9       # CUs x SIMDs x lanes x clock: 32-bit VALU lane-ops/s
+HBM_PEAK = 8e12                             # MI355X HBM3E bytes/s (context: the path is not memory bound)
 K_MIN = 3                                   # sub, max, min per relaxation (32-bit DP)
 # Distribute: 32-bit lane-ops of one stage-cost evaluation counted from its
 # integer arithmetic, leaving out the two all-reduce divisions: time
@@ -303,6 +304,8 @@ def main():
                                 (" + expert tiling" if args.tiling else "")},
         "roofline": dict({"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
                           "unit": "Tlane-op/s", "frac": achieved / PEAK_LANE_OPS, "traffic": traffic,
+                          "traffic_GBps": None if traffic is None else traffic / kern_s / 1e9,
+                          "hbm_frac": None if traffic is None else traffic / kern_s / HBM_PEAK,
                           "kernel_ms": float(np.mean(kern_ms))}, **roof),
         "statuses": statuses,
         "tiling": None if not args.tiling else dict({

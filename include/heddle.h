@@ -33,7 +33,7 @@
  * calls until the process ends. The exception is the pricing path's per-plan
  * scratch (heddle_price_plans and the entry points built on it): a profile
  * keeps one buffer per stream it was used on, grown on demand, until
- * heddle_free_profile, which waits for the last use of each. Pricing calls
+ * heddle_free_profile. Pricing calls
  * that share a profile take its lock while they enqueue their launches (their
  * device work still overlaps across streams). With hipStreamPerThread the
  * buffer is a fresh stream-ordered block per call. The argmin entry points
@@ -148,9 +148,10 @@ typedef struct heddle_profile heddle_profile;   /* opaque, device-resident table
  */
 int heddle_load_profile(const heddle_profile_desc *d, heddle_profile **out);
 
-/* Release a profile and its per-stream scratch buffers (waiting for the
- * device work that last used each). NULL is ignored. No host thread may be
- * inside a call that uses it. */
+/* Release a profile and its per-stream scratch buffers. Waits for the work
+ * on the profile's device first, so device work of earlier calls may still
+ * be in flight; no host thread may be inside a call that uses the profile.
+ * NULL is ignored. */
 void heddle_free_profile(heddle_profile *p);
 
 /*

@@ -553,12 +553,17 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
 extern "C" void heddle_free_profile(heddle_profile *p)
 {
     if (!p) return;
-    for (auto &sl : p->scratch) {                              // waits for the last use of each buffer
-        (void)hipEventSynchronize(sl.done);
+    // device work of earlier calls may still read the tables or the scratch
+    // buffers: wait for the profile's device before releasing them
+    int prev = -1;
+    const bool switched = hipGetDevice(&prev) == hipSuccess && prev != p->device && hipSetDevice(p->device) == hipSuccess;
+    (void)hipDeviceSynchronize();
+    for (auto &sl : p->scratch) {
         if (sl.ptr) (void)hipFree(sl.ptr);
         (void)hipEventDestroy(sl.done);
     }
     (void)hipFree(p->dev_block);
+    if (switched) (void)hipSetDevice(prev);
     delete p;
 }
 

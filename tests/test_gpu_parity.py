@@ -398,6 +398,27 @@ def test_scratch_growth_streams_and_per_thread_stream(H):
     prof.handle = C.c_void_p(None)
 
 
+def test_free_profile_waits_for_work_in_flight(H):
+    """heddle_free_profile right after an asynchronous pricing call on another
+    stream: the release waits for the device, so the call's outputs are whole."""
+    import ctypes as C
+    import torch
+    w = sub_workload(workload("c4_moe"), np.arange(3000))
+    want = oracle_price(w, 0)
+    prof = H.heddle_load_profile(w.profile)
+    ns, st = H.to_device(w.n_stages, w.stages)
+    out = H.alloc_outputs(w.n, len(w.m), w.s_max, 0)
+    for v in out.values():
+        v.view(torch.uint8).fill_(POISON)
+    torch.cuda.synchronize()
+    s2 = torch.cuda.Stream()
+    H.heddle_price_plans(prof, ns, st, [int(x) for x in w.m], 0, out, stream=s2)
+    H.lib().heddle_free_profile(prof.handle)
+    prof.handle = C.c_void_p(None)
+    torch.cuda.synchronize()
+    assert_same({k: v.cpu().numpy() for k, v in out.items()}, want, 0, "free while in flight")
+
+
 # ------------------------------------------------------------------ argmin
 @pytest.mark.parametrize("flags", [0, F32, CO])
 def test_argmin_matches_oracle(H, flags):

@@ -727,3 +727,77 @@ def test_fill_plans_single_size_is_pricing():
     for k in ("status", "iter", "bottleneck", "peak_mem", "layers"):
         assert np.array_equal(r[k], o[k]), k
     assert not r["mbs_index"].any()
+
+
+def _fill_profiles(g, c):
+    """the per-size profiles of one size case: the base profile with that
+    size's layer times and activation bytes"""
+    out = []
+    for s in c["sizes"]:
+        d = dict(g["profile_fill"], layer_ns=s["layer_ns"], act_bytes=s["act_bytes"], mem_cap_bytes=[c["cap"]])
+        out.append(profile_from_json(d))
+    return out
+
+
+def test_fill_size_worked_examples():
+    """micro-batch size choice with two or more sizes (section 5.3): the
+    fastest fitting size, ties to the smaller, the smallest when none fits,
+    a size that does not fit never kept even when faster"""
+    g = json.load(open(GOLD))
+    for c in g["fill_size_cases"]:
+        profs = _fill_profiles(g, c)
+        ops = [O.OracleProfile(p) for p in profs]
+        ns, rec = _recs(c["stages"])
+        r = O.fill_plans(ops, [s["mbs"] for s in c["sizes"]], c["n_nodes"], c["node_gpus"], c["global_batch"],
+                         c["dp_cap"], ns, rec, c["flags"])
+        got = dict(dp=int(r["dp"][0]), mbs_index=int(r["mbs_index"][0]), status=int(r["status"][0, 0]),
+                   iter=int(r["iter"][0, 0]), bottleneck=int(r["bottleneck"][0, 0]), peak_mem=int(r["peak_mem"][0, 0]),
+                   layers=[int(x) for x in r["layers"][0, 0]])
+        want = {k: c[k] for k in got}
+        assert got == want, (c["_what"], got, want)
+
+
+@pytest.mark.parametrize("flags", [0, 2])
+def test_fill_plans_matches_brute_force(flags):
+    """BestFill with three sizes against an independent composition: DP by
+    the count-form packing, every size priced by brute force (every split
+    enumerated in pure Python), the size picked by the rule of section 5.3"""
+    from workloads.gen import cluster_nodes, mbs_profile
+    mbs = [1, 2, 4]
+    picked = np.zeros(len(mbs), dtype=np.int64)
+    for seed in (71, 72, 73, 74):
+        # a global batch of 64 samples over at most 2 replicas keeps enough
+        # micro-batches per replica for the larger sizes to pay off on some
+        # templates, and activations growing with the size make others OOM
+        w = random_instance(seed, L=8, s_max=4, n=40, moe=seed == 72, invalid_frac=0.05,
+                            cap_scale=[3.0, 1.0, 3.0, 100.0][seed % 4])
+        profs = [mbs_profile(w.profile, b) for b in mbs]
+        ops = [O.OracleProfile(p) for p in profs]
+        nn, ng = cluster_nodes(w.profile)
+        G, cap = 64, 2
+        r = O.fill_plans(ops, mbs, nn, ng, G, cap, w.n_stages, w.stages, flags)
+        s_max = w.stages.shape[1]
+        for t in range(w.n):
+            S = int(w.n_stages[t])
+            packable = 1 <= S <= s_max and all(int(x) & 0xFF < len(nn) and (int(x) >> 8) & 15 <= 6
+                                               for x in w.stages[t, :S])
+            D = _pack_by_counts(nn, ng, w.stages[t], S, cap) if packable else 0
+            assert int(r["dp"][t]) == D, (seed, t)
+            # records of templates that cannot be packed keep their DP field
+            recs = [(int(x) & 0xFFFF) | (D << 16) if packable else int(x) for x in w.stages[t, :S]] + \
+                [0] * (s_max - S)
+            res = [brute.price(p, S, s_max, recs, -(-G // b), compute_only=flags == 2) for p, b in zip(profs, mbs)]
+            pick = None
+            for b, x in enumerate(res):
+                if x["status"] == 0 and (pick is None or x["iter"] < res[pick]["iter"]):
+                    pick = b
+            pick = 0 if pick is None else pick
+            assert int(r["mbs_index"][t]) == pick, (seed, t)
+            picked[pick] += 1
+            x = res[pick]
+            assert int(r["status"][t, 0]) == x["status"], (seed, t)
+            assert [int(v) for v in r["layers"][t, 0]] == x["layers"], (seed, t)
+            if x["iter"] is not None:
+                assert int(r["iter"][t, 0]) == x["iter"] and int(r["bottleneck"][t, 0]) == x["bottleneck"], (seed, t)
+                assert int(r["peak_mem"][t, 0]) == x["peak_mem"], (seed, t)
+    assert (picked > 0).all(), picked                              # every size is the answer somewhere

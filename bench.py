@@ -91,36 +91,73 @@ _ALL_CORES = {}
 
 
 def _oracle_chunk(task):
-    lo, n = task
+    lo, hi = task
     from oracle import oracle as O
-    w, flags = _ALL_CORES["w"], _ALL_CORES["flags"]
+    w, flags, idx = _ALL_CORES["w"], _ALL_CORES["flags"], _ALL_CORES["idx"]
     op = O.OracleProfile(w.profile)
-    O.price_plans(op, w.n_stages, w.stages, w.m, flags, lo, lo + n)   # templates [lo, lo + n)
-    return n
+    if idx is None:
+        return O.price_plans(op, w.n_stages, w.stages, w.m, flags, lo, hi)   # templates [lo, hi)
+    sel = idx[lo:hi]
+    return O.price_plans(op, w.n_stages[sel], w.stages[sel], w.m, flags)
 
 
 def cpu_baseline_all_cores(w, flags, budget_s):
-    """The same unmodified oracle, one process per host core over disjoint
-    chunks of the batch (forked before the GPU is initialised)."""
+    """The same unmodified oracle, one process per host core (the cores this
+    process may run on) over disjoint chunks: the whole batch when it fits the
+    budget, else a seeded sample of templates. Forked before the GPU is
+    initialised. Returns the rate and the oracle's outputs with the template
+    indices they cover, for the parity check of the GPU's outputs."""
     import multiprocessing as mp
+
+    import numpy as np
+
     from oracle import oracle as O
     op = O.OracleProfile(w.profile)
     probe = min(20, w.n)
     t0 = time.perf_counter()
     O.price_plans(op, w.n_stages, w.stages, w.m, flags, 0, probe)
     per = (time.perf_counter() - t0) / probe
-    cores = min(16, len(os.sched_getaffinity(0)))
-    n_each = int(max(1, min(w.n // cores, budget_s / max(per, 1e-9))))
-    _ALL_CORES.update(w=w, flags=flags)
-    tasks = [(i * n_each, n_each) for i in range(cores)]
+    cores = len(os.sched_getaffinity(0))
+    n_fit = int(budget_s * cores / max(per, 1e-9))
+    if n_fit >= w.n:
+        idx, what = None, f"all {w.n} templates"
+        n_done = w.n
+    else:
+        idx = np.sort(np.random.default_rng(0).choice(w.n, size=max(n_fit, 1), replace=False))
+        n_done, what = len(idx), f"a seeded sample of {len(idx)} of {w.n} templates"
+    step = max(1, min(4096, -(-n_done // (4 * cores))))
+    tasks = [(lo, min(lo + step, n_done)) for lo in range(0, n_done, step)]
+    _ALL_CORES.update(w=w, flags=flags, idx=idx)
     with mp.get_context("fork").Pool(cores) as pool:
         t0 = time.perf_counter()
-        done = sum(pool.map(_oracle_chunk, tasks, chunksize=1))
+        parts = pool.map(_oracle_chunk, tasks, chunksize=1)
         dt = time.perf_counter() - t0
     _ALL_CORES.clear()
-    return {"value": done * len(w.m) / dt, "unit": "plans/s", "cores": cores, "kind": "oracle",
-            "sample": f"first {done} of {w.n} templates x {len(w.m)} m in {cores} chunks, one oracle process "
-                      f"per core, {dt:.1f} s wall"}
+    outs = {k: np.concatenate([p[k] for p in parts]) for k in parts[0]}
+    rate = {"value": n_done * len(w.m) / dt, "unit": "plans/s", "cores": cores, "kind": "oracle",
+            "sample": f"{what} x {len(w.m)} m in {len(tasks)} chunks over {cores} oracle processes "
+                      f"(one per host core), {dt:.1f} s wall"}
+    return rate, outs, (np.arange(w.n) if idx is None else idx)
+
+
+def parity_check(gpu, oracle_out, idx, flags):
+    """element-by-element comparison of the GPU's outputs (status, layers,
+    peak memory, iteration time, bottleneck) with the oracle's"""
+    import numpy as np
+    bad = np.zeros(oracle_out["status"].shape, dtype=bool)
+    fields = {}
+    for k in ("status", "layers", "peak_mem", "iter", "bottleneck"):
+        a, b = gpu[k][idx], oracle_out[k]
+        if a.dtype == np.float32:
+            a, b = a.view(np.uint32), b.view(np.uint32)
+        d = a != b
+        if d.ndim == 3:
+            d = d.any(axis=2)
+        fields[k] = int(d.sum())
+        bad |= d
+    return {"compared_templates": int(len(idx)), "compared_plans": int(bad.size),
+            "mismatching_plans": int(bad.sum()), "mismatches_by_output": fields,
+            "method": "all-core oracle run, every output of every compared plan compared exactly"}
 
 
 def cpu_baseline(w, flags, budget_s):
@@ -160,7 +197,10 @@ def main():
     ap.add_argument("--enum-types", type=int, default=3, help="GPU types 0..n-1 of the enumerated space")
     ap.add_argument("--enum-tps", type=int, default=3, help="TP degrees 1, 2, 4, ... of the enumerated space")
     ap.add_argument("--enum-depth", type=int, default=8, help="largest stage count of the enumerated space")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the single-core oracle baseline")
+    ap.add_argument("--parity-seconds", type=float, default=90.0,
+                    help="budget of the all-core oracle run whose outputs are compared with the GPU's (the whole "
+                         "batch when it fits, else a seeded sample)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (reference for HBM counters)")
@@ -185,8 +225,9 @@ def main():
         w = make_workload(args.config)
         log(f"workload {args.config}: {w.n} templates x {len(w.m)} m generated in {time.perf_counter() - t0:.1f}s")
         if not args.no_cpu_baseline:
-            log(f"oracle baseline on every host core, about {args.cpu_seconds:.0f} s (before the GPU is initialised)")
-            cpu_all = cpu_baseline_all_cores(w, flags, args.cpu_seconds)
+            log(f"oracle on every host core, at most about {args.parity_seconds:.0f} s (before the GPU is initialised)")
+            cpu_all = cpu_baseline_all_cores(w, flags, args.parity_seconds)
+            log(f"oracle all-core leg: {cpu_all[0]['sample']}")
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.copy_calibration:
@@ -206,7 +247,14 @@ def main():
     prof = H.heddle_load_profile(w.profile)
     load_ms = (time.perf_counter() - t0) * 1e3
     info = H.heddle_profile_info_get(prof)
-    ns, st = H.to_device(w.n_stages, w.stages)
+    h2d = []
+    for _ in range(3):                     # host-to-device copy of the template records (pageable host memory)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ns, st = H.to_device(w.n_stages, w.stages)
+        torch.cuda.synchronize()
+        h2d.append((time.perf_counter() - t0) * 1e3)
+    h2d_ms = float(np.median(h2d))
     m = [int(x) for x in w.m]
     out = H.alloc_outputs(w.n, len(m), w.s_max, flags)
     torch.cuda.synchronize()
@@ -246,9 +294,16 @@ def main():
         f"(min {np.min(kern_ms):.3f}); best plan {best}")
     status_np = out["status"].cpu().numpy()
     statuses = np.bincount(status_np.ravel(), minlength=9).tolist()
-    # the unpruned recurrence's work, (S-1)(L-S+1)(L-S+2)/2 per valid plan and
-    # distinct split: context only, the kernel relaxes far fewer pairs
-    valid = ((status_np == 0) | (status_np == 8))[:, 0]
+    parity = None
+    if cpu_all is not None and not args.tiling:
+        gpu_np = {k: v.cpu().numpy() for k, v in out.items()}
+        parity = parity_check(gpu_np, cpu_all[1], cpu_all[2], flags)
+        log(f"parity: {parity['mismatching_plans']} of {parity['compared_plans']} plans differ from the oracle")
+    # the unpruned recurrence's work, (S-1)(L-S+1)(L-S+2)/2 per distinct split
+    # of every plan whose split was computed: context only, the kernel relaxes
+    # far fewer pairs (row windows), so this is not an achieved rate
+    lay_np = out["layers"].cpu().numpy()[:, :, 0]
+    valid = ((status_np == 0) | ((status_np == 8) & (lay_np > 0))).any(axis=1)
     S_np = w.n_stages.astype(np.int64)
     L = w.profile.L
     r_np = (S_np - 1) * (L - S_np + 1) * (L - S_np + 2) // 2
@@ -283,7 +338,11 @@ def main():
     else:
         roof = {"kernel": "window_kernel + split_kernel + evaluate_kernel (one heddle_price_plans call)",
                 "work_per_launch": relax, "work_unit": unit_name, "ops_per_unit": k_unit,
-                "dense_R_per_launch": dense_r, "frac_at_dense_R": dense_r * K_MIN / kern_s / PEAK_LANE_OPS}
+                "context_dense_R": {
+                    "per_launch": dense_r,
+                    "note": "relaxations of the unpruned suffix recurrence over the plans whose split was computed; "
+                            "the kernel performs work_per_launch of them, so this is context, not an achieved rate",
+                    "equivalent_frac": dense_r * K_MIN / kern_s / PEAK_LANE_OPS}}
     result = {
         "metric": "candidate plans priced/sec (partition+evaluate) on 1 MI355X; % VALU roofline",
         "value": n_plans * args.steps / elapsed,
@@ -314,11 +373,14 @@ def main():
             **tiling_gain(H, prof, ns, st, m, flags, w, out)),
         "best_plan": {"template": best[0], "m_index": best[1], "iter": best[2]} if best else None,
         "profile_load_ms": load_ms,
+        "template_h2d_ms": h2d_ms,
+        "plans_per_s_with_h2d": n_plans / (elapsed / args.steps + h2d_ms / 1e3),
+        "parity": parity,
     }
     if not args.no_cpu_baseline:
         log(f"oracle baseline, about {args.cpu_seconds:.0f} s on one host core")
         result["cpu_baseline"] = cpu_baseline(w, flags, args.cpu_seconds)
-        result["cpu_baseline"]["all_cores"] = cpu_all
+        result["cpu_baseline"]["all_cores"] = cpu_all[0]
     print(json.dumps(result), flush=True)
 
 

@@ -1,6 +1,7 @@
 // Argmin over priced plans: the feasible plan of highest throughput m / iter
-// (Heddle, arXiv 2609.34244: the cost model "ranks the resulting plans by
-// predicted throughput" and the fill "keeps the fastest", section 5).
+// (Heddle, arXiv 2609.34244, section 5 overview: candidates are ordered by
+// the throughput the cost model predicts; section 5.3: the fastest fitting
+// choice is kept).
 //
 // Key: iter / m, compared exactly by cross-multiplication (128-bit for int64
 // iteration times; fp32 times scaled by m <= 2^24 are exact in fp64). Ties
@@ -28,7 +29,12 @@ __device__ __forceinline__ bool better(const Cand &a, const Cand &b, bool f32)
     if (a.idx < 0) return false;
     if (b.idx < 0) return true;
     bool lt, eq;
-    if (f32) {
+    if (a.m == b.m) {
+        // one micro-batch count: iter / m orders as iter (non-negative floats
+        // order as their bit patterns)
+        lt = a.iter < b.iter;
+        eq = a.iter == b.iter;
+    } else if (f32) {
         const double x = (double)__uint_as_float((uint32_t)a.iter) * (double)b.m;
         const double y = (double)__uint_as_float((uint32_t)b.iter) * (double)a.m;
         lt = x < y;
@@ -42,23 +48,57 @@ __device__ __forceinline__ bool better(const Cand &a, const Cand &b, bool f32)
     return lt || (eq && a.idx < b.idx);
 }
 
-__device__ __forceinline__ Cand shfl_xor_cand(const Cand &c, int o)
+// A candidate from another lane: DPP within rows of 16 lanes, ds_swizzle
+// across the two rows of a 32-lane half, one value per word.
+template <int CTRL> __device__ __forceinline__ uint32_t dpp_word(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
+}
+template <int PAT> __device__ __forceinline__ uint32_t swz_word(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, PAT);
+}
+template <class F> __device__ __forceinline__ Cand move_cand(const Cand &c, F mv)
 {
     Cand r;
-    r.iter = __shfl_xor((unsigned long long)c.iter, o);
-    r.idx = __shfl_xor((long long)c.idx, o);
-    r.m = __shfl_xor(c.m, o);
+    r.iter = ((uint64_t)mv((uint32_t)(c.iter >> 32)) << 32) | mv((uint32_t)c.iter);
+    r.idx = (int64_t)(((uint64_t)mv((uint32_t)((uint64_t)c.idx >> 32)) << 32) | mv((uint32_t)(uint64_t)c.idx));
+    r.m = (int32_t)mv((uint32_t)c.m);
     return r;
+}
+__device__ __forceinline__ Cand from_lane(const Cand &c, int lane)
+{
+    return move_cand(c, [lane](uint32_t v) { return (uint32_t)__builtin_amdgcn_readlane((int)v, lane); });
+}
+
+// best candidate of the wavefront, valid in lane 0: pairs of lanes, quads
+// (quad permutations), groups of 8 and 16 (row half-mirror and mirror: after
+// the earlier steps every lane of a group holds the group's best, so any
+// pairing of two groups combines them), the two rows of 16 of each half
+// (swizzle, bit mode: and 0x1F, xor 0x10), then the halves (lane 32 read into
+// lane 0). The order is total, so the result does not depend on the pairing.
+__device__ __forceinline__ Cand wave_best(Cand c, bool f32)
+{
+    Cand u;
+    u = move_cand(c, dpp_word<0xB1>);            // quad_perm [1, 0, 3, 2]
+    if (better(u, c, f32)) c = u;
+    u = move_cand(c, dpp_word<0x4E>);            // quad_perm [2, 3, 0, 1]
+    if (better(u, c, f32)) c = u;
+    u = move_cand(c, dpp_word<0x141>);           // row_half_mirror
+    if (better(u, c, f32)) c = u;
+    u = move_cand(c, dpp_word<0x140>);           // row_mirror
+    if (better(u, c, f32)) c = u;
+    u = move_cand(c, swz_word<(0x10 << 10) | 0x1F>);
+    if (better(u, c, f32)) c = u;
+    u = from_lane(c, 32);
+    const Cand l0 = from_lane(c, 0);
+    return better(u, l0, f32) ? u : l0;
 }
 
 __device__ Cand block_best(Cand c, bool f32)
 {
     __shared__ Cand part[kArgBlock / 64];
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        Cand u = shfl_xor_cand(c, o);
-        if (better(u, c, f32)) c = u;
-    }
+    c = wave_best(c, f32);
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     if (lane == 0) part[w] = c;
     __syncthreads();
@@ -89,13 +129,20 @@ __global__ void __launch_bounds__(kArgBlock) argmin_pass1(ArgArgs A)
     best.iter = 0;
     best.m = 1;
     const bool f32 = A.f32 != 0;
-    for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < A.total; o += (int64_t)gridDim.x * blockDim.x) {
-        if (A.status[o] != HEDDLE_S_OK) continue;
-        Cand c;
-        c.idx = o;
-        c.m = sm[o % A.n_m];
-        c.iter = f32 ? (uint64_t)__float_as_uint(((const float *)A.iter)[o]) : (uint64_t)((const int64_t *)A.iter)[o];
-        if (better(c, best, f32)) best = c;
+    const int64_t o0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, stride = (int64_t)gridDim.x * blockDim.x;
+    // m index of plan o = t * n_m + k, advanced with o (no division per plan)
+    int k = (int)(o0 % A.n_m);
+    const int dk = (int)(stride % A.n_m);
+    for (int64_t o = o0; o < A.total; o += stride) {
+        if (A.status[o] == HEDDLE_S_OK) {
+            Cand c;
+            c.idx = o;
+            c.m = sm[k];
+            c.iter = f32 ? (uint64_t)__float_as_uint(((const float *)A.iter)[o]) : (uint64_t)((const int64_t *)A.iter)[o];
+            if (better(c, best, f32)) best = c;
+        }
+        k += dk;
+        k -= k >= A.n_m ? A.n_m : 0;
     }
     best = block_best(best, f32);
     if (threadIdx.x == 0) A.partial[blockIdx.x] = best;

@@ -16,8 +16,8 @@
  *     1F1B iteration time (M-1) max_s t_s + sum_s t_s + max_s g_s (section
  *     5.3, expert tiling paragraph) and the per-GPU peak memory;
  *   - the best plan is the one of highest throughput m / iter among the
- *     feasible ones ("ranks the resulting plans by predicted throughput",
- *     section 5 overview).
+ *     feasible ones (section 5 overview: candidate plans are ordered by the
+ *     throughput the cost model predicts for them).
  *
  * All time quantities are int64 nanoseconds and all sizes int64 bytes; with
  * HEDDLE_F_FP32 the time quantities are fp32 (see heddle_price_plans).
@@ -151,7 +151,10 @@ int heddle_load_profile(const heddle_profile_desc *d, heddle_profile **out);
 /* Release a profile and its per-stream scratch buffers. Waits for the work
  * on the profile's device first, so device work of earlier calls may still
  * be in flight; no host thread may be inside a call that uses the profile.
- * NULL is ignored. */
+ * The scratch buffers go back to the library's memory pool (reused by later
+ * calls), the tables to the device. There is no return code: if the device
+ * reports an error while releasing, heddle_last_error() of the calling
+ * thread names it. NULL is ignored. */
 void heddle_free_profile(heddle_profile *p);
 
 /*
@@ -233,10 +236,15 @@ int heddle_argmin_plans(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t fla
                         hipStream_t stream);
 
 /*
- * heddle_best_plan -- heddle_price_plans into library-allocated device
- * buffers followed by heddle_argmin_plans. Synchronous. Arguments as in
- * those two calls. The library allocates and frees its own buffers as
- * scratch on `stream`.
+ * heddle_best_plan -- the whole planning step of one batch: every plan
+ * priced (heddle_price_plans, into library-allocated device buffers) and the
+ * plan of highest predicted throughput m / iter among those that fit
+ * returned (heddle_argmin_plans). This is the selection the planner makes
+ * over its priced candidates (section 5 overview: candidates ordered by
+ * predicted throughput; section 5.3: among a template's fill choices the
+ * fastest fitting one is kept). Synchronous. Arguments as in those two
+ * calls; the library allocates and frees its own buffers as scratch on
+ * `stream`.
  */
 int heddle_best_plan(const heddle_profile *p, int64_t n, int32_t s_max,
                      const uint8_t *d_n_stages, const uint32_t *d_stages,

@@ -557,12 +557,22 @@ extern "C" void heddle_free_profile(heddle_profile *p)
     // buffers: wait for the profile's device before releasing them
     int prev = -1;
     const bool switched = hipGetDevice(&prev) == hipSuccess && prev != p->device && hipSetDevice(p->device) == hipSuccess;
-    (void)hipDeviceSynchronize();
+    hipError_t e = hipDeviceSynchronize();
+    // the per-stream buffers came from the library's memory pool: they go
+    // back to it stream-ordered (on the device's null stream, since the
+    // streams they were used on may no longer exist), so later calls reuse them
     for (auto &sl : p->scratch) {
-        if (sl.ptr) (void)hipFree(sl.ptr);
+        if (sl.ptr) {
+            const hipError_t f = hipFreeAsync(sl.ptr, nullptr);
+            e = e == hipSuccess ? f : e;
+        }
         (void)hipEventDestroy(sl.done);
     }
-    (void)hipFree(p->dev_block);
+    const hipError_t q = hipStreamSynchronize(nullptr);
+    e = e == hipSuccess ? q : e;
+    const hipError_t b = hipFree(p->dev_block);
+    e = e == hipSuccess ? b : e;
+    if (e != hipSuccess) (void)hip_fail(e, "heddle_free_profile: releasing the profile's device memory");
     if (switched) (void)hipSetDevice(prev);
     delete p;
 }

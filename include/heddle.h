@@ -36,7 +36,8 @@
  * heddle_free_profile. Pricing calls
  * that share a profile take its lock while they enqueue their launches (their
  * device work still overlaps across streams). With hipStreamPerThread the
- * buffer is a fresh stream-ordered block per call. The argmin entry points
+ * buffer is a fresh stream-ordered block per call. heddle_price_plans_noalloc
+ * allocates nothing: it uses a fixed buffer per GPU instead. The argmin entry points
  * return their result through a small pinned host buffer per host thread,
  * allocated on the thread's first call and kept until the process ends.
  */
@@ -216,6 +217,37 @@ int heddle_price_plans(const heddle_profile *p, int64_t n, int32_t s_max,
                        const int32_t *h_m, int32_t n_m, uint32_t flags,
                        void *d_iter, void *d_bottleneck, int64_t *d_peak_mem,
                        uint8_t *d_layers, uint8_t *d_status, hipStream_t stream);
+
+/* Device memory the allocation-free pricing entry point holds, per GPU. */
+#define HEDDLE_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/*
+ * heddle_price_plans_noalloc -- heddle_price_plans for callers that cannot
+ * allocate device memory: code under HIP graph capture, serving loops that
+ * forbid hipMalloc, harnesses that count allocations. Same arguments,
+ * outputs, kernels and results as heddle_price_plans; it calls no hipMalloc,
+ * hipFree or allocating library routine and does not touch the profile's
+ * per-stream buffers.
+ * Scratch: the per-plan validation and row windows go to a buffer of
+ * HEDDLE_NOALLOC_SCRATCH_BYTES that the library holds in each GPU's memory
+ * from the first call on that GPU until the process ends. Without DISTRIBUTE
+ * a call needs R(4 * n * n_m, 256) + 2 * n * n_m * R(s_max, 4) bytes of it
+ * (R(x, k): x rounded up to a multiple of k) -- 36 MB for a million
+ * templates of 16 stage slots at one m; with DISTRIBUTE none. Every cell
+ * the kernels read is written earlier in the same call, so what an earlier
+ * call left there does not matter.
+ * Every call on one GPU shares that GPU's buffer: calls whose device work
+ * overlaps (calls on different streams without an ordering between them)
+ * race on it and give undefined outputs; calls on one stream are ordered.
+ * Returns what heddle_price_plans returns, except HEDDLE_E_NOMEM, plus
+ * HEDDLE_E_RANGE (nothing enqueued) when the call needs more than
+ * HEDDLE_NOALLOC_SCRATCH_BYTES of the buffer.
+ */
+int heddle_price_plans_noalloc(const heddle_profile *p, int64_t n, int32_t s_max,
+                               const uint8_t *d_n_stages, const uint32_t *d_stages,
+                               const int32_t *h_m, int32_t n_m, uint32_t flags,
+                               void *d_iter, void *d_bottleneck, int64_t *d_peak_mem,
+                               uint8_t *d_layers, uint8_t *d_status, hipStream_t stream);
 
 /*
  * heddle_argmin_plans -- best plan among priced outputs: the plan of status
@@ -455,6 +487,8 @@ typedef struct heddle_profile_info {
     int32_t fx_exp;
     int32_t L, n_types, n_tp, n_ep;
     int64_t max_stage_ns;        /* bound on any stage time, ns            */
+    int64_t scratch_bytes;       /* device bytes of the per-stream buffers the
+                                    profile holds now (see heddle_price_plans) */
 } heddle_profile_info;
 int heddle_profile_info_get(const heddle_profile *p, heddle_profile_info *info);
 

@@ -156,6 +156,8 @@ struct PriceArgs {
                                      // | rows of the windows W_1 .. W_{S-1} << 16 (status 0 only)
     uint16_t *wwin;                  // [n][n_m][win_stride(s_max)] window of stage s: first row | last row << 8
     bool scratch_owned;              // host side: wst lives in a block of its own (hipStreamPerThread)
+    unsigned char *ext_scratch;      // host side: a fixed device buffer for wst and wwin (no
+    size_t ext_bytes;                // allocation, no profile buffer); NULL: the profile's buffer
 };
 
 int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,

@@ -441,6 +441,14 @@ int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const
     return HEDDLE_OK;
 }
 
+// bytes of the window pass's outputs: the status word of every plan (256-byte
+// aligned) and then the row windows of every plan
+static size_t window_scratch_bytes(int64_t n, int32_t n_m, int32_t s_max)
+{
+    const size_t plans = (size_t)n * n_m;
+    return ((plans * sizeof(uint32_t) + 255) & ~size_t(255)) + plans * win_stride(s_max) * sizeof(uint16_t);
+}
+
 template <class V, bool F32, bool COUNT>
 static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t stream)
 {
@@ -488,10 +496,15 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     // stream (the caller holds its lock and marks the end of its use)
     const size_t plans = (size_t)a.n * a.n_m;
     const size_t st_bytes = (plans * sizeof(uint32_t) + 255) & ~size_t(255);
+    const size_t bytes = window_scratch_bytes(a.n, a.n_m, a.s_max);
     unsigned char *buf = nullptr;
-    const int rs = profile_scratch(p, stream, st_bytes + plans * win_stride(a.s_max) * sizeof(uint16_t),
-                                   (void **)&buf, &a.scratch_owned);
-    if (rs != HEDDLE_OK) return rs;
+    if (a.ext_scratch) {
+        if (bytes > a.ext_bytes) return fail(HEDDLE_E_RANGE, "window scratch exceeds the fixed buffer");
+        buf = a.ext_scratch;
+    } else {
+        const int rs = profile_scratch(p, stream, bytes, (void **)&buf, &a.scratch_owned);
+        if (rs != HEDDLE_OK) return rs;
+    }
     a.wst = (uint32_t *)buf;
     a.wwin = (uint16_t *)(buf + st_bytes);
     const int rw = launch_windows(p, a, w_lds, stream);
@@ -516,7 +529,10 @@ int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool
     if (a.flags & HEDDLE_F_DISTRIBUTE) return launch_distribute(p, a, stream, count_only);
     // validation and windows of every plan (window_kernel), then the split
     // kernel over the plans with windows, then Evaluate
-    std::lock_guard<std::mutex> lock(p->scratch_mu);
+    // the profile's buffer of the stream is taken under its lock; a fixed
+    // buffer of the caller's needs no lock
+    std::unique_lock<std::mutex> lock(p->scratch_mu, std::defer_lock);
+    if (!a.ext_scratch) lock.lock();
     a.wst = nullptr;
     a.wwin = nullptr;
     a.scratch_owned = false;
@@ -525,7 +541,7 @@ int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool
     else if (f32) rc = narrow ? launch_split<uint32_t, true, false>(p, a, stream) : launch_split<uint64_t, true, false>(p, a, stream);
     else rc = narrow ? launch_split<uint32_t, false, false>(p, a, stream) : launch_split<uint64_t, false, false>(p, a, stream);
     if (rc == HEDDLE_OK && !count_only) rc = launch_evaluate(p, a, stream);
-    if (a.wst) {
+    if (a.wst && !a.ext_scratch) {
         const int rd = profile_scratch_done(p, stream, a.wst, a.scratch_owned);
         if (rc == HEDDLE_OK) rc = rd;
     }
@@ -594,4 +610,63 @@ extern "C" int heddle_count_work(const heddle_profile *p, int64_t n, int32_t s_m
     if (rc == HEDDLE_OK && e != hipSuccess) rc = hip_fail(e, "reading the work counter back");
     if (rc == HEDDLE_OK) *h_relaxations = (int64_t)h;
     return rc;
+}
+
+// ---------------------------------------------------------------------------
+// Pricing without allocation. The window pass's outputs go to this fixed
+// array, one copy per GPU, held until the process ends. Host code never uses
+// the array's name as a device address: the address of each GPU's copy is
+// taken once per device with hipGetSymbolAddress (with that device current)
+// and kept below.
+static __device__ __align__(256) unsigned char scratch[HEDDLE_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+unsigned char *g_scratch_ptr[kMaxDevices];   // device address of `scratch` on each device, or NULL
+
+// the current device's copy of `scratch` (the caller has checked that the
+// current device is the profile's)
+int noalloc_scratch(int dev, unsigned char **ptr)
+{
+    if (dev < 0 || dev >= kMaxDevices) return fail(HEDDLE_E_INVAL, "device index beyond the library's device table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *q = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&q, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress of the fixed pricing scratch");
+        if (!q) return fail(HEDDLE_E_DEVICE, "hipGetSymbolAddress gave no address for the fixed pricing scratch");
+        g_scratch_ptr[dev] = (unsigned char *)q;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return HEDDLE_OK;
+}
+}  // namespace
+
+extern "C" int heddle_price_plans_noalloc(const heddle_profile *p, int64_t n, int32_t s_max,
+                                          const uint8_t *d_n_stages, const uint32_t *d_stages,
+                                          const int32_t *h_m, int32_t n_m, uint32_t flags,
+                                          void *d_iter, void *d_bottleneck, int64_t *d_peak_mem,
+                                          uint8_t *d_layers, uint8_t *d_status, hipStream_t stream)
+{
+    int rc = validate_price_args(p, n, s_max, d_n_stages, d_stages, h_m, n_m, flags);
+    if (rc) return rc;
+    if (n > 0 && (!d_iter || !d_bottleneck || !d_peak_mem || !d_layers || !d_status))
+        return fail(HEDDLE_E_INVAL, "output pointer is NULL");
+    PriceArgs a = make_args(n, s_max, d_n_stages, d_stages, h_m, n_m, flags);
+    a.iter = d_iter;
+    a.bottleneck = d_bottleneck;
+    a.peak_mem = d_peak_mem;
+    a.layers = d_layers;
+    a.status = d_status;
+    if (n > 0 && !(flags & HEDDLE_F_DISTRIBUTE)) {
+        const size_t need = window_scratch_bytes(n, n_m, s_max);
+        if (need > (size_t)HEDDLE_NOALLOC_SCRATCH_BYTES)
+            return fail(HEDDLE_E_RANGE, "this batch needs more window scratch than the fixed buffer of "
+                                        "heddle_price_plans_noalloc holds (HEDDLE_NOALLOC_SCRATCH_BYTES)");
+        rc = noalloc_scratch(p->device, &a.ext_scratch);
+        if (rc) return rc;
+        a.ext_bytes = HEDDLE_NOALLOC_SCRATCH_BYTES;
+    }
+    return launch_price(p, a, stream, false);
 }

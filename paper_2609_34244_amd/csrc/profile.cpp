@@ -588,5 +588,9 @@ extern "C" int heddle_profile_info_get(const heddle_profile *p, heddle_profile_i
     info->n_tp = p->dev.n_tp;
     info->n_ep = p->dev.n_ep;
     info->max_stage_ns = p->max_stage_ns;
+    std::lock_guard<std::mutex> lock(p->scratch_mu);
+    int64_t bytes = 0;
+    for (const auto &sl : p->scratch) bytes += (int64_t)sl.bytes;
+    info->scratch_bytes = bytes;
     return HEDDLE_OK;
 }

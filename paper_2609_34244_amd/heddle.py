@@ -18,8 +18,10 @@ LIB_PATH = os.path.join(HERE, "libheddle.so")
 
 HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_NOMEM, HEDDLE_E_DEVICE, HEDDLE_E_RANGE, HEDDLE_E_NOFEASIBLE = 0, -1, -2, -3, -4, -5
 HEDDLE_F_FP32, HEDDLE_F_COMPUTE_ONLY, HEDDLE_F_DISTRIBUTE = 1, 2, 4
+NOALLOC_SCRATCH_BYTES = 64 << 20   # HEDDLE_NOALLOC_SCRATCH_BYTES
 STATUS_NAMES = ["OK", "BAD_SHAPE", "BAD_TYPE", "BAD_TP", "UNPROFILED", "BAD_DP", "BAD_EP", "OVERSUBSCRIBED", "OOM"]
-EXPORTS = ["heddle_load_profile", "heddle_free_profile", "heddle_price_plans", "heddle_argmin_plans",
+EXPORTS = ["heddle_load_profile", "heddle_free_profile", "heddle_price_plans", "heddle_price_plans_noalloc",
+           "heddle_argmin_plans",
            "heddle_best_plan", "heddle_count_work", "heddle_profile_info_get", "heddle_last_error",
            "heddle_enum_count", "heddle_enum_templates", "heddle_best_enumerated", "heddle_tile_plans",
            "heddle_load_cluster", "heddle_free_cluster", "heddle_fill_dp", "heddle_fill_plans"]
@@ -54,7 +56,7 @@ class heddle_cluster_desc(C.Structure):
 
 class heddle_profile_info(C.Structure):
     _fields_ = [("narrow", C.c_int32 * 2), ("fx_exp", C.c_int32), ("L", C.c_int32), ("n_types", C.c_int32),
-                ("n_tp", C.c_int32), ("n_ep", C.c_int32), ("max_stage_ns", C.c_int64)]
+                ("n_tp", C.c_int32), ("n_ep", C.c_int32), ("max_stage_ns", C.c_int64), ("scratch_bytes", C.c_int64)]
 
 
 _lib = None
@@ -72,6 +74,7 @@ def lib():
         L.heddle_free_profile.argtypes = [P]
         L.heddle_free_profile.restype = None
         L.heddle_price_plans.argtypes = [P, I64, I32, P, P, P, I32, U32, P, P, P, P, P, P]
+        L.heddle_price_plans_noalloc.argtypes = [P, I64, I32, P, P, P, I32, U32, P, P, P, P, P, P]
         L.heddle_argmin_plans.argtypes = [I64, P, I32, U32, P, P, C.POINTER(C.c_int64), C.POINTER(C.c_int32), P, P]
         L.heddle_best_plan.argtypes = [P, I64, I32, P, P, P, I32, U32, C.POINTER(C.c_int64), C.POINTER(C.c_int32),
                                        P, P]
@@ -88,7 +91,8 @@ def lib():
         L.heddle_best_enumerated.argtypes = [P, C.POINTER(heddle_enum_spec), P, I32, U32, I64,
                                              C.POINTER(C.c_int64), C.POINTER(C.c_int32), P, C.POINTER(C.c_int64), P]
         L.heddle_last_error.restype = C.c_char_p
-        for f in ("heddle_load_profile", "heddle_price_plans", "heddle_argmin_plans", "heddle_best_plan",
+        for f in ("heddle_load_profile", "heddle_price_plans", "heddle_price_plans_noalloc", "heddle_argmin_plans",
+                  "heddle_best_plan",
                   "heddle_count_work", "heddle_profile_info_get", "heddle_enum_count", "heddle_enum_templates",
                   "heddle_best_enumerated", "heddle_tile_plans", "heddle_load_cluster", "heddle_fill_dp",
                   "heddle_fill_plans"):
@@ -165,7 +169,8 @@ def heddle_profile_info_get(prof):
     info = heddle_profile_info()
     _check(lib().heddle_profile_info_get(prof.handle, C.byref(info)))
     return dict(narrow_i64=bool(info.narrow[0]), narrow_f32=bool(info.narrow[1]), fx_exp=info.fx_exp, L=info.L,
-                n_types=info.n_types, n_tp=info.n_tp, n_ep=info.n_ep, max_stage_ns=info.max_stage_ns)
+                n_types=info.n_types, n_tp=info.n_tp, n_ep=info.n_ep, max_stage_ns=info.max_stage_ns,
+                scratch_bytes=info.scratch_bytes)
 
 
 def _mlist(m):
@@ -193,6 +198,25 @@ def heddle_price_plans(prof, n_stages, stages, m, flags, out, stream=None):
                                     _ptr(out["iter"]), _ptr(out["bottleneck"]), _ptr(out["peak_mem"]),
                                     _ptr(out["layers"]), _ptr(out["status"]), _stream(stream)))
     return out
+
+
+def heddle_price_plans_noalloc(prof, n_stages, stages, m, flags, out, stream=None):
+    """heddle_price_plans with the window scratch in the library's fixed
+    per-GPU buffer: no device allocation in the call."""
+    n, s_max = int(stages.shape[0]), int(stages.shape[1])
+    mm, mp = _mlist(m)
+    _check(lib().heddle_price_plans_noalloc(prof.handle, n, s_max, _ptr(n_stages), _ptr(stages), mp, len(mm), flags,
+                                            _ptr(out["iter"]), _ptr(out["bottleneck"]), _ptr(out["peak_mem"]),
+                                            _ptr(out["layers"]), _ptr(out["status"]), _stream(stream)))
+    return out
+
+
+def noalloc_scratch_bytes(n, n_m, s_max, flags=0):
+    """bytes of the fixed buffer a heddle_price_plans_noalloc call needs"""
+    if n == 0 or flags & 4:
+        return 0
+    plans = n * n_m
+    return (plans * 4 + 255) // 256 * 256 + plans * 2 * ((s_max + 3) // 4 * 4)
 
 
 def heddle_tile_plans(prof, n_stages, stages, m, flags, out, stream=None):

@@ -125,6 +125,8 @@ def test_load_profile_range_errors(lib):
 def test_price_calls_reject_null_profile(lib):
     m = (C.c_int32 * 1)(4)
     assert lib.heddle_price_plans(None, 0, 4, None, None, m, 1, 0, None, None, None, None, None, None) == H.HEDDLE_E_INVAL
+    assert lib.heddle_price_plans_noalloc(None, 0, 4, None, None, m, 1, 0, None, None, None, None, None,
+                                          None) == H.HEDDLE_E_INVAL
     bt, bk = C.c_int64(), C.c_int32()
     assert lib.heddle_best_plan(None, 1, 4, None, None, m, 1, 0, C.byref(bt), C.byref(bk), None, None) == H.HEDDLE_E_INVAL
     w = C.c_int64()
@@ -133,6 +135,15 @@ def test_price_calls_reject_null_profile(lib):
     assert lib.heddle_argmin_plans(1, m, 1, 8, None, None, C.byref(bt), C.byref(bk), None, None) == H.HEDDLE_E_INVAL
     assert lib.heddle_profile_info_get(None, None) == H.HEDDLE_E_INVAL
     lib.heddle_free_profile(None)          # no-op
+
+
+def test_noalloc_scratch_size_rule():
+    """the fixed buffer's size rule of the header: R(4 n n_m, 256) + 2 n n_m R(s_max, 4)"""
+    assert H.noalloc_scratch_bytes(1_000_000, 1, 16) == 36_000_000
+    assert H.noalloc_scratch_bytes(3, 2, 5) == 256 + 2 * 6 * 8
+    assert H.noalloc_scratch_bytes(0, 2, 5) == 0 and H.noalloc_scratch_bytes(10, 1, 4, flags=4) == 0
+    src = open(HEADER).read()
+    assert "#define HEDDLE_NOALLOC_SCRATCH_BYTES (64u << 20)" in src and H.NOALLOC_SCRATCH_BYTES == 64 << 20
 
 
 def _spec(d_max=3, types=(0, 1), tps=(0, 1), dps=(1,), ep=0):

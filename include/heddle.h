@@ -489,6 +489,7 @@ typedef struct heddle_profile_info {
     int64_t max_stage_ns;        /* bound on any stage time, ns            */
     int64_t scratch_bytes;       /* device bytes of the per-stream buffers the
                                     profile holds now (see heddle_price_plans) */
+    int32_t narrow_tile;         /* 1 if expert tiling holds times in 32 bits */
 } heddle_profile_info;
 int heddle_profile_info_get(const heddle_profile *p, heddle_profile_info *info);
 

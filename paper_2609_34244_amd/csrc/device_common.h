@@ -110,6 +110,21 @@ template <class T> __device__ __forceinline__ T group_min(T v, int k)
     return v;
 }
 
+// inclusive prefix sum over the wavefront: row_shr 1, 2, 4 and 8 within rows
+// of 16 (a lane without a source adds 0), then row_bcast 15 carries row 0's
+// total into row 1 and row 2's into row 3, and row_bcast 31 carries the total
+// of rows 0 and 1 into rows 2 and 3
+__device__ __forceinline__ int wave_inclusive_sum(int v)
+{
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);
+    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);
+    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);
+    return v;
+}
+
 // sum over the wavefront, in every lane (pairs across the halves of groups of
 // 2, 4, 8, 16 lanes, then the four rows of 16 through scalar reads)
 __device__ __forceinline__ uint32_t wave_sum(uint32_t v)

@@ -172,6 +172,8 @@ int prepare_windows(const heddle_profile *p, const PriceArgs &a, int max_lds, si
 int launch_windows(const heddle_profile *p, const PriceArgs &a, size_t lds, hipStream_t stream);
 int launch_distribute(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool count_only);
 int launch_tile(const heddle_profile *p, const PriceArgs &a, uint8_t *tiling, hipStream_t stream);
+// expert tiling holds stage times and synchronisation values in 32 bits
+bool tile_narrow(const heddle_profile *p);
 int launch_argmin(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t flags, const void *d_iter,
                   const uint8_t *d_status, int64_t *h_best_template, int32_t *h_best_m_index,
                   void *h_best_iter, hipStream_t stream);

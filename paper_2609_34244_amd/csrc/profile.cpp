@@ -592,5 +592,6 @@ extern "C" int heddle_profile_info_get(const heddle_profile *p, heddle_profile_i
     int64_t bytes = 0;
     for (const auto &sl : p->scratch) bytes += (int64_t)sl.bytes;
     info->scratch_bytes = bytes;
+    info->narrow_tile = tile_narrow(p) ? 1 : 0;
     return HEDDLE_OK;
 }

@@ -22,15 +22,21 @@
 // per stage the fastest layout wins, then the smaller synchronisation, then
 // the first in (EP list, TP list) order.
 //
-// Mapping: one wavefront per plan (grid-stride). Lanes are (stage, layout)
-// slots while the layouts are priced (time, synchronisation and memory into
-// LDS; time all ones when the layout is not allowed or does not fit); then
-// lanes are stages, each keeping in place the layouts that no other layout of
-// its stage beats in both time and synchronisation (only those can be chosen,
-// and only their synchronisation values need to be tried as bounds); then
-// lanes are the kept layouts as thresholds G, each pricing the plan under its
-// G from the kept table (broadcast reads); a wavefront minimum of (iteration
-// time, G) decides, and lanes as stages write the layouts back.
+// Mapping: one wavefront per plan (grid-stride). Lanes are stages while the
+// stage constants are formed (an LDS record per stage). Lanes are then (stage,
+// layout) slots that only test which layouts are allowed, and the allowed
+// ones are compacted, in (stage, layout) order, into a list by ballot and
+// prefix count; lanes over that list price the layouts (time,
+// synchronisation, memory) and compact the ones that fit memory into a second
+// list, with each stage's segment of it. Lanes over the fitting list keep the
+// layouts that no other layout of their stage beats in both time and
+// synchronisation (only those can be chosen under a bound, and only their
+// synchronisation values need to be tried as bounds), compacted in place.
+// Lanes are then the kept layouts as thresholds G, each pricing the plan under
+// its G from the kept list (broadcast reads); a wavefront minimum of
+// (iteration time, G) decides, and lanes as stages write the layouts back.
+// Times and synchronisation values are held in 32 bits when the profile's
+// bounds on them allow it.
 #include <cstring>
 
 #include "exact_math.h"
@@ -38,8 +44,6 @@
 #include "device_common.h"
 
 namespace heddle {
-
-constexpr uint64_t kNoLayout = ~0ull;
 
 // per-stage constants of the layout pricing, one LDS record per stage
 struct StageK {
@@ -58,33 +62,97 @@ __device__ __forceinline__ void wave_min_pair(uint64_t &a, uint64_t &b)
     }
 }
 
+// set lanes of a wavefront mask below this lane
+__device__ __forceinline__ int lanes_below(uint64_t m)
+{
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// time and synchronisation of a list entry, read together
+template <class TT> struct alignas(2 * sizeof(TT)) TGPair {
+    TT x, y;
+};
+
+// LDS of one wavefront: the stage records, then per list entry (at most
+// s_cap * F) memory, time and synchronisation, the allowed-layout list, layout
+// index, stage and kept flag, then the per-stage segment bounds
+template <class TT> __host__ __device__ inline size_t tile_lds_bytes(int s_cap, int F)
+{
+    const size_t n = (size_t)s_cap * F;
+    return (size_t)s_cap * sizeof(StageK) + n * (8 + 2 * sizeof(TT) + 4 + 3) + 3 + (size_t)s_cap * 4;
+}
+
+// TT: uint32_t when every stage time and synchronisation value is below
+// 2^32 - 1 (the profile's bounds), else uint64_t; all ones marks no layout
+template <class TT>
 __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, uint8_t *tiling)
 {
+    constexpr TT kNone = (TT)~(TT)0;
     extern __shared__ __align__(16) unsigned char smem[];      // one wavefront per workgroup
     const int lane = threadIdx.x;
     const int L = P.L, R = L + 1, N = P.n_types, K = P.n_tp, E = P.n_ep, F = K * E;
-    // rows of Fp = F rounded up to odd 8-byte entries: lanes reading their own
-    // stage's row touch distinct LDS banks
-    const int Fp = F | 1;
-    uint64_t *cT = (uint64_t *)smem;                           // [s_cap][Fp] time (kNoLayout: none)
-    uint64_t *cG = cT + (size_t)A.s_cap * Fp;                  // [s_cap][Fp] synchronisation
-    int64_t *cM = (int64_t *)(cG + (size_t)A.s_cap * Fp);      // [s_cap][Fp] memory
-    uint8_t *cC = (uint8_t *)(cM + (size_t)A.s_cap * Fp);      // [s_cap][Fp] layout index of a kept entry
-    uint8_t *cN = cC + (size_t)A.s_cap * Fp;                   // [s_cap] kept layouts of a stage
-    const size_t sk_off = ((size_t)A.s_cap * Fp * 25 + A.s_cap + 15) & ~size_t(15);
-    StageK *SK = (StageK *)(smem + sk_off);                    // [s_cap]
-    uint8_t *tS = (uint8_t *)(SK + A.s_cap);                   // [s_cap * Fp] stage of a threshold entry
-    uint8_t *tJ = tS + (size_t)A.s_cap * Fp;                   // [s_cap * Fp] its index among the stage's kept
+    const int nmax = A.s_cap * F;
+    StageK *SK = (StageK *)smem;                               // [s_cap]
+    int64_t *cM = (int64_t *)(SK + A.s_cap);                   // [nmax] memory of a list entry
+    TGPair<TT> *cTG = (TGPair<TT> *)(cM + nmax);               // [nmax] time, synchronisation
+    uint32_t *AL = (uint32_t *)(cTG + nmax);                   // [nmax] allowed: s | c << 8 | ei << 16 | ti << 24
+    uint8_t *cC = (uint8_t *)(AL + nmax);                      // [nmax] layout index c = ei * K + ti
+    uint8_t *cS = cC + nmax;                                   // [nmax] stage
+    uint8_t *kf = cS + nmax;                                   // [nmax] kept flag
+    uint16_t *seg_lo = (uint16_t *)(kf + nmax + ((4 - (3 * nmax) % 4) % 4));   // [s_cap] first entry of a stage
+    uint16_t *seg_hi = seg_lo + A.s_cap;                       // [s_cap] one past its last
     const int64_t total = A.n * A.n_m;
-    // slot q -> stage q / F as a high product with ceil(2^32 / F), exact for
-    // q * F < 2^32 (here q < s_cap * F <= 255 * 256); F = 1 maps q to itself
+    // slot q -> stage q / F and layout c -> EP index c / K as high products with
+    // ceil(2^32 / F) and ceil(2^32 / K), exact for q * F, c * K < 2^32 (here
+    // q < 64 * 256); a divisor of 1 maps to itself
     const uint32_t invF = F > 1 ? (uint32_t)(0xFFFFFFFFu / (uint32_t)F) + 1u : 0u;
+    const uint32_t invK = K > 1 ? (uint32_t)(0xFFFFFFFFu / (uint32_t)K) + 1u : 0u;
+
+    // the segments of a list whose entries are in stage order: lanes over the
+    // entries mark where each stage's run starts and ends (stages with no
+    // entry keep 0 .. 0); returns, in lane s, first | end << 16 of stage s
+    auto segments = [&](int n, bool act) -> uint32_t {
+        if (act) {
+            seg_lo[lane] = 0;
+            seg_hi[lane] = 0;
+        }
+        wave_sync();
+        for (int q0 = 0; q0 < n; q0 += 64) {
+            const int q = q0 + lane;
+            if (q < n) {
+                const int s = cS[q];
+                if (q == 0 || cS[q - 1] != s) seg_lo[s] = (uint16_t)q;
+                if (q == n - 1 || cS[q + 1] != s) seg_hi[s] = (uint16_t)(q + 1);
+            }
+        }
+        wave_sync();
+        return act ? (uint32_t)seg_lo[lane] | (uint32_t)seg_hi[lane] << 16 : 0u;
+    };
+
+    auto template_of = [&](int64_t oo) -> int64_t {
+        return A.n_m == 1 ? oo : total <= 0xFFFFFFFFll ? (int64_t)((uint32_t)oo / (uint32_t)A.n_m) : oo / A.n_m;
+    };
+    // a plan's status, layer counts, stage count and records, loaded one
+    // iteration ahead (plans are this wavefront's alone, so the status read
+    // ahead is not one it writes)
+    int st_n = 0, S_n = 0, nl_n = 0;
+    uint32_t rec_n = 0;
+    auto fetch = [&](int64_t oo) {
+        const int64_t tt = template_of(oo);
+        st_n = A.status[oo];
+        S_n = A.n_stages[tt];
+        nl_n = lane < A.s_max ? A.layers[oo * A.s_max + lane] : 0;
+        rec_n = lane < A.s_max ? A.stages[tt * A.s_max + lane] : 0u;
+    };
+    if ((int64_t)blockIdx.x < total) fetch(blockIdx.x);
 
     for (int64_t o = blockIdx.x; o < total; o += gridDim.x) {
-        const int64_t t = A.n_m == 1 ? o : total <= 0xFFFFFFFFll ? (int64_t)((uint32_t)o / (uint32_t)A.n_m) : o / A.n_m;
+        const int st_in = st_n, S = S_n, nl_all = nl_n;
+        const uint32_t rec_all = rec_n;
+        if (o + gridDim.x < total) fetch(o + gridDim.x);
+        const int64_t t = template_of(o);
         const int k = (int)(o - t * A.n_m);
-        const int st_in = A.status[o];
-        const bool has_split = (st_in == HEDDLE_S_OK || st_in == HEDDLE_S_OOM) && A.layers[o * A.s_max] > 0;
+        const bool has_split = (st_in == HEDDLE_S_OK || st_in == HEDDLE_S_OOM) && rl32(nl_all, 0) > 0;
         if (!has_split) {                                      // no split: nothing to tile
             if (lane < A.s_max) tiling[o * A.s_max + lane] = 0;
             continue;
@@ -92,17 +160,11 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
         // a split implies a valid template; buffers that do not describe one
         // (inconsistent with the templates) are left alone rather than read out
         // of range
-        const int S = A.n_stages[t];
         const bool act = lane < S && lane < A.s_cap;
-        const uint32_t rec = act ? A.stages[t * A.s_max + lane] : 0u;
-        const int nl = act ? A.layers[o * A.s_max + lane] : 0;
-        int i0 = nl;                                           // inclusive scan, then exclusive
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int u = __shfl_up(i0, d);
-            i0 += lane >= d ? u : 0;
-        }
-        const int total_layers = __shfl(i0, 63);
+        const uint32_t rec = act ? rec_all : 0u;
+        const int nl = act ? nl_all : 0;
+        int i0 = wave_inclusive_sum(nl);                       // inclusive scan, then exclusive
+        const int total_layers = rl32(i0, 63);
         i0 -= nl;
         const int j0 = i0 + nl;
         const int g = rec & 0xFF, l2tp = (rec >> 8) & 15, l2ep = (rec >> 12) & 15;
@@ -117,158 +179,193 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
         }
         const int32_t m = A.m[k];
         const int64_t Mp = (int64_t)(((uint32_t)m + (uint32_t)D - 1) / (uint32_t)D);
-        const int64_t inflight = (int64_t)(S - lane) < Mp ? (int64_t)(S - lane) : Mp;
-        const int g_next = __builtin_amdgcn_update_dpp(g, g, kDppWaveShl1, 0xF, 0xF, false);
-        const int64_t p2p = lane + 1 < S ? P.p2p_ns[g * N + g_next] : 0;
-        const int node = P.node_size[g];
-        const int64_t cap = P.mem_cap[g];
-        const int64_t W = (int64_t)tp * D;
-        const int64_t bw = W <= node ? P.intra_bw[g] : P.link_bw[g * N + g];
-        const uint64_t *base = P.rows64[0] + ((size_t)(g * K + ki) * 3 + kA2ANone) * R;
-        const uint64_t T0 = base[j0] - base[i0] + (uint64_t)p2p;
-        const int64_t n_moe = P.pre_moe[j0] - P.pre_moe[i0];
-        const int64_t dstate = P.pre_dstate[ki * R + j0] - P.pre_dstate[ki * R + i0];
-        const int64_t act_b = P.pre_act[ki * R + j0] - P.pre_act[ki * R + i0];
-        const int64_t gd = P.pre_grad[ki * R + j0] - P.pre_grad[ki * R + i0];
-        const int64_t g_dense = allreduce_ns(gd, D, bw);
 
-        // ---- lanes = (stage, layout) slots q = s * F + c: price every layout
-        wave_sync();                                           // the previous plan's table reads are done
+        // ---- lanes = stages: the stage constants
+        wave_sync();                                           // the previous plan's reads are done
         if (act) {
+            const int64_t inflight = (int64_t)(S - lane) < Mp ? (int64_t)(S - lane) : Mp;
+            const int g_next = __builtin_amdgcn_update_dpp(g, g, kDppWaveShl1, 0xF, 0xF, false);
+            const int64_t p2p = lane + 1 < S ? P.p2p_ns[g * N + g_next] : 0;
+            const int node = P.node_size[g];
+            const int64_t W = (int64_t)tp * D;
+            const int64_t bw = W <= node ? P.intra_bw[g] : P.link_bw[g * N + g];
+            const uint64_t *base = P.rows64[0] + ((size_t)(g * K + ki) * 3 + kA2ANone) * R;
+            const int64_t gd = P.pre_grad[ki * R + j0] - P.pre_grad[ki * R + i0];
             StageK &sk = SK[lane];
-            sk.W = W; sk.cap = cap; sk.bw = bw; sk.T0 = (int64_t)T0; sk.n_moe = n_moe; sk.dstate = dstate;
-            sk.act_b = act_b; sk.inflight = inflight; sk.g_dense = g_dense;
+            sk.W = W;
+            sk.cap = P.mem_cap[g];
+            sk.bw = bw;
+            sk.T0 = (int64_t)(base[j0] - base[i0] + (uint64_t)p2p);
+            sk.n_moe = P.pre_moe[j0] - P.pre_moe[i0];
+            sk.dstate = P.pre_dstate[ki * R + j0] - P.pre_dstate[ki * R + i0];
+            sk.act_b = P.pre_act[ki * R + j0] - P.pre_act[ki * R + i0];
+            sk.inflight = inflight;
+            sk.g_dense = allreduce_ns(gd, D, bw);
             sk.g = g; sk.ki = ki; sk.node = node; sk.i0 = i0; sk.j0 = j0;
         }
         wave_sync();
+
+        // ---- lanes = (stage, layout) slots q = s * F + c: which layouts are
+        // allowed (a profiled ETP within the node, EP x ETP dividing the
+        // stage's GPUs), compacted in slot order
         const int n_cand = S * F;
+        int n_al = 0;
         for (int q0 = 0; q0 < n_cand; q0 += 64) {
             const int q = q0 + lane;
+            bool allowed = false;
+            uint32_t ent = 0;
             if (q < n_cand) {
                 const int s = F > 1 ? (int)__umulhi((uint32_t)q, invF) : q, c = q - s * F;
+                const int ei = K > 1 ? (int)__umulhi((uint32_t)c, invK) : c, ti = c - ei * K;
+                const StageK &sk = SK[s];
+                const int l2e = nibble(P.ep_log2, ei), l2t = nibble(P.tp_log2, ti);
+                const int64_t gmask = ((int64_t)1 << (l2e + l2t)) - 1;    // EP x ETP, a power of two
+                allowed = P.profiled[sk.g * K + ti] && (1 << l2t) <= sk.node && (sk.W & gmask) == 0;
+                ent = (uint32_t)s | (uint32_t)c << 8 | (uint32_t)ei << 16 | (uint32_t)ti << 24;
+            }
+            const uint64_t mk = ballot(allowed);
+            if (allowed) AL[n_al + lanes_below(mk)] = ent;
+            n_al += __popcll(mk);
+        }
+        wave_sync();
+
+        // ---- lanes = allowed layouts: price them; the ones that fit memory
+        // go, in the same order, to the fitting list
+        int n_fit = 0;
+        for (int q0 = 0; q0 < n_al; q0 += 64) {
+            const int q = q0 + lane;
+            bool fits = false;
+            uint64_t T = 0;
+            int64_t mem = 0, gs = 0;
+            uint32_t ent = 0;
+            if (q < n_al) {
+                ent = AL[q];
+                const int s = ent & 255, ei = (ent >> 16) & 255, ti = ent >> 24;
                 const StageK &sk = SK[s];
                 const int sg = sk.g, ski = sk.ki, snode = sk.node, si0 = sk.i0, sj0 = sk.j0;
-                const int ei = c / K, ti = c - ei * K;
                 const int l2e = nibble(P.ep_log2, ei), l2t = nibble(P.tp_log2, ti);
-                const int et = 1 << l2t;
-                const int64_t gmask = ((int64_t)1 << (l2e + l2t)) - 1;    // EP x ETP, a power of two
-                const bool allowed = P.profiled[sg * K + ti] && et <= snode && (sk.W & gmask) == 0;
                 const int64_t *xd = P.xdelta + ((size_t)(sg * K + ski) * K + ti) * R;
-                const uint64_t T = (uint64_t)sk.T0 + (uint64_t)(xd[sj0] - xd[si0]) +
-                                   (uint64_t)(sk.n_moe * P.a2a_ns[sg * 3 + a2a_variant(1 << l2e, et, snode)]);
+                T = (uint64_t)sk.T0 + (uint64_t)(xd[sj0] - xd[si0]) +
+                    (uint64_t)(sk.n_moe * P.a2a_ns[sg * 3 + a2a_variant(1 << l2e, 1 << l2t, snode)]);
                 const int64_t *xs = P.pre_xstate + (size_t)(ti * E + ei) * R;
-                const int64_t mem = sk.dstate + (xs[sj0] - xs[si0]) + sk.inflight * sk.act_b;
+                mem = sk.dstate + (xs[sj0] - xs[si0]) + sk.inflight * sk.act_b;
                 const int64_t *xg = P.pre_xgrad + (size_t)(ti * E + ei) * R;
-                const int64_t edp = allowed ? sk.W >> (l2e + l2t) : 1;
-                const int64_t gs = sk.g_dense + allreduce_ns(xg[sj0] - xg[si0], edp, sk.bw);
-                const int qs = s * Fp + c;
-                cT[qs] = allowed && mem <= sk.cap ? T : kNoLayout;
-                cG[qs] = (uint64_t)gs;
-                cM[qs] = mem;
+                gs = sk.g_dense + allreduce_ns(xg[sj0] - xg[si0], sk.W >> (l2e + l2t), sk.bw);
+                fits = mem <= sk.cap;
             }
+            const uint64_t mk = ballot(fits);
+            if (fits) {
+                const int pos = n_fit + lanes_below(mk);
+                cTG[pos] = TGPair<TT>{(TT)T, (TT)gs};
+                cM[pos] = mem;
+                cC[pos] = (uint8_t)(ent >> 8);
+                cS[pos] = (uint8_t)ent;
+            }
+            n_fit += __popcll(mk);
         }
         wave_sync();
+        uint32_t sgv = segments(n_fit, act);
+        if (ballot(act && (sgv >> 16) == (sgv & 0xFFFF))) {    // a stage with no fitting layout: unchanged
+            if (lane < A.s_max) tiling[o * A.s_max + lane] = act ? (uint8_t)(l2ep | l2tp << 4) : 0;
+            continue;
+        }
 
-        // ---- lanes = (stage, layout) slots again: a layout is kept when no other
-        // layout of its stage beats it in both time and synchronisation (an earlier
-        // one also by being equal in both); only these can be a stage's fastest
-        // layout under a bound on the synchronisation, and only their
-        // synchronisation values need to be tried as bounds. The kept layouts move
-        // to the front of their stage's row in layout order (a slot's new place is
-        // at or before its old one, so no row entry is overwritten before it is read).
-        uint8_t *kf = tS;                                      // [n_cand] kept flags, by slot
-        for (int q0 = 0; q0 < n_cand; q0 += 64) {
+        // ---- lanes = fitting layouts: a layout is kept when no other layout of
+        // its stage beats it in both time and synchronisation (an earlier one
+        // also by being equal in both)
+        for (int q0 = 0; q0 < n_fit; q0 += 64) {
             const int q = q0 + lane;
-            const bool in = q < n_cand;
-            const int s = !in ? 0 : F > 1 ? (int)__umulhi((uint32_t)q, invF) : q, c = in ? q - s * F : 0;
-            const int rb = s * Fp;
-            const uint64_t x = in ? cT[rb + c] : kNoLayout, y = in ? cG[rb + c] : 0;
-            bool keep = x != kNoLayout;
-            for (int c2 = 0; c2 < F; c2++) {
-                const uint64_t x2 = cT[rb + c2], y2 = cG[rb + c2];
-                keep = keep && !(c2 != c && x2 <= x && y2 <= y && (c2 < c || x2 < x || y2 < y));
+            if (q < n_fit) {
+                const int s = cS[q];
+                const TGPair<TT> e = cTG[q];
+                const int lo = seg_lo[s], hi = seg_hi[s];
+                auto beats = [&](int j, TGPair<TT> f) {
+                    return j != q && f.x <= e.x && f.y <= e.y && (j < q || f.x < e.x || f.y < e.y);
+                };
+                bool keep = true;
+                int j = lo;
+                for (; j + 1 < hi; j += 2) {                   // two entries per step
+                    const TGPair<TT> f0 = cTG[j], f1 = cTG[j + 1];
+                    keep = keep && !beats(j, f0) && !beats(j + 1, f1);
+                }
+                if (j < hi) keep = keep && !beats(j, cTG[j]);
+                kf[q] = (uint8_t)keep;
             }
-            if (in) kf[q] = (uint8_t)keep;
         }
         wave_sync();
-        for (int q0 = 0; q0 < n_cand; q0 += 64) {
+        // compacted in place: an entry's new place is at or before its old one
+        // and after every place an earlier pass wrote
+        int n_k = 0;
+        for (int q0 = 0; q0 < n_fit; q0 += 64) {
             const int q = q0 + lane;
-            const bool in = q < n_cand;
-            const int s = !in ? 0 : F > 1 ? (int)__umulhi((uint32_t)q, invF) : q, c = in ? q - s * F : 0;
-            const int rb = s * Fp;
-            const bool keep = in && kf[q];
-            int rank = 0, tot = 0;
-            for (int c2 = 0; c2 < F; c2++) {
-                const int f = kf[s * F + c2];
-                rank += c2 < c ? f : 0;
-                tot += f;
+            const bool keep = q < n_fit && kf[q];
+            TGPair<TT> e = {0, 0};
+            int64_t mx = 0;
+            uint8_t c = 0, s = 0;
+            if (keep) {
+                e = cTG[q];
+                mx = cM[q];
+                c = cC[q];
+                s = cS[q];
             }
-            const uint64_t x = cT[rb + c], y = cG[rb + c];
-            const int64_t mx = cM[rb + c];
+            const uint64_t mk = ballot(keep);
             wave_sync();
             if (keep) {
-                cT[rb + rank] = x;
-                cG[rb + rank] = y;
-                cM[rb + rank] = mx;
-                cC[rb + rank] = (uint8_t)c;
+                const int pos = n_k + lanes_below(mk);
+                cTG[pos] = e;
+                cM[pos] = mx;
+                cC[pos] = c;
+                cS[pos] = s;
             }
-            if (in && c == 0) cN[s] = (uint8_t)tot;
-            wave_sync();
-        }
-        // threshold list: every kept layout of every stage, (stage, index) per entry
-        int n_thr = 0;
-        {
-            const int nfl = act ? cN[lane] : 0;
-            int off = nfl;                                     // exclusive scan of the kept counts
-#pragma unroll
-            for (int d = 1; d < 64; d <<= 1) {
-                const int u = __shfl_up(off, d);
-                off += lane >= d ? u : 0;
-            }
-            n_thr = __shfl(off, 63);
-            off -= nfl;
-            for (int j = 0; j < nfl; j++) {
-                tS[off + j] = (uint8_t)lane;
-                tJ[off + j] = (uint8_t)j;
-            }
+            n_k += __popcll(mk);
         }
         wave_sync();
+        sgv = segments(n_k, act);
 
-        // ---- lanes = frontier layouts as thresholds G: the plan's iteration time
+        // ---- lanes = kept layouts as thresholds G: the plan's iteration time
         // with every stage at its fastest kept layout of synchronisation <= G
-        uint64_t best_it = kNoLayout, best_G = kNoLayout;
-        for (int q0 = 0; q0 < n_thr; q0 += 64) {
+        uint64_t best_it = ~0ull, best_G = ~0ull;
+        for (int q0 = 0; q0 < n_k; q0 += 64) {
             const int q = q0 + lane;
-            uint64_t it = kNoLayout, G = kNoLayout;
-            if (q < n_thr) {
-                G = cG[tS[q] * Fp + tJ[q]];
-                uint64_t maxT = 0, sumT = 0, maxg = 0;
-                bool ok = true;
-                for (int s2 = 0; s2 < S && ok; s2++) {
-                    uint64_t bT = kNoLayout, bG = 0;
-                    const int n2 = cN[s2];
-                    for (int j2 = 0; j2 < n2; j2++) {
-                        const uint64_t x = cT[s2 * Fp + j2], y = cG[s2 * Fp + j2];
-                        const bool take = y <= G && x < bT;        // kept layouts have distinct times
-                        bT = take ? x : bT;
-                        bG = take ? y : bG;
-                    }
-                    ok = bT != kNoLayout;
-                    maxT = bT > maxT ? bT : maxT;
-                    sumT += bT;
-                    maxg = bG > maxg ? bG : maxg;
+            const TT G = q < n_k ? cTG[q].y : (TT)0;
+            TT maxT = 0, maxg = 0;
+            uint64_t sumT = 0;
+            bool ok = true;
+            for (int s2 = 0; s2 < S; s2++) {
+                const uint32_t b = uni64(sgv, s2);
+                TT bT = kNone, bG = 0;
+                auto consider = [&](TGPair<TT> f) {
+                    const bool take = f.y <= G && f.x < bT;    // kept layouts have distinct times
+                    bT = take ? f.x : bT;
+                    bG = take ? f.y : bG;
+                };
+                const int hi = (int)(b >> 16);
+                int j = (int)(b & 0xFFFF);
+                for (; j + 1 < hi; j += 2) {                   // two entries per step
+                    const TGPair<TT> f0 = cTG[j], f1 = cTG[j + 1];
+                    consider(f0);
+                    consider(f1);
                 }
-                if (ok) it = (uint64_t)(Mp - 1) * maxT + sumT + maxg;
+                if (j < hi) consider(cTG[j]);
+                ok = ok && bT != kNone;
+                maxT = bT > maxT ? bT : maxT;
+                sumT += (uint64_t)bT;
+                maxg = bG > maxg ? bG : maxg;
             }
-            wave_min_pair(it, G);
-            if (it < best_it || (it == best_it && G < best_G)) {
+            uint64_t it = ~0ull, Gq = ~0ull;
+            if (q < n_k && ok) {
+                it = (uint64_t)(Mp - 1) * (uint64_t)maxT + sumT + (uint64_t)maxg;
+                Gq = (uint64_t)G;
+            }
+            wave_min_pair(it, Gq);
+            if (it < best_it || (it == best_it && Gq < best_G)) {
                 best_it = it;
-                best_G = G;
+                best_G = Gq;
             }
         }
 
         // ---- lanes = stages: write the chosen layouts
-        if (best_it == kNoLayout) {                            // some stage has no fitting layout: unchanged
+        if (best_it == ~0ull) {                                // no bound serves every stage: unchanged
             if (lane < A.s_max) tiling[o * A.s_max + lane] = act ? (uint8_t)(l2ep | l2tp << 4) : 0;
             continue;
         }
@@ -276,14 +373,14 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
         int64_t bM = 0;
         int bc = 0;
         if (act) {
-            bT = kNoLayout;
-            const int rb = lane * Fp, nf = cN[lane];
-            for (int j = 0; j < nf; j++) {
-                const uint64_t x = cT[rb + j], y = cG[rb + j];
+            bT = ~0ull;
+            for (int j = (int)(sgv & 0xFFFF); j < (int)(sgv >> 16); j++) {
+                const TGPair<TT> f = cTG[j];
+                const uint64_t x = f.x, y = f.y;
                 const bool take = y <= best_G && x < bT;
                 bT = take ? x : bT;
-                bM = take ? cM[rb + j] : bM;
-                bc = take ? cC[rb + j] : bc;
+                bM = take ? cM[j] : bM;
+                bc = take ? cC[j] : bc;
             }
         }
         const uint64_t B = wave_max(bT);
@@ -294,30 +391,36 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
             ((int64_t *)A.bottleneck)[o] = (int64_t)B;
             A.peak_mem[o] = peak;
         }
-        const int bei = bc / K, bti = bc - bei * K;
+        const int bei = K > 1 ? (int)__umulhi((uint32_t)bc, invK) : bc, bti = bc - bei * K;
         if (lane < A.s_max)
             tiling[o * A.s_max + lane] = act ? (uint8_t)(nibble(P.ep_log2, bei) | nibble(P.tp_log2, bti) << 4) : 0;
     }
 }
 
-int launch_tile(const heddle_profile *p, const PriceArgs &a, uint8_t *tiling, hipStream_t stream)
+template <class TT> static int launch_tile_t(const heddle_profile *p, const PriceArgs &a, uint8_t *tiling, hipStream_t stream)
 {
     const int64_t total = a.n * a.n_m;
-    if (total == 0) return HEDDLE_OK;
-    const size_t F = (size_t)p->dev.n_tp * p->dev.n_ep;
-    // layout tables (time, synchronisation, memory: 8 bytes each; layout index),
-    // kept counts, per-stage constants, threshold list (stage, index)
-    const size_t lds = (((size_t)a.s_cap * (F | 1) * 25 + a.s_cap + 15) & ~size_t(15)) + (size_t)a.s_cap * sizeof(StageK) +
-                       (size_t)a.s_cap * (F | 1) * 2;
+    const size_t lds = tile_lds_bytes<TT>(a.s_cap, p->dev.n_tp * p->dev.n_ep);
     int max_lds = 0;
     HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
     if (lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "layout table of this (s_max, n_tp, n_ep) does not fit in LDS");
     if (lds > 65536)
-        HEDDLE_HIP(hipFuncSetAttribute((const void *)tile_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+        HEDDLE_HIP(hipFuncSetAttribute((const void *)tile_kernel<TT>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
     const int blocks = (int)(total < 65536 ? total : 65536);
-    hipLaunchKernelGGL(tile_kernel, dim3(blocks), dim3(64), lds, stream, p->dev, a, tiling);
+    hipLaunchKernelGGL(tile_kernel<TT>, dim3(blocks), dim3(64), lds, stream, p->dev, a, tiling);
     HEDDLE_HIP(hipGetLastError());
     return HEDDLE_OK;
+}
+
+bool tile_narrow(const heddle_profile *p)
+{
+    return p->max_tiled_ns < (int64_t)0xFFFFFFFFll && p->max_ar_tiled_ns < (int64_t)0xFFFFFFFFll;
+}
+
+int launch_tile(const heddle_profile *p, const PriceArgs &a, uint8_t *tiling, hipStream_t stream)
+{
+    if (a.n * a.n_m == 0) return HEDDLE_OK;
+    return tile_narrow(p) ? launch_tile_t<uint32_t>(p, a, tiling, stream) : launch_tile_t<uint64_t>(p, a, tiling, stream);
 }
 
 }  // namespace heddle

@@ -56,7 +56,8 @@ class heddle_cluster_desc(C.Structure):
 
 class heddle_profile_info(C.Structure):
     _fields_ = [("narrow", C.c_int32 * 2), ("fx_exp", C.c_int32), ("L", C.c_int32), ("n_types", C.c_int32),
-                ("n_tp", C.c_int32), ("n_ep", C.c_int32), ("max_stage_ns", C.c_int64), ("scratch_bytes", C.c_int64)]
+                ("n_tp", C.c_int32), ("n_ep", C.c_int32), ("max_stage_ns", C.c_int64), ("scratch_bytes", C.c_int64),
+                ("narrow_tile", C.c_int32)]
 
 
 _lib = None
@@ -170,7 +171,7 @@ def heddle_profile_info_get(prof):
     _check(lib().heddle_profile_info_get(prof.handle, C.byref(info)))
     return dict(narrow_i64=bool(info.narrow[0]), narrow_f32=bool(info.narrow[1]), fx_exp=info.fx_exp, L=info.L,
                 n_types=info.n_types, n_tp=info.n_tp, n_ep=info.n_ep, max_stage_ns=info.max_stage_ns,
-                scratch_bytes=info.scratch_bytes)
+                scratch_bytes=info.scratch_bytes, narrow_tile=bool(info.narrow_tile))
 
 
 def _mlist(m):

@@ -67,6 +67,30 @@ def test_tile_random_instances(H, flags):
     say("tiled random plans", n_plans)
 
 
+@pytest.mark.parametrize("flags", [0, CO, DIST])
+def test_tile_wide_costs(H, flags):
+    """layer costs above 2^32 ns: the tile kernel's 64-bit variant"""
+    n_plans = 0
+    for seed in range(30):
+        w = random_instance(2700 + seed, moe=True, s_max=int([6, 9, 13][seed % 3]), n=41)
+        p = w.profile
+        p.layer_ns = np.ascontiguousarray(p.layer_ns << 30)
+        p.xlayer_ns = np.ascontiguousarray(p.xlayer_ns << 30)
+        prof = H.heddle_load_profile(p)
+        assert not H.heddle_profile_info_get(prof)["narrow_tile"]
+        check(gpu_tiled(H, prof, w, flags), oracle_tiled(w, flags), flags, f"wide seed {2700 + seed} flags {flags}")
+        n_plans += w.n * len(w.m)
+    say("tiled wide-cost plans", n_plans)
+
+
+def test_tile_variants_of_the_configs(H):
+    """the MoE benchmark config tiles in 32 bits, the stress config in 64"""
+    got = {name: H.heddle_profile_info_get(H.heddle_load_profile(make_workload(name, n=8).profile))["narrow_tile"]
+           for name in ("c2_7b_dense", "c4_moe", "c5_stress")}
+    say("32-bit tiling", got)
+    assert got["c4_moe"] and not got["c5_stress"]
+
+
 @pytest.mark.parametrize("name,n", [("c4_moe", 1500), ("c5_stress", 30), ("c2_7b_dense", 500)])
 @pytest.mark.parametrize("flags", [0, CO])
 def test_tile_config_subsets(H, name, n, flags):

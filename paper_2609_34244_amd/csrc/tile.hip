@@ -51,17 +51,6 @@ struct StageK {
     int32_t g, ki, node, i0, j0, pad;
 };
 
-__device__ __forceinline__ void wave_min_pair(uint64_t &a, uint64_t &b)
-{
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        const uint64_t x = __shfl_xor((unsigned long long)a, o), y = __shfl_xor((unsigned long long)b, o);
-        const bool take = x < a || (x == a && y < b);
-        a = take ? x : a;
-        b = take ? y : b;
-    }
-}
-
 // set lanes of a wavefront mask below this lane
 __device__ __forceinline__ int lanes_below(uint64_t m)
 {
@@ -73,13 +62,20 @@ template <class TT> struct alignas(2 * sizeof(TT)) TGPair {
     TT x, y;
 };
 
+// table entry i of a profile table, addressed by a 32-bit byte offset (every
+// profile table is far below 4 GB)
+template <class T> __device__ __forceinline__ T ld_at(const T *base, uint32_t i)
+{
+    return *(const T *)((const char *)base + i * (uint32_t)sizeof(T));
+}
+
 // LDS of one wavefront: the stage records, then per list entry (at most
 // s_cap * F) memory, time and synchronisation, the allowed-layout list, layout
 // index, stage and kept flag, then the per-stage segment bounds
 template <class TT> __host__ __device__ inline size_t tile_lds_bytes(int s_cap, int F)
 {
     const size_t n = (size_t)s_cap * F;
-    return (size_t)s_cap * sizeof(StageK) + n * (8 + 2 * sizeof(TT) + 4 + 3) + 3 + (size_t)s_cap * 4;
+    return (size_t)s_cap * sizeof(StageK) + n * (8 + sizeof(TGPair<TT>) + 4 + 3) + 3 + (size_t)s_cap * 4;
 }
 
 // TT: uint32_t when every stage time and synchronisation value is below
@@ -185,20 +181,21 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
         if (act) {
             const int64_t inflight = (int64_t)(S - lane) < Mp ? (int64_t)(S - lane) : Mp;
             const int g_next = __builtin_amdgcn_update_dpp(g, g, kDppWaveShl1, 0xF, 0xF, false);
-            const int64_t p2p = lane + 1 < S ? P.p2p_ns[g * N + g_next] : 0;
-            const int node = P.node_size[g];
+            const uint32_t ug = (uint32_t)g, uj = (uint32_t)j0, ui = (uint32_t)i0, ur = (uint32_t)(ki * R);
+            const int64_t p2p = lane + 1 < S ? ld_at(P.p2p_ns, ug * N + (uint32_t)g_next) : 0;
+            const int node = ld_at(P.node_size, ug);
             const int64_t W = (int64_t)tp * D;
-            const int64_t bw = W <= node ? P.intra_bw[g] : P.link_bw[g * N + g];
-            const uint64_t *base = P.rows64[0] + ((size_t)(g * K + ki) * 3 + kA2ANone) * R;
-            const int64_t gd = P.pre_grad[ki * R + j0] - P.pre_grad[ki * R + i0];
+            const int64_t bw = W <= node ? ld_at(P.intra_bw, ug) : ld_at(P.link_bw, ug * (N + 1));
+            const uint32_t trow = ((ug * K + (uint32_t)ki) * 3 + kA2ANone) * R;
+            const int64_t gd = ld_at(P.pre_grad, ur + uj) - ld_at(P.pre_grad, ur + ui);
             StageK &sk = SK[lane];
             sk.W = W;
-            sk.cap = P.mem_cap[g];
+            sk.cap = ld_at(P.mem_cap, ug);
             sk.bw = bw;
-            sk.T0 = (int64_t)(base[j0] - base[i0] + (uint64_t)p2p);
-            sk.n_moe = P.pre_moe[j0] - P.pre_moe[i0];
-            sk.dstate = P.pre_dstate[ki * R + j0] - P.pre_dstate[ki * R + i0];
-            sk.act_b = P.pre_act[ki * R + j0] - P.pre_act[ki * R + i0];
+            sk.T0 = (int64_t)(ld_at(P.rows64[0], trow + uj) - ld_at(P.rows64[0], trow + ui) + (uint64_t)p2p);
+            sk.n_moe = ld_at(P.pre_moe, uj) - ld_at(P.pre_moe, ui);
+            sk.dstate = ld_at(P.pre_dstate, ur + uj) - ld_at(P.pre_dstate, ur + ui);
+            sk.act_b = ld_at(P.pre_act, ur + uj) - ld_at(P.pre_act, ur + ui);
             sk.inflight = inflight;
             sk.g_dense = allreduce_ns(gd, D, bw);
             sk.g = g; sk.ki = ki; sk.node = node; sk.i0 = i0; sk.j0 = j0;
@@ -220,7 +217,7 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
                 const StageK &sk = SK[s];
                 const int l2e = nibble(P.ep_log2, ei), l2t = nibble(P.tp_log2, ti);
                 const int64_t gmask = ((int64_t)1 << (l2e + l2t)) - 1;    // EP x ETP, a power of two
-                allowed = P.profiled[sk.g * K + ti] && (1 << l2t) <= sk.node && (sk.W & gmask) == 0;
+                allowed = ld_at(P.profiled, (uint32_t)(sk.g * K + ti)) && (1 << l2t) <= sk.node && (sk.W & gmask) == 0;
                 ent = (uint32_t)s | (uint32_t)c << 8 | (uint32_t)ei << 16 | (uint32_t)ti << 24;
             }
             const uint64_t mk = ballot(allowed);
@@ -244,13 +241,15 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
                 const StageK &sk = SK[s];
                 const int sg = sk.g, ski = sk.ki, snode = sk.node, si0 = sk.i0, sj0 = sk.j0;
                 const int l2e = nibble(P.ep_log2, ei), l2t = nibble(P.tp_log2, ti);
-                const int64_t *xd = P.xdelta + ((size_t)(sg * K + ski) * K + ti) * R;
-                T = (uint64_t)sk.T0 + (uint64_t)(xd[sj0] - xd[si0]) +
-                    (uint64_t)(sk.n_moe * P.a2a_ns[sg * 3 + a2a_variant(1 << l2e, 1 << l2t, snode)]);
-                const int64_t *xs = P.pre_xstate + (size_t)(ti * E + ei) * R;
-                mem = sk.dstate + (xs[sj0] - xs[si0]) + sk.inflight * sk.act_b;
-                const int64_t *xg = P.pre_xgrad + (size_t)(ti * E + ei) * R;
-                gs = sk.g_dense + allreduce_ns(xg[sj0] - xg[si0], sk.W >> (l2e + l2t), sk.bw);
+                const uint32_t xd = ((uint32_t)(sg * K + ski) * K + (uint32_t)ti) * R;
+                const uint32_t xe = (uint32_t)(ti * E + ei) * R;
+                const uint32_t uj = (uint32_t)sj0, ui = (uint32_t)si0;
+                T = (uint64_t)sk.T0 + (uint64_t)(ld_at(P.xdelta, xd + uj) - ld_at(P.xdelta, xd + ui)) +
+                    (uint64_t)(sk.n_moe * ld_at(P.a2a_ns, (uint32_t)(sg * 3 + a2a_variant(1 << l2e, 1 << l2t, snode))));
+                mem = sk.dstate + (ld_at(P.pre_xstate, xe + uj) - ld_at(P.pre_xstate, xe + ui)) +
+                      (int64_t)(int32_t)sk.inflight * sk.act_b;
+                gs = sk.g_dense + allreduce_ns(ld_at(P.pre_xgrad, xe + uj) - ld_at(P.pre_xgrad, xe + ui),
+                                               sk.W >> (l2e + l2t), sk.bw);
                 fits = mem <= sk.cap;
             }
             const uint64_t mk = ballot(fits);
@@ -299,7 +298,7 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
         for (int q0 = 0; q0 < n_fit; q0 += 64) {
             const int q = q0 + lane;
             const bool keep = q < n_fit && kf[q];
-            TGPair<TT> e = {0, 0};
+            TGPair<TT> e = {};
             int64_t mx = 0;
             uint8_t c = 0, s = 0;
             if (keep) {
@@ -324,7 +323,7 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
 
         // ---- lanes = kept layouts as thresholds G: the plan's iteration time
         // with every stage at its fastest kept layout of synchronisation <= G
-        uint64_t best_it = ~0ull, best_G = ~0ull;
+        uint64_t best_it = ~0ull, best_G = ~0ull, best_B = 0;
         for (int q0 = 0; q0 < n_k; q0 += 64) {
             const int q = q0 + lane;
             const TT G = q < n_k ? cTG[q].y : (TT)0;
@@ -334,33 +333,35 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
             for (int s2 = 0; s2 < S; s2++) {
                 const uint32_t b = uni64(sgv, s2);
                 TT bT = kNone, bG = 0;
-                auto consider = [&](TGPair<TT> f) {
-                    const bool take = f.y <= G && f.x < bT;    // kept layouts have distinct times
-                    bT = take ? f.x : bT;
-                    bG = take ? f.y : bG;
+                auto consider = [&](TT x, TT y) {
+                    const bool take = y <= G && x < bT;        // kept layouts have distinct times
+                    bT = take ? x : bT;
+                    bG = take ? y : bG;
                 };
                 const int hi = (int)(b >> 16);
                 int j = (int)(b & 0xFFFF);
                 for (; j + 1 < hi; j += 2) {                   // two entries per step
-                    const TGPair<TT> f0 = cTG[j], f1 = cTG[j + 1];
-                    consider(f0);
-                    consider(f1);
+                    const TT x0 = cTG[j].x, y0 = cTG[j].y, x1 = cTG[j + 1].x, y1 = cTG[j + 1].y;
+                    consider(x0, y0);
+                    consider(x1, y1);
                 }
-                if (j < hi) consider(cTG[j]);
+                if (j < hi) consider(cTG[j].x, cTG[j].y);
                 ok = ok && bT != kNone;
                 maxT = bT > maxT ? bT : maxT;
                 sumT += (uint64_t)bT;
                 maxg = bG > maxg ? bG : maxg;
             }
-            uint64_t it = ~0ull, Gq = ~0ull;
-            if (q < n_k && ok) {
-                it = (uint64_t)(Mp - 1) * (uint64_t)maxT + sumT + (uint64_t)maxg;
-                Gq = (uint64_t)G;
-            }
-            wave_min_pair(it, Gq);
-            if (it < best_it || (it == best_it && Gq < best_G)) {
-                best_it = it;
-                best_G = Gq;
+            const bool valid = q < n_k && ok;
+            const uint64_t it = valid ? (uint64_t)(Mp - 1) * (uint64_t)maxT + sumT + (uint64_t)maxg : ~0ull;
+            // the smallest iteration time, then the smallest bound among the lanes
+            // that reach it; the bottleneck is the slowest chosen stage of such a lane
+            const uint64_t it_min = group_min<uint64_t>(it, 64);
+            const TT g_min = group_min<TT>(valid && it == it_min ? G : kNone, 64);
+            const uint64_t win = ballot(valid && it == it_min && G == g_min);
+            if (win && (it_min < best_it || (it_min == best_it && (uint64_t)g_min < best_G))) {
+                best_it = it_min;
+                best_G = (uint64_t)g_min;
+                best_B = (uint64_t)(TT)rl64((int64_t)(uint64_t)maxT, __ffsll((unsigned long long)win) - 1);
             }
         }
 
@@ -369,21 +370,19 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
             if (lane < A.s_max) tiling[o * A.s_max + lane] = act ? (uint8_t)(l2ep | l2tp << 4) : 0;
             continue;
         }
-        uint64_t bT = 0;
         int64_t bM = 0;
         int bc = 0;
         if (act) {
-            bT = ~0ull;
+            uint64_t bT = ~0ull;
             for (int j = (int)(sgv & 0xFFFF); j < (int)(sgv >> 16); j++) {
-                const TGPair<TT> f = cTG[j];
-                const uint64_t x = f.x, y = f.y;
+                const uint64_t x = cTG[j].x, y = cTG[j].y;
                 const bool take = y <= best_G && x < bT;
                 bT = take ? x : bT;
                 bM = take ? cM[j] : bM;
                 bc = take ? cC[j] : bc;
             }
         }
-        const uint64_t B = wave_max(bT);
+        const uint64_t B = best_B;
         const int64_t peak = wave_max(bM);
         if (lane == 0) {
             A.status[o] = HEDDLE_S_OK;

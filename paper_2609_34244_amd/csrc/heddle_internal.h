@@ -68,6 +68,7 @@ struct DevProfile {
     const int64_t *pre_dstate;       // [n_tp][L+1]
     const int64_t *pre_xstate;       // [n_tp][n_ep][L+1]
     const int64_t *xdelta;           // [n_types][n_tp][n_tp][L+1]
+    const uint32_t *etp_mask;        // [n_types] bit k: tp_degrees[k] is profiled and fits a node
     // [n_types][n_tp][n_ep][n_f][2][lim_stride]: per row, the largest end that
     // fits from row i, then its inverse (smallest row whose limit reaches x)
     const uint8_t *mem_lim;

@@ -491,6 +491,13 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
            o_link = B.add(d->link_bw_MBps, (size_t)N * N * 8), o_epd = B.add(d->ep_degrees, (size_t)E * 4),
            o_lim = B.add(lim_tab), o_dstate = B.add(pre_dstate), o_xstate = B.add(pre_xstate),
            o_xdelta = B.add(xdelta);
+    // expert tiling: per GPU type the TP indices usable as ETP (profiled, at
+    // most the type's node size), one bit each
+    std::vector<uint32_t> etp_mask(N, 0);
+    for (int g = 0; g < N; g++)
+        for (int k = 0; k < K; k++)
+            if (d->profiled[(size_t)g * K + k] && d->tp_degrees[k] <= d->node_size[g]) etp_mask[g] |= 1u << k;
+    const size_t o_etp = B.add(etp_mask);
 
     heddle_profile *p = new (std::nothrow) heddle_profile;
     if (!p) return fail(HEDDLE_E_NOMEM, "host allocation failed");
@@ -527,6 +534,7 @@ extern "C" int heddle_load_profile(const heddle_profile_desc *d, heddle_profile 
     dp.pre_dstate = (const int64_t *)(base + o_dstate);
     dp.pre_xstate = (const int64_t *)(base + o_xstate);
     dp.xdelta = (const int64_t *)(base + o_xdelta);
+    dp.etp_mask = (const uint32_t *)(base + o_etp);
     dp.rows64[0] = (const uint64_t *)(base + o_r64a);
     dp.rows64[1] = (const uint64_t *)(base + o_r64b);
     dp.rows32[0] = (const uint32_t *)(base + o_r32a);

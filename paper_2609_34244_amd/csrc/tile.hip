@@ -47,8 +47,8 @@ namespace heddle {
 
 // per-stage constants of the layout pricing, one LDS record per stage
 struct StageK {
-    int64_t W, cap, bw, T0, n_moe, dstate, act_b, inflight, g_dense;
-    int32_t g, ki, node, i0, j0, pad;
+    int64_t cap, bw, T0, dstate, act_b, g_dense;
+    int32_t W, n_moe, inflight, etp, g, ki, node, i0, j0, pad;
 };
 
 // set lanes of a wavefront mask below this lane
@@ -189,14 +189,15 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
             const uint32_t trow = ((ug * K + (uint32_t)ki) * 3 + kA2ANone) * R;
             const int64_t gd = ld_at(P.pre_grad, ur + uj) - ld_at(P.pre_grad, ur + ui);
             StageK &sk = SK[lane];
-            sk.W = W;
+            sk.W = (int32_t)W;
+            sk.etp = (int32_t)ld_at(P.etp_mask, ug);
             sk.cap = ld_at(P.mem_cap, ug);
             sk.bw = bw;
             sk.T0 = (int64_t)(ld_at(P.rows64[0], trow + uj) - ld_at(P.rows64[0], trow + ui) + (uint64_t)p2p);
             sk.n_moe = ld_at(P.pre_moe, uj) - ld_at(P.pre_moe, ui);
             sk.dstate = ld_at(P.pre_dstate, ur + uj) - ld_at(P.pre_dstate, ur + ui);
             sk.act_b = ld_at(P.pre_act, ur + uj) - ld_at(P.pre_act, ur + ui);
-            sk.inflight = inflight;
+            sk.inflight = (int32_t)inflight;
             sk.g_dense = allreduce_ns(gd, D, bw);
             sk.g = g; sk.ki = ki; sk.node = node; sk.i0 = i0; sk.j0 = j0;
         }
@@ -216,8 +217,8 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
                 const int ei = K > 1 ? (int)__umulhi((uint32_t)c, invK) : c, ti = c - ei * K;
                 const StageK &sk = SK[s];
                 const int l2e = nibble(P.ep_log2, ei), l2t = nibble(P.tp_log2, ti);
-                const int64_t gmask = ((int64_t)1 << (l2e + l2t)) - 1;    // EP x ETP, a power of two
-                allowed = ld_at(P.profiled, (uint32_t)(sk.g * K + ti)) && (1 << l2t) <= sk.node && (sk.W & gmask) == 0;
+                const int32_t gmask = (int32_t)((1u << (l2e + l2t)) - 1);    // EP x ETP, a power of two
+                allowed = ((sk.etp >> ti) & 1) && (sk.W & gmask) == 0;
                 ent = (uint32_t)s | (uint32_t)c << 8 | (uint32_t)ei << 16 | (uint32_t)ti << 24;
             }
             const uint64_t mk = ballot(allowed);
@@ -245,11 +246,11 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
                 const uint32_t xe = (uint32_t)(ti * E + ei) * R;
                 const uint32_t uj = (uint32_t)sj0, ui = (uint32_t)si0;
                 T = (uint64_t)sk.T0 + (uint64_t)(ld_at(P.xdelta, xd + uj) - ld_at(P.xdelta, xd + ui)) +
-                    (uint64_t)(sk.n_moe * ld_at(P.a2a_ns, (uint32_t)(sg * 3 + a2a_variant(1 << l2e, 1 << l2t, snode))));
+                    (uint64_t)((int64_t)sk.n_moe * ld_at(P.a2a_ns, (uint32_t)(sg * 3 + a2a_variant(1 << l2e, 1 << l2t, snode))));
                 mem = sk.dstate + (ld_at(P.pre_xstate, xe + uj) - ld_at(P.pre_xstate, xe + ui)) +
-                      (int64_t)(int32_t)sk.inflight * sk.act_b;
+                      (int64_t)sk.inflight * sk.act_b;
                 gs = sk.g_dense + allreduce_ns(ld_at(P.pre_xgrad, xe + uj) - ld_at(P.pre_xgrad, xe + ui),
-                                               sk.W >> (l2e + l2t), sk.bw);
+                                               (int64_t)(sk.W >> (l2e + l2t)), sk.bw);
                 fits = mem <= sk.cap;
             }
             const uint64_t mk = ballot(fits);

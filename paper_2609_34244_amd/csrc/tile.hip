@@ -75,7 +75,10 @@ template <class T> __device__ __forceinline__ T ld_at(const T *base, uint32_t i)
 template <class TT> __host__ __device__ inline size_t tile_lds_bytes(int s_cap, int F)
 {
     const size_t n = (size_t)s_cap * F;
-    return (size_t)s_cap * sizeof(StageK) + n * (8 + sizeof(TGPair<TT>) + 4 + 3) + 3 + (size_t)s_cap * 4;
+    // (the time-synchronisation list has F + 1 entries of padding: the Pareto
+    // pass reads up to that far past a segment start)
+    return (size_t)s_cap * sizeof(StageK) + n * (8 + sizeof(TGPair<TT>) + 4 + 3) + (size_t)(F + 1) * sizeof(TGPair<TT>) +
+           3 + (size_t)s_cap * 4;
 }
 
 // TT: uint32_t when every stage time and synchronisation value is below
@@ -91,7 +94,7 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
     StageK *SK = (StageK *)smem;                               // [s_cap]
     int64_t *cM = (int64_t *)(SK + A.s_cap);                   // [nmax] memory of a list entry
     TGPair<TT> *cTG = (TGPair<TT> *)(cM + nmax);               // [nmax] time, synchronisation
-    uint32_t *AL = (uint32_t *)(cTG + nmax);                   // [nmax] allowed: s | c << 8 | ei << 16 | ti << 24
+    uint32_t *AL = (uint32_t *)(cTG + nmax + F + 1);           // [nmax] allowed: s | c << 8 | ei << 16 | ti << 24
     uint8_t *cC = (uint8_t *)(AL + nmax);                      // [nmax] layout index c = ei * K + ti
     uint8_t *cS = cC + nmax;                                   // [nmax] stage
     uint8_t *kf = cS + nmax;                                   // [nmax] kept flag
@@ -272,25 +275,38 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
 
         // ---- lanes = fitting layouts: a layout is kept when no other layout of
         // its stage beats it in both time and synchronisation (an earlier one
-        // also by being equal in both)
+        // also by being equal in both). Every lane walks the longest segment's
+        // length (a wave-uniform loop, so the tests stay lane masks); the steps
+        // past its own segment are masked (their reads stay inside the list's
+        // padded LDS region).
+        const int max_seg = uni(wave_max(act ? (int)(sgv >> 16) - (int)(sgv & 0xFFFF) : 0));
         for (int q0 = 0; q0 < n_fit; q0 += 64) {
             const int q = q0 + lane;
-            if (q < n_fit) {
-                const int s = cS[q];
-                const TGPair<TT> e = cTG[q];
-                const int lo = seg_lo[s], hi = seg_hi[s];
-                auto beats = [&](int j, TGPair<TT> f) {
-                    return j != q && f.x <= e.x && f.y <= e.y && (j < q || f.x < e.x || f.y < e.y);
-                };
-                bool keep = true;
-                int j = lo;
-                for (; j + 1 < hi; j += 2) {                   // two entries per step
-                    const TGPair<TT> f0 = cTG[j], f1 = cTG[j + 1];
-                    keep = keep && !beats(j, f0) && !beats(j + 1, f1);
+            const bool in = q < n_fit;
+            const int qc = in ? q : n_fit - 1;
+            const int s = cS[qc];
+            const TGPair<TT> e = cTG[qc];
+            const int lo = seg_lo[s], len = seg_hi[s] - lo, qo = qc - lo;
+            const TGPair<TT> *row = cTG + lo;
+            auto beats = [&](int d, TGPair<TT> f) {
+                if constexpr (sizeof(TT) == 4) {
+                    // the pair compared as one 64-bit word: at most e in both and a
+                    // different pair, or the same pair earlier
+                    uint64_t fw, ew;
+                    __builtin_memcpy(&fw, &f, 8);
+                    __builtin_memcpy(&ew, &e, 8);
+                    return (d < len) & (((f.x <= e.x) & (f.y <= e.y) & (fw != ew)) | ((fw == ew) & (d < qo)));
+                } else {
+                    return (d < len) & (d != qo) & (f.x <= e.x) & (f.y <= e.y) & ((d < qo) | (f.x < e.x) | (f.y < e.y));
                 }
-                if (j < hi) keep = keep && !beats(j, cTG[j]);
-                kf[q] = (uint8_t)keep;
+            };
+            bool keep = true;
+            for (int d = 0; d < max_seg; d += 2) {             // two entries per step
+                const TGPair<TT> f0 = row[d], f1 = row[d + 1];
+                keep &= !beats(d, f0);
+                keep &= !beats(d + 1, f1);
             }
+            if (in) kf[q] = (uint8_t)keep;
         }
         wave_sync();
         // compacted in place: an entry's new place is at or before its old one

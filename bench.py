@@ -370,7 +370,7 @@ def main():
         "tiling": None if not args.tiling else dict({
             "tile_kernel_ms": float(np.mean(tile_ms)),
             "note": "heddle_tile_plans re-tiles every plan's expert layouts after pricing, inside the timed step"},
-            **tiling_gain(H, prof, ns, st, m, flags, w, out)),
+            **tiling_gain(H, prof, ns, st, m, flags, w, out, float(np.mean(tile_ms)))),
         "best_plan": {"template": best[0], "m_index": best[1], "iter": best[2]} if best else None,
         "profile_load_ms": load_ms,
         "template_h2d_ms": h2d_ms,
@@ -384,20 +384,37 @@ def main():
     print(json.dumps(result), flush=True)
 
 
-def tiling_gain(H, prof, ns, st, m, flags, w, tiled):
+# lane-ops per unit of the tile kernel's work: a priced layout (time 8:
+# prefix difference, all-to-all product, two sums; memory 10: prefix
+# difference, in-flight product, two sums, capacity compare; synchronisation
+# 12: prefix difference, the ring formula's two products, quotient and
+# ceiling, sum), a dominance test (two compares and the tie rule's two) and a
+# bound test (a kept layout under a bound: two compares, two selects; or a
+# stage fold: two maxima and a 64-bit sum); 64-bit values count two lane-ops
+TILE_OPS = {"layouts_priced": 30, "dominance_tests": 4, "bound_tests": 4}
+
+
+def tiling_gain(H, prof, ns, st, m, flags, w, tiled, tile_ms):
     """the same plans priced without tiling (one launch outside the timed
-    region) against the tiled outputs"""
+    region) against the tiled outputs, and the tile kernel's rate in lane-ops
+    over the work heddle_count_tile_work counts on those priced plans"""
     import numpy as np
     import torch
     ref = H.alloc_outputs(w.n, len(m), w.s_max, flags)
     H.heddle_price_plans(prof, ns, st, m, flags, ref)
     torch.cuda.synchronize()
+    counts = dict(zip(TILE_OPS, H.heddle_count_tile_work(prof, ns, st, m, flags, ref)))
+    ops = sum(TILE_OPS[k] * v for k, v in counts.items())
+    achieved = ops / (tile_ms / 1e3)
     s0, s1 = ref["status"].cpu().numpy(), tiled["status"].cpu().numpy()
     i0, i1 = ref["iter"].cpu().numpy().astype(np.float64), tiled["iter"].cpu().numpy().astype(np.float64)
     both = (s0 == 0) & (s1 == 0)
     return {"plans_ok_untiled": int((s0 == 0).sum()), "plans_ok_tiled": int((s1 == 0).sum()),
             "faster_after_tiling": int((i1[both] < i0[both]).sum()),
-            "mean_iter_ratio": float(np.mean(i1[both] / i0[both])) if both.any() else None}
+            "mean_iter_ratio": float(np.mean(i1[both] / i0[both])) if both.any() else None,
+            "tile_roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
+                              "unit": "Tlane-op/s", "frac": achieved / PEAK_LANE_OPS, "kernel_ms": tile_ms,
+                              "work_per_launch": counts, "ops_per_unit": TILE_OPS}}
 
 
 def run_fill(args, H, flags):

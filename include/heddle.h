@@ -349,6 +349,30 @@ int heddle_tile_plans(const heddle_profile *p, int64_t n, int32_t s_max,
                       hipStream_t stream);
 
 /*
+ * heddle_count_tile_work -- algorithmic work of heddle_tile_plans on the same
+ * priced plans (section 5.3, expert tiling paragraph), for throughput
+ * reports. Synchronous. Over the plans that are tiled (a split and a valid
+ * template):
+ *   h_counts[0]  layouts priced: the allowed (stage, EP x ETP) layouts, each
+ *                priced for time, memory and synchronisation;
+ *   h_counts[1]  dominance tests: for every stage, its fitting layouts
+ *                squared (each against each, to keep the layouts no other
+ *                one beats in both time and synchronisation);
+ *   h_counts[2]  bound tests: kept layouts x (kept layouts + stages), every
+ *                kept layout's synchronisation tried as the bound against
+ *                every kept layout and folded over every stage;
+ * plans with a stage that has no fitting layout add only to h_counts[0].
+ *   d_layers, d_status  DEVICE outputs of heddle_price_plans (unchanged).
+ * Returns HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_RANGE, HEDDLE_E_NOMEM or
+ * HEDDLE_E_DEVICE.
+ */
+int heddle_count_tile_work(const heddle_profile *p, int64_t n, int32_t s_max,
+                           const uint8_t *d_n_stages, const uint32_t *d_stages,
+                           const int32_t *h_m, int32_t n_m, uint32_t flags,
+                           const uint8_t *d_layers, const uint8_t *d_status,
+                           int64_t *h_counts, hipStream_t stream);
+
+/*
  * GPU composition as a node list per GPU type (section 5.1, non-uniform
  * composition support): the nodes of a type may differ in size. HOST memory,
  * read during heddle_load_cluster.

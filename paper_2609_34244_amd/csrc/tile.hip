@@ -83,7 +83,9 @@ template <class TT> __host__ __device__ inline size_t tile_lds_bytes(int s_cap, 
 
 // TT: uint32_t when every stage time and synchronisation value is below
 // 2^32 - 1 (the profile's bounds), else uint64_t; all ones marks no layout
-template <class TT>
+// COUNT: no outputs; the work of the batch is added to A.work[0..2] (layouts
+// priced, dominance tests, bound tests).
+template <class TT, bool COUNT>
 __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, uint8_t *tiling)
 {
     constexpr TT kNone = (TT)~(TT)0;
@@ -144,6 +146,7 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
         rec_n = lane < A.s_max ? A.stages[tt * A.s_max + lane] : 0u;
     };
     if ((int64_t)blockIdx.x < total) fetch(blockIdx.x);
+    unsigned long long w_priced = 0, w_dom = 0, w_bound = 0;  // COUNT: this wavefront's work
 
     for (int64_t o = blockIdx.x; o < total; o += gridDim.x) {
         const int st_in = st_n, S = S_n, nl_all = nl_n;
@@ -153,7 +156,7 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
         const int k = (int)(o - t * A.n_m);
         const bool has_split = (st_in == HEDDLE_S_OK || st_in == HEDDLE_S_OOM) && rl32(nl_all, 0) > 0;
         if (!has_split) {                                      // no split: nothing to tile
-            if (lane < A.s_max) tiling[o * A.s_max + lane] = 0;
+            if (!COUNT && lane < A.s_max) tiling[o * A.s_max + lane] = 0;
             continue;
         }
         // a split implies a valid template; buffers that do not describe one
@@ -173,7 +176,7 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
         const bool bad = S < 1 || S > A.s_cap || total_layers != L || D < 1 ||
                          __ballot(act && (g >= N || nl < 1 || !((P.tp_present >> l2tp) & 1))) != 0;
         if (bad) {
-            if (lane < A.s_max) tiling[o * A.s_max + lane] = 0;
+            if (!COUNT && lane < A.s_max) tiling[o * A.s_max + lane] = 0;
             continue;
         }
         const int32_t m = A.m[k];
@@ -229,6 +232,7 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
             n_al += __popcll(mk);
         }
         wave_sync();
+        w_priced += (unsigned long long)n_al;
 
         // ---- lanes = allowed layouts: price them; the ones that fit memory
         // go, in the same order, to the fitting list
@@ -269,7 +273,7 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
         wave_sync();
         uint32_t sgv = segments(n_fit, act);
         if (ballot(act && (sgv >> 16) == (sgv & 0xFFFF))) {    // a stage with no fitting layout: unchanged
-            if (lane < A.s_max) tiling[o * A.s_max + lane] = act ? (uint8_t)(l2ep | l2tp << 4) : 0;
+            if (!COUNT && lane < A.s_max) tiling[o * A.s_max + lane] = act ? (uint8_t)(l2ep | l2tp << 4) : 0;
             continue;
         }
 
@@ -279,7 +283,9 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
         // length (a wave-uniform loop, so the tests stay lane masks); the steps
         // past its own segment are masked (their reads stay inside the list's
         // padded LDS region).
-        const int max_seg = uni(wave_max(act ? (int)(sgv >> 16) - (int)(sgv & 0xFFFF) : 0));
+        const int seg_len = act ? (int)(sgv >> 16) - (int)(sgv & 0xFFFF) : 0;
+        const int max_seg = uni(wave_max(seg_len));
+        if (COUNT) w_dom += wave_sum((uint32_t)(seg_len * seg_len));   // every pair of a stage's fitting layouts
         for (int q0 = 0; q0 < n_fit; q0 += 64) {
             const int q = q0 + lane;
             const bool in = q < n_fit;
@@ -337,6 +343,10 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
         }
         wave_sync();
         sgv = segments(n_k, act);
+        if (COUNT) {                                           // every bound against every kept layout and stage
+            w_bound += (unsigned long long)n_k * (unsigned long long)(n_k + S);
+            continue;
+        }
 
         // ---- lanes = kept layouts as thresholds G: the plan's iteration time
         // with every stage at its fastest kept layout of synchronisation <= G
@@ -384,7 +394,7 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
 
         // ---- lanes = stages: write the chosen layouts
         if (best_it == ~0ull) {                                // no bound serves every stage: unchanged
-            if (lane < A.s_max) tiling[o * A.s_max + lane] = act ? (uint8_t)(l2ep | l2tp << 4) : 0;
+            if (!COUNT && lane < A.s_max) tiling[o * A.s_max + lane] = act ? (uint8_t)(l2ep | l2tp << 4) : 0;
             continue;
         }
         int64_t bM = 0;
@@ -411,9 +421,15 @@ __global__ void __launch_bounds__(64, 6) tile_kernel(DevProfile P, PriceArgs A, 
         if (lane < A.s_max)
             tiling[o * A.s_max + lane] = act ? (uint8_t)(nibble(P.ep_log2, bei) | nibble(P.tp_log2, bti) << 4) : 0;
     }
+    if (COUNT && lane == 0) {
+        if (w_priced) atomicAdd(&A.work[0], w_priced);
+        if (w_dom) atomicAdd(&A.work[1], w_dom);
+        if (w_bound) atomicAdd(&A.work[2], w_bound);
+    }
 }
 
-template <class TT> static int launch_tile_t(const heddle_profile *p, const PriceArgs &a, uint8_t *tiling, hipStream_t stream)
+template <class TT, bool COUNT>
+static int launch_tile_t(const heddle_profile *p, const PriceArgs &a, uint8_t *tiling, hipStream_t stream)
 {
     const int64_t total = a.n * a.n_m;
     const size_t lds = tile_lds_bytes<TT>(a.s_cap, p->dev.n_tp * p->dev.n_ep);
@@ -421,9 +437,9 @@ template <class TT> static int launch_tile_t(const heddle_profile *p, const Pric
     HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
     if (lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "layout table of this (s_max, n_tp, n_ep) does not fit in LDS");
     if (lds > 65536)
-        HEDDLE_HIP(hipFuncSetAttribute((const void *)tile_kernel<TT>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+        HEDDLE_HIP(hipFuncSetAttribute((const void *)tile_kernel<TT, COUNT>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
     const int blocks = (int)(total < 65536 ? total : 65536);
-    hipLaunchKernelGGL(tile_kernel<TT>, dim3(blocks), dim3(64), lds, stream, p->dev, a, tiling);
+    hipLaunchKernelGGL((tile_kernel<TT, COUNT>), dim3(blocks), dim3(64), lds, stream, p->dev, a, tiling);
     HEDDLE_HIP(hipGetLastError());
     return HEDDLE_OK;
 }
@@ -436,29 +452,27 @@ bool tile_narrow(const heddle_profile *p)
 int launch_tile(const heddle_profile *p, const PriceArgs &a, uint8_t *tiling, hipStream_t stream)
 {
     if (a.n * a.n_m == 0) return HEDDLE_OK;
-    return tile_narrow(p) ? launch_tile_t<uint32_t>(p, a, tiling, stream) : launch_tile_t<uint64_t>(p, a, tiling, stream);
+    if (a.work)
+        return tile_narrow(p) ? launch_tile_t<uint32_t, true>(p, a, tiling, stream) : launch_tile_t<uint64_t, true>(p, a, tiling, stream);
+    return tile_narrow(p) ? launch_tile_t<uint32_t, false>(p, a, tiling, stream) : launch_tile_t<uint64_t, false>(p, a, tiling, stream);
 }
 
 }  // namespace heddle
 
 using namespace heddle;
 
-extern "C" int heddle_tile_plans(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,
-                                 const uint32_t *d_stages, const int32_t *h_m, int32_t n_m, uint32_t flags,
-                                 void *d_iter, void *d_bottleneck, int64_t *d_peak_mem, const uint8_t *d_layers,
-                                 uint8_t *d_status, uint8_t *d_tiling, hipStream_t stream)
+// host checks and arguments of a tiling launch over priced plans
+static int tile_args(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,
+                     const uint32_t *d_stages, const int32_t *h_m, int32_t n_m, uint32_t flags, PriceArgs &a)
 {
     int rc = validate_price_args(p, n, s_max, d_n_stages, d_stages, h_m, n_m, flags);
     if (rc) return rc;
     if (flags & HEDDLE_F_FP32) return fail(HEDDLE_E_INVAL, "expert tiling is defined for int64 costs (no HEDDLE_F_FP32)");
-    if (n > 0 && (!d_iter || !d_bottleneck || !d_peak_mem || !d_layers || !d_status || !d_tiling))
-        return fail(HEDDLE_E_INVAL, "device pointer is NULL");
     int64_t m_max = 0;
     for (int k = 0; k < n_m; k++) m_max = h_m[k] > m_max ? h_m[k] : m_max;
     const int64_t s_cap = s_max < p->dev.L ? s_max : p->dev.L;
     const __int128 bound = (__int128)(m_max - 1 + s_cap) * p->max_tiled_ns + p->max_ar_tiled_ns;
     if (bound >= kLimit62) return fail(HEDDLE_E_RANGE, "tiled iteration time could exceed 2^62 for these m");
-    PriceArgs a;
     std::memset(&a, 0, sizeof(a));
     a.n = n;
     a.s_max = s_max;
@@ -468,10 +482,51 @@ extern "C" int heddle_tile_plans(const heddle_profile *p, int64_t n, int32_t s_m
     for (int k = 0; k < n_m; k++) a.m[k] = h_m[k];
     a.n_stages = d_n_stages;
     a.stages = d_stages;
+    return HEDDLE_OK;
+}
+
+extern "C" int heddle_tile_plans(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,
+                                 const uint32_t *d_stages, const int32_t *h_m, int32_t n_m, uint32_t flags,
+                                 void *d_iter, void *d_bottleneck, int64_t *d_peak_mem, const uint8_t *d_layers,
+                                 uint8_t *d_status, uint8_t *d_tiling, hipStream_t stream)
+{
+    PriceArgs a;
+    int rc = tile_args(p, n, s_max, d_n_stages, d_stages, h_m, n_m, flags, a);
+    if (rc) return rc;
+    if (n > 0 && (!d_iter || !d_bottleneck || !d_peak_mem || !d_layers || !d_status || !d_tiling))
+        return fail(HEDDLE_E_INVAL, "device pointer is NULL");
     a.iter = d_iter;
     a.bottleneck = d_bottleneck;
     a.peak_mem = d_peak_mem;
     a.layers = const_cast<uint8_t *>(d_layers);
     a.status = d_status;
     return launch_tile(p, a, d_tiling, stream);
+}
+
+extern "C" int heddle_count_tile_work(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,
+                                      const uint32_t *d_stages, const int32_t *h_m, int32_t n_m, uint32_t flags,
+                                      const uint8_t *d_layers, const uint8_t *d_status, int64_t *h_counts,
+                                      hipStream_t stream)
+{
+    PriceArgs a;
+    int rc = tile_args(p, n, s_max, d_n_stages, d_stages, h_m, n_m, flags, a);
+    if (rc) return rc;
+    if (!h_counts) return fail(HEDDLE_E_INVAL, "h_counts is NULL");
+    if (n > 0 && (!d_layers || !d_status)) return fail(HEDDLE_E_INVAL, "device pointer is NULL");
+    a.layers = const_cast<uint8_t *>(d_layers);
+    a.status = const_cast<uint8_t *>(d_status);
+    unsigned long long *d_work = nullptr;
+    hipError_t e = scratch_alloc((void **)&d_work, 3 * sizeof(unsigned long long), stream);
+    if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "device scratch for the work counters could not be allocated");
+    e = hipMemsetAsync(d_work, 0, 3 * sizeof(unsigned long long), stream);
+    a.work = d_work;
+    rc = e == hipSuccess ? launch_tile(p, a, nullptr, stream) : hip_fail(e, "hipMemsetAsync");
+    unsigned long long h[3] = {0, 0, 0};
+    if (rc == HEDDLE_OK) e = hipMemcpyAsync(h, d_work, sizeof(h), hipMemcpyDeviceToHost, stream);
+    (void)hipFreeAsync(d_work, stream);                        // stream-ordered after the copy
+    if (rc == HEDDLE_OK && e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (rc == HEDDLE_OK && e != hipSuccess) rc = hip_fail(e, "reading the work counters back");
+    if (rc == HEDDLE_OK)
+        for (int i = 0; i < 3; i++) h_counts[i] = (int64_t)h[i];
+    return rc;
 }

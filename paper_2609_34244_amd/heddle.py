@@ -24,6 +24,7 @@ EXPORTS = ["heddle_load_profile", "heddle_free_profile", "heddle_price_plans", "
            "heddle_argmin_plans",
            "heddle_best_plan", "heddle_count_work", "heddle_profile_info_get", "heddle_last_error",
            "heddle_enum_count", "heddle_enum_templates", "heddle_best_enumerated", "heddle_tile_plans",
+           "heddle_count_tile_work",
            "heddle_load_cluster", "heddle_free_cluster", "heddle_fill_dp", "heddle_fill_plans"]
 
 
@@ -82,6 +83,7 @@ def lib():
         L.heddle_count_work.argtypes = [P, I64, I32, P, P, P, I32, U32, C.POINTER(C.c_int64), P]
         L.heddle_profile_info_get.argtypes = [P, C.POINTER(heddle_profile_info)]
         L.heddle_tile_plans.argtypes = [P, I64, I32, P, P, P, I32, U32, P, P, P, P, P, P, P]
+        L.heddle_count_tile_work.argtypes = [P, I64, I32, P, P, P, I32, U32, P, P, C.POINTER(C.c_int64), P]
         L.heddle_load_cluster.argtypes = [C.POINTER(heddle_cluster_desc), C.POINTER(C.c_void_p)]
         L.heddle_free_cluster.argtypes = [P]
         L.heddle_free_cluster.restype = None
@@ -95,7 +97,8 @@ def lib():
         for f in ("heddle_load_profile", "heddle_price_plans", "heddle_price_plans_noalloc", "heddle_argmin_plans",
                   "heddle_best_plan",
                   "heddle_count_work", "heddle_profile_info_get", "heddle_enum_count", "heddle_enum_templates",
-                  "heddle_best_enumerated", "heddle_tile_plans", "heddle_load_cluster", "heddle_fill_dp",
+                  "heddle_best_enumerated", "heddle_tile_plans", "heddle_count_tile_work", "heddle_load_cluster",
+                  "heddle_fill_dp",
                   "heddle_fill_plans"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -233,6 +236,17 @@ def heddle_tile_plans(prof, n_stages, stages, m, flags, out, stream=None):
                                    _ptr(out["iter"]), _ptr(out["bottleneck"]), _ptr(out["peak_mem"]),
                                    _ptr(out["layers"]), _ptr(out["status"]), _ptr(out["tiling"]), _stream(stream)))
     return out
+
+
+def heddle_count_tile_work(prof, n_stages, stages, m, flags, out, stream=None):
+    """(layouts priced, dominance tests, bound tests) of tiling the plans in
+    out (the dict heddle_price_plans filled)."""
+    n, s_max = int(stages.shape[0]), int(stages.shape[1])
+    mm, mp = _mlist(m)
+    h = (C.c_int64 * 3)()
+    _check(lib().heddle_count_tile_work(prof.handle, n, s_max, _ptr(n_stages), _ptr(stages), mp, len(mm), flags,
+                                        _ptr(out["layers"]), _ptr(out["status"]), h, _stream(stream)))
+    return int(h[0]), int(h[1]), int(h[2])
 
 
 def heddle_argmin_plans(m, flags, iter_, status, stream=None):

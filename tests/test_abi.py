@@ -127,6 +127,8 @@ def test_price_calls_reject_null_profile(lib):
     assert lib.heddle_price_plans(None, 0, 4, None, None, m, 1, 0, None, None, None, None, None, None) == H.HEDDLE_E_INVAL
     assert lib.heddle_price_plans_noalloc(None, 0, 4, None, None, m, 1, 0, None, None, None, None, None,
                                           None) == H.HEDDLE_E_INVAL
+    cnt = (C.c_int64 * 3)()
+    assert lib.heddle_count_tile_work(None, 0, 4, None, None, m, 1, 0, None, None, cnt, None) == H.HEDDLE_E_INVAL
     bt, bk = C.c_int64(), C.c_int32()
     assert lib.heddle_best_plan(None, 1, 4, None, None, m, 1, 0, C.byref(bt), C.byref(bk), None, None) == H.HEDDLE_E_INVAL
     w = C.c_int64()

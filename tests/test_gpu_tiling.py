@@ -186,3 +186,68 @@ def test_tile_max_shapes_and_empty(H):
     H.heddle_price_plans(prof, ns, st, [4], 0, out)
     H.heddle_tile_plans(prof, ns, st, [4], 0, out)
     torch.cuda.synchronize()
+
+
+def _tiled_plans(w, g):
+    """(template, m index) of the plans the tile kernel works on: a split and
+    a valid template"""
+    has = ((g["status"] == 0) | (g["status"] == 8)) & (g["layers"][:, :, 0] > 0)
+    return np.argwhere(has)
+
+
+def _allowed_layouts(p, rec):
+    """allowed (EP, ETP) layouts of one stage record: a profiled ETP within the
+    type's node, EP x ETP dividing the stage's TP x DP GPUs (counted here on
+    the host from the profile arrays)"""
+    g, l2tp, dp = int(rec & 0xFF), int((rec >> 8) & 15), int(rec >> 16)
+    W = (1 << l2tp) * dp
+    n = 0
+    for e in p.ep_degrees:
+        for k, t in enumerate(p.tp_degrees):
+            n += bool(p.profiled[g, k]) and t <= p.node_size[g] and W % (int(e) * int(t)) == 0
+    return n
+
+
+@pytest.mark.parametrize("flags", [0, CO])
+def test_tile_work_counts(H, flags):
+    """the counted layouts priced equal a host count of the allowed layouts of
+    the tiled plans; the other two counts lie within their definitions'
+    bounds; on one-layout profiles every count has its closed form"""
+    import torch
+    for seed in range(40):
+        w = random_instance(2900 + seed, moe=seed % 3 != 0, s_max=int([6, 9, 13][seed % 3]), n=41)
+        p = w.profile
+        prof = H.heddle_load_profile(p)
+        ns, st = H.to_device(w.n_stages, w.stages)
+        m = [int(x) for x in w.m]
+        out = H.alloc_outputs(w.n, len(m), w.s_max, flags)
+        H.heddle_price_plans(prof, ns, st, m, flags, out)
+        torch.cuda.synchronize()
+        g = {k: v.cpu().numpy() for k, v in out.items()}
+        priced, dom, bound = H.heddle_count_tile_work(prof, ns, st, m, flags, out)
+        plans = _tiled_plans(w, g)
+        allowed = [[_allowed_layouts(p, w.stages[t, s]) for s in range(w.n_stages[t])] for t, _ in plans]
+        assert priced == sum(sum(a) for a in allowed), f"seed {2900 + seed}"
+        assert dom <= sum(sum(x * x for x in a) for a in allowed)
+        F = len(p.tp_degrees) * len(p.ep_degrees)
+        if F == 1:
+            S = np.array([w.n_stages[t] for t, _ in plans], dtype=np.int64)
+            assert priced == S.sum() and dom <= S.sum() and bound <= int((2 * S * S).sum())
+            # every stage's one layout fits exactly when the plan keeps its status
+            fits = np.array([g["status"][t, k] == 0 for t, k in plans])
+            assert dom == int(S[fits].sum()) and bound == int((2 * S[fits] * S[fits]).sum())
+    # the MoE config subset: bounds only
+    w = sub_workload(make_workload("c4_moe", n=2000), np.arange(1500))
+    prof = H.heddle_load_profile(w.profile)
+    ns, st = H.to_device(w.n_stages, w.stages)
+    m = [int(x) for x in w.m]
+    out = H.alloc_outputs(w.n, len(m), w.s_max, flags)
+    H.heddle_price_plans(prof, ns, st, m, flags, out)
+    priced, dom, bound = H.heddle_count_tile_work(prof, ns, st, m, flags, out)
+    g = {k: v.cpu().numpy() for k, v in out.items()}
+    plans = _tiled_plans(w, g)
+    allowed = [[_allowed_layouts(w.profile, w.stages[t, s]) for s in range(w.n_stages[t])] for t, _ in plans]
+    assert priced == sum(sum(a) for a in allowed)
+    assert 0 < dom <= sum(sum(x * x for x in a) for a in allowed) and bound > 0
+    say("c4 subset tile work", priced, dom, bound, "per tiled plan", priced / len(plans), dom / len(plans),
+        bound / len(plans))

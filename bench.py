@@ -255,6 +255,20 @@ def main():
         torch.cuda.synchronize()
         h2d.append((time.perf_counter() - t0) * 1e3)
     h2d_ms = float(np.median(h2d))
+    # the same copy from page-locked host buffers (a caller that keeps its
+    # templates in pinned memory): DMA only, no staging through pageable pages
+    pin_ns = torch.from_numpy(np.ascontiguousarray(w.n_stages, dtype=np.uint8)).pin_memory()
+    pin_st = torch.from_numpy(np.ascontiguousarray(w.stages, dtype=np.uint32).view(np.int32)).pin_memory()
+    h2d_pin = []
+    for _ in range(3):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ns.copy_(pin_ns, non_blocking=True)
+        st.copy_(pin_st, non_blocking=True)
+        torch.cuda.synchronize()
+        h2d_pin.append((time.perf_counter() - t0) * 1e3)
+    h2d_pin_ms = float(np.median(h2d_pin))
+    del pin_ns, pin_st
     m = [int(x) for x in w.m]
     out = H.alloc_outputs(w.n, len(m), w.s_max, flags)
     torch.cuda.synchronize()
@@ -375,6 +389,8 @@ def main():
         "profile_load_ms": load_ms,
         "template_h2d_ms": h2d_ms,
         "plans_per_s_with_h2d": n_plans / (elapsed / args.steps + h2d_ms / 1e3),
+        "template_h2d_pinned_ms": h2d_pin_ms,
+        "plans_per_s_with_pinned_h2d": n_plans / (elapsed / args.steps + h2d_pin_ms / 1e3),
         "parity": parity,
     }
     if not args.no_cpu_baseline:

@@ -75,7 +75,10 @@ __device__ __forceinline__ void fetch_rows(RowRegs<V, NS> &r, const V *prow, int
 // smallest admissible end keeping an optimal completion at every stage, i.e.
 // the lexicographically smallest optimal split.
 
-template <class V, bool F32, bool COUNT, int NS>
+// GL: the stages' memory-limit rows are read from the profile in global
+// memory (through the caches) instead of being copied into LDS, for shapes
+// whose limit rows would otherwise cap the wavefronts per CU
+template <class V, bool F32, bool COUNT, int NS, bool GL>
 __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevProfile P, PriceArgs A)
 {
     typedef typename Vec2<V>::type V2;
@@ -153,11 +156,11 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
 
                 // ---------------- limit rows of every stage (this class) into LDS:
                 // 16-byte pieces, the rows of `per` stages per load
-                if (mem_aware) {
+                int f_row = min(S - lane, key);
+                f_row = f_row < 1 ? 1 : f_row;
+                const int my_row = x.lrow + (f_row - 1) * 2 * ls;       // lane s: byte offset of stage s's rows
+                if (mem_aware && !GL) {
                     wave_sync();                                        // earlier reads of JX are done
-                    int f = min(S - lane, key);
-                    f = f < 1 ? 1 : f;
-                    const int my_row = x.lrow + (f - 1) * 2 * ls;       // lane s: byte offset of stage s's rows
                     for (int s0 = 0; s0 < S; s0 += per) {
                         const int st = s0 + su;
                         const int row = __shfl(my_row, min(st, 63));
@@ -235,7 +238,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         // taken in increasing order and every end read lies above its row.
                         const V p2p = (V)uni64(x.p2p, s);
                         const int jhi = L - (S - 1 - s);
-                        const uint8_t *Js = jrow(s);
+                        const uint8_t *Js = GL ? P.mem_lim + uni(rl32(my_row, s)) : jrow(s);
                         const int r = b - a + 1;
                         const int lk = r >= 64 ? 0 : 6 - (r > 1 ? 32 - __clz(r - 1) : 0);
                         const int k = 1 << lk;
@@ -335,7 +338,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         const V p2p = (V)uni64(x.p2p, s);
                         const int a_next = s < S - 1 ? uni(rl32(Al, s + 1)) : L;
                         const int jhi = jhi_of(s);
-                        const uint8_t *Js = jrow(s);
+                        const uint8_t *Js = GL ? P.mem_lim + uni(rl32(my_row, s)) : jrow(s);
                         const uint8_t *NXn = xrow(s + 1);
                         uint8_t *NXs = xrow(s);
                         int first_above = kNone;                           // smallest row with F true in higher slots
@@ -460,14 +463,22 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     // arena shares and extends up to the wavefront's share of the CU's LDS at
     // the occupancy the other parts allow
     const size_t j_off = ((size_t)a.g_stride * 2 * sizeof(V) + 15) & ~size_t(15);
-    const size_t x_off = j_off + (size_t)a.s_cap * ls;
-    size_t x_bytes = (size_t)a.s_cap * ls;
+    const size_t rows_lds = (size_t)a.s_cap * ls;            // the limit rows of every stage
     int max_lds = 0, lds_cu = 0;
     HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
     HEDDLE_HIP(hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, p->device));
+    const size_t waves_regs = sizeof(V) == 4 ? 32 : 20;       // wavefronts per CU the registers allow
+    // limit rows from global memory when their LDS copy would hold the CU
+    // below three quarters of the wavefronts the registers allow (long
+    // models with many stages): the reads then go through the caches, and
+    // the occupancy hides their latency
+    const bool mem_aware = (a.flags & HEDDLE_F_COMPUTE_ONLY) == 0;
+    const bool gl = !COUNT && mem_aware && lds_cu > 0 &&
+                    (size_t)lds_cu / (j_off + 2 * rows_lds) * 4 < waves_regs * 3;
+    const size_t x_off = j_off + (gl ? 0 : rows_lds);
+    size_t x_bytes = rows_lds;
     if (!COUNT && lds_cu > 0) {
         const size_t need = x_off + x_bytes;
-        const size_t waves_regs = sizeof(V) == 4 ? 32 : 20;   // wavefronts per CU the registers allow
         size_t waves = (size_t)lds_cu / need;
         waves = waves < waves_regs ? waves : waves_regs;
         if (waves > 0) {
@@ -485,10 +496,12 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     const int wpb = 1;
     const size_t lds = (size_t)wpb * a.lds_per_wave;
     if (lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "DP table of this (L, s_max) does not fit in LDS");
-    if (lds > 65536)
-        HEDDLE_HIP(hipFuncSetAttribute(L + 1 <= 128 ? (const void *)split_kernel<V, F32, COUNT, 2>
-                                                   : (const void *)split_kernel<V, F32, COUNT, 4>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+    // time-prefix slots of 64 entries held in registers: 2 cover L + 1 <= 128
+    const void *kern = L + 1 <= 128 ? (gl ? (const void *)split_kernel<V, F32, COUNT, 2, !COUNT>
+                                          : (const void *)split_kernel<V, F32, COUNT, 2, false>)
+                                    : (gl ? (const void *)split_kernel<V, F32, COUNT, 4, !COUNT>
+                                          : (const void *)split_kernel<V, F32, COUNT, 4, false>);
+    if (lds > 65536) HEDDLE_HIP(hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
     size_t w_lds = 0;
     const int rc = prepare_windows(p, a, max_lds, &w_lds);
     if (rc != HEDDLE_OK) return rc;
@@ -512,12 +525,9 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     const int64_t want = (a.n + wpb - 1) / wpb;
     int blocks = (int)(want < 65536 ? want : 65536);
     if (blocks >= 512) blocks = (blocks + 511) & ~511;        // XCD-aware runs (see the kernel's start)
-    // time-prefix slots of 64 entries held in registers: 2 cover L + 1 <= 128
-    if (L + 1 <= 128)
-        hipLaunchKernelGGL((split_kernel<V, F32, COUNT, 2>), dim3(blocks), dim3(64 * wpb), lds, stream, p->dev, a);
-    else
-        hipLaunchKernelGGL((split_kernel<V, F32, COUNT, 4>), dim3(blocks), dim3(64 * wpb), lds, stream, p->dev, a);
-    HEDDLE_HIP(hipGetLastError());
+    const DevProfile dev = p->dev;
+    void *args[] = {(void *)&dev, (void *)&a};
+    HEDDLE_HIP(hipLaunchKernel(kern, dim3(blocks), dim3(64 * wpb), args, lds, stream));
     return HEDDLE_OK;
 }
 

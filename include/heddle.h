@@ -270,11 +270,12 @@ int heddle_argmin_plans(int64_t n, const int32_t *h_m, int32_t n_m, uint32_t fla
 /*
  * heddle_best_plan -- the whole planning step of one batch: every plan
  * priced (heddle_price_plans, into library-allocated device buffers) and the
- * plan of highest predicted throughput m / iter among those that fit
- * returned (heddle_argmin_plans). This is the selection the planner makes
- * over its priced candidates (section 5 overview: candidates ordered by
- * predicted throughput; section 5.3: among a template's fill choices the
- * fastest fitting one is kept). Synchronous. Arguments as in those two
+ * fitting plan with the largest m / iter, the throughput the cost model
+ * gives it, returned (heddle_argmin_plans). This is the selection the
+ * planner makes over its priced candidates (section 5 overview: candidates
+ * are ordered by the cost model's throughput estimate; section 5.3: of a
+ * template's fill choices the quickest one that fits is retained).
+ * Synchronous. Arguments as in those two
  * calls; the library allocates and frees its own buffers as scratch on
  * `stream`.
  */

@@ -18,8 +18,9 @@
  *      max_s g_s (section 5.3, expert tiling paragraph) and the per-GPU peak
  *      memory (section 5.2),
  * and finally the argmin over all feasible plans of iteration time per
- * micro-batch (plans are ranked by predicted throughput, section 5
- * overview; the fastest candidate is kept, section 5.3).
+ * micro-batch (section 5 overview: candidates are ordered by the cost
+ * model's throughput estimate; section 5.3: the quickest fitting choice is
+ * retained).
  *
  * Expert tiling (oracle_tile_plans): each stage of a priced plan re-chooses
  * its expert layout EP x ETP x EDP among the factorisations of its GPUs that

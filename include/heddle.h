@@ -14,7 +14,7 @@
  *     layer and fitting its GPUs' memory (memory validation, section 5.2);
  *   - Evaluate (section 3.1 backbone; section 5.2 cost model) returns the
  *     1F1B iteration time (M-1) max_s t_s + sum_s t_s + max_s g_s (section
- *     5.3, expert tiling paragraph) and the per-GPU peak memory;
+ *     5.3, expert tiling paragraph) and the peak memory of each GPU;
  *   - the best plan is the one of highest throughput m / iter among the
  *     feasible ones (section 5 overview: candidate plans are ordered by the
  *     throughput the cost model predicts for them).
@@ -374,8 +374,9 @@ int heddle_count_tile_work(const heddle_profile *p, int64_t n, int32_t s_max,
                            int64_t *h_counts, hipStream_t stream);
 
 /*
- * GPU composition as a node list per GPU type (section 5.1, non-uniform
- * composition support): the nodes of a type may differ in size. HOST memory,
+ * The cluster's machines (section 5.1, support for non-uniform GPU
+ * compositions): for every GPU type, the GPU count of each of its nodes;
+ * the nodes of a type may differ in size. HOST memory,
  * read during heddle_load_cluster.
  */
 typedef struct heddle_cluster_desc {
@@ -421,9 +422,9 @@ int heddle_fill_dp(const heddle_cluster *c, int64_t n, int32_t s_max, const uint
  * the profile measured at micro-batch size h_mbs[b] (ascending), and a
  * global batch of `global_batch` samples is m_b = ceil(global_batch /
  * h_mbs[b]) micro-batches. Each template is priced at every size (as
- * heddle_price_plans with m = m_b and `flags`), and the size with the
- * shortest iteration time among those that fit (status OK) is kept, the
- * smaller size on ties; with none OK the smallest size's results are kept.
+ * heddle_price_plans with m = m_b and `flags`); among the sizes whose plan
+ * fits (status OK) the one of smallest iteration time wins, the smaller
+ * size on ties; with none OK the smallest size's results are kept.
  * Outputs as heddle_price_plans with n_m = 1, plus d_dp [n] int32 and
  * d_mbs_index [n] uint8 (index into h_mbs). The library allocates one set
  * of outputs per size on `stream` and frees it before returning.

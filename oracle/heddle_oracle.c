@@ -190,7 +190,7 @@ static int64_t stage_time(const oracle_profile *p, const ostage *st, int s, int 
     return t;
 }
 
-/* Mem(s, i, j): per-GPU peak memory of stage s holding layers [i, j) with
+/* Mem(s, i, j): the peak memory of one GPU of stage s holding layers [i, j) with
  * `inflight` micro-batches of activations resident (memory validation,
  * section 5.2: parameters + optimizer state + gradients + activations). */
 static int64_t stage_mem(const oracle_profile *p, const ostage *st, int i, int j, int64_t inflight)

@@ -21,8 +21,8 @@
 // Micro-batch size: each size has its own profile (profile entries are keyed
 // by GPU type, TP degree and micro-batch size, section 5.2); every template is
 // priced once per size at the micro-batch count that covers the global batch,
-// and a per-template pass keeps the fitting size with the shortest iteration
-// time (the smaller size on ties).
+// and a per-template pass keeps, among the sizes whose plan fits, the one of
+// smallest iteration time (the smaller size on ties).
 #include <cstring>
 #include <vector>
 

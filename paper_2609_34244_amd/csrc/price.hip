@@ -247,7 +247,11 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         do {
                             const int i = base + (lane >> lk);
                             const int ic = min(i, b);
-                            const int lo = max(ic + 1, a_next);
+                            int lo = max(ic + 1, a_next);
+                            // one copy of the row's first end: the compiler otherwise keeps a
+                            // second induction variable for the chunk addresses and derives
+                            // the first end again from it
+                            asm volatile("" : "+v"(lo));
                             const int hi = mem_aware ? min((int)Js[ic], jhi) : jhi;
                             if (COUNT) {
                                 if (part == 0 && i <= b && hi >= lo) work += (unsigned long long)(hi - lo + 1);
@@ -256,8 +260,11 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                             const int hv = i <= b ? hi : 0;                  // no chunk for lanes past b
                             // a relaxation past the row's last end is forced to INF by a mask
                             // taken into its max (ends 1..3 of a row with fewer than four ends)
-                            const V m1 = hi > lo ? V(0) : INF, m2 = hi > lo + 1 ? V(0) : INF;
-                            const V m3 = hi > lo + 2 ? V(0) : INF;
+                            // (as the sign of hi - lo - e spread over the word: all ones, i.e.
+                            // INF, for a missing end e)
+                            const int d = hi - lo;
+                            const V m1 = (V)(int64_t)((d - 1) >> 31), m2 = (V)(int64_t)((d - 2) >> 31);
+                            const V m3 = (V)(int64_t)((d - 3) >> 31);
                             const V pi = X[ic].x - p2p;                      // T(s,i,j) = P_s[j] - pi
                             // chunk starts walk by 4k ends and stop at the row's last chunk start
                             const V2 *cm = X + max(hi - 3, lo);

@@ -196,6 +196,15 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                                     ((uint32_t)(last ? L : An) << 24);
                 const uint32_t prv = (uint32_t)__builtin_amdgcn_update_dpp(
                     0, (int)((uint32_t)x.prow | ((uint32_t)Al << 24)), kDppWaveShr1, 0xF, 0xF, false);
+                // lane s: lk_s | jhi_s << 8, with 2^lk_s the lanes per row at stage s
+                // (64 >> ceil(log2 r) for r window rows, one when r >= 64) and jhi_s the
+                // last end leaving a layer to every later stage
+                uint32_t aux;
+                {
+                    const int r = Bl - Al + 1;
+                    const int lk = r >= 64 ? 0 : 6 - (r > 1 ? 32 - __clz(r - 1) : 0);
+                    aux = (uint32_t)lk | (uint32_t)(L - (S - 1 - lane)) << 8;
+                }
                 RowRegs<V, NS> rr;
                 fetch_rows<V, NS>(rr, rows + uni(rl32(x.prow, S - 1)), uni(rl32(Al, S - 1)), L, lane);
                 V Bv = INF;
@@ -237,10 +246,9 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         // shorter row are masked. G_s[i] replaces G_{s+1}[i] in place: rows are
                         // taken in increasing order and every end read lies above its row.
                         const V p2p = (V)uni64(x.p2p, s);
-                        const int jhi = L - (S - 1 - s);
+                        const uint32_t ax = uni64(aux, s);
+                        const int jhi = (int)(ax >> 8), lk = (int)(ax & 7);
                         const uint8_t *Js = GL ? P.mem_lim + uni(rl32(my_row, s)) : jrow(s);
-                        const int r = b - a + 1;
-                        const int lk = r >= 64 ? 0 : 6 - (r > 1 ? 32 - __clz(r - 1) : 0);
                         const int k = 1 << lk;
                         const int part = lane & (k - 1);
                         int base = a;                                      // windows are not empty
@@ -257,20 +265,24 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                                 if (part == 0 && i <= b && hi >= lo) work += (unsigned long long)(hi - lo + 1);
                                 continue;
                             }
-                            const int hv = i <= b ? hi : 0;                  // no chunk for lanes past b
+                            // lanes past b repeat row b (the same ends, so no longer loop);
+                            // only the lanes of rows up to b store
                             // a relaxation past the row's last end is forced to INF by a mask
-                            // taken into its max (ends 1..3 of a row with fewer than four ends)
-                            // (as the sign of hi - lo - e spread over the word: all ones, i.e.
-                            // INF, for a missing end e)
-                            const int d = hi - lo;
-                            const V m1 = (V)(int64_t)((d - 1) >> 31), m2 = (V)(int64_t)((d - 2) >> 31);
-                            const V m3 = (V)(int64_t)((d - 3) >> 31);
+                            // taken into its max (ends 1..3 of a row with fewer than four ends):
+                            // end e of the chunk is missing when hi - lo < e, and bit t of
+                            // 0b1, 0b11, 0b111 at t = min(hi - lo, 3), spread over the word,
+                            // is all ones (INF) exactly then. A lane with hi < lo has no chunk.
+                            const int t3 = min(hi - lo, 3);
+                            const V m1 = (V)(int64_t)__builtin_amdgcn_sbfe(1, t3, 1);
+                            const V m2 = (V)(int64_t)__builtin_amdgcn_sbfe(3, t3, 1);
+                            const V m3 = (V)(int64_t)__builtin_amdgcn_sbfe(7, t3, 1);
                             const V pi = X[ic].x - p2p;                      // T(s,i,j) = P_s[j] - pi
                             // chunk starts walk by 4k ends and stop at the row's last chunk start
                             const V2 *cm = X + max(hi - 3, lo);
-                            const V2 *ce = X + hv;
+                            const V2 *ce = X + hi;
                             const V2 *cx = X + lo + 4 * part;
                             V acc = INF;
+                            asm volatile("" : "+v"(acc));                    // one definition, not one per path
                             for (; cx <= ce; cx += 4 * k) {
                                 const V2 *c = cx < cm ? cx : cm;
                                 const V2 c0 = c[0], c1 = c[1], c2 = c[2], c3 = c[3];

@@ -272,10 +272,12 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                             // end e of the chunk is missing when hi - lo < e, and bit t of
                             // 0b1, 0b11, 0b111 at t = min(hi - lo, 3), spread over the word,
                             // is all ones (INF) exactly then. A lane with hi < lo has no chunk.
+                            // (the builtin's result type is unsigned: taken as int before it is
+                            // widened, so that the 64-bit DP gets all ones too)
                             const int t3 = min(hi - lo, 3);
-                            const V m1 = (V)(int64_t)__builtin_amdgcn_sbfe(1, t3, 1);
-                            const V m2 = (V)(int64_t)__builtin_amdgcn_sbfe(3, t3, 1);
-                            const V m3 = (V)(int64_t)__builtin_amdgcn_sbfe(7, t3, 1);
+                            const V m1 = (V)(int64_t)(int)__builtin_amdgcn_sbfe(1, t3, 1);
+                            const V m2 = (V)(int64_t)(int)__builtin_amdgcn_sbfe(3, t3, 1);
+                            const V m3 = (V)(int64_t)(int)__builtin_amdgcn_sbfe(7, t3, 1);
                             const V pi = X[ic].x - p2p;                      // T(s,i,j) = P_s[j] - pi
                             // chunk starts walk by 4k ends and stop at the row's last chunk start
                             const V2 *cm = X + max(hi - 3, lo);

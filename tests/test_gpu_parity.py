@@ -269,6 +269,28 @@ def test_wide_values_use_64bit_dp(H):
         run_pair(H, p, ns, st, [1, 7], flags, 40)
 
 
+@pytest.mark.parametrize("flags", [0, CO])
+def test_random_instances_above_2_32(H, flags):
+    """random MoE instances with layer costs scaled past 2^32 ns per stage: the
+    64-bit DP, with rows of fewer than four ends whose missing ends must count
+    as infinite above 32 bits too"""
+    n_plans = n_big = 0
+    for seed in range(40):
+        w = random_instance(6100 + seed, moe=True, s_max=int([6, 9, 13][seed % 3]), n=41)
+        p = w.profile
+        p.layer_ns = np.ascontiguousarray(p.layer_ns << 30)
+        p.xlayer_ns = np.ascontiguousarray(p.xlayer_ns << 30)
+        prof = H.heddle_load_profile(p)
+        assert not H.heddle_profile_info_get(prof)["narrow_i64"]
+        g = gpu_price(H, prof, w, flags)
+        o = oracle_price(w, flags)
+        assert_same(g, o, flags, f"2^32 seed {6100 + seed} flags {flags}")
+        n_plans += g["status"].size
+        n_big += int((o["bottleneck"][o["status"] == 0] >= 1 << 32).sum())
+    say("plans checked", n_plans, "with a bottleneck of 2^32 or more", n_big)
+    assert n_big > 0
+
+
 def test_every_stage_one_layer_and_m_extremes(H):
     p = synthetic_profile(12)
     ns, st = templates([12, 12, 11, 1], 12, dp=3)

@@ -105,6 +105,14 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
     const int h16 = ls >> 4, per = 64 / h16;
     const int su = lane / h16, pc = lane - su * h16;
     unsigned long long work = 0;
+    // without memory limits every stage reads one limit row of 255s (no limit
+    // below the last end of a row), so that a row's last end is always a read
+    // of its stage's limit row, capped
+    if (!mem_aware) {
+        for (int q = lane; 4 * q < ls; q += 64) ((uint32_t *)JX)[q] = ~0u;
+        wave_sync();
+    }
+    const int ls_dp = mem_aware ? ls : 0;                      // the DP's stride between limit rows
 
     // the template records of the next iteration are loaded one iteration ahead
     // Workgroups are handed to the 8 XCDs round robin (workgroup b to XCD
@@ -248,7 +256,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         const V p2p = (V)uni64(x.p2p, s);
                         const uint32_t ax = uni64(aux, s);
                         const int jhi = (int)(ax >> 8), lk = (int)(ax & 7);
-                        const uint8_t *Js = GL ? P.mem_lim + uni(rl32(my_row, s)) : jrow(s);
+                        const uint8_t *Js = GL ? P.mem_lim + uni(rl32(my_row, s)) : JX + s * ls_dp;
                         const int k = 1 << lk;
                         const int part = lane & (k - 1);
                         int base = a;                                      // windows are not empty
@@ -260,7 +268,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                             // second induction variable for the chunk addresses and derives
                             // the first end again from it
                             asm volatile("" : "+v"(lo));
-                            const int hi = mem_aware ? min((int)Js[ic], jhi) : jhi;
+                            const int hi = min((int)Js[ic], jhi);
                             if (COUNT) {
                                 if (part == 0 && i <= b && hi >= lo) work += (unsigned long long)(hi - lo + 1);
                                 continue;

@@ -8,9 +8,10 @@ namespace heddle {
 
 // Validation in status order (section 5.1 feasibility masks, section 5.2
 // exact profile match), one lane over its own stages; cnt is the lane's
-// column of per-type GPU counters (all zero on entry and on exit).
+// column of per-type GPU counters (all zero on entry and on exit), cs words
+// apart.
 __device__ __forceinline__ int validate_lane(const DevProfile &P, const PriceArgs &A, int S, const uint32_t *rec,
-                                             uint32_t *cnt)
+                                             uint32_t *cnt, int cs = 64)
 {
     if (S < 1 || S > A.s_max || S > P.L) return HEDDLE_S_BAD_SHAPE;
     const int N = P.n_types;
@@ -33,13 +34,13 @@ __device__ __forceinline__ int validate_lane(const DevProfile &P, const PriceArg
     if (b_dp) return HEDDLE_S_BAD_DP;
     if (b_ep) return HEDDLE_S_BAD_EP;
     // GPUs of each type: sum of TP over the stages of that type, times D
-    for (int s = 0; s < S; s++) cnt[(rec[s] & 0xFF) * 64] += 1u << ((rec[s] >> 8) & 15);
+    for (int s = 0; s < S; s++) cnt[(rec[s] & 0xFF) * cs] += 1u << ((rec[s] >> 8) & 15);
     bool over = false;
     for (int s = 0; s < S; s++) {
         const int g = rec[s] & 0xFF;
-        over |= (int64_t)cnt[g * 64] * D > P.n_gpus[g];
+        over |= (int64_t)cnt[g * cs] * D > P.n_gpus[g];
     }
-    for (int s = 0; s < S; s++) cnt[(rec[s] & 0xFF) * 64] = 0;
+    for (int s = 0; s < S; s++) cnt[(rec[s] & 0xFF) * cs] = 0;
     return over ? HEDDLE_S_OVERSUBSCRIBED : HEDDLE_S_OK;
 }
 

@@ -13,47 +13,70 @@
 // inverse-limit table lookup); W_s = [Bk_s, min(R_s, L - (S - s))] (row 0 only
 // for s = 0). A plan with an empty window has no split that fits memory.
 //
-// Mapping: one lane per template, 64 templates per wavefront. The
-// wavefront's template records are staged in LDS with coalesced loads
-// (row stride s_max + 1 words, so that the lanes' column reads do not share
-// banks); each lane validates its template (per-type GPU counters in an LDS
-// column of its own), then chases its own limit rows in global memory (the
-// forward and backward chases are independent and taken in one loop),
+// Mapping: one lane per template, 256 templates per workgroup (128 or 64
+// when the staged records of 256 would not fit the workgroup's LDS). The
+// workgroup's template records are staged in LDS with coalesced loads (row
+// stride s_max + 1 words, so that the lanes' column reads do not share
+// banks) and its templates are ranked by stage count (a counting sort in LDS,
+// most stages first), so that each wavefront takes 64 templates of nearly the
+// same length and its per-stage loops do not run for the longest template of
+// an unsorted 64. Each lane validates its template (per-type GPU counters in
+// an LDS column of its own), then chases its own limit rows in global memory
+// (the forward and backward chases are independent and taken in one loop),
 // keeping R_s and Bk_s in the two upper bytes of its staged record s (the DP
 // degree they held is read before), and writes its windows four at a time.
 #include "validate.h"
 
 namespace heddle {
 
-__global__ void __launch_bounds__(64, 8) window_kernel(DevProfile P, PriceArgs A)
+constexpr int kWinTpl = 256;                                   // most templates (and lanes) per workgroup
+
+__global__ void __launch_bounds__(kWinTpl) window_kernel(DevProfile P, PriceArgs A)
 {
-    extern __shared__ __align__(16) unsigned char smem[];      // one wavefront per workgroup
-    const int lane = threadIdx.x;
+    extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ uint32_t bins[64];                              // templates per stage-count bin, then bin offsets
+    __shared__ uint16_t order[kWinTpl];                        // local template indices, most stages first
+    const int tid = threadIdx.x;
+    const int nw = blockDim.x;                                 // templates per workgroup: 64, 128 or 256
     const int rs = A.s_max + 1;                                // staged record stride, words
-    uint32_t *cnt = (uint32_t *)smem + lane;                   // [n_types][64] GPU counters of validation
-    uint32_t *recs = (uint32_t *)smem + (size_t)P.n_types * 64;   // [64][rs] the wavefront's records
+    uint32_t *cnt = (uint32_t *)smem + tid;                    // [n_types][nw] GPU counters of validation
+    uint32_t *recs = (uint32_t *)smem + (size_t)P.n_types * nw;   // [nw][rs] the workgroup's records
     const int L = P.L, ls = P.lim_stride;
     const int ws = win_stride(A.s_max);
     const bool mem_aware = (A.flags & HEDDLE_F_COMPUTE_ONLY) == 0;
-    for (int g = 0; g < P.n_types; g++) cnt[g * 64] = 0;
+    for (int g = 0; g < P.n_types; g++) cnt[g * nw] = 0;
 
-    for (int64_t t0 = (int64_t)blockIdx.x * 64; t0 < A.n; t0 += (int64_t)gridDim.x * 64) {
-        // ---------------- the records of templates t0 .. t0 + 63 into LDS
-        const int nt = A.n - t0 < 64 ? (int)(A.n - t0) : 64;
+    for (int64_t t0 = (int64_t)blockIdx.x * nw; t0 < A.n; t0 += (int64_t)gridDim.x * nw) {
+        // ---------------- the records of templates t0 .. t0 + nw - 1 into LDS, and
+        // their ranking by stage count (bin 63 - min(S, 63))
+        const int nt = A.n - t0 < nw ? (int)(A.n - t0) : nw;
         const uint32_t *src = A.stages + t0 * A.s_max;
-        wave_sync();                                           // earlier reads of recs are done
-        for (int i = lane; i < nt * A.s_max; i += 64) {
+        __syncthreads();                                       // earlier reads of recs and order are done
+        if (tid < 64) bins[tid] = 0;
+        for (int i = tid; i < nt * A.s_max; i += nw) {
             const int j = i / A.s_max;
             recs[j * rs + (i - j * A.s_max)] = src[i];
         }
-        wave_sync();
-        if (lane >= nt) continue;
-        const int64_t t = t0 + lane;
+        const int S_own = tid < nt ? (int)A.n_stages[t0 + tid] : 0;
+        __syncthreads();
+        const int bin = 63 - (S_own < 63 ? S_own : 63);
+        const uint32_t rank = tid < nt ? atomicAdd(&bins[bin], 1u) : 0u;
+        __syncthreads();
+        if (tid < 64) {
+            const int c = (int)bins[tid];
+            bins[tid] = (uint32_t)(wave_inclusive_sum(c) - c);
+        }
+        __syncthreads();
+        if (tid < nt) order[bins[bin] + rank] = (uint16_t)tid;
+        __syncthreads();
+        if (tid >= nt) continue;
+        const int me = order[tid];                             // the template this lane takes
+        const int64_t t = t0 + me;
         const int S = A.n_stages[t];
-        const uint32_t *rec = recs + lane * rs;
-        uint8_t *rk = (uint8_t *)(recs + lane * rs);           // byte 4s + 2: R_s, byte 4s + 3: Bk_s
+        const uint32_t *rec = recs + me * rs;
+        uint8_t *rk = (uint8_t *)(recs + me * rs);             // byte 4s + 2: R_s, byte 4s + 3: Bk_s
         const size_t obase = (size_t)t * A.n_m;
-        const int status = validate_lane(P, A, S, rec, cnt);
+        const int status = validate_lane(P, A, S, rec, cnt, nw);
         if (status != HEDDLE_S_OK) {
             for (int k = 0; k < A.n_m; k++) A.wst[obase + k] = (uint32_t)status;
             continue;
@@ -118,9 +141,23 @@ __global__ void __launch_bounds__(64, 8) window_kernel(DevProfile P, PriceArgs A
     }
 }
 
+// templates per workgroup: the most (256, 128 or 64) whose staged records and
+// counters fit 63 KB of LDS beside the ranking's own 768 bytes and that still
+// give every CU four workgroups of the batch (a small batch in large
+// workgroups leaves CUs idle)
+static int window_tile(const heddle_profile *p, const PriceArgs &a)
+{
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device) != hipSuccess || cus < 1) cus = 1;
+    int nw = kWinTpl;
+    while (nw > 64 && ((size_t)nw * (p->dev.n_types + a.s_max + 1) * 4 > 63 * 1024 || a.n < (int64_t)nw * 4 * cus))
+        nw >>= 1;
+    return nw;
+}
+
 int prepare_windows(const heddle_profile *p, const PriceArgs &a, int max_lds, size_t *lds)
 {
-    *lds = (size_t)p->dev.n_types * 256 + (size_t)64 * (a.s_max + 1) * 4;
+    *lds = (size_t)window_tile(p, a) * (p->dev.n_types + a.s_max + 1) * 4;
     if (*lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "per-lane tables of this profile do not fit in LDS");
     if (*lds > 65536)
         HEDDLE_HIP(hipFuncSetAttribute((const void *)window_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)*lds));
@@ -130,9 +167,10 @@ int prepare_windows(const heddle_profile *p, const PriceArgs &a, int max_lds, si
 int launch_windows(const heddle_profile *p, const PriceArgs &a, size_t lds, hipStream_t stream)
 {
     if (a.n == 0) return HEDDLE_OK;
-    const int64_t want = (a.n + 63) / 64;
+    const int wg = window_tile(p, a);
+    const int64_t want = (a.n + wg - 1) / wg;
     const int blocks = (int)(want < 65536 ? want : 65536);
-    hipLaunchKernelGGL(window_kernel, dim3(blocks), dim3(64), lds, stream, p->dev, a);
+    hipLaunchKernelGGL(window_kernel, dim3(blocks), dim3(wg), lds, stream, p->dev, a);
     HEDDLE_HIP(hipGetLastError());
     return HEDDLE_OK;
 }

@@ -15,10 +15,12 @@
 // fitting leaves the plan OOM without a split. With HEDDLE_F_COMPUTE_ONLY the
 // proportional split is kept and only flagged.
 //
-// Mapping: one lane per template (grid-stride over templates, one wavefront
-// per workgroup); each lane validates its template, computes the cuts and
-// walks its stages on its own, so the 64 lanes of a wavefront price 64
-// templates side by side. Per lane, LDS holds the stage starts c_0..c_S
+// Mapping: one lane per template, 256 templates per workgroup (128 or 64
+// for small batches or large tables; grid-stride over such tiles). The
+// tile's templates are ranked by stage count (a counting sort in LDS, most
+// stages first) so that each wavefront takes 64 templates of nearly the same
+// length; each lane then validates its template, computes the cuts and walks
+// its stages on its own. Per lane, LDS holds the stage starts c_0..c_S
 // (bytes) and one GPU counter per type for the oversubscription check; both
 // are laid out [index][lane], so every LDS access of a wavefront hits 64
 // distinct banks. For the fallback list, the first pass keeps the three
@@ -65,25 +67,48 @@ __device__ __forceinline__ int stage_prow(const DevProfile &P, uint32_t r)
 
 // COUNT: only count the stage-cost evaluations into A.work (S for the
 // proportional split, 2 per alternative priced)
+constexpr int kDistTpl = 256;                                  // most templates (and lanes) per workgroup
+
 template <bool F32, bool COUNT>
-__global__ void __launch_bounds__(64, 3) distribute_kernel(DevProfile P, PriceArgs A)
+__global__ void __launch_bounds__(kDistTpl, 3) distribute_kernel(DevProfile P, PriceArgs A)
 {
-    extern __shared__ __align__(16) unsigned char smem[];      // one wavefront per workgroup
-    const int lane = threadIdx.x;
-    uint32_t *cnt = (uint32_t *)smem + lane;                   // [n_types][64]: this lane's column
-    uint8_t *cut = smem + (size_t)P.n_types * 256 + lane;      // [s_cap + 1][64]: stage starts c_0..c_S
-    auto C = [&](int s) -> int { return cut[s * 64]; };
+    extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ uint32_t bins[64];                              // templates per stage-count bin, then bin offsets
+    __shared__ uint16_t order[kDistTpl];                       // local template indices, most stages first
+    const int tid = threadIdx.x;
+    const int nw = blockDim.x;                                 // templates per workgroup: 64, 128 or 256
+    uint32_t *cnt = (uint32_t *)smem + tid;                    // [n_types][nw]: this lane's column
+    uint8_t *cut = smem + (size_t)P.n_types * nw * 4 + tid;    // [s_cap + 1][nw]: stage starts c_0..c_S
+    auto C = [&](int s) -> int { return cut[s * nw]; };
     const int L = P.L;
     const bool compute_only = (A.flags & HEDDLE_F_COMPUTE_ONLY) != 0;
     const bool word_layers = (A.s_max & 3) == 0 && ((uintptr_t)A.layers & 3) == 0;
     unsigned long long work = 0;
-    for (int g = 0; g < P.n_types; g++) cnt[g * 64] = 0;
+    for (int g = 0; g < P.n_types; g++) cnt[g * nw] = 0;
 
-    for (int64_t t = (int64_t)blockIdx.x * 64 + lane; t < A.n; t += (int64_t)gridDim.x * 64) {
+    for (int64_t t0 = (int64_t)blockIdx.x * nw; t0 < A.n; t0 += (int64_t)gridDim.x * nw) {
+        // ---- rank the tile's templates by stage count (bin 63 - min(S, 63))
+        const int nt = A.n - t0 < nw ? (int)(A.n - t0) : nw;
+        __syncthreads();                                       // earlier reads of order are done
+        if (tid < 64) bins[tid] = 0;
+        const int S_own = tid < nt ? (int)A.n_stages[t0 + tid] : 0;
+        __syncthreads();
+        const int bin = 63 - (S_own < 63 ? S_own : 63);
+        const uint32_t rank = tid < nt ? atomicAdd(&bins[bin], 1u) : 0u;
+        __syncthreads();
+        if (tid < 64) {
+            const int c = (int)bins[tid];
+            bins[tid] = (uint32_t)(wave_inclusive_sum(c) - c);
+        }
+        __syncthreads();
+        if (tid < nt) order[bins[bin] + rank] = (uint16_t)tid;
+        __syncthreads();
+        if (tid >= nt) continue;
+        const int64_t t = t0 + order[tid];                     // the template this lane takes
         const int S = A.n_stages[t];
         const uint32_t *rec = A.stages + t * A.s_max;
         const size_t obase = (size_t)t * A.n_m;
-        const int status = validate_lane(P, A, S, rec, cnt);
+        const int status = validate_lane(P, A, S, rec, cnt, nw);
         if (status != HEDDLE_S_OK) {
             if (COUNT) continue;
             for (int k = 0; k < A.n_m; k++) {
@@ -119,10 +144,10 @@ __global__ void __launch_bounds__(64, 3) distribute_kernel(DevProfile P, PriceAr
                 int c = (int)floor((double)L * below / total + 0.5);
                 c = c < prev + 1 ? prev + 1 : c;
                 c = c > L - (S - s) ? L - (S - s) : c;
-                cut[s * 64] = (uint8_t)c;
+                cut[s * nw] = (uint8_t)c;
                 prev = c;
             }
-            cut[S * 64] = (uint8_t)L;
+            cut[S * nw] = (uint8_t)L;
         }
 
         for (int k = 0; k < A.n_m; k++) {
@@ -221,7 +246,7 @@ __global__ void __launch_bounds__(64, 3) distribute_kernel(DevProfile P, PriceAr
     if (COUNT) {
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) work += __shfl_xor(work, off);
-        if (lane == 0 && work) atomicAdd(A.work, work);
+        if ((tid & 63) == 0 && work) atomicAdd(A.work, work);
     }
 }
 
@@ -229,23 +254,30 @@ int launch_distribute(const heddle_profile *p, PriceArgs &a, hipStream_t stream,
 {
     if (a.n == 0) return HEDDLE_OK;
     const int s_cap = a.s_max < p->dev.L ? a.s_max : p->dev.L;
-    const size_t lds = (size_t)p->dev.n_types * 256 + (size_t)(s_cap + 1) * 64;
-    int max_lds = 0;
+    // templates per workgroup: the most (256, 128 or 64) whose per-lane tables
+    // fit 63 KB of LDS beside the ranking's own 768 bytes and that still give
+    // every CU four workgroups of the batch
+    int max_lds = 0, cus = 0;
     HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
+    HEDDLE_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device));
+    const size_t per_lane = (size_t)p->dev.n_types * 4 + (size_t)(s_cap + 1);
+    int nw = kDistTpl;
+    while (nw > 64 && (per_lane * nw > 63 * 1024 || a.n < (int64_t)nw * 4 * (cus > 0 ? cus : 1))) nw >>= 1;
+    const size_t lds = per_lane * nw;
     if (lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "per-lane tables of this profile do not fit in LDS");
-    const int64_t want = (a.n + 63) / 64;
+    const int64_t want = (a.n + nw - 1) / nw;
     const int blocks = (int)(want < 65536 ? want : 65536);
     const bool f32 = a.flags & HEDDLE_F_FP32;
     const void *fn = count_only ? (f32 ? (const void *)distribute_kernel<true, true> : (const void *)distribute_kernel<false, true>)
                                 : (f32 ? (const void *)distribute_kernel<true, false> : (const void *)distribute_kernel<false, false>);
     if (lds > 65536) HEDDLE_HIP(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
     if (count_only) {
-        if (f32) hipLaunchKernelGGL((distribute_kernel<true, true>), dim3(blocks), dim3(64), lds, stream, p->dev, a);
-        else hipLaunchKernelGGL((distribute_kernel<false, true>), dim3(blocks), dim3(64), lds, stream, p->dev, a);
+        if (f32) hipLaunchKernelGGL((distribute_kernel<true, true>), dim3(blocks), dim3(nw), lds, stream, p->dev, a);
+        else hipLaunchKernelGGL((distribute_kernel<false, true>), dim3(blocks), dim3(nw), lds, stream, p->dev, a);
     } else if (f32) {
-        hipLaunchKernelGGL((distribute_kernel<true, false>), dim3(blocks), dim3(64), lds, stream, p->dev, a);
+        hipLaunchKernelGGL((distribute_kernel<true, false>), dim3(blocks), dim3(nw), lds, stream, p->dev, a);
     } else {
-        hipLaunchKernelGGL((distribute_kernel<false, false>), dim3(blocks), dim3(64), lds, stream, p->dev, a);
+        hipLaunchKernelGGL((distribute_kernel<false, false>), dim3(blocks), dim3(nw), lds, stream, p->dev, a);
     }
     HEDDLE_HIP(hipGetLastError());
     return HEDDLE_OK;

@@ -251,6 +251,31 @@ def test_max_sizes(H):
     assert H.heddle_profile_info_get(prof)["narrow_i64"]
 
 
+def test_large_batch_with_64_stage_slots(H):
+    """140,000 templates with up to 64 stages: a batch large enough that the
+    window pass and Distribute rank it in workgroups of 128 templates (256
+    would not fit their LDS with 64 stage slots); a seeded sample of 1,500
+    templates compared with the oracle in both partition modes"""
+    from workloads.gen import Workload
+    rng = np.random.default_rng(77)
+    n, s_max, L = 140_000, 64, 70
+    p = synthetic_profile(L, caps=1500, seed=3)
+    S = rng.integers(1, s_max + 1, size=n)
+    g = rng.integers(0, 2, size=(n, s_max))
+    tp = rng.integers(0, 2, size=(n, s_max))
+    st = np.where(np.arange(s_max)[None, :] < S[:, None], pack_stage(g, tp, 0, 1), 0).astype(np.uint32)
+    w = Workload(name="slots64", profile=p, n_stages=S.astype(np.uint8), stages=np.ascontiguousarray(st),
+                 m=np.array([1, 16], np.int32), s_max=s_max)
+    prof = H.heddle_load_profile(p)
+    idx = np.sort(rng.choice(n, size=1500, replace=False))
+    for flags in (0, DI):
+        gfull = gpu_price(H, prof, w, flags)
+        g = {k: v[idx] for k, v in gfull.items()}
+        o = oracle_price(sub_workload(w, idx), flags)
+        assert_same(g, o, flags, f"64-slot batch flags {flags}")
+        say("64-slot batch flags", flags, "statuses", np.bincount(gfull["status"].ravel(), minlength=9).tolist())
+
+
 def test_memory_binding_max_sizes(H):
     p = synthetic_profile(200, caps=2500, moe=True)
     ns, st = templates([1, 5, 20, 64, 50, 33], 64, dp=2, ep=True)

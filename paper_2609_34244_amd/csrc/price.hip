@@ -152,10 +152,15 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
         V r_b = INF;
 
         if (todo) {
-            const int S = uni(S_in);
-            const StageInfo<V> x = stage_info<V, F32>(P, A, S, rec_in, lane);
+            const int S_t = uni(S_in);
+            const StageInfo<V> x = stage_info<V, F32>(P, A, S_t, rec_in, lane);
 
             while (todo) {
+                // an opaque copy of the stage count per class: tests on it are formed
+                // where they are used, not hoisted out of this loop and kept in scalar
+                // registers across the DP
+                int S = S_t;
+                asm volatile("" : "+s"(S));
                 const int key = A.n_m == 1 ? uni(key_k)
                                            : uni((int)group_min<uint32_t>(((todo >> lane) & 1) ? (uint32_t)key_k : 0x7FFFFFFFu, 64));
                 const uint64_t cls = ballot(lane < A.n_m && key_k == key) & todo;

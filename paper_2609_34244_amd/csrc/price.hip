@@ -148,6 +148,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
         const uint32_t wv = lane < A.n_m ? A.wst[obase + lane] : (uint32_t)HEDDLE_S_OOM;
         const int pst = (int)(wv & 255), key_k = (int)((wv >> 8) & 255);
         uint64_t todo = ballot(lane < A.n_m && pst == HEDDLE_S_OK);
+        if (!todo) continue;                                   // the window pass wrote this template's outputs
         bool r_split = false;                                  // lane k: a split was found for m index k
         V r_b = INF;
 

@@ -76,9 +76,30 @@ __global__ void __launch_bounds__(kWinTpl) window_kernel(DevProfile P, PriceArgs
         const uint32_t *rec = recs + me * rs;
         uint8_t *rk = (uint8_t *)(recs + me * rs);             // byte 4s + 2: R_s, byte 4s + 3: Bk_s
         const size_t obase = (size_t)t * A.n_m;
+        // the final outputs of a template none of whose plans has windows (it
+        // failed validation, or no split fits memory): status, no bottleneck and
+        // no layers; the split kernel skips such templates. Not written when the
+        // call only counts work (no outputs are given then).
+        auto close_template = [&](uint32_t code) {
+            if (!A.status) return;
+            const bool f32 = (A.flags & HEDDLE_F_FP32) != 0;
+            const bool words = (A.s_max & 3) == 0 && ((uintptr_t)A.layers & 3) == 0;
+            for (int k = 0; k < A.n_m; k++) {
+                const size_t o = obase + k;
+                A.status[o] = (uint8_t)code;
+                if (f32) ((float *)A.bottleneck)[o] = __builtin_inff();
+                else ((int64_t *)A.bottleneck)[o] = INT64_MAX;
+                if (words) {
+                    for (int w = 0; w < A.s_max; w += 4) *(uint32_t *)&A.layers[o * A.s_max + w] = 0u;
+                } else {
+                    for (int w = 0; w < A.s_max; w++) A.layers[o * A.s_max + w] = 0;
+                }
+            }
+        };
         const int status = validate_lane(P, A, S, rec, cnt, nw);
         if (status != HEDDLE_S_OK) {
             for (int k = 0; k < A.n_m; k++) A.wst[obase + k] = (uint32_t)status;
+            close_template((uint32_t)status);
             continue;
         }
         const uint32_t D = rec[0] >> 16;
@@ -86,6 +107,7 @@ __global__ void __launch_bounds__(kWinTpl) window_kernel(DevProfile P, PriceArgs
             const int Mp = (int)(((uint32_t)A.m[k] + D - 1) / D);
             return mem_aware ? (Mp < S ? Mp : S) : 0;
         };
+        bool any_ok = false;                                   // a plan of the template has windows
         for (int k = 0; k < A.n_m; k++) {
             const size_t o = obase + k;
             uint2 *wout = (uint2 *)(A.wwin + o * ws);
@@ -97,7 +119,7 @@ __global__ void __launch_bounds__(kWinTpl) window_kernel(DevProfile P, PriceArgs
                 const uint2 *win0 = (const uint2 *)(A.wwin + o0 * ws);
                 A.wst[o] = A.wst[o0];
                 for (int s = 0; s < S; s += 4) wout[s >> 2] = win0[s >> 2];
-                continue;
+                continue;                                      // any_ok already holds plan k0's outcome
             }
             if (mem_aware) {
                 int c = 0, nxt = L;                            // R_s, Bk_{u+1}
@@ -137,7 +159,9 @@ __global__ void __launch_bounds__(kWinTpl) window_kernel(DevProfile P, PriceArgs
                 wout[s0 >> 2] = make_uint2(w[0] | w[1] << 16, w[2] | w[3] << 16);
             }
             A.wst[o] = fits ? (uint32_t)HEDDLE_S_OK | (uint32_t)key << 8 | rows << 16 : (uint32_t)HEDDLE_S_OOM;
+            any_ok = any_ok || fits;
         }
+        if (!any_ok) close_template((uint32_t)HEDDLE_S_OOM);
     }
 }
 

@@ -21,9 +21,10 @@
 // Mapping. One wavefront splits one template at a time (grid-stride over
 // templates); templates whose plans all failed validation or have an empty
 // window cost one status read. Lanes are stages while the per-stage table
-// offsets are formed. The memory-limit rows of all stages are copied into
-// LDS, and the DP relaxes only the rows of each stage's window (rows that can
-// lie on a complete split, see the split kernel). Lanes are split rows
+// offsets are formed. A row's last admissible end is read from its stage's
+// memory-limit row in the profile (through the caches; one byte per row),
+// and the DP relaxes only the rows of each stage's window (rows that can lie
+// on a complete split, see the split kernel). Lanes are split rows
 // during the DP: r rows of a window take 64 >> ceil(log2 r) lanes each, which
 // share the row's ends and combine with a cross-lane minimum. Per wavefront,
 // one LDS pair row holds X[j] = {P_s[j], G[s+1][j]}, so one 64-bit read feeds
@@ -75,10 +76,9 @@ __device__ __forceinline__ void fetch_rows(RowRegs<V, NS> &r, const V *prow, int
 // smallest admissible end keeping an optimal completion at every stage, i.e.
 // the lexicographically smallest optimal split.
 
-// GL: the stages' memory-limit rows are read from the profile in global
-// memory (through the caches) instead of being copied into LDS, for shapes
-// whose limit rows would otherwise cap the wavefronts per CU
-template <class V, bool F32, bool COUNT, int NS, bool GL>
+// MA: memory-aware (the flags do not ask to ignore memory); a compile-time
+// choice, so that the hot loops carry no test of the mode
+template <class V, bool F32, bool COUNT, int NS, bool MA>
 __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevProfile P, PriceArgs A)
 {
     typedef typename Vec2<V>::type V2;
@@ -86,33 +86,27 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
     extern __shared__ __align__(16) unsigned char smem[];      // one wavefront per workgroup
     const int lane = threadIdx.x;
     const int L = P.L, ls = P.lim_stride;
-    const bool mem_aware = (A.flags & HEDDLE_F_COMPUTE_ONLY) == 0;
+    constexpr bool mem_aware = MA;
     const V INF = DPInf<V>::value;
     V2 *X = (V2 *)smem;                                        // [gs] pair row {P_s[j], G_{s+1}[j]}
-    // [s_cap][ls] limit rows; [s_cap][ls] next-row tables of the second
-    // backward pass, a region that, with what follows it up to the end of the
-    // wavefront's LDS, holds the G arena instead when the template's windows
-    // fit it
+    // [ls] a limit row of 255s (no memory limit); [s_cap][ls] next-row tables
+    // of the second backward pass, a region that, with what follows it up to
+    // the end of the wavefront's LDS, holds the G arena instead when the
+    // template's windows fit it
     uint8_t *JX = smem + A.off_j;
     uint8_t *IX = smem + A.off_x;
     V *GA = (V *)IX;
     const V *rows = stage_rows<V>(P, F32);
-    auto jrow = [&](int s) -> uint8_t * { return JX + s * ls; };
     auto xrow = [&](int s) -> uint8_t * { return IX + s * ls; };
 
-    // limit-row copy: the limit row of a stage is h16 pieces of 16 bytes; lane
-    // (su, pc) copies piece pc of stage s0 + su
-    const int h16 = ls >> 4, per = 64 / h16;
-    const int su = lane / h16, pc = lane - su * h16;
     unsigned long long work = 0;
-    // without memory limits every stage reads one limit row of 255s (no limit
+    // without memory limits every stage reads the limit row of 255s (no limit
     // below the last end of a row), so that a row's last end is always a read
-    // of its stage's limit row, capped
+    // of a limit row, capped
     if (!mem_aware) {
         for (int q = lane; 4 * q < ls; q += 64) ((uint32_t *)JX)[q] = ~0u;
         wave_sync();
     }
-    const int ls_dp = mem_aware ? ls : 0;                      // the DP's stride between limit rows
 
     // the template records of the next iteration are loaded one iteration ahead
     // Workgroups are handed to the 8 XCDs round robin (workgroup b to XCD
@@ -168,22 +162,11 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                 todo &= ~cls;
                 auto jhi_of = [&](int s) { return L - (S - 1 - s); };   // last end leaving a layer per later stage
 
-                // ---------------- limit rows of every stage (this class) into LDS:
-                // 16-byte pieces, the rows of `per` stages per load
+                // lane s: offset of stage s's memory-limit row for this class (in-flight
+                // count min(S - s, class key), at least one)
                 int f_row = min(S - lane, key);
                 f_row = f_row < 1 ? 1 : f_row;
-                const int my_row = x.lrow + (f_row - 1) * 2 * ls;       // lane s: byte offset of stage s's rows
-                if (mem_aware && !GL) {
-                    wave_sync();                                        // earlier reads of JX are done
-                    for (int s0 = 0; s0 < S; s0 += per) {
-                        const int st = s0 + su;
-                        const int row = __shfl(my_row, min(st, 63));
-                        if (su < per && st < S) {
-                            *(uint4 *)(JX + st * ls + pc * 16) = *(const uint4 *)(P.mem_lim + row + pc * 16);
-                        }
-                    }
-                    wave_sync();
-                }
+                const int my_row = x.lrow + (f_row - 1) * 2 * ls;
 
                 // ---------------- row windows (from the window pass): lane s holds [a_s, b_s]
                 int Al, Bl, g_total;
@@ -262,7 +245,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         const V p2p = (V)uni64(x.p2p, s);
                         const uint32_t ax = uni64(aux, s);
                         const int jhi = (int)(ax >> 8), lk = (int)(ax & 7);
-                        const uint8_t *Js = GL ? P.mem_lim + uni(rl32(my_row, s)) : JX + s * ls_dp;
+                        const uint8_t *Js = mem_aware ? P.mem_lim + uni(rl32(my_row, s)) : JX;
                         const int k = 1 << lk;
                         const int part = lane & (k - 1);
                         int base = a;                                      // windows are not empty
@@ -373,7 +356,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         const V p2p = (V)uni64(x.p2p, s);
                         const int a_next = s < S - 1 ? uni(rl32(Al, s + 1)) : L;
                         const int jhi = jhi_of(s);
-                        const uint8_t *Js = GL ? P.mem_lim + uni(rl32(my_row, s)) : jrow(s);
+                        const uint8_t *Js = mem_aware ? P.mem_lim + uni(rl32(my_row, s)) : JX;
                         const uint8_t *NXn = xrow(s + 1);
                         uint8_t *NXs = xrow(s);
                         int first_above = kNone;                           // smallest row with F true in higher slots
@@ -493,24 +476,19 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     const int L = p->dev.L, ls = p->dev.lim_stride;
     a.s_cap = a.s_max < L ? a.s_max : L;
     a.g_stride = L + 5;                                       // L + 1 ends and 4 of padding
-    // per wavefront: one pair row {P_s, G_{s+1}}; per stage its limit row; per
-    // stage its next-row table (second backward pass), a region that the G
-    // arena shares and extends up to the wavefront's share of the CU's LDS at
-    // the occupancy the other parts allow
+    // per wavefront: one pair row {P_s, G_{s+1}}; one limit row of 255s (read
+    // in place of the stages' limit rows when memory is ignored; with memory
+    // limits a row's last end is read from the profile's limit rows through
+    // the caches); per stage its next-row table (second backward pass), a
+    // region that the G arena shares and extends up to the wavefront's share
+    // of the CU's LDS at the occupancy the registers allow
     const size_t j_off = ((size_t)a.g_stride * 2 * sizeof(V) + 15) & ~size_t(15);
-    const size_t rows_lds = (size_t)a.s_cap * ls;            // the limit rows of every stage
+    const size_t rows_lds = (size_t)a.s_cap * ls;            // the next-row tables of every stage
     int max_lds = 0, lds_cu = 0;
     HEDDLE_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device));
     HEDDLE_HIP(hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, p->device));
     const size_t waves_regs = sizeof(V) == 4 ? 32 : 20;       // wavefronts per CU the registers allow
-    // limit rows from global memory when their LDS copy would hold the CU
-    // below three quarters of the wavefronts the registers allow (long
-    // models with many stages): the reads then go through the caches, and
-    // the occupancy hides their latency
-    const bool mem_aware = (a.flags & HEDDLE_F_COMPUTE_ONLY) == 0;
-    const bool gl = !COUNT && mem_aware && lds_cu > 0 &&
-                    (size_t)lds_cu / (j_off + 2 * rows_lds) * 4 < waves_regs * 3;
-    const size_t x_off = j_off + (gl ? 0 : rows_lds);
+    const size_t x_off = j_off + (size_t)ls;
     size_t x_bytes = rows_lds;
     if (!COUNT && lds_cu > 0) {
         const size_t need = x_off + x_bytes;
@@ -532,9 +510,10 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     const size_t lds = (size_t)wpb * a.lds_per_wave;
     if (lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "DP table of this (L, s_max) does not fit in LDS");
     // time-prefix slots of 64 entries held in registers: 2 cover L + 1 <= 128
-    const void *kern = L + 1 <= 128 ? (gl ? (const void *)split_kernel<V, F32, COUNT, 2, !COUNT>
+    const bool ma = (a.flags & HEDDLE_F_COMPUTE_ONLY) == 0;
+    const void *kern = L + 1 <= 128 ? (ma ? (const void *)split_kernel<V, F32, COUNT, 2, true>
                                           : (const void *)split_kernel<V, F32, COUNT, 2, false>)
-                                    : (gl ? (const void *)split_kernel<V, F32, COUNT, 4, !COUNT>
+                                    : (ma ? (const void *)split_kernel<V, F32, COUNT, 4, true>
                                           : (const void *)split_kernel<V, F32, COUNT, 4, false>);
     if (lds > 65536) HEDDLE_HIP(hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
     size_t w_lds = 0;

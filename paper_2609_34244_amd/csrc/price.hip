@@ -76,9 +76,10 @@ __device__ __forceinline__ void fetch_rows(RowRegs<V, NS> &r, const V *prow, int
 // smallest admissible end keeping an optimal completion at every stage, i.e.
 // the lexicographically smallest optimal split.
 
-// MA: memory-aware (the flags do not ask to ignore memory); a compile-time
-// choice, so that the hot loops carry no test of the mode
-template <class V, bool F32, bool COUNT, int NS, bool MA>
+// MA: memory-aware (the flags do not ask to ignore memory); M1: one
+// micro-batch count per template. Compile-time choices, so that the hot
+// loops carry no test of them.
+template <class V, bool F32, bool COUNT, int NS, bool MA, bool M1>
 __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevProfile P, PriceArgs A)
 {
     typedef typename Vec2<V>::type V2;
@@ -87,6 +88,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
     const int lane = threadIdx.x;
     const int L = P.L, ls = P.lim_stride;
     constexpr bool mem_aware = MA;
+    const int n_m = M1 ? 1 : A.n_m;                            // plans per template
     const V INF = DPInf<V>::value;
     V2 *X = (V2 *)smem;                                        // [gs] pair row {P_s[j], G_{s+1}[j]}
     // [ls] a limit row of 255s (no memory limit); [s_cap][ls] next-row tables
@@ -134,14 +136,14 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
             S_next = A.n_stages[t + stride];
             rec_next = lane < A.s_max ? A.stages[(t + stride) * A.s_max + lane] : 0u;
         }
-        const size_t obase = (size_t)t * A.n_m;
+        const size_t obase = (size_t)t * n_m;
         // lane k: status of plan k after validation and windows (0: windows found),
         // its in-flight class min(M_p, S) (0 when memory is ignored), which fixes
         // the split (M_p = ceil(m / D) micro-batches per replica), and the rows of
         // its windows W_1 .. W_{S-1}
-        const uint32_t wv = lane < A.n_m ? A.wst[obase + lane] : (uint32_t)HEDDLE_S_OOM;
+        const uint32_t wv = lane < n_m ? A.wst[obase + lane] : (uint32_t)HEDDLE_S_OOM;
         const int pst = (int)(wv & 255), key_k = (int)((wv >> 8) & 255);
-        uint64_t todo = ballot(lane < A.n_m && pst == HEDDLE_S_OK);
+        uint64_t todo = ballot(lane < n_m && pst == HEDDLE_S_OK);
         if (!todo) continue;                                   // the window pass wrote this template's outputs
         bool r_split = false;                                  // lane k: a split was found for m index k
         V r_b = INF;
@@ -156,9 +158,9 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                 // registers across the DP
                 int S = S_t;
                 asm volatile("" : "+s"(S));
-                const int key = A.n_m == 1 ? uni(key_k)
+                const int key = n_m == 1 ? uni(key_k)
                                            : uni((int)group_min<uint32_t>(((todo >> lane) & 1) ? (uint32_t)key_k : 0x7FFFFFFFu, 64));
-                const uint64_t cls = ballot(lane < A.n_m && key_k == key) & todo;
+                const uint64_t cls = M1 ? todo : ballot(lane < n_m && key_k == key) & todo;
                 todo &= ~cls;
                 auto jhi_of = [&](int s) { return L - (S - 1 - s); };   // last end leaving a layer per later stage
 
@@ -395,7 +397,10 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                     }
                 }
                 // lane s: c_s (c_0 = 0)
-                const int my_start = __builtin_amdgcn_update_dpp(0, my_end, kDppWaveShr1, 0xF, 0xF, false);
+                int my_start = __builtin_amdgcn_update_dpp(0, my_end, kDppWaveShr1, 0xF, 0xF, false);
+                // kept a value of its own: folded into the subtraction below as one
+                // DPP subtract-reverse, the shift gave negated layer counts on gfx950
+                asm volatile("" : "+v"(my_start));
                 const uint8_t my_layers = lane < S ? (uint8_t)(my_end - my_start) : 0;
                 for (uint64_t c = cls; c; c &= c - 1) {            // s_max <= 64: a lane per stage
                     const int k = __ffsll((unsigned long long)c) - 1;
@@ -408,14 +413,14 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
             }
         }
         if (COUNT) continue;
-        if (lane < A.n_m) {
+        if (lane < n_m) {
             const size_t o = obase + lane;
             A.status[o] = (uint8_t)(pst != HEDDLE_S_OK ? pst : (r_split ? HEDDLE_S_OK : HEDDLE_S_OOM));
             if (F32) ((float *)A.bottleneck)[o] = r_split ? exact_float(rne24((uint64_t)r_b), P.fx_exp) : __builtin_inff();
             else ((int64_t *)A.bottleneck)[o] = r_split ? (int64_t)r_b : INT64_MAX;
         }
         // zero layer counts of the plans without a split (invalid template, or no split fits)
-        const uint64_t without = ballot(lane < A.n_m && !r_split);
+        const uint64_t without = ballot(lane < n_m && !r_split);
         for (uint64_t c = without; c; c &= c - 1) {
             const int k = __ffsll((unsigned long long)c) - 1;
             if (lane < A.s_max) A.layers[(obase + k) * A.s_max + lane] = 0;
@@ -511,10 +516,17 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     if (lds > (size_t)max_lds) return fail(HEDDLE_E_RANGE, "DP table of this (L, s_max) does not fit in LDS");
     // time-prefix slots of 64 entries held in registers: 2 cover L + 1 <= 128
     const bool ma = (a.flags & HEDDLE_F_COMPUTE_ONLY) == 0;
-    const void *kern = L + 1 <= 128 ? (ma ? (const void *)split_kernel<V, F32, COUNT, 2, true>
-                                          : (const void *)split_kernel<V, F32, COUNT, 2, false>)
-                                    : (ma ? (const void *)split_kernel<V, F32, COUNT, 4, true>
-                                          : (const void *)split_kernel<V, F32, COUNT, 4, false>);
+    const void *kern;
+    if (a.n_m == 1)
+        kern = L + 1 <= 128 ? (ma ? (const void *)split_kernel<V, F32, COUNT, 2, true, true>
+                                  : (const void *)split_kernel<V, F32, COUNT, 2, false, true>)
+                            : (ma ? (const void *)split_kernel<V, F32, COUNT, 4, true, true>
+                                  : (const void *)split_kernel<V, F32, COUNT, 4, false, true>);
+    else
+        kern = L + 1 <= 128 ? (ma ? (const void *)split_kernel<V, F32, COUNT, 2, true, false>
+                                  : (const void *)split_kernel<V, F32, COUNT, 2, false, false>)
+                            : (ma ? (const void *)split_kernel<V, F32, COUNT, 4, true, false>
+                                  : (const void *)split_kernel<V, F32, COUNT, 4, false, false>);
     if (lds > 65536) HEDDLE_HIP(hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
     size_t w_lds = 0;
     const int rc = prepare_windows(p, a, max_lds, &w_lds);

@@ -247,7 +247,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         const V p2p = (V)uni64(x.p2p, s);
                         const uint32_t ax = uni64(aux, s);
                         const int jhi = (int)(ax >> 8), lk = (int)(ax & 7);
-                        const uint8_t *Js = mem_aware ? P.mem_lim + uni(rl32(my_row, s)) : JX;
+                        const uint8_t *Js = mem_aware ? P.mem_lim + (uint32_t)uni(rl32(my_row, s)) : JX;
                         const int k = 1 << lk;
                         const int part = lane & (k - 1);
                         int base = a;                                      // windows are not empty
@@ -290,7 +290,11 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                                 acc = vmin(vmin(acc, relax<V>(c0, pi)), vmax(relax<V>(c1, pi), m1));
                                 acc = vmin(vmin(acc, vmax(relax<V>(c2, pi), m2)), vmax(relax<V>(c3, pi), m3));
                             }
-                            if (s == 0) {
+                            // the stage index re-read opaquely: the test is made here, not held
+                            // as a lane mask built once per stage
+                            int s_here = s;
+                            asm volatile("" : "+s"(s_here));
+                            if (s_here == 0) {
                                 Bv = (V)rl64((int64_t)group_min<V>(acc, 64), 0);   // row 0 only
                             } else {
                                 // an opaque copy of k keeps the level tests of the minimum at

@@ -44,12 +44,14 @@ template <class V, int NS> struct RowRegs {
     V p[NS];
 };
 
+// (row: the row's offset in the table, in entries; it joins the lanes' index
+// rather than the table's base, so the base stays one scalar pair)
 template <class V, int NS>
-__device__ __forceinline__ void fetch_rows(RowRegs<V, NS> &r, const V *prow, int a, int e, int lane)
+__device__ __forceinline__ void fetch_rows(RowRegs<V, NS> &r, const V *rows, uint32_t row, int a, int e, int lane)
 {
 #pragma unroll
     for (int q = 0; q < NS; q++)
-        if (q == 0 || 64 * q <= e - a) r.p[q] = prow[(uint32_t)min(a + lane + 64 * q, e)];   // uniform; e >= a
+        if (q == 0 || 64 * q <= e - a) r.p[q] = rows[row + (uint32_t)min(a + lane + 64 * q, e)];   // uniform; e >= a
 }
 
 // ------------------------------------------------------------ split kernel
@@ -205,7 +207,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                     aux = (uint32_t)lk | (uint32_t)(L - (S - 1 - lane)) << 8;
                 }
                 RowRegs<V, NS> rr;
-                fetch_rows<V, NS>(rr, rows + uni(rl32(x.prow, S - 1)), uni(rl32(Al, S - 1)), L, lane);
+                fetch_rows<V, NS>(rr, rows, (uint32_t)uni(rl32(x.prow, S - 1)), uni(rl32(Al, S - 1)), L, lane);
                 V Bv = INF;
                 int goff = 0;                                          // arena index of G_s[a_s]
                 for (int s = S - 1; s >= 0; s--) {
@@ -217,7 +219,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         if (q == 0 || 64 * q <= e - a) ((V *)&X[min(a + lane + 64 * q, e)])[0] = rr.p[q];
                     if (s > 0) {
                         const uint32_t kp = uni64(prv, s);
-                        fetch_rows<V, NS>(rr, rows + (kp & 0xFFFFFFu), (int)(kp >> 24), b, lane);
+                        fetch_rows<V, NS>(rr, rows, kp & 0xFFFFFFu, (int)(kp >> 24), b, lane);
                     }
                     wave_sync();
                     if (s == S - 1) {
@@ -228,7 +230,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                             const V pL = X[L].x;
                             for (int i = a + lane; i <= b; i += 64) {
                                 const V gv = (V)(pL - X[i].x);
-                                if (s > 0) {
+                                if (S > 1) {                           // s = S - 1 > 0
                                     ((V *)&X[i])[1] = gv;
                                     if (arena) GA[goff + i - a] = gv;
                                 } else {
@@ -247,7 +249,10 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         const V p2p = (V)uni64(x.p2p, s);
                         const uint32_t ax = uni64(aux, s);
                         const int jhi = (int)(ax >> 8), lk = (int)(ax & 7);
-                        const uint8_t *Js = mem_aware ? P.mem_lim + (uint32_t)uni(rl32(my_row, s)) : JX;
+                        // a row's last admissible end: byte jrow + ic of the limit table (the
+                        // row's offset joins the lanes' index, the table's base stays fixed)
+                        const uint8_t *Jb = mem_aware ? P.mem_lim : JX;
+                        const uint32_t jrow = mem_aware ? (uint32_t)uni(rl32(my_row, s)) : 0u;
                         const int k = 1 << lk;
                         const int part = lane & (k - 1);
                         int base = a;                                      // windows are not empty
@@ -259,7 +264,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                             // second induction variable for the chunk addresses and derives
                             // the first end again from it
                             asm volatile("" : "+v"(lo));
-                            const int hi = min((int)Js[ic], jhi);
+                            const int hi = min((int)Jb[jrow + (uint32_t)ic], jhi);
                             if (COUNT) {
                                 if (part == 0 && i <= b && hi >= lo) work += (unsigned long long)(hi - lo + 1);
                                 continue;

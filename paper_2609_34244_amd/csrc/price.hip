@@ -200,19 +200,25 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                 // lane s: lk_s | jhi_s << 8, with 2^lk_s the lanes per row at stage s
                 // (64 >> ceil(log2 r) for r window rows, one when r >= 64) and jhi_s the
                 // last end leaving a layer to every later stage
+                // and (bits 16..31) 256 + the arena index of G_s[a_s] minus a_s: the
+                // arena holds the windows of stages S-1 .. 1 in that order, so stage
+                // s's starts after those of stages s+1 .. S-1
                 uint32_t aux;
                 {
                     const int r = Bl - Al + 1;
                     const int lk = r >= 64 ? 0 : 6 - (r > 1 ? 32 - __clz(r - 1) : 0);
-                    aux = (uint32_t)lk | (uint32_t)(L - (S - 1 - lane)) << 8;
+                    const int before = wave_inclusive_sum(lane >= 1 && lane < S ? r : 0);   // windows of stages 1..s
+                    aux = (uint32_t)lk | (uint32_t)(L - (S - 1 - lane)) << 8 |
+                          (uint32_t)(g_total - before - Al + 256) << 16;
                 }
                 RowRegs<V, NS> rr;
                 fetch_rows<V, NS>(rr, rows, (uint32_t)uni(rl32(x.prow, S - 1)), uni(rl32(Al, S - 1)), L, lane);
                 V Bv = INF;
-                int goff = 0;                                          // arena index of G_s[a_s]
                 for (int s = S - 1; s >= 0; s--) {
                     const uint32_t ks = uni64(pk, s);
                     const int a = ks & 255, b = (ks >> 8) & 255, e = (ks >> 16) & 255, a_next = ks >> 24;
+                    const uint32_t ax = uni64(aux, s);
+                    const int gba = (int)(ax >> 16) - 256;             // G_s[i] at arena index gba + i
                     // P_s into the pair row over [a, e]; G_{s+1} stays in place
 #pragma unroll
                     for (int q = 0; q < NS; q++)
@@ -232,7 +238,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                                 const V gv = (V)(pL - X[i].x);
                                 if (S > 1) {                           // s = S - 1 > 0
                                     ((V *)&X[i])[1] = gv;
-                                    if (arena) GA[goff + i - a] = gv;
+                                    if (arena) GA[gba + i] = gv;
                                 } else {
                                     Bv = gv;                           // S = 1: row 0, lane 0
                                 }
@@ -247,8 +253,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         // shorter row are masked. G_s[i] replaces G_{s+1}[i] in place: rows are
                         // taken in increasing order and every end read lies above its row.
                         const V p2p = (V)uni64(x.p2p, s);
-                        const uint32_t ax = uni64(aux, s);
-                        const int jhi = (int)(ax >> 8), lk = (int)(ax & 7);
+                        const int jhi = (int)((ax >> 8) & 255), lk = (int)(ax & 7);
                         // a row's last admissible end: byte jrow + ic of the limit table (the
                         // row's offset joins the lanes' index, the table's base stays fixed)
                         const uint8_t *Jb = mem_aware ? P.mem_lim : JX;
@@ -310,12 +315,11 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                                 acc = group_min<V>(acc, kr);
                                 if (i <= b && part == 0) {
                                     ((V *)&X[i])[1] = acc;
-                                    if (arena) GA[goff + i - a] = acc;
+                                    if (arena) GA[gba + i] = acc;
                                 }
                             }
                         } while ((base += 64 >> lk) <= b);
                     }
-                    goff += b - a + 1;
                     wave_sync();
                 }
                 if (COUNT) continue;

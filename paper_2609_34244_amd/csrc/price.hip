@@ -342,24 +342,27 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                         rem -= w1 + 1;
                         const int lo = max(cs + 1, a1) - a1;           // lowest admissible row, from a1
                         // the window in words of 64 rows, from the word holding lo (a later
-                        // word only when the window is longer than 64 rows)
+                        // word only when the window is longer than 64 rows). Bits past the
+                        // window's last row repeat that row's bit (the read is clamped to it),
+                        // and a set bit at or after lo and at or before the last row always
+                        // exists: G_s[c_s] is within B*, so is G_{s+1} at the end minimising
+                        // it, an admissible row of W_{s+1} at or after lo (rounding to fp32 is
+                        // monotone, so this holds for the fp32 test too). The first set bit
+                        // is therefore the row sought, with no test of the window's end.
                         auto word = [&](int w0) -> uint64_t {
-                            const int r = w0 + lane;
-                            const V g = GA[rem + min(r, w1)];
-                            return ballot(r <= w1) &
-                                   ballot(F32 ? g != INF && within((uint64_t)g) : (uint64_t)g <= B);
+                            const V g = GA[rem + min(w0 + lane, w1)];
+                            return ballot(F32 ? g != INF && within((uint64_t)g) : (uint64_t)g <= B);
                         };
                         int w0 = lo & ~63;
                         uint64_t mk = word(w0) & (~0ull << (lo - w0));   // rows from lo
-                        if (!mk) {
+                        if (!mk) {                                     // a window longer than 64 rows
                             while (w0 + 64 <= w1) {
                                 w0 += 64;
                                 mk = word(w0);
                                 if (mk) break;
                             }
                         }
-                        const int nx = mk ? a1 + w0 + __ffsll((unsigned long long)mk) - 1 : L;   // L: unreachable
-                        cs = nx;
+                        cs = a1 + w0 + __builtin_ctzll(mk);           // mk is not zero (see above)
                         my_end = lane == s ? cs : my_end;
                     }
                 } else {

@@ -294,11 +294,21 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                             const V2 *cx = X + lo + 4 * part;
                             V acc = INF;
                             asm volatile("" : "+v"(acc));                    // one definition, not one per path
-                            for (; cx <= ce; cx += 4 * k) {
-                                const V2 *c = cx < cm ? cx : cm;
-                                const V2 c0 = c[0], c1 = c[1], c2 = c[2], c3 = c[3];
-                                acc = vmin(vmin(acc, relax<V>(c0, pi)), vmax(relax<V>(c1, pi), m1));
-                                acc = vmin(vmin(acc, vmax(relax<V>(c2, pi), m2)), vmax(relax<V>(c3, pi), m3));
+                            if (lo <= hi) {
+                                // the chunk loop runs while any lane of the group has a chunk
+                                // left; a lane past its own chunks relaxes the row's last chunk
+                                // again, which leaves its minimum as it is
+                                bool more;
+                                do {
+                                    const V2 *c = cx < cm ? cx : cm;
+                                    const V2 c0 = c[0], c1 = c[1], c2 = c[2], c3 = c[3];
+                                    acc = vmin(vmin(acc, relax<V>(c0, pi)), vmax(relax<V>(c1, pi), m1));
+                                    acc = vmin(vmin(acc, vmax(relax<V>(c2, pi), m2)), vmax(relax<V>(c3, pi), m3));
+                                    cx += 4 * k;
+                                    // the stage time grows with the end: once the chunk's last end
+                                    // alone reaches the lane's minimum, no later end can lower it
+                                    more = cx <= ce && (V)(c3.x - pi) < acc;
+                                } while (ballot(more));
                             }
                             // the stage index re-read opaquely: the test is made here, not held
                             // as a lane mask built once per stage
@@ -313,9 +323,9 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                                 int kr = k;
                                 asm volatile("" : "+s"(kr));
                                 acc = group_min<V>(acc, kr);
-                                if (i <= b && part == 0) {
-                                    ((V *)&X[i])[1] = acc;
-                                    if (arena) GA[gba + i] = acc;
+                                if (i <= b && part == 0) {             // then ic = i
+                                    ((V *)&X[ic])[1] = acc;
+                                    if (arena) GA[gba + ic] = acc;
                                 }
                             }
                         } while ((base += 64 >> lk) <= b);

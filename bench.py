@@ -272,10 +272,13 @@ def main():
     m = [int(x) for x in w.m]
     out = H.alloc_outputs(w.n, len(m), w.s_max, flags)
     torch.cuda.synchronize()
-    relax = H.heddle_count_work(prof, ns, st, m, flags)
+    # work: the pairs the split kernel relaxes (its exit rule skips part of the
+    # window pairs); the window count is kept as context
+    relax_win = H.heddle_count_work(prof, ns, st, m, flags)
+    relax = relax_win if args.distribute else H.heddle_count_work(prof, ns, st, m, flags | H.HEDDLE_F_COUNT_EVALUATED)
     n_plans = w.n * len(m)
-    log(f"profile loaded in {load_ms:.1f} ms; work per step {relax:,} x {unit_name} ({relax / w.n:.0f} per template); "
-        f"32-bit DP: {info['narrow_f32' if args.fp32 else 'narrow_i64']}")
+    log(f"profile loaded in {load_ms:.1f} ms; work per step {relax:,} x {unit_name} ({relax / w.n:.0f} per template; "
+        f"{relax_win:,} over the windows); 32-bit DP: {info['narrow_f32' if args.fp32 else 'narrow_i64']}")
 
     stream = torch.cuda.current_stream()
 
@@ -351,7 +354,13 @@ def main():
                               "mean_iter_ratio": float(np.mean(it_d[both] / it_r[both])) if both.any() else None}
     else:
         roof = {"kernel": "window_kernel + split_kernel + evaluate_kernel (one heddle_price_plans call)",
-                "work_per_launch": relax, "work_unit": unit_name, "ops_per_unit": k_unit,
+                "work_per_launch": relax, "work_unit": unit_name + " (pairs the split kernel relaxes)",
+                "ops_per_unit": k_unit,
+                "context_window": {
+                    "per_launch": relax_win,
+                    "note": "pairs of the recurrence over the row windows; the row loop's exit rule leaves "
+                            "per_launch - work_per_launch of them unrelaxed, so this is context, not an achieved rate",
+                    "equivalent_frac": relax_win * K_MIN / kern_s / PEAK_LANE_OPS},
                 "context_dense_R": {
                     "per_launch": dense_r,
                     "note": "relaxations of the unpruned suffix recurrence over the plans whose split was computed; "
@@ -514,7 +523,7 @@ def run_enumerate(args, H, flags, k_unit, unit_name):
     relax, chunk = 0, 1 << 22
     for first in range(0, total, chunk):
         ns, st = H.heddle_enum_templates(spec, first, min(chunk, total - first))
-        relax += H.heddle_count_work(prof, ns, st, m, flags)
+        relax += H.heddle_count_work(prof, ns, st, m, flags if args.distribute else flags | H.HEDDLE_F_COUNT_EVALUATED)
     del ns, st
     torch.cuda.synchronize()
     log(f"space: {total:,} templates x {len(m)} m (types {types}, log2 TP {tps}, S <= {args.enum_depth}); "
@@ -552,7 +561,8 @@ def run_enumerate(args, H, flags, k_unit, unit_name):
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12, "unit": "Tlane-op/s",
                      "frac": achieved / PEAK_LANE_OPS, "traffic": None,
                      "kernel": "whole pass (generator, split, evaluate and argmin kernels, per-chunk host syncs)",
-                     "kernel_ms": step_s * 1e3, "work_per_launch": relax, "work_unit": unit_name,
+                     "kernel_ms": step_s * 1e3, "work_per_launch": relax,
+                     "work_unit": unit_name if args.distribute else unit_name + " (pairs the split kernel relaxes)",
                      "ops_per_unit": k_unit},
         "best_plan": {"template": best[0], "m_index": best[1], "iter": best[2], "ok_plans": best[3]},
     }

@@ -63,6 +63,7 @@ extern "C" {
 #define HEDDLE_F_FP32         1u  /* fp32 time quantities (iter, bottleneck outputs are float) */
 #define HEDDLE_F_COMPUTE_ONLY 2u  /* split ignores memory; the fit is checked afterwards       */
 #define HEDDLE_F_DISTRIBUTE   4u  /* speed-proportional split with a fallback list (section 5.3) */
+#define HEDDLE_F_COUNT_EVALUATED 8u  /* heddle_count_work only: count what the kernel evaluates */
 
 /* ---- per-plan status codes (data, not errors); the first failing check wins ---- */
 #define HEDDLE_S_OK             0  /* priced and fits                                         */
@@ -299,10 +300,21 @@ int heddle_best_plan(const heddle_profile *p, int64_t n, int32_t s_max,
  * counts one. A template with an empty range at some stage has no split
  * that fits memory and counts zero. Synchronous.
  *   h_relaxations  HOST result.
+ * With HEDDLE_F_COUNT_EVALUATED the count is of the pairs the split kernel
+ * actually relaxes, which is at most the count above: it runs the recurrence
+ * and a row's ends are taken in chunks of four by 64 >> ceil(log2 r) lanes
+ * for r window rows (one lane when r >= 64), lane p taking chunks p, p + k,
+ * ... from the first end; a lane stops after a chunk whose last end has a
+ * stage time at or above the lane's running minimum (later ends cannot
+ * lower it). Each chunk counts the ends it adds (a last chunk moved back to
+ * end at the row's last end counts those from its own start); a last-stage
+ * row counts one. The values follow the flags' arithmetic (HEDDLE_F_FP32:
+ * the fp32 image), so the count is exact, not a model.
  * With HEDDLE_F_DISTRIBUTE the unit is one stage-cost evaluation (time,
  * memory and gradient synchronisation of one stage): S for the proportional
  * split and, when it does not fit, 2 per alternative priced (only the two
- * stages around the moved cut change).
+ * stages around the moved cut change); HEDDLE_F_COUNT_EVALUATED changes
+ * nothing there.
  * Returns HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_NOMEM or HEDDLE_E_DEVICE.
  */
 int heddle_count_work(const heddle_profile *p, int64_t n, int32_t s_max,

@@ -270,7 +270,7 @@ extern "C" int heddle_best_plan(const heddle_profile *p, int64_t n, int32_t s_ma
     a.peak_mem = (int64_t *)(buf + o_pk);
     a.status = buf + o_st;
     a.layers = buf + o_ly;
-    rc = launch_price(p, a, stream, false);
+    rc = launch_price(p, a, stream, 0);
     if (rc == HEDDLE_OK)
         rc = launch_argmin(n, h_m, n_m, flags, a.iter, a.status, h_best_template, h_best_m_index, h_best_iter,
                            stream);

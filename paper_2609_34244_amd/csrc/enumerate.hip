@@ -240,7 +240,7 @@ extern "C" int heddle_best_enumerated(const heddle_profile *p, const heddle_enum
         a.peak_mem = (int64_t *)(buf + o_pk);
         a.status = buf + o_ss;
         a.layers = buf + o_ly;
-        rc = launch_price(p, a, stream, false);
+        rc = launch_price(p, a, stream, 0);
         if (rc) break;
         if (h_n_ok) {
             const int64_t want = ((int64_t)n * n_m + 255) / 256;

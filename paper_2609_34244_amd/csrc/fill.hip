@@ -308,7 +308,7 @@ extern "C" int heddle_fill_plans(const heddle_profile *const *profiles, const in
         a.peak_mem = (int64_t *)(base + o_pk);
         a.status = base + o_st;
         a.layers = base + o_ly;
-        rc = launch_price(profiles[b], a, stream, false);
+        rc = launch_price(profiles[b], a, stream, 0);
         sa.iter[b] = a.iter;
         sa.bottleneck[b] = a.bottleneck;
         sa.peak_mem[b] = a.peak_mem;

@@ -163,7 +163,9 @@ struct PriceArgs {
 
 int validate_price_args(const heddle_profile *p, int64_t n, int32_t s_max, const uint8_t *d_n_stages,
                         const uint32_t *d_stages, const int32_t *h_m, int32_t n_m, uint32_t flags);
-int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool count_only);
+// count: 0 prices; 1 counts the relaxations over the windows; 2 counts those the
+// split kernel evaluates (it runs the DP); 1 and 2 write no plan outputs
+int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, int count);
 int launch_evaluate(const heddle_profile *p, const PriceArgs &a, hipStream_t stream);
 // window pass outputs: row stride of a plan's windows, in entries (a
 // multiple of 4, so that rows are stored 8 bytes at a time)

@@ -81,7 +81,9 @@ __device__ __forceinline__ void fetch_rows(RowRegs<V, NS> &r, const V *rows, uin
 // MA: memory-aware (the flags do not ask to ignore memory); M1: one
 // micro-batch count per template. Compile-time choices, so that the hot
 // loops carry no test of them.
-template <class V, bool F32, bool COUNT, int NS, bool MA, bool M1>
+// COUNT: 0 prices; 1 counts the relaxations over the windows (no DP); 2 runs the DP
+// and counts the (row, end) pairs it relaxes under the row loop's exit rule
+template <class V, bool F32, int COUNT, int NS, bool MA, bool M1>
 __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevProfile P, PriceArgs A)
 {
     typedef typename Vec2<V>::type V2;
@@ -183,7 +185,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                 }
                 // G arena: G_s over the rows of W_s for s = S-1 .. 1, stored in that order,
                 // when all of them fit; else the second backward pass rebuilds F
-                const bool arena = !COUNT && g_total <= A.arena_cap;
+                const bool arena = COUNT == 0 && g_total <= A.arena_cap;
 
                 // ---------------- PartitionLayers: suffix min-max DP over the windows, stages S-1 .. 0
                 // Per-stage constants packed into lanes, one readlane per stage each:
@@ -230,9 +232,8 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                     wave_sync();
                     if (s == S - 1) {
                         // last stage: every window row ends at L
-                        if (COUNT) {
-                            if (lane == 0) work += (unsigned long long)(b - a + 1);
-                        } else {
+                        if (COUNT != 0 && lane == 0) work += (unsigned long long)(b - a + 1);
+                        if (COUNT != 1) {
                             const V pL = X[L].x;
                             for (int i = a + lane; i <= b; i += 64) {
                                 const V gv = (V)(pL - X[i].x);
@@ -270,7 +271,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                             // the first end again from it
                             asm volatile("" : "+v"(lo));
                             const int hi = min((int)Jb[jrow + (uint32_t)ic], jhi);
-                            if (COUNT) {
+                            if (COUNT == 1) {
                                 if (part == 0 && i <= b && hi >= lo) work += (unsigned long long)(hi - lo + 1);
                                 continue;
                             }
@@ -298,8 +299,11 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                                 // the chunk loop runs while any lane of the group has a chunk
                                 // left; a lane past its own chunks relaxes the row's last chunk
                                 // again, which leaves its minimum as it is
-                                bool more;
+                                bool more, own = cx <= ce;         // own: the lane's chunk is its own
                                 do {
+                                    // the ends the chunk adds: four, or those from its start to the
+                                    // row's last end when it was moved back (rows past b repeat b)
+                                    if (COUNT == 2 && own && i <= b) work += (unsigned long long)min(4, (int)(ce - cx) + 1);
                                     const V2 *c = cx < cm ? cx : cm;
                                     const V2 c0 = c[0], c1 = c[1], c2 = c[2], c3 = c[3];
                                     acc = vmin(vmin(acc, relax<V>(c0, pi)), vmax(relax<V>(c1, pi), m1));
@@ -308,6 +312,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                                     // the stage time grows with the end: once the chunk's last end
                                     // alone reaches the lane's minimum, no later end can lower it
                                     more = cx <= ce && (V)(c3.x - pi) < acc;
+                                    own = more;
                                 } while (ballot(more));
                             }
                             // the stage index re-read opaquely: the test is made here, not held
@@ -501,7 +506,7 @@ static size_t window_scratch_bytes(int64_t n, int32_t n_m, int32_t s_max)
     return ((plans * sizeof(uint32_t) + 255) & ~size_t(255)) + plans * win_stride(s_max) * sizeof(uint16_t);
 }
 
-template <class V, bool F32, bool COUNT>
+template <class V, bool F32, int COUNT>
 static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t stream)
 {
     const int L = p->dev.L, ls = p->dev.lim_stride;
@@ -583,12 +588,12 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     return HEDDLE_OK;
 }
 
-int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool count_only)
+int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, int count)
 {
     if (a.n == 0) return HEDDLE_OK;
     const bool f32 = a.flags & HEDDLE_F_FP32;
     const bool narrow = f32 ? p->narrow_f32 : p->narrow_i64;
-    if (a.flags & HEDDLE_F_DISTRIBUTE) return launch_distribute(p, a, stream, count_only);
+    if (a.flags & HEDDLE_F_DISTRIBUTE) return launch_distribute(p, a, stream, count != 0);
     // validation and windows of every plan (window_kernel), then the split
     // kernel over the plans with windows, then Evaluate
     // the profile's buffer of the stream is taken under its lock; a fixed
@@ -599,10 +604,11 @@ int launch_price(const heddle_profile *p, PriceArgs &a, hipStream_t stream, bool
     a.wwin = nullptr;
     a.scratch_owned = false;
     int rc;
-    if (count_only) rc = launch_split<uint64_t, false, true>(p, a, stream);
-    else if (f32) rc = narrow ? launch_split<uint32_t, true, false>(p, a, stream) : launch_split<uint64_t, true, false>(p, a, stream);
-    else rc = narrow ? launch_split<uint32_t, false, false>(p, a, stream) : launch_split<uint64_t, false, false>(p, a, stream);
-    if (rc == HEDDLE_OK && !count_only) rc = launch_evaluate(p, a, stream);
+    if (count == 1) rc = launch_split<uint64_t, false, 1>(p, a, stream);
+    else if (count == 2) rc = f32 ? launch_split<uint64_t, true, 2>(p, a, stream) : launch_split<uint64_t, false, 2>(p, a, stream);
+    else if (f32) rc = narrow ? launch_split<uint32_t, true, 0>(p, a, stream) : launch_split<uint64_t, true, 0>(p, a, stream);
+    else rc = narrow ? launch_split<uint32_t, false, 0>(p, a, stream) : launch_split<uint64_t, false, 0>(p, a, stream);
+    if (rc == HEDDLE_OK && count == 0) rc = launch_evaluate(p, a, stream);
     if (a.wst && !a.ext_scratch) {
         const int rd = profile_scratch_done(p, stream, a.wst, a.scratch_owned);
         if (rc == HEDDLE_OK) rc = rd;
@@ -647,7 +653,7 @@ extern "C" int heddle_price_plans(const heddle_profile *p, int64_t n, int32_t s_
     a.peak_mem = d_peak_mem;
     a.layers = d_layers;
     a.status = d_status;
-    return launch_price(p, a, stream, false);
+    return launch_price(p, a, stream, 0);
 }
 
 extern "C" int heddle_count_work(const heddle_profile *p, int64_t n, int32_t s_max,
@@ -655,6 +661,8 @@ extern "C" int heddle_count_work(const heddle_profile *p, int64_t n, int32_t s_m
                                  const int32_t *h_m, int32_t n_m, uint32_t flags,
                                  int64_t *h_relaxations, hipStream_t stream)
 {
+    const int mode = (flags & HEDDLE_F_COUNT_EVALUATED) ? 2 : 1;
+    flags &= ~HEDDLE_F_COUNT_EVALUATED;
     int rc = validate_price_args(p, n, s_max, d_n_stages, d_stages, h_m, n_m, flags);
     if (rc) return rc;
     if (!h_relaxations) return fail(HEDDLE_E_INVAL, "h_relaxations is NULL");
@@ -664,7 +672,7 @@ extern "C" int heddle_count_work(const heddle_profile *p, int64_t n, int32_t s_m
     if (e != hipSuccess) return fail(HEDDLE_E_NOMEM, "device scratch for the work counter could not be allocated");
     e = hipMemsetAsync(d_work, 0, sizeof(unsigned long long), stream);
     a.work = d_work;
-    rc = e == hipSuccess ? launch_price(p, a, stream, true) : hip_fail(e, "hipMemsetAsync");
+    rc = e == hipSuccess ? launch_price(p, a, stream, mode) : hip_fail(e, "hipMemsetAsync");
     unsigned long long h = 0;
     if (rc == HEDDLE_OK) e = hipMemcpyAsync(&h, d_work, sizeof(h), hipMemcpyDeviceToHost, stream);
     (void)hipFreeAsync(d_work, stream);                        // stream-ordered after the copy
@@ -730,5 +738,5 @@ extern "C" int heddle_price_plans_noalloc(const heddle_profile *p, int64_t n, in
         if (rc) return rc;
         a.ext_bytes = HEDDLE_NOALLOC_SCRATCH_BYTES;
     }
-    return launch_price(p, a, stream, false);
+    return launch_price(p, a, stream, 0);
 }

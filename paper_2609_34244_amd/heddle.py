@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(HERE, "libheddle.so")
 
 HEDDLE_OK, HEDDLE_E_INVAL, HEDDLE_E_NOMEM, HEDDLE_E_DEVICE, HEDDLE_E_RANGE, HEDDLE_E_NOFEASIBLE = 0, -1, -2, -3, -4, -5
 HEDDLE_F_FP32, HEDDLE_F_COMPUTE_ONLY, HEDDLE_F_DISTRIBUTE = 1, 2, 4
+HEDDLE_F_COUNT_EVALUATED = 8
 NOALLOC_SCRATCH_BYTES = 64 << 20   # HEDDLE_NOALLOC_SCRATCH_BYTES
 STATUS_NAMES = ["OK", "BAD_SHAPE", "BAD_TYPE", "BAD_TP", "UNPROFILED", "BAD_DP", "BAD_EP", "OVERSUBSCRIBED", "OOM"]
 EXPORTS = ["heddle_load_profile", "heddle_free_profile", "heddle_price_plans", "heddle_price_plans_noalloc",

@@ -568,6 +568,28 @@ def test_count_work(H, flags):
         assert H.heddle_count_work(prof, ns, st, [int(x) for x in w.m], flags) == oracle_work(w, flags), w.name
 
 
+@pytest.mark.parametrize("flags", [0, CO])
+def test_count_evaluated(H, flags):
+    """the kernel's count of the (row, end) pairs it relaxes equals the model of
+    its chunk schedule and exit rule, and stays within the window count"""
+    import kernel_schedule as KS
+    cases = [random_instance(7000 + s, L=20 + 5 * (s % 8), s_max=8, n=24, max_cost=40) for s in range(16)]
+    cases += [sub_workload(workload("c3_70b_dense"), np.arange(120)), sub_workload(workload("c4_moe"), np.arange(40))]
+    below = 0
+    for w in cases:
+        m = int(w.m[0])
+        prof = H.heddle_load_profile(w.profile)
+        ns, st = H.to_device(w.n_stages, w.stages)
+        got = H.heddle_count_work(prof, ns, st, [m], flags | H.HEDDLE_F_COUNT_EVALUATED)
+        want = sum(KS.evaluated_relaxations(w.profile, int(w.n_stages[t]), w.s_max, w.stages[t], m, bool(flags & CO))
+                   for t in range(w.n))
+        window = H.heddle_count_work(prof, ns, st, [m], flags)
+        assert got == want and got <= window, (w.name, got, want, window)
+        below += got < window
+    say("cases with pairs skipped by the exit rule", below, "of", len(cases))
+    assert below >= 4
+
+
 # ------------------------------------------------------------- Distribute mode
 DI = O.F_DISTRIBUTE
 DIST_SETS = [DI, DI | CO, DI | F32, DI | F32 | CO]

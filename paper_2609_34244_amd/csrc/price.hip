@@ -101,7 +101,6 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
     // template's windows fit it
     uint8_t *JX = smem + A.off_j;
     uint8_t *IX = smem + A.off_x;
-    V *GA = (V *)IX;
     const V *rows = stage_rows<V>(P, F32);
     auto xrow = [&](int s) -> uint8_t * { return IX + s * ls; };
 
@@ -202,16 +201,19 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                 // lane s: lk_s | jhi_s << 8, with 2^lk_s the lanes per row at stage s
                 // (64 >> ceil(log2 r) for r window rows, one when r >= 64) and jhi_s the
                 // last end leaving a layer to every later stage
-                // and (bits 16..31) 256 + the arena index of G_s[a_s] minus a_s: the
-                // arena holds the windows of stages S-1 .. 1 in that order, so stage
-                // s's starts after those of stages s+1 .. S-1
+                // and (bits 16..31) the LDS byte address at which G_s[i] would sit for
+                // i = 0 (G_s[i] at that address + i * sizeof(V)): the arena holds the
+                // windows of stages S-1 .. 1 in that order, so stage s's starts after
+                // those of stages s+1 .. S-1. The address is positive (the pair row
+                // before the arena is longer than L entries of V) and, while the arena
+                // is used, within the wavefront's LDS, which the host keeps under 64 KB
                 uint32_t aux;
                 {
                     const int r = Bl - Al + 1;
                     const int lk = r >= 64 ? 0 : 6 - (r > 1 ? 32 - __clz(r - 1) : 0);
                     const int before = wave_inclusive_sum(lane >= 1 && lane < S ? r : 0);   // windows of stages 1..s
                     aux = (uint32_t)lk | (uint32_t)(L - (S - 1 - lane)) << 8 |
-                          (uint32_t)(g_total - before - Al + 256) << 16;
+                          (uint32_t)(A.off_x + (int)sizeof(V) * (g_total - before - Al)) << 16;
                 }
                 RowRegs<V, NS> rr;
                 fetch_rows<V, NS>(rr, rows, (uint32_t)uni(rl32(x.prow, S - 1)), uni(rl32(Al, S - 1)), L, lane);
@@ -220,7 +222,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                     const uint32_t ks = uni64(pk, s);
                     const int a = ks & 255, b = (ks >> 8) & 255, e = (ks >> 16) & 255, a_next = ks >> 24;
                     const uint32_t ax = uni64(aux, s);
-                    const int gba = (int)(ax >> 16) - 256;             // G_s[i] at arena index gba + i
+                    V *Gs = (V *)(smem + (ax >> 16));                   // G_s[i] in the arena at Gs[i]
                     // P_s into the pair row over [a, e]; G_{s+1} stays in place
 #pragma unroll
                     for (int q = 0; q < NS; q++)
@@ -239,7 +241,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                                 const V gv = (V)(pL - X[i].x);
                                 if (S > 1) {                           // s = S - 1 > 0
                                     ((V *)&X[i])[1] = gv;
-                                    if (arena) GA[gba + i] = gv;
+                                    if (arena) Gs[i] = gv;
                                 } else {
                                     Bv = gv;                           // S = 1: row 0, lane 0
                                 }
@@ -330,7 +332,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                                 acc = group_min<V>(acc, kr);
                                 if (i <= b && part == 0) {             // then ic = i
                                     ((V *)&X[ic])[1] = acc;
-                                    if (arena) GA[gba + ic] = acc;
+                                    if (arena) Gs[ic] = acc;
                                 }
                             }
                         } while ((base += 64 >> lk) <= b);
@@ -350,34 +352,33 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                     // B*. Such a j is admissible from c_s and T(s, c_s, j) is within B*: some
                     // row with both properties exists (F_s[c_s] holds on the path) and T grows
                     // with j.
-                    int rem = g_total;                                 // arena index of G_{s+1}[a_{s+1}]
                     for (int s = 0; s < S - 1; s++) {
                         const uint32_t k1 = uni64(pk, s + 1);
-                        const int a1 = k1 & 255, w1 = ((k1 >> 8) & 255) - a1;   // rows a1 .. a1 + w1
-                        rem -= w1 + 1;
-                        const int lo = max(cs + 1, a1) - a1;           // lowest admissible row, from a1
-                        // the window in words of 64 rows, from the word holding lo (a later
-                        // word only when the window is longer than 64 rows). Bits past the
-                        // window's last row repeat that row's bit (the read is clamped to it),
-                        // and a set bit at or after lo and at or before the last row always
-                        // exists: G_s[c_s] is within B*, so is G_{s+1} at the end minimising
-                        // it, an admissible row of W_{s+1} at or after lo (rounding to fp32 is
-                        // monotone, so this holds for the fp32 test too). The first set bit
-                        // is therefore the row sought, with no test of the window's end.
-                        auto word = [&](int w0) -> uint64_t {
-                            const V g = GA[rem + min(w0 + lane, w1)];
+                        const int a1 = k1 & 255, b1 = (k1 >> 8) & 255;  // W_{s+1}: rows a1 .. b1
+                        const V *G1 = (const V *)(smem + (uni64(aux, s + 1) >> 16));   // G_{s+1}[j] at G1[j]
+                        const int lo = max(cs + 1, a1);                // lowest admissible row
+                        // 64 rows at a time from lo (a later word only when the window runs
+                        // more than 64 rows past lo). Bits past the window's last row repeat
+                        // that row's bit (the read is clamped to it), and a set bit at or
+                        // after lo and at or before the last row always exists: G_s[c_s] is
+                        // within B*, so is G_{s+1} at the end minimising it, an admissible row
+                        // of W_{s+1} at or after lo (rounding to fp32 is monotone, so this
+                        // holds for the fp32 test too). The first set bit is therefore the
+                        // row sought, with no test of the window's end.
+                        auto word = [&](int r0) -> uint64_t {
+                            const V g = G1[min(r0 + lane, b1)];
                             return ballot(F32 ? g != INF && within((uint64_t)g) : (uint64_t)g <= B);
                         };
-                        int w0 = lo & ~63;
-                        uint64_t mk = word(w0) & (~0ull << (lo - w0));   // rows from lo
-                        if (!mk) {                                     // a window longer than 64 rows
-                            while (w0 + 64 <= w1) {
-                                w0 += 64;
-                                mk = word(w0);
+                        int r0 = lo;
+                        uint64_t mk = word(r0);
+                        if (!mk) {                                     // more than 64 rows from lo
+                            while (r0 + 64 <= b1) {
+                                r0 += 64;
+                                mk = word(r0);
                                 if (mk) break;
                             }
                         }
-                        cs = a1 + w0 + __builtin_ctzll(mk);           // mk is not zero (see above)
+                        cs = r0 + __builtin_ctzll(mk);                 // mk is not zero (see above)
                         my_end = lane == s ? cs : my_end;
                     }
                 } else {
@@ -538,7 +539,9 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     }
     a.off_j = (int32_t)j_off;
     a.off_x = (int32_t)x_off;
-    a.arena_cap = (int32_t)(x_bytes / sizeof(V));
+    // the split kernel addresses the arena with 16-bit LDS byte offsets
+    const size_t x_max = x_off < 65535 ? 65535 - x_off : 0;
+    a.arena_cap = (int32_t)((x_bytes < x_max ? x_bytes : x_max) / sizeof(V));
     a.lds_per_wave = (int32_t)(x_off + x_bytes);
     // one wavefront per workgroup: a wavefront's LDS is released as soon as it
     // is done, whatever the other wavefronts on the CU are doing

@@ -379,7 +379,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                             }
                         }
                         cs = r0 + __builtin_ctzll(mk);                 // mk is not zero (see above)
-                        my_end = lane == s ? cs : my_end;
+                        asm volatile("v_writelane_b32 %0, %1, m0" : "+v"(my_end) : "s"(cs), "{m0}"(s));   // lane s := c_{s+1}
                     }
                 } else {
                     // ---------------- F_s for stages S-1 .. 1; xrow(s)[i] := the smallest row >= i

@@ -590,6 +590,22 @@ def test_count_evaluated(H, flags):
     assert below >= 4
 
 
+@pytest.mark.parametrize("flags", [F32, F32 | CO])
+def test_count_evaluated_fp32(H, flags):
+    """fp32 pricing runs the recurrence on the fixed-point image of its costs:
+    its counted pairs stay within the window count, which does not depend on
+    the costs, and the exit rule skips pairs there too"""
+    for w in [sub_workload(workload("c3_70b_dense"), np.arange(2000)), sub_workload(workload("c4_moe"), np.arange(1000)),
+              with_f32_table(random_instance(7006, L=50, s_max=8, n=64, max_cost=40), 7006)]:
+        prof = H.heddle_load_profile(w.profile)
+        ns, st = H.to_device(w.n_stages, w.stages)
+        m = [int(x) for x in w.m]
+        got = H.heddle_count_work(prof, ns, st, m, flags | H.HEDDLE_F_COUNT_EVALUATED)
+        window = H.heddle_count_work(prof, ns, st, m, flags)
+        assert window == H.heddle_count_work(prof, ns, st, m, flags & ~F32), w.name
+        assert 0 < got < window, (w.name, got, window)
+
+
 # ------------------------------------------------------------- Distribute mode
 DI = O.F_DISTRIBUTE
 DIST_SETS = [DI, DI | CO, DI | F32, DI | F32 | CO]

@@ -155,6 +155,15 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
             const int S_t = uni(S_in);
             const StageInfo<V> x = stage_info<V, F32>(P, A, S_t, rec_in, lane);
 
+            // Classes are taken from the largest key down: a larger key holds more
+            // micro-batches in flight at every stage, so fewer splits fit memory and
+            // its B* bounds those of the classes after it. A row's running minimum
+            // starts at U = that bound + 1 instead of INF: every row whose G is at
+            // most the bound keeps its exact value, the others end at U or above
+            // (above every B* to come), and the row loop's exit rule stops lanes once
+            // a stage time exceeds the bound. (Not under fp32 pricing, whose tests of the
+            // reconstruction round: a row held at U could round level with B*.)
+            V U = INF;
             while (todo) {
                 // an opaque copy of the stage count per class: tests on it are formed
                 // where they are used, not hoisted out of this loop and kept in scalar
@@ -162,7 +171,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                 int S = S_t;
                 asm volatile("" : "+s"(S));
                 const int key = n_m == 1 ? uni(key_k)
-                                           : uni((int)group_min<uint32_t>(((todo >> lane) & 1) ? (uint32_t)key_k : 0x7FFFFFFFu, 64));
+                                           : 255 - uni((int)group_min<uint32_t>(((todo >> lane) & 1) ? 255u - (uint32_t)key_k : 255u, 64));
                 const uint64_t cls = M1 ? todo : ballot(lane < n_m && key_k == key) & todo;
                 todo &= ~cls;
                 auto jhi_of = [&](int s) { return L - (S - 1 - s); };   // last end leaving a layer per later stage
@@ -295,7 +304,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                             const V2 *cm = X + max(hi - 3, lo);
                             const V2 *ce = X + hi;
                             const V2 *cx = X + lo + 4 * part;
-                            V acc = INF;
+                            V acc = M1 || F32 ? INF : U;
                             asm volatile("" : "+v"(acc));                    // one definition, not one per path
                             if (lo <= hi) {
                                 // the chunk loop runs while any lane of the group has a chunk
@@ -339,6 +348,7 @@ __global__ void __launch_bounds__(64, sizeof(V) == 4 ? 8 : 4) split_kernel(DevPr
                     }
                     wave_sync();
                 }
+                if (!M1 && !F32 && Bv != INF) U = Bv + 1;
                 if (COUNT) continue;
                 if (Bv == INF) continue;                       // no split fits memory
                 const uint64_t B = (uint64_t)Bv;

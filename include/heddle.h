@@ -309,7 +309,10 @@ int heddle_best_plan(const heddle_profile *p, int64_t n, int32_t s_max,
  * lower it). Each chunk counts the ends it adds (a last chunk moved back to
  * end at the row's last end counts those from its own start); a last-stage
  * row counts one. The values follow the flags' arithmetic (HEDDLE_F_FP32:
- * the fp32 image), so the count is exact, not a model.
+ * the fp32 image), so the count is exact, not a model. For a template with
+ * several in-flight classes (int64 pricing), the classes run from the
+ * largest key down, and a row's running minimum starts at the previous
+ * class's B* + 1, so lanes also stop once a stage time passes that bound.
  * With HEDDLE_F_DISTRIBUTE the unit is one stage-cost evaluation (time,
  * memory and gradient synchronisation of one stage): S for the proportional
  * split and, when it does not fit, 2 per alternative priced (only the two

@@ -9,6 +9,9 @@ lie on a complete split, with each row's ends taken in chunks of four by k
 lanes and a lane stopping after a chunk whose last end has a stage time at
 or above the lane's running minimum. Stage times and memory come from
 brute.Plan (plain sums of the per-layer terms), here as prefix differences.
+It models one in-flight class: when a template has several, the kernel
+starts the rows of later classes from an earlier class's B* + 1, which this
+model leaves out (the GPU test prices one m per template).
 """
 from __future__ import annotations
 

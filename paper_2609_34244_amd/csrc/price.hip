@@ -592,9 +592,18 @@ static int launch_split(const heddle_profile *p, PriceArgs &a, hipStream_t strea
     a.wwin = (uint16_t *)(buf + st_bytes);
     const int rw = launch_windows(p, a, w_lds, stream);
     if (rw != HEDDLE_OK) return rw;
-    const int64_t want = (a.n + wpb - 1) / wpb;
-    int blocks = (int)(want < 65536 ? want : 65536);
-    if (blocks >= 512) blocks = (blocks + 511) & ~511;        // XCD-aware runs (see the kernel's start)
+    // at least 65,536 workgroups (one per template for a smaller batch) and at
+    // least one per four templates, as a power of two: the hardware hands a
+    // finished workgroup's slot to the next one, which evens out the
+    // templates' uneven costs better than long grid-stride runs, while a few
+    // templates per workgroup keep the next one's records loaded ahead and the
+    // set-up shared (c3, 1,000,000 templates: 1.29 ms at 65,536 workgroups,
+    // 1.22 ms at 262,144, 1.26 ms at one per template)
+    const int64_t per_wg = (a.n + 4 * wpb - 1) / (4 * wpb);
+    const int64_t floor_wg = a.n < 65536 ? a.n : 65536;
+    const int64_t want = per_wg > floor_wg ? per_wg : floor_wg;
+    int blocks = 1;
+    while (blocks < want && blocks < (1 << 30)) blocks <<= 1;  // from 512 on, a multiple of 512: XCD-aware runs
     const DevProfile dev = p->dev;
     void *args[] = {(void *)&dev, (void *)&a};
     HEDDLE_HIP(hipLaunchKernel(kern, dim3(blocks), dim3(64 * wpb), args, lds, stream));

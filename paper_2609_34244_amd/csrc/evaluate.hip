@@ -36,10 +36,14 @@ __device__ __forceinline__ void evaluate_plan(const DevProfile &P, const PriceAr
     bool oom = false;
     int i = 0;
     uint32_t r_next = rec[0];
+    int l_next = lay[0];                                      // layer counts, like the records, one stage ahead
     for (int s = 0; s < S; s++) {
         const uint32_t r = r_next;
-        if (s + 1 < S) r_next = rec[s + 1];
-        const int j = i + lay[s];
+        const int j = i + l_next;
+        if (s + 1 < S) {
+            r_next = rec[s + 1];
+            l_next = lay[s + 1];
+        }
         const StageCost c = stage_cost<F32>(P, r, (int)(r_next & 0xFF), s, S, i, j, D, Mp);
         sumT += F32 ? rne24(c.T) : c.T;
         peak = c.mem > peak ? c.mem : peak;

@@ -9,9 +9,10 @@ lie on a complete split, with each row's ends taken in chunks of four by k
 lanes and a lane stopping after a chunk whose last end has a stage time at
 or above the lane's running minimum. Stage times and memory come from
 brute.Plan (plain sums of the per-layer terms), here as prefix differences.
-It models one in-flight class: when a template has several, the kernel
-starts the rows of later classes from an earlier class's B* + 1, which this
-model leaves out (the GPU test prices one m per template).
+template_relaxations() takes a template's several micro-batch counts the
+way the kernel does: one recurrence per in-flight class (key min(ceil(m/D),
+S), or 0 when memory is ignored), from the largest key down, each later
+class's rows starting at the previous class's B* + 1 instead of INF.
 """
 from __future__ import annotations
 
@@ -26,10 +27,12 @@ def _prefix(xs):
     return np.concatenate([[0], np.cumsum(np.asarray(xs, dtype=object))])
 
 
-def evaluated_relaxations(p, S, s_max, recs, m, compute_only=False, exit_rule=True, bottleneck=False):
+def evaluated_relaxations(p, S, s_max, recs, m, compute_only=False, exit_rule=True, bottleneck=False, start=None):
     """pairs relaxed for one plan (one in-flight class), as the kernel counts them;
     without the exit rule every end of every window row is relaxed. With
-    bottleneck=True also returns G_0[0] (None when no split fits)."""
+    bottleneck=True also returns G_0[0] (None when no split fits). start: the
+    value a row's running minimum starts from (INF when None)."""
+    acc0 = INF if start is None else start
     stt, st = status_of(p, S, s_max, recs)
     if stt != 0:
         return (0, None) if bottleneck else 0
@@ -77,11 +80,11 @@ def evaluated_relaxations(p, S, s_max, recs, m, compute_only=False, exit_rule=Tr
         Gs = {}
         for i in range(a, b + 1):
             lo, hi = max(i + 1, Bk[s + 1]), lim(s, i)
-            best = INF
+            best = acc0
             if lo <= hi:
                 cm = max(hi - 3, lo)
                 for part in range(k):
-                    cx, acc = lo + 4 * part, INF
+                    cx, acc = lo + 4 * part, acc0
                     while cx <= hi:
                         count += min(4, hi - cx + 1)
                         c = min(cx, cm)
@@ -94,5 +97,25 @@ def evaluated_relaxations(p, S, s_max, recs, m, compute_only=False, exit_rule=Tr
             Gs[i] = best
         G = Gs
     if bottleneck:
-        return count, (G[0] if G[0] < INF else None)
+        return count, (G[0] if G[0] < acc0 else None)
     return count
+
+
+def template_relaxations(p, S, s_max, recs, ms, compute_only=False):
+    """pairs relaxed for one template priced at every m of ms, as the kernel
+    counts them, and B* per m (None when no split fits)"""
+    stt, st = status_of(p, S, s_max, recs)
+    if stt != 0:
+        return 0, [None] * len(ms)
+    D = st[0]["dp"]
+    key = [0 if compute_only else min(ceil_div(int(m), D), S) for m in ms]
+    total, U, best = 0, None, {}
+    for k in sorted(set(key), reverse=True):
+        m = ms[key.index(k)]
+        c, b = evaluated_relaxations(p, S, s_max, recs, m, compute_only, bottleneck=True,
+                                     start=None if U is None else U + 1)
+        total += c
+        best[k] = b
+        if b is not None:
+            U = b
+    return total, [best[k] for k in key]

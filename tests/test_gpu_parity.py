@@ -590,6 +590,21 @@ def test_count_evaluated(H, flags):
     assert below >= 4
 
 
+def test_count_evaluated_class_bound(H):
+    """several micro-batch counts per template: the kernel's count of the pairs
+    it relaxes equals the model with the classes from the largest key down and
+    later rows starting at the previous class's B* + 1"""
+    import kernel_schedule as KS
+    for w in [sub_workload(workload("c5_stress"), np.arange(12))] + \
+             [random_instance(7000 + s, L=20 + 5 * (s % 8), s_max=8, n=24, max_cost=40) for s in range(8)]:
+        ms = [int(m) for m in w.m]
+        prof = H.heddle_load_profile(w.profile)
+        ns, st = H.to_device(w.n_stages, w.stages)
+        got = H.heddle_count_work(prof, ns, st, ms, H.HEDDLE_F_COUNT_EVALUATED)
+        want = sum(KS.template_relaxations(w.profile, int(w.n_stages[t]), w.s_max, w.stages[t], ms)[0]
+                   for t in range(w.n))
+        assert got == want, (w.name, got, want)
+
 @pytest.mark.parametrize("flags", [F32, F32 | CO])
 def test_count_evaluated_fp32(H, flags):
     """fp32 pricing runs the recurrence on the fixed-point image of its costs:

@@ -8,7 +8,7 @@ import pytest
 
 import kernel_schedule as KS
 from oracle import oracle as O
-from workloads.gen import random_instance
+from workloads.gen import make_workload, random_instance
 
 # lengths 20..55 with costs up to 40, so that rows are long enough for a lane
 # to take several chunks and the exit rule to fire
@@ -37,3 +37,34 @@ def test_schedule_model_against_oracle(co):
             fired += ev < full
             checked += b_ev is not None
     assert fired >= 10 and checked >= 50, (fired, checked)
+
+
+def test_class_ordered_bound_keeps_every_bottleneck():
+    """several micro-batch counts per template: classes from the largest key
+    down, later rows starting at the previous B* + 1, still reach the
+    oracle's bottleneck at every m, and never relax more pairs than pricing
+    each class from INF"""
+    checked = classes = fired = 0
+    cases = [random_instance(seed, L=L, s_max=8, n=24, max_cost=40) for seed, L in CASES]
+    # the stress workload's first templates (128 layers, up to 32 stages, six
+    # micro-batch counts), where the bound cuts rows
+    c5 = make_workload("c5_stress", n=12)
+    for w in cases + [c5]:
+        ms = [int(m) for m in w.m]
+        op = O.OracleProfile(w.profile)
+        o = O.price_plans(op, w.n_stages, w.stages, ms, 0)
+        for t in range(w.n):
+            S = int(w.n_stages[t])
+            total, best = KS.template_relaxations(w.profile, S, w.s_max, w.stages[t], ms)
+            for k in range(len(ms)):
+                want = int(o["bottleneck"][t, k])
+                assert (best[k] if best[k] is not None else I64_MAX) == want, (w.name, t, k)
+                checked += best[k] is not None
+            D = int(w.stages[t, 0] >> 16) or 1
+            keys = {min(-(-m // D), S) for m in ms}
+            plain = sum(KS.evaluated_relaxations(w.profile, S, w.s_max, w.stages[t], ms[[min(-(-m // D), S) for m in ms].index(k)])
+                        for k in keys)
+            assert total <= plain, (w.name, t)
+            classes += len(keys)
+            fired += total < plain
+    assert checked >= 50 and classes > len(CASES) * 24 and fired >= 5, (checked, classes, fired)
